@@ -1,0 +1,197 @@
+"""ORACLE — test infrastructure only.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the bench's ``cpu_baseline`` leg
+may import this package.  It is a plain, slow CPU calling context tree (a
+``std::map`` trie, see ``oracle.cpp``) written from the paper's description of the
+profiler's tree (Design, "Profiler", "Calling Context Tree"): call paths are
+inserted with frames that name the same location collapsed, metrics are summed at
+the node a path ends on (exclusive) and propagated to the root along the whole path
+(inclusive).  It shares no code with the HIP path.
+
+Readings fixed here (the paper is silent on them): frames are uint32 ids; the root
+is the empty path with id 0, parent 0xFFFFFFFF, frame 0, depth 0; node ids are the
+unsigned lexicographic rank of the root path (a proper prefix sorts first); sums are
+uint64 modulo 2^64; a zero-length path adds to the root's exclusive sum.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+NO_PARENT = 0xFFFFFFFF
+
+
+def build(verbose: bool = False) -> str:
+    """Compile liboracle.so in place (host C++, g++ -O2, single-threaded trie)."""
+    src = os.path.join(_HERE, "oracle.cpp")
+    tmp = _LIB_PATH + ".tmp"
+    cmd = ["g++", "-O2", "-std=c++17", "-fPIC", "-shared", "-pthread", src, "-o", tmp]
+    if verbose:
+        print(" ".join(cmd))
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _p(a):
+    return None if a is None else ctypes.c_void_p(a.ctypes.data)
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build()
+        lib = ctypes.CDLL(_LIB_PATH)
+        vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+        lib.or_create.restype = vp
+        lib.or_create.argtypes = [i32]
+        lib.or_destroy.argtypes = [vp]
+        lib.or_destroy.restype = None
+        lib.or_ingest.argtypes = [vp, i64, vp, vp, vp]
+        lib.or_finalize.restype = i64
+        lib.or_finalize.argtypes = [vp]
+        lib.or_export.argtypes = [vp, vp, vp, vp, vp, vp]
+        lib.or_brute.restype = i64
+        lib.or_brute.argtypes = [i64, vp, vp, vp, i32, vp, vp, vp, vp, vp]
+        lib.or_point_query.argtypes = [i64, vp, vp, vp, i32, i64, vp, vp, vp, vp, vp, ctypes.c_int]
+        lib.or_check.argtypes = [i64, i32, vp, vp, vp, vp, vp, vp, vp]
+        _lib = lib
+    return _lib
+
+
+def _csr(offsets, frames, metrics, m=None):
+    offsets = np.ascontiguousarray(offsets, dtype=np.int64)
+    frames = np.ascontiguousarray(frames, dtype=np.uint32)
+    if frames.size == 0:
+        frames = np.zeros(1, np.uint32)
+    n = offsets.size - 1
+    if metrics is None:
+        metrics = np.zeros((n, m or 1), np.uint64)
+    metrics = np.ascontiguousarray(metrics, dtype=np.uint64).reshape(n, -1) if n else \
+        np.zeros((0, m or (metrics.shape[1] if metrics.ndim == 2 else 1)), np.uint64)
+    return offsets, frames, metrics
+
+
+class Tree(dict):
+    """Canonical tree: keys parent, frame, depth (uint32[U]), excl, incl (uint64[U, M])."""
+
+    @property
+    def n_nodes(self):
+        return int(self["parent"].size)
+
+
+class Oracle:
+    """Incremental std::map trie: ``ingest`` any number of CSR batches, then ``tree``."""
+
+    def __init__(self, n_metrics):
+        self.m = int(n_metrics)
+        self._h = _load().or_create(self.m)
+        if not self._h:
+            raise ValueError("bad metric count")
+
+    def ingest(self, offsets, frames, metrics):
+        o, f, w = _csr(offsets, frames, metrics, self.m)
+        if w.shape[1] != self.m:
+            raise ValueError("metric count mismatch")
+        if _load().or_ingest(self._h, o.size - 1, _p(o), _p(f), _p(w)) != 0:
+            raise ValueError("malformed offsets")
+
+    def tree(self) -> Tree:
+        lib = _load()
+        U = lib.or_finalize(self._h)
+        t = Tree(parent=np.empty(U, np.uint32), frame=np.empty(U, np.uint32), depth=np.empty(U, np.uint32),
+                 excl=np.empty((U, self.m), np.uint64), incl=np.empty((U, self.m), np.uint64))
+        lib.or_export(self._h, _p(t["parent"]), _p(t["frame"]), _p(t["depth"]), _p(t["excl"]), _p(t["incl"]))
+        return t
+
+    def close(self):
+        if self._h:
+            _load().or_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def build_tree(offsets, frames, metrics) -> Tree:
+    """One-shot oracle tree of a CSR trace."""
+    o, f, w = _csr(offsets, frames, metrics)
+    orc = Oracle(w.shape[1])
+    try:
+        orc.ingest(o, f, w)
+        return orc.tree()
+    finally:
+        orc.close()
+
+
+def brute_tree(offsets, frames, metrics) -> Tree:
+    """Brute-force prefix enumeration (tiny inputs only)."""
+    o, f, w = _csr(offsets, frames, metrics)
+    n, m = o.size - 1, w.shape[1]
+    lib = _load()
+    U = lib.or_brute(n, _p(o), _p(f), _p(w), m, None, None, None, None, None)
+    if U < 0:
+        raise ValueError("malformed offsets")
+    t = Tree(parent=np.empty(U, np.uint32), frame=np.empty(U, np.uint32), depth=np.empty(U, np.uint32),
+             excl=np.empty((U, m), np.uint64), incl=np.empty((U, m), np.uint64))
+    lib.or_brute(n, _p(o), _p(f), _p(w), m, _p(t["parent"]), _p(t["frame"]), _p(t["depth"]),
+                 _p(t["excl"]), _p(t["incl"]))
+    return t
+
+
+def point_query(offsets, frames, metrics, q_offsets, q_frames, threads=None):
+    """(count[Q], excl[Q, M], incl[Q, M]) of query paths by a full scan of the events."""
+    o, f, w = _csr(offsets, frames, metrics)
+    qo = np.ascontiguousarray(q_offsets, dtype=np.int64)
+    qf = np.ascontiguousarray(q_frames, dtype=np.uint32)
+    if qf.size == 0:
+        qf = np.zeros(1, np.uint32)
+    nq, m = qo.size - 1, w.shape[1]
+    cnt = np.empty(nq, np.int64)
+    ex = np.empty((nq, m), np.uint64)
+    inc = np.empty((nq, m), np.uint64)
+    th = threads or max(1, min(16, len(os.sched_getaffinity(0))))
+    if _load().or_point_query(o.size - 1, _p(o), _p(f), _p(w), m, nq, _p(qo), _p(qf), _p(cnt), _p(ex),
+                              _p(inc), th) != 0:
+        raise ValueError("malformed offsets")
+    return cnt, ex, inc
+
+
+CHECK_MESSAGES = {
+    1: "root fields", 2: "parent id not smaller than node id", 3: "depth != parent depth + 1",
+    4: "siblings not in strictly increasing frame order", 5: "ids are not a preorder",
+    6: "inclusive != exclusive + sum of children's inclusive", 7: "root inclusive != total",
+    8: "sum of exclusive != root inclusive",
+}
+
+
+def check(tree, total=None):
+    """Run the invariant checker; returns (code, node) with code 0 when all hold."""
+    parent = np.ascontiguousarray(tree["parent"], np.uint32)
+    U = parent.size
+    excl = np.ascontiguousarray(tree["excl"], np.uint64).reshape(U, -1)
+    incl = np.ascontiguousarray(tree["incl"], np.uint64).reshape(U, -1)
+    tot = None if total is None else np.ascontiguousarray(total, np.uint64)
+    bad = np.zeros(1, np.int64)
+    code = _load().or_check(U, excl.shape[1], _p(parent), _p(np.ascontiguousarray(tree["frame"], np.uint32)),
+                            _p(np.ascontiguousarray(tree["depth"], np.uint32)), _p(excl), _p(incl),
+                            _p(tot), _p(bad))
+    return int(code), int(bad[0])
+
+
+def total_metrics(metrics):
+    """Column sums of uint64 metrics modulo 2^64."""
+    w = np.asarray(metrics, np.uint64)
+    if w.size == 0:
+        return np.zeros(w.shape[1] if w.ndim == 2 else 1, np.uint64)
+    return w.sum(axis=0, dtype=np.uint64)

@@ -1,0 +1,253 @@
+// ORACLE — test infrastructure only.  Only tests/, __graft_entry__.smoke() and the
+// bench's cpu_baseline leg may load this library.  It shares no code with the HIP
+// path (no headers, helpers, tables or kernels) and never sees its outputs except as
+// data handed to or_check.
+//
+// What it computes: the calling context tree of the paper's profiler (Design,
+// "Profiler", paragraph "Calling Context Tree"): call paths are inserted into a tree
+// whose nodes collapse frames that refer to the same location, each node holds a list
+// of metrics, a metric is added at the bottom node of its call path and propagated to
+// the root along the whole path.  Frames are uint32 ids (equal iff the ids are equal),
+// the sum is the only aggregate, sums wrap modulo 2^64, the root is the empty path,
+// and node ids are the rank of a node's root path in unsigned lexicographic order
+// (a proper prefix first), i.e. preorder with children visited by ascending frame.
+//
+// Parity of every function here is pinned by tests against hand-worked trees,
+// brute-force prefix enumeration, closed forms and invariants; the paper itself prints
+// no tree values, so nothing here is pinned to a printed number.
+#include <cstdint>
+#include <cstring>
+#include <map>
+#include <set>
+#include <thread>
+#include <vector>
+
+namespace {
+
+constexpr uint32_t kNoParent = 0xFFFFFFFFu;
+
+// A plain trie: one std::map of children per node, metrics summed at the node where
+// a path ends ("exclusive").
+struct Trie {
+  struct Node {
+    std::map<uint32_t, uint32_t> kids;  // frame -> node index
+  };
+  int32_t m;
+  std::vector<Node> nodes;
+  std::vector<uint64_t> excl;  // [node][m]
+  // canonical arrays after finalize()
+  std::vector<uint32_t> parent, frame, depth;
+  std::vector<uint64_t> c_excl, c_incl;
+
+  explicit Trie(int32_t m_) : m(m_), nodes(1), excl(m_, 0) {}
+
+  // Insert one call path and add its metrics at the node it ends on.
+  void insert(const uint32_t *path, int64_t len, const uint64_t *w) {
+    uint32_t v = 0;
+    for (int64_t k = 0; k < len; ++k) {
+      auto it = nodes[v].kids.find(path[k]);
+      if (it == nodes[v].kids.end()) {
+        uint32_t c = (uint32_t)nodes.size();
+        nodes[v].kids.emplace(path[k], c);
+        nodes.emplace_back();
+        excl.insert(excl.end(), m, 0);
+        v = c;
+      } else {
+        v = it->second;
+      }
+    }
+    for (int32_t j = 0; j < m; ++j) excl[(size_t)v * m + j] += w ? w[j] : 0;  // wraps mod 2^64
+  }
+
+  // Number the nodes in preorder with children in ascending frame order (std::map
+  // iterates keys in ascending unsigned order), then propagate every node's metrics to
+  // all of its ancestors: inclusive = exclusive + sum of the children's inclusive.
+  int64_t finalize() {
+    const size_t U = nodes.size();
+    parent.assign(U, 0); frame.assign(U, 0); depth.assign(U, 0);
+    c_excl.assign(U * m, 0); c_incl.assign(U * m, 0);
+    std::vector<uint32_t> id_of(U);
+    struct Item { uint32_t node, parent_id, frame, depth; };
+    std::vector<Item> stack{{0, kNoParent, 0, 0}};
+    uint32_t next = 0;
+    while (!stack.empty()) {
+      Item it = stack.back();
+      stack.pop_back();
+      uint32_t id = next++;
+      id_of[it.node] = id;
+      parent[id] = it.parent_id; frame[id] = it.frame; depth[id] = it.depth;
+      for (int32_t j = 0; j < m; ++j) c_excl[(size_t)id * m + j] = excl[(size_t)it.node * m + j];
+      // push children in descending frame order so the smallest is visited first
+      const auto &kids = nodes[it.node].kids;
+      for (auto r = kids.rbegin(); r != kids.rend(); ++r) stack.push_back({r->second, id, r->first, it.depth + 1});
+    }
+    // post-order accumulation: in preorder every child has a larger id than its parent
+    c_incl = c_excl;
+    for (size_t v = U; v-- > 1;)
+      for (int32_t j = 0; j < m; ++j) c_incl[(size_t)parent[v] * m + j] += c_incl[v * m + j];
+    return (int64_t)U;
+  }
+};
+
+bool valid_offsets(int64_t n, const int64_t *off) {
+  if (n < 0 || !off || off[0] != 0) return false;
+  for (int64_t i = 0; i < n; ++i) if (off[i + 1] < off[i]) return false;
+  return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+// ---- std::map trie oracle (incremental: ingest any number of event batches) ----
+void *or_create(int32_t n_metrics) {
+  if (n_metrics < 1 || n_metrics > 64) return nullptr;
+  return new Trie(n_metrics);
+}
+void or_destroy(void *h) { delete static_cast<Trie *>(h); }
+
+// Insert events [0, n) of one CSR batch.  Returns 0, or -1 on malformed offsets.
+int or_ingest(void *h, int64_t n, const int64_t *offsets, const uint32_t *frames, const uint64_t *metrics) {
+  Trie *t = static_cast<Trie *>(h);
+  if (!t || !valid_offsets(n, offsets)) return -1;
+  for (int64_t i = 0; i < n; ++i)
+    t->insert(frames + offsets[i], offsets[i + 1] - offsets[i], metrics ? metrics + (size_t)i * t->m : nullptr);
+  return 0;
+}
+
+// Compute the canonical arrays; returns the node count U (root included).
+int64_t or_finalize(void *h) { return static_cast<Trie *>(h)->finalize(); }
+
+// Copy canonical arrays out (any pointer may be NULL).  excl/incl are [U][M].
+int or_export(void *h, uint32_t *parent, uint32_t *frame, uint32_t *depth, uint64_t *excl, uint64_t *incl) {
+  Trie *t = static_cast<Trie *>(h);
+  const size_t U = t->parent.size();
+  if (parent) std::memcpy(parent, t->parent.data(), U * 4);
+  if (frame) std::memcpy(frame, t->frame.data(), U * 4);
+  if (depth) std::memcpy(depth, t->depth.data(), U * 4);
+  if (excl) std::memcpy(excl, t->c_excl.data(), U * t->m * 8);
+  if (incl) std::memcpy(incl, t->c_incl.data(), U * t->m * 8);
+  return 0;
+}
+
+// ---- brute force: every prefix of every event into an ordered set of vectors ----
+// std::set<std::vector<uint32_t>> orders by std::lexicographical_compare on unsigned
+// elements, so iteration order is the node id.  excl/incl by a double loop over
+// events x nodes.  O(N * L^2 * log); tiny inputs only.  Call with NULL outputs to get U.
+int64_t or_brute(int64_t n, const int64_t *offsets, const uint32_t *frames, const uint64_t *metrics,
+                 int32_t m, uint32_t *parent, uint32_t *frame, uint32_t *depth, uint64_t *excl,
+                 uint64_t *incl) {
+  if (!valid_offsets(n, offsets) || m < 1) return -1;
+  std::set<std::vector<uint32_t>> prefixes;
+  for (int64_t i = 0; i < n; ++i)
+    for (int64_t k = 0; k <= offsets[i + 1] - offsets[i]; ++k)
+      prefixes.insert(std::vector<uint32_t>(frames + offsets[i], frames + offsets[i] + k));
+  prefixes.insert(std::vector<uint32_t>());
+  const int64_t U = (int64_t)prefixes.size();
+  if (!parent && !frame && !depth && !excl && !incl) return U;
+  std::vector<std::vector<uint32_t>> nodes(prefixes.begin(), prefixes.end());
+  std::map<std::vector<uint32_t>, uint32_t> id;
+  for (int64_t v = 0; v < U; ++v) id[nodes[v]] = (uint32_t)v;
+  for (int64_t v = 0; v < U; ++v) {
+    const auto &p = nodes[v];
+    if (parent) parent[v] = p.empty() ? kNoParent : id[std::vector<uint32_t>(p.begin(), p.end() - 1)];
+    if (frame) frame[v] = p.empty() ? 0 : p.back();
+    if (depth) depth[v] = (uint32_t)p.size();
+    for (int32_t j = 0; j < m; ++j) {
+      uint64_t se = 0, si = 0;
+      for (int64_t i = 0; i < n; ++i) {
+        const int64_t L = offsets[i + 1] - offsets[i];
+        const uint32_t *f = frames + offsets[i];
+        if ((int64_t)p.size() > L) continue;
+        if (!std::equal(p.begin(), p.end(), f)) continue;
+        const uint64_t w = metrics[(size_t)i * m + j];
+        si += w;
+        if ((int64_t)p.size() == L) se += w;
+      }
+      if (excl) excl[(size_t)v * m + j] = se;
+      if (incl) incl[(size_t)v * m + j] = si;
+    }
+  }
+  return U;
+}
+
+// ---- point queries: one node's sums by a scan over all events ----
+// For each query path q: count = #events whose path has q as a prefix,
+// excl[j] = sum of w_j over events whose path equals q, incl[j] = sum over events
+// whose path has q as a prefix.  Works at any trace size (O(F) per query); queries
+// are spread over `threads` threads.
+int or_point_query(int64_t n, const int64_t *offsets, const uint32_t *frames, const uint64_t *metrics,
+                   int32_t m, int64_t nq, const int64_t *q_offsets, const uint32_t *q_frames,
+                   int64_t *count, uint64_t *excl, uint64_t *incl, int threads) {
+  if (!valid_offsets(n, offsets) || !valid_offsets(nq, q_offsets) || m < 1) return -1;
+  auto work = [&](int64_t qa, int64_t qb) {
+    for (int64_t q = qa; q < qb; ++q) {
+      const int64_t ql = q_offsets[q + 1] - q_offsets[q];
+      const uint32_t *qf = q_frames + q_offsets[q];
+      int64_t c = 0;
+      std::vector<uint64_t> se(m, 0), si(m, 0);
+      for (int64_t i = 0; i < n; ++i) {
+        const int64_t L = offsets[i + 1] - offsets[i];
+        if (L < ql) continue;
+        if (std::memcmp(frames + offsets[i], qf, (size_t)ql * 4) != 0) continue;
+        ++c;
+        for (int32_t j = 0; j < m; ++j) {
+          si[j] += metrics[(size_t)i * m + j];
+          if (L == ql) se[j] += metrics[(size_t)i * m + j];
+        }
+      }
+      count[q] = c;
+      for (int32_t j = 0; j < m; ++j) { excl[(size_t)q * m + j] = se[j]; incl[(size_t)q * m + j] = si[j]; }
+    }
+  };
+  if (threads < 1) threads = 1;
+  std::vector<std::thread> ts;
+  int64_t step = (nq + threads - 1) / threads;
+  for (int t = 0; t < threads && t * step < nq; ++t)
+    ts.emplace_back(work, t * step, std::min(nq, (t + 1) * step));
+  for (auto &t : ts) t.join();
+  return 0;
+}
+
+// ---- invariant checker for any calling context tree in canonical form ----
+// Returns 0 if every invariant holds, else a positive code naming the first failure
+// (and writes the offending node to *bad):
+//  1 root fields (parent sentinel, frame 0, depth 0)     2 parent[v] >= v
+//  3 depth[v] != depth[parent[v]] + 1                     4 siblings not strictly
+//    increasing in frame as ids increase                  5 ids are not a preorder
+//    (the parent of v is not on the current root path)    6 incl != excl + sum of
+//    children's incl (mod 2^64)                           7 incl[root] != total
+//  8 sum of excl != incl[root]
+int or_check(int64_t U, int32_t m, const uint32_t *parent, const uint32_t *frame, const uint32_t *depth,
+             const uint64_t *excl, const uint64_t *incl, const uint64_t *total, int64_t *bad) {
+  auto fail = [&](int code, int64_t v) { if (bad) *bad = v; return code; };
+  if (U < 1) return fail(1, 0);
+  if (parent[0] != kNoParent || frame[0] != 0 || depth[0] != 0) return fail(1, 0);
+  std::vector<int64_t> last_child(U, -1);
+  std::vector<uint32_t> path{0};
+  for (int64_t v = 1; v < U; ++v) {
+    const uint32_t p = parent[v];
+    if (p >= (uint64_t)v) return fail(2, v);
+    if (depth[v] != depth[p] + 1) return fail(3, v);
+    if (last_child[p] >= 0 && !(frame[last_child[p]] < frame[v])) return fail(4, v);
+    last_child[p] = v;
+    while (!path.empty() && path.back() != p) path.pop_back();
+    if (path.empty()) return fail(5, v);
+    path.push_back((uint32_t)v);
+  }
+  std::vector<uint64_t> acc(excl, excl + (size_t)U * m);
+  for (int64_t v = U - 1; v >= 1; --v)
+    for (int32_t j = 0; j < m; ++j) acc[(size_t)parent[v] * m + j] += incl[(size_t)v * m + j];
+  for (int64_t v = 0; v < U; ++v)
+    for (int32_t j = 0; j < m; ++j)
+      if (acc[(size_t)v * m + j] != incl[(size_t)v * m + j]) return fail(6, v);
+  for (int32_t j = 0; j < m; ++j) {
+    if (total && incl[j] != total[j]) return fail(7, 0);
+    uint64_t s = 0;
+    for (int64_t v = 0; v < U; ++v) s += excl[(size_t)v * m + j];
+    if (s != incl[j]) return fail(8, 0);
+  }
+  return 0;
+}
+
+}  // extern "C"

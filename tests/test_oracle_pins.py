@@ -1,0 +1,262 @@
+"""Pins for the CPU oracle (no GPU).
+
+The paper prints no calling-context-tree values, so the oracle is pinned to what the
+definition and mathematics fix: hand-worked trees (tests/golden), brute-force prefix
+enumeration in two independent implementations (C++ std::set and pure Python tuple
+sorting), closed forms for special shapes, algebraic laws, and an invariant checker
+that is itself shown to catch planted mistakes.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import tracegen
+from conftest import load_golden
+
+FIELDS = ("parent", "frame", "depth", "excl", "incl")
+
+
+def assert_tree_equal(a, b, ctx=""):
+    for k in FIELDS:
+        x, y = np.asarray(a[k]), np.asarray(b[k])
+        assert x.shape == y.shape, f"{ctx}: {k} shape {x.shape} vs {y.shape}"
+        assert np.array_equal(x, y), f"{ctx}: {k} differs at {np.flatnonzero((x != y).ravel())[:5]}"
+
+
+def py_brute(offsets, frames, metrics):
+    """Independent pure-Python definition: nodes = distinct prefixes sorted as tuples
+    (Python orders tuples lexicographically, a proper prefix first; ints compare as
+    unsigned here because the frames are non-negative Python ints)."""
+    n = len(offsets) - 1
+    m = metrics.shape[1]
+    paths = [tuple(int(x) for x in frames[offsets[i]:offsets[i + 1]]) for i in range(n)]
+    nodes = sorted({p[:k] for p in paths for k in range(len(p) + 1)} | {()})
+    idx = {p: i for i, p in enumerate(nodes)}
+    mask = (1 << 64) - 1
+    excl = [[0] * m for _ in nodes]
+    incl = [[0] * m for _ in nodes]
+    for i, p in enumerate(paths):
+        for j in range(m):
+            w = int(metrics[i, j])
+            excl[idx[p]][j] = (excl[idx[p]][j] + w) & mask
+            for k in range(len(p) + 1):
+                incl[idx[p[:k]]][j] = (incl[idx[p[:k]]][j] + w) & mask
+    return {
+        "parent": np.array([0xFFFFFFFF if not p else idx[p[:-1]] for p in nodes], np.uint32),
+        "frame": np.array([0 if not p else p[-1] for p in nodes], np.uint32),
+        "depth": np.array([len(p) for p in nodes], np.uint32),
+        "excl": np.array(excl, np.uint64).reshape(len(nodes), m),
+        "incl": np.array(incl, np.uint64).reshape(len(nodes), m),
+    }
+
+
+@pytest.mark.parametrize("name", ["W1.txt", "W2.txt", "W3.txt", "W4.txt"])
+def test_hand_worked(name):
+    o, f, w, want = load_golden(name)
+    got = oracle.build_tree(o, f, w)
+    assert_tree_equal(got, want, name)
+    assert_tree_equal(oracle.brute_tree(o, f, w), want, name + " brute")
+    assert_tree_equal(py_brute(o, f, w), want, name + " py")
+    assert oracle.check(got, oracle.total_metrics(w)) == (0, 0)
+
+
+@pytest.mark.parametrize("seed", range(300))
+def test_oracle_vs_brute_tiny_random(seed):
+    # alphabet <= 4 and length <= 8 force shared prefixes, interior end nodes and
+    # zero-length paths; metrics span the full uint64 range (wrap-around)
+    n = 1 + seed % 60
+    alphabet = 2 + seed % 3
+    o, f, w = tracegen.random_small(n, alphabet, 8, 1 + seed % 3, seed)
+    got = oracle.build_tree(o, f, w)
+    assert_tree_equal(got, oracle.brute_tree(o, f, w), f"seed {seed}")
+    assert oracle.check(got, oracle.total_metrics(w)) == (0, 0)
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_oracle_vs_python_definition(seed):
+    o, f, w = tracegen.random_small(1 + seed % 30, 3 + seed % 6, 6, 2, 10_000 + seed)
+    assert_tree_equal(oracle.build_tree(o, f, w), py_brute(o, f, w), f"seed {seed}")
+
+
+def test_all_length_one_is_sort_unique_and_histogram():
+    rng = np.random.default_rng(5)
+    ids = np.array([0, 1, 0x7FFFFFFF, 0x80000000, 0xFFFFFFFF, 12345], np.uint32)
+    f = ids[rng.integers(0, ids.size, 500)]
+    o = np.arange(501, dtype=np.int64)
+    w = rng.integers(0, 2**63, size=(500, 2), dtype=np.uint64) * np.uint64(2) + np.uint64(1)
+    t = oracle.build_tree(o, f, w)
+    uniq = np.unique(f)  # numpy sorts uint32 as unsigned
+    assert t.n_nodes == 1 + uniq.size
+    assert np.array_equal(t["frame"][1:], uniq)
+    assert np.all(t["parent"][1:] == 0) and np.all(t["depth"][1:] == 1)
+    hist = np.zeros((uniq.size, 2), np.uint64)
+    np.add.at(hist, np.searchsorted(uniq, f), w)  # uint64 adds wrap mod 2^64
+    assert np.array_equal(t["excl"][1:], hist) and np.array_equal(t["incl"][1:], hist)
+    assert np.array_equal(t["incl"][0], w.sum(axis=0, dtype=np.uint64))
+    assert np.all(t["excl"][0] == 0)
+
+
+@pytest.mark.parametrize("L", [1, 2, 7, 64, 512, 3000])
+def test_single_path_is_a_chain(L):
+    f = np.arange(L, dtype=np.uint32)[::-1].copy() * np.uint32(2654435761)
+    o = np.array([0, L], np.int64)
+    w = np.array([[123456789]], np.uint64)
+    t = oracle.build_tree(o, f, w)
+    assert t.n_nodes == L + 1
+    assert np.array_equal(t["parent"][1:], np.arange(L, dtype=np.uint32))
+    assert np.array_equal(t["frame"][1:], f)
+    assert np.array_equal(t["depth"], np.arange(L + 1, dtype=np.uint32))
+    assert np.all(t["incl"] == 123456789)
+    assert np.all(t["excl"][:-1] == 0) and t["excl"][-1, 0] == 123456789
+
+
+def test_all_events_identical():
+    path = np.array([9, 3, 3, 9, 0xFFFFFFFF], np.uint32)
+    n = 1000
+    f = np.tile(path, n)
+    o = np.arange(n + 1, dtype=np.int64) * path.size
+    w = np.full((n, 1), 3, np.uint64)
+    t = oracle.build_tree(o, f, w)
+    assert t.n_nodes == path.size + 1
+    assert np.all(t["incl"][:, 0] == 3 * n)
+    assert t["excl"][-1, 0] == 3 * n and np.all(t["excl"][:-1] == 0)
+
+
+def test_empty_input_is_root_only():
+    t = oracle.build_tree(np.zeros(1, np.int64), np.zeros(0, np.uint32), np.zeros((0, 2), np.uint64))
+    assert t.n_nodes == 1
+    assert t["parent"][0] == 0xFFFFFFFF and np.all(t["excl"] == 0) and np.all(t["incl"] == 0)
+
+
+def test_metrics_are_independent_columns():
+    o, f, w = tracegen.random_paths(400, 20, 12, 4, seed=77)
+    t = oracle.build_tree(o, f, w)
+    for j in range(4):
+        tj = oracle.build_tree(o, f, w[:, j:j + 1])
+        for k in ("parent", "frame", "depth"):
+            assert np.array_equal(t[k], tj[k])
+        assert np.array_equal(t["excl"][:, j], tj["excl"][:, 0])
+        assert np.array_equal(t["incl"][:, j], tj["incl"][:, 0])
+
+
+def _subset(o, f, w, idx):
+    lens = (o[1:] - o[:-1])[idx]
+    oo = np.zeros(idx.size + 1, np.int64)
+    oo[1:] = np.cumsum(lens)
+    ff = np.concatenate([f[o[i]:o[i + 1]] for i in idx]) if idx.size else np.zeros(0, np.uint32)
+    return oo, ff.astype(np.uint32), w[idx]
+
+
+def test_permutation_invariance():
+    o, f, w = tracegen.random_paths(500, 8, 10, 2, seed=3)
+    perm = np.random.default_rng(0).permutation(500)
+    assert_tree_equal(oracle.build_tree(o, f, w), oracle.build_tree(*_subset(o, f, w, perm)))
+
+
+def test_incremental_ingest_equals_one_shot():
+    o, f, w = tracegen.random_paths(900, 30, 16, 3, seed=11)
+    one = oracle.build_tree(o, f, w)
+    inc = oracle.Oracle(3)
+    for a, b in [(0, 100), (100, 101), (101, 101), (101, 650), (650, 900)]:
+        inc.ingest(*_subset(o, f, w, np.arange(a, b)))
+    assert_tree_equal(one, inc.tree())
+
+
+def test_exclusive_is_additive_over_a_split():
+    o, f, w = tracegen.random_paths(600, 6, 8, 1, seed=21)
+    idx = np.arange(600)
+    a, b = idx[idx % 3 == 0], idx[idx % 3 != 0]
+    t = oracle.build_tree(o, f, w)
+    ta, tb = oracle.build_tree(*_subset(o, f, w, a)), oracle.build_tree(*_subset(o, f, w, b))
+
+    def keyed(tr):
+        # map root path -> excl via parent pointers
+        paths = {0: ()}
+        out = {}
+        for v in range(1, tr.n_nodes):
+            paths[v] = paths[int(tr["parent"][v])] + (int(tr["frame"][v]),)
+        for v in range(tr.n_nodes):
+            out[paths[v]] = int(tr["excl"][v, 0])
+        return out
+    ka, kb, kt = keyed(ta), keyed(tb), keyed(t)
+    for p, e in kt.items():
+        assert e == (ka.get(p, 0) + kb.get(p, 0)) % (1 << 64)
+
+
+def test_point_query_matches_tree():
+    o, f, w = tracegen.random_paths(300, 5, 7, 2, seed=8)
+    t = oracle.build_tree(o, f, w)
+    paths = {0: []}
+    for v in range(1, t.n_nodes):
+        paths[v] = paths[int(t["parent"][v])] + [int(t["frame"][v])]
+    qs = list(range(t.n_nodes))
+    qo = np.zeros(len(qs) + 1, np.int64)
+    qo[1:] = np.cumsum([len(paths[v]) for v in qs])
+    qf = np.array([x for v in qs for x in paths[v]], np.uint32)
+    cnt, ex, inc = oracle.point_query(o, f, w, qo, qf, threads=2)
+    assert np.all(cnt > 0)
+    assert np.array_equal(ex, t["excl"]) and np.array_equal(inc, t["incl"])
+    # a path that is not in the tree
+    cnt, ex, inc = oracle.point_query(o, f, w, np.array([0, 2]), np.array([123456, 7], np.uint32))
+    assert cnt[0] == 0 and np.all(inc == 0)
+
+
+def test_malformed_offsets_rejected():
+    with pytest.raises(ValueError):
+        oracle.build_tree(np.array([1, 2]), np.zeros(2, np.uint32), np.zeros((1, 1), np.uint64))
+    with pytest.raises(ValueError):
+        oracle.build_tree(np.array([0, 3, 2]), np.zeros(3, np.uint32), np.zeros((2, 1), np.uint64))
+
+
+# ---- the invariant checker catches planted mistakes (planted on the CPU, in oracle output)
+def _good_tree():
+    o, f, w = tracegen.random_paths(300, 6, 9, 2, seed=99)
+    return oracle.build_tree(o, f, w), oracle.total_metrics(w)
+
+
+def _plant(kind):
+    t, tot = _good_tree()
+    t = {k: v.copy() for k, v in t.items()}
+    U = t["parent"].size
+    if kind == "root":
+        t["parent"][0] = 0
+    elif kind == "parent_forward":
+        t["parent"][5] = 7
+    elif kind == "depth":
+        t["depth"][9] += 1
+    elif kind == "sibling_order":
+        kids = np.flatnonzero(t["parent"] == 0)
+        a, b = kids[0], kids[1]
+        t["frame"][a], t["frame"][b] = t["frame"][b], t["frame"][a]
+    elif kind == "not_preorder":
+        # re-parent a node onto a finished subtree
+        # W1's node [4] (id 5) re-parented under [1,2] (id 2, whose subtree ended at
+        # id 3): depth and sibling order stay valid, only the preorder breaks
+        o, f, w, _ = load_golden("W1.txt")
+        t = {k: v.copy() for k, v in oracle.build_tree(o, f, w).items()}
+        tot = oracle.total_metrics(w)
+        t["parent"][5], t["depth"][5] = 2, 3
+    elif kind == "dropped_child_term":
+        v = int(np.flatnonzero(t["depth"] == 2)[0])
+        t["incl"][v, 0] -= np.uint64(1)
+    elif kind == "total":
+        t["incl"][0, 1] += np.uint64(1)
+        t["excl"][0, 1] += np.uint64(1)
+    return t, tot
+
+
+@pytest.mark.parametrize("kind,code", [("root", 1), ("parent_forward", 2), ("depth", 3),
+                                       ("sibling_order", 4), ("not_preorder", 5),
+                                       ("dropped_child_term", 6), ("total", 7)])
+def test_checker_catches_planted_mistakes(kind, code):
+    t, tot = _plant(kind)
+    got, _ = oracle.check(t, tot)
+    assert got == code, f"{kind}: expected code {code}, got {got}"
+
+
+def test_checker_passes_workload_trees():
+    for name in ("tiny", "layered_1m"):
+        n = None if name == "tiny" else 100_000
+        o, f, w = tracegen.generate(name, n_events=n)
+        t = oracle.build_tree(o, f, w)
+        assert oracle.check(t, oracle.total_metrics(w)) == (0, 0)
