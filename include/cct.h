@@ -1,0 +1,129 @@
+/* cct.h — calling context tree construction on one AMD MI355X (gfx950).
+ *
+ * C ABI of libcct.so.  The library turns a batch of call paths, each carrying
+ * integer metrics, into a calling context tree (CCT): the profiler's tree of the
+ * paper (Design, "Profiler", paragraph "Calling Context Tree"), built by inserting
+ * call paths with frames that name the same location collapsed into one node, each
+ * node holding a list of metrics, every metric added at the bottom node of its
+ * call path and propagated to the root along the whole path.  cct_merge
+ * aggregates a further batch into an existing tree, as the profiler does when it
+ * flushes a full metric buffer into its tree (Design, "Profiler", "GPU Metrics");
+ * cct_query looks up the metrics of given call paths, the "query the metric data
+ * associated with the tree nodes" step of the analysis API (Design, "Performance
+ * Analyzer", "Analysis API").
+ *
+ * Data conventions (the paper is silent on all of them; these are this library's
+ * readings):
+ *   - A frame is a uint32 id; two frames are the same location iff their ids are
+ *     equal (interning of (library, PC), (file, line) or operator names happens
+ *     upstream).  Every uint32 value is a legal frame id.
+ *   - A call path is root-first: outermost caller first, GPU-kernel leaf last.
+ *   - The root is the empty path: id 0, parent CCT_NO_PARENT, frame 0, depth 0.
+ *     A zero-length path adds its metrics to the root's exclusive sums.
+ *   - Node ids are canonical: the rank of the node's root path in unsigned
+ *     lexicographic order, a proper prefix before its extensions (preorder, children
+ *     by ascending frame id).  Subtrees are therefore contiguous id ranges.
+ *   - The only aggregate is the sum, over uint64 modulo 2^64.
+ *   - excl[v][j] = sum of metric j over events whose path ends at v;
+ *     incl[v][j] = sum of metric j over events whose path passes through v.
+ *
+ * Threads and streams: calls order all their device work on the given HIP stream
+ * (NULL = the default stream) of the current device and return only after that
+ * work has completed; input buffers may be freed on return.  Distinct trees may be
+ * used from different threads at once; one tree must not be used concurrently.
+ *
+ * Errors: every call returns a cct_status; nothing aborts, throws or prints.  On an
+ * error, out-parameters are untouched and a tree passed to cct_merge is unchanged.
+ * cct_last_error() gives a message for the calling thread's last failure.
+ */
+#ifndef CCT_H
+#define CCT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  CCT_OK = 0,
+  CCT_EINVAL = -1,    /* bad argument or malformed offsets */
+  CCT_ENOMEM = -2,    /* a device allocation failed */
+  CCT_EDEVICE = -3,   /* a HIP runtime call failed */
+  CCT_EMISMATCH = -4, /* merge batch has a different metric count than the tree */
+  CCT_EOVERFLOW = -5  /* the tree would exceed 2^32 - 2 nodes, or a batch 2^31 - 2 events */
+} cct_status;
+
+#define CCT_MAX_METRICS 8          /* metrics per event (uint64 each) */
+#define CCT_NO_PARENT 0xFFFFFFFFu  /* parent of the root */
+#define CCT_MAX_EVENTS 0x7FFFFFFELL /* events per cct_build / cct_merge / cct_query call */
+
+typedef struct cct_tree cct_tree; /* opaque; owns its device memory */
+
+/* A batch of call paths in CSR form.  All pointers are DEVICE pointers of the
+ * current device, borrowed for the duration of the call.
+ *   n_events   N >= 0 (N <= CCT_MAX_EVENTS)
+ *   n_frames   F = offsets[N], the number of elements of `frames`
+ *   n_metrics  M, 1..CCT_MAX_METRICS
+ *   offsets    int64[N+1]; offsets[0] = 0, non-decreasing, offsets[N] = F.
+ *              Path i is frames[offsets[i] .. offsets[i+1]).  Checked on the device:
+ *              a violation makes the call return CCT_EINVAL.
+ *   frames     uint32[F], 4-byte aligned; may be NULL when F = 0
+ *   metrics    uint64[N][M] row-major, 8-byte aligned; ignored by cct_query (may be NULL) */
+typedef struct {
+  int64_t n_events;
+  int64_t n_frames;
+  int32_t n_metrics;
+  const int64_t *offsets;
+  const uint32_t *frames;
+  const uint64_t *metrics;
+} cct_paths;
+
+/* Build a new tree from one batch (calling-context-tree construction: insert every
+ * path, aggregate metrics at its end node, propagate to the root).  On success
+ * *out receives a tree owned by the caller (release with cct_free). */
+cct_status cct_build(const cct_paths *events, void *hip_stream, cct_tree **out);
+
+/* Aggregate one more batch into `tree` (the flush of a full metric buffer into the
+ * existing tree).  The result equals cct_build over the concatenation of every batch
+ * the tree has seen; node ids are renumbered.  chunk->n_metrics must equal the
+ * tree's metric count (else CCT_EMISMATCH). */
+cct_status cct_merge(cct_tree *tree, const cct_paths *chunk, void *hip_stream);
+
+/* Look up Q call paths (queries->offsets/frames, metrics ignored) in `tree`.
+ * Writes DEVICE arrays: node_ids int64[Q] (the canonical id, or -1 if the path is
+ * not a node), and, when non-NULL, excl/incl uint64[Q][M] (zeros for absent paths). */
+cct_status cct_query(const cct_tree *tree, const cct_paths *queries, void *hip_stream,
+                     int64_t *node_ids, uint64_t *excl, uint64_t *incl);
+
+/* Sizes of a tree: node count U (root included), metric count M, and the number of
+ * distinct full call paths D seen so far.  Any out-pointer may be NULL (host memory). */
+cct_status cct_info(const cct_tree *tree, int64_t *n_nodes, int32_t *n_metrics, int64_t *n_paths);
+
+/* Copy the canonical node arrays into caller buffers (host or device memory):
+ * parent/frame/depth uint32[U], excl/incl uint64[U][M].  Any pointer may be NULL. */
+cct_status cct_export(const cct_tree *tree, void *hip_stream, uint32_t *parent, uint32_t *frame,
+                      uint32_t *depth, uint64_t *excl, uint64_t *incl);
+
+/* Release a tree and its device memory (returned to the library's pool).  NULL-safe. */
+void cct_free(cct_tree *tree);
+
+/* Return every cached device block of the library's pool to the HIP runtime.  Trees
+ * still alive keep their memory. */
+void cct_release_cached_memory(void);
+
+/* Message describing the calling thread's most recent failure ("" if none). */
+const char *cct_last_error(void);
+
+/* Per-call timing of the most recent cct_build/cct_merge on the calling thread, in
+ * milliseconds measured with HIP events on the call's stream: [0] ingest (hash,
+ * dedup, exclusive aggregation), [1] publish of new paths, [2] canonical ordering
+ * (sort, LCP, scans), [3] node emission (parents, exclusive, inclusive), [4] whole
+ * call.  Returns the number of values written (<= n). */
+int cct_last_timings(double *ms, int n);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CCT_H */

@@ -1,0 +1,204 @@
+"""Calling context tree construction on one AMD MI355X (gfx950).
+
+Thin ctypes binding over ``libcct.so`` (see ``include/cct.h``): argument marshalling
+only, every step of the tree construction runs in the library's HIP kernels.  PyTorch
+provides device memory and the current stream.  If ``libcct.so`` is missing or fails
+to load, every call raises; there is no CPU fallback.
+
+    tree = build(offsets, frames, metrics)   # int64[N+1], int32/uint32[F], int64/uint64[N, M]
+    tree.merge(offsets2, frames2, metrics2)  # aggregate one more batch
+    ids, excl, incl = tree.query(q_offsets, q_frames)
+    arrays = tree.to_tensors()               # parent, frame, depth, excl, incl on the GPU
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+__all__ = ["build", "Tree", "CctError", "library_path", "load_library", "EXPORTED_SYMBOLS", "NO_PARENT"]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libcct.so")
+_lib = None
+
+NO_PARENT = 0xFFFFFFFF
+MAX_METRICS = 8
+EXPORTED_SYMBOLS = ("cct_build", "cct_merge", "cct_query", "cct_info", "cct_export", "cct_free",
+                    "cct_release_cached_memory", "cct_last_error", "cct_last_timings")
+_STATUS = {0: "CCT_OK", -1: "CCT_EINVAL", -2: "CCT_ENOMEM", -3: "CCT_EDEVICE", -4: "CCT_EMISMATCH",
+           -5: "CCT_EOVERFLOW"}
+
+
+class CctError(RuntimeError):
+    def __init__(self, status, message):
+        self.status = status
+        self.name = _STATUS.get(status, str(status))
+        super().__init__(f"{self.name}: {message}")
+
+
+class _Paths(ctypes.Structure):
+    _fields_ = [("n_events", ctypes.c_int64), ("n_frames", ctypes.c_int64), ("n_metrics", ctypes.c_int32),
+                ("offsets", ctypes.c_void_p), ("frames", ctypes.c_void_p), ("metrics", ctypes.c_void_p)]
+
+
+def library_path():
+    return _LIB_PATH
+
+
+def load_library():
+    """Load libcct.so (built by ``__graft_entry__.build()``); raises if it is absent."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(f"{_LIB_PATH} is missing: run __graft_entry__.build() (hipcc, gfx950) first")
+    lib = ctypes.CDLL(_LIB_PATH)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    P = ctypes.POINTER
+    lib.cct_build.argtypes = [P(_Paths), vp, P(vp)]
+    lib.cct_merge.argtypes = [vp, P(_Paths), vp]
+    lib.cct_query.argtypes = [vp, P(_Paths), vp, vp, vp, vp]
+    lib.cct_info.argtypes = [vp, P(i64), P(i32), P(i64)]
+    lib.cct_export.argtypes = [vp, vp, vp, vp, vp, vp, vp]
+    lib.cct_free.argtypes = [vp]
+    lib.cct_free.restype = None
+    lib.cct_release_cached_memory.argtypes = []
+    lib.cct_release_cached_memory.restype = None
+    lib.cct_last_error.restype = ctypes.c_char_p
+    lib.cct_last_timings.argtypes = [P(ctypes.c_double), ctypes.c_int]
+    for name in ("cct_build", "cct_merge", "cct_query", "cct_info", "cct_export"):
+        getattr(lib, name).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _check(status):
+    if status != 0:
+        raise CctError(status, load_library().cct_last_error().decode())
+
+
+def _stream():
+    import torch
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _paths(offsets, frames, metrics, need_metrics=True):
+    import torch
+    if not (offsets.is_cuda and frames.is_cuda):
+        raise ValueError("offsets and frames must be device tensors")
+    if offsets.dtype != torch.int64 or offsets.dim() != 1 or not offsets.is_contiguous():
+        raise ValueError("offsets must be a contiguous int64[N+1] tensor")
+    if frames.dtype not in (torch.int32, torch.uint32) or frames.dim() != 1 or not frames.is_contiguous():
+        raise ValueError("frames must be a contiguous int32/uint32[F] tensor")
+    n = offsets.numel() - 1
+    if n < 0:
+        raise ValueError("offsets must hold N+1 >= 1 elements")
+    m = 1
+    mp = None
+    if metrics is not None:
+        if not metrics.is_cuda or metrics.dtype not in (torch.int64, torch.uint64) or not metrics.is_contiguous():
+            raise ValueError("metrics must be a contiguous int64/uint64 [N, M] device tensor")
+        if metrics.dim() == 1:
+            metrics = metrics.view(-1, 1)
+        if metrics.shape[0] != n:
+            raise ValueError("metrics must have N rows")
+        m = metrics.shape[1]
+        mp = metrics.data_ptr() if metrics.numel() else None
+    elif need_metrics:
+        raise ValueError("metrics required")
+    p = _Paths(n, frames.numel(), m, offsets.data_ptr(), frames.data_ptr() if frames.numel() else None, mp)
+    return p, m
+
+
+class Tree:
+    """A calling context tree owned by libcct (device memory, canonical node ids)."""
+
+    def __init__(self, handle):
+        self._h = ctypes.c_void_p(handle)
+
+    @property
+    def handle(self):
+        return self._h
+
+    def _info(self):
+        u, m, d = ctypes.c_int64(), ctypes.c_int32(), ctypes.c_int64()
+        _check(load_library().cct_info(self._h, ctypes.byref(u), ctypes.byref(m), ctypes.byref(d)))
+        return u.value, m.value, d.value
+
+    @property
+    def n_nodes(self):
+        return self._info()[0]
+
+    @property
+    def n_metrics(self):
+        return self._info()[1]
+
+    @property
+    def n_paths(self):
+        return self._info()[2]
+
+    def merge(self, offsets, frames, metrics):
+        p, _ = _paths(offsets, frames, metrics)
+        _check(load_library().cct_merge(self._h, ctypes.byref(p), _stream()))
+        return self
+
+    def query(self, offsets, frames, want_metrics=True):
+        import torch
+        p, _ = _paths(offsets, frames, None, need_metrics=False)
+        u, m, d = self._info()
+        q = offsets.numel() - 1
+        dev = offsets.device
+        ids = torch.empty(max(q, 1), dtype=torch.int64, device=dev)[:q]
+        ex = torch.empty((q, m), dtype=torch.int64, device=dev) if want_metrics else None
+        inc = torch.empty((q, m), dtype=torch.int64, device=dev) if want_metrics else None
+        _check(load_library().cct_query(self._h, ctypes.byref(p), _stream(), ids.data_ptr() if q else None,
+                                        ex.data_ptr() if want_metrics and q else None,
+                                        inc.data_ptr() if want_metrics and q else None))
+        return ids, ex, inc
+
+    def to_tensors(self, device=None):
+        """Canonical arrays as tensors: parent/frame/depth int32[U] (bit patterns of
+        uint32), excl/incl int64[U, M] (bit patterns of uint64)."""
+        import torch
+        u, m, _ = self._info()
+        dev = torch.device(device) if device is not None else torch.device("cuda", torch.cuda.current_device())
+        out = {k: torch.empty(u, dtype=torch.int32, device=dev) for k in ("parent", "frame", "depth")}
+        out["excl"] = torch.empty((u, m), dtype=torch.int64, device=dev)
+        out["incl"] = torch.empty((u, m), dtype=torch.int64, device=dev)
+        _check(load_library().cct_export(self._h, _stream(), *(out[k].data_ptr() for k in
+                                                                ("parent", "frame", "depth", "excl", "incl"))))
+        return out
+
+    def to_numpy(self):
+        """Canonical arrays as numpy (uint32 / uint64)."""
+        import numpy as np
+        t = self.to_tensors(device="cpu")
+        return {k: (v.numpy().view(np.uint32) if v.dtype.itemsize == 4 else v.numpy().view(np.uint64))
+                for k, v in t.items()}
+
+    def free(self):
+        if self._h is not None and self._h.value:
+            load_library().cct_free(self._h)
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
+def build(offsets, frames, metrics):
+    """Build a calling context tree from one CSR batch of device tensors."""
+    p, _ = _paths(offsets, frames, metrics)
+    h = ctypes.c_void_p()
+    _check(load_library().cct_build(ctypes.byref(p), _stream(), ctypes.byref(h)))
+    return Tree(h.value)
+
+
+def last_timings():
+    """Per-phase HIP-event times (ms) of this thread's last build/merge: ingest,
+    publish, sort, canonical emission, total."""
+    buf = (ctypes.c_double * 5)()
+    n = load_library().cct_last_timings(buf, 5)
+    return list(buf)[:n]

@@ -1,0 +1,365 @@
+// Canonical tree from the D distinct full paths (path store + exclusive sums).
+//
+// The paper's tree is a pointer structure with no node numbering (Design,
+// "Profiler", "Calling Context Tree"); this library numbers nodes by the unsigned
+// lexicographic rank of their root path.  With the D distinct full paths sorted
+// lexicographically (p_0 < p_1 < ...) and lcp_i the length of the longest common
+// prefix of p_{i-1} and p_i (lcp_0 = 0):
+//   - path i contributes exactly the nodes p_i[0..l) for l in (lcp_i, len_i] (its
+//     chain), which are new and, in id order, follow every node of the earlier
+//     paths; so node ids are base_i + (l - lcp_i - 1) with base_i = 1 + sum of the
+//     chain lengths (len - lcp) of earlier paths, and U = 1 + sum of all of them;
+//   - the parent of a chain's first node is the node p_i[0..lcp_i), created by the
+//     largest c < i with lcp_c < lcp_i (previous smaller value); every other chain
+//     node's parent is the node before it;
+//   - the paths through node (i, l) are exactly p_i .. p_{e-1}, e the first j > i
+//     with lcp_j < l (next smaller value), and since a metric lands at the end node
+//     of its path ("at the bottom of a call path") and is propagated "along the
+//     entire call path" to the root, inclusive(i, l) = S[e] - S[i] with S the
+//     exclusive prefix sum of the per-path sums in sorted order (mod 2^64);
+//   - exclusive(i, len_i) = the sums of path i, every other node has none (the empty
+//     path, which sorts first, puts its sums on the root).
+// Every step is a sort, a scan or an O(log D) search: the number of kernel launches
+// does not grow with the tree depth.
+#include "common.h"
+
+namespace cct {
+
+namespace {
+
+constexpr uint32_t kInf = 0xFFFFFFFFu;
+constexpr int kSortBlock = 1024;   // keys per block-local bitonic sort
+constexpr int kMergeItems = 8;     // outputs per thread per merge pass
+constexpr int kScanRows = 1024;    // rows per scan block
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ inline u32x4 ld4(const uint32_t *p) { return *(const u32x4 *)p; }
+
+// Exact comparison of two stored paths: returns <0, 0, >0 and their lcp.  Starts are
+// 16-frame aligned and tails are padded, so 16-byte loads never leave a path's slot.
+__device__ int path_cmp_exact(const CanonArgs &a, uint32_t x, uint32_t y, uint32_t from, uint32_t *lcp) {
+  const uint32_t lx = a.plen[x], ly = a.plen[y];
+  const uint32_t *px = a.pframes + a.pstart[x], *py = a.pframes + a.pstart[y];
+  const uint32_t n = min(lx, ly);
+  for (uint32_t q = from & ~15u; q < n; q += 16) {
+    u32x4 vx[4], vy[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) { vx[c] = ld4(px + q + 4 * c); vy[c] = ld4(py + q + 4 * c); }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t k = q + 4 * c + e;
+        if (k < n && vx[c][e] != vy[c][e]) {
+          *lcp = k;
+          return vx[c][e] < vy[c][e] ? -1 : 1;
+        }
+      }
+    }
+  }
+  *lcp = n;
+  return lx < ly ? -1 : (lx > ly ? 1 : 0);
+}
+
+// Comparison accelerated by checkpoint hashes (prefix hashes every 16 frames): skip
+// to the first 16-frame block whose prefix hashes differ, then compare frames
+// there.  A hash collision can only make this answer wrong, never loop or fault;
+// the exact verification after the sort catches any resulting misorder.
+__device__ bool path_less(const CanonArgs &a, uint32_t x, uint32_t y) {
+  if (x == kInf) return false;
+  if (y == kInf) return true;
+  uint32_t l;
+  if (a.exact) return path_cmp_exact(a, x, y, 0, &l) < 0;
+  const uint32_t lx = a.plen[x], ly = a.plen[y];
+  const int64_t sx = a.pstart[x], sy = a.pstart[y];
+  const uint32_t n = min(lx, ly), nb = n / kStoreAlign;
+  const uint64_t *cx = a.pcp + sx / kStoreAlign, *cy = a.pcp + sy / kStoreAlign;
+  uint32_t b = 0;
+  for (; b + 4 <= nb; b += 4) {
+    uint64_t hx[4], hy[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) { hx[c] = cx[b + c]; hy[c] = cy[b + c]; }
+    int c = 0;
+    while (c < 4 && hx[c] == hy[c]) ++c;
+    if (c < 4) { b += c; goto found; }
+  }
+  for (; b < nb; ++b)
+    if (cx[b] != cy[b]) break;
+found:
+  {
+    // first differing frame is in block b (or in the partial block past nb)
+    const int r = path_cmp_exact(a, x, y, b * kStoreAlign, &l);
+    if (l < min(n, (b + 1) * kStoreAlign) || b >= nb) return r < 0;
+    return path_cmp_exact(a, x, y, 0, &l) < 0;  // hashes differed, frames did not
+  }
+}
+
+// ---- sort -------------------------------------------------------------------------
+__global__ __launch_bounds__(512) void sort_block_kernel(CanonArgs a, uint32_t *out) {
+  __shared__ uint32_t key[kSortBlock];
+  const int tid = threadIdx.x;
+  const int64_t base = (int64_t)blockIdx.x * kSortBlock;
+  for (int i = tid; i < kSortBlock; i += 512) key[i] = base + i < a.d ? (uint32_t)(base + i) : kInf;
+  __syncthreads();
+  for (int k = 2; k <= kSortBlock; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      const int i = 2 * j * (tid / j) + (tid % j), l = i + j;
+      const uint32_t x = key[i], y = key[l];
+      const bool up = (i & k) == 0;
+      const bool swap = up ? path_less(a, y, x) : path_less(a, x, y);
+      __syncthreads();
+      if (swap) { key[i] = y; key[l] = x; }
+      __syncthreads();
+    }
+  }
+  for (int i = tid; i < kSortBlock; i += 512)
+    if (base + i < a.d) out[base + i] = key[i];
+}
+
+__global__ __launch_bounds__(256) void merge_pass_kernel(CanonArgs a, const uint32_t *src, uint32_t *dst,
+                                                         int64_t run) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t o0 = t * kMergeItems;
+  if (o0 >= a.d) return;
+  const int64_t pair = o0 / (2 * run), pb = pair * 2 * run;
+  const int64_t la = min(run, a.d - pb), lb = max((int64_t)0, min(run, a.d - pb - run));
+  const uint32_t *A = src + pb, *B = src + pb + la;
+  const int64_t dgl = o0 - pb;
+  int64_t lo = max((int64_t)0, dgl - lb), hi = min(dgl, la);
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) >> 1;
+    if (path_less(a, A[mid], B[dgl - 1 - mid])) lo = mid + 1; else hi = mid;
+  }
+  int64_t ia = lo, ib = dgl - lo;
+  const int64_t cnt = min((int64_t)kMergeItems, la + lb - dgl);
+  for (int64_t k = 0; k < cnt; ++k) {
+    bool take_a;
+    if (ia >= la) take_a = false;
+    else if (ib >= lb) take_a = true;
+    else take_a = !path_less(a, B[ib], A[ia]);
+    dst[o0 + k] = take_a ? A[ia++] : B[ib++];
+  }
+}
+
+// ---- exact verification, lcp, scan rows ------------------------------------------------
+__global__ void lcp_kernel(CanonArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i > a.d) return;
+  const int C = 1 + a.m;
+  if (i == a.d) { a.lcp[i] = 0; return; }
+  const uint32_t p = a.order[i];
+  uint32_t l = 0;
+  if (i > 0) {
+    const int r = path_cmp_exact(a, a.order[i - 1], p, 0, &l);
+    if (r >= 0) atomicOr(&a.u_out[1], 1ull);  // not strictly increasing
+  }
+  a.lcp[i] = l;
+  uint64_t *row = a.scan_in + i * C;
+  row[0] = (uint64_t)(a.plen[p] - l);
+  for (int j = 0; j < a.m; ++j) row[1 + j] = a.psums[(int64_t)p * a.m + j];
+}
+
+// ---- multi-column exclusive scan (uint64, mod 2^64) -------------------------------------
+__device__ inline uint64_t shfl_up_u64(uint64_t v, int o) {
+  uint32_t lo = __shfl_up((uint32_t)v, o, 64), hi = __shfl_up((uint32_t)(v >> 32), o, 64);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+__global__ __launch_bounds__(256) void scan_reduce_kernel(const uint64_t *in, int64_t rows, int C, uint64_t *blk) {
+  __shared__ uint64_t part[4];
+  const int tid = threadIdx.x;
+  const int64_t r0 = (int64_t)blockIdx.x * kScanRows;
+  for (int c = 0; c < C; ++c) {
+    uint64_t s = 0;
+    for (int64_t r = r0 + tid; r < min(rows, r0 + kScanRows); r += 256) s += in[r * C + c];
+    for (int o = 32; o > 0; o >>= 1) {
+      uint32_t lo = __shfl_xor((uint32_t)s, o, 64), hi = __shfl_xor((uint32_t)(s >> 32), o, 64);
+      s += ((uint64_t)hi << 32) | lo;
+    }
+    if ((tid & 63) == 0) part[tid >> 6] = s;
+    __syncthreads();
+    if (tid == 0) blk[blockIdx.x * C + c] = part[0] + part[1] + part[2] + part[3];
+    __syncthreads();
+  }
+}
+
+// exclusive scan of the block sums in place; totals into out row `rows`
+__global__ __launch_bounds__(256) void scan_blocks_kernel(uint64_t *blk, int64_t nblk, int C, uint64_t *out,
+                                                          int64_t rows) {
+  __shared__ uint64_t part[4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  for (int c = 0; c < C; ++c) {
+    uint64_t carry = 0;
+    for (int64_t b0 = 0; b0 < nblk; b0 += 256) {
+      const int64_t b = b0 + tid;
+      const uint64_t v = b < nblk ? blk[b * C + c] : 0;
+      uint64_t x = v;
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint64_t y = shfl_up_u64(x, o);
+        if (lane >= o) x += y;
+      }
+      if (lane == 63) part[wave] = x;
+      __syncthreads();
+      uint64_t before = carry;
+      for (int w = 0; w < wave; ++w) before += part[w];
+      if (b < nblk) blk[b * C + c] = before + x - v;
+      const uint64_t tot = part[0] + part[1] + part[2] + part[3];
+      __syncthreads();
+      carry += tot;
+    }
+    if (tid == 0) out[rows * C + c] = carry;
+  }
+}
+
+__global__ __launch_bounds__(256) void scan_final_kernel(const uint64_t *in, int64_t rows, int C, const uint64_t *blk,
+                                                         uint64_t *out) {
+  __shared__ uint64_t part[4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t r0 = (int64_t)blockIdx.x * kScanRows + tid * 4;
+  for (int c = 0; c < C; ++c) {
+    uint64_t v[4], s = 0;
+    for (int k = 0; k < 4; ++k) {
+      v[k] = r0 + k < rows ? in[(r0 + k) * C + c] : 0;
+      s += v[k];
+    }
+    uint64_t x = s;
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint64_t y = shfl_up_u64(x, o);
+      if (lane >= o) x += y;
+    }
+    if (lane == 63) part[wave] = x;
+    __syncthreads();
+    uint64_t run = blk[blockIdx.x * C + c] + x - s;
+    for (int w = 0; w < wave; ++w) run += part[w];
+    for (int k = 0; k < 4; ++k) {
+      if (r0 + k < rows) out[(r0 + k) * C + c] = run;
+      run += v[k];
+    }
+    __syncthreads();
+  }
+}
+
+// ---- range minima of lcp over [0, D] (lcp[D] = 0 is the sentinel) --------------------
+__global__ void sparse_level_kernel(uint32_t *sp, int64_t n, int k) {
+  // level k from level k-1 (k >= 1): minimum of lcp over [x, min(n, x + 2^k))
+  const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (x >= n) return;
+  const uint32_t *prev = sp + (int64_t)(k - 1) * n;
+  const int64_t h = (int64_t)1 << (k - 1);
+  uint32_t v = prev[x];
+  if (x + h < n) v = min(v, prev[x + h]);
+  sp[(int64_t)k * n + x] = v;
+}
+
+// first j >= s with lcp[j] < t (exists: lcp[D] = 0 < t for t >= 1)
+__device__ inline int64_t next_smaller(const CanonArgs &a, int64_t n, int64_t s, uint32_t t) {
+  int64_t j = s;
+  for (int k = a.levels - 1; k >= 0; --k) {
+    const int64_t w = (int64_t)1 << k;
+    if (j + w <= n && a.sparse[(int64_t)k * n + j] >= t) j += w;
+  }
+  return j;
+}
+// largest j <= s with lcp[j] < t (exists: lcp[0] = 0 < t for t >= 1)
+__device__ inline int64_t prev_smaller(const CanonArgs &a, int64_t n, int64_t s, uint32_t t) {
+  int64_t j = s;
+  for (int k = a.levels - 1; k >= 0; --k) {
+    const int64_t w = (int64_t)1 << k;
+    if (j - w + 1 >= 0 && a.sparse[(int64_t)k * n + (j - w + 1)] >= t) j -= w;
+  }
+  return j;
+}
+
+__device__ inline uint64_t node_base(const CanonArgs &a, int64_t i) { return 1 + a.scan_out[i * (1 + a.m)]; }
+
+// chain parent of each path and the node -> path map
+__global__ void chain_kernel(CanonArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= a.d) return;
+  const int64_t n = a.d + 1;
+  const uint32_t L = a.lcp[i];
+  uint32_t par = 0;
+  if (L > 0) {
+    const int64_t c = prev_smaller(a, n, i - 1, L);
+    par = (uint32_t)(node_base(a, c) + L - a.lcp[c] - 1);
+  }
+  a.chain_parent[i] = par;
+  const uint64_t b = node_base(a, i);
+  const uint32_t cnt = a.plen[a.order[i]] - L;
+  for (uint32_t k = 0; k < cnt; ++k) a.node_path[b + k] = (uint32_t)i;
+}
+
+__global__ __launch_bounds__(256) void emit_kernel(CanonArgs a) {
+  const int C = 1 + a.m, m = a.m;
+  const int64_t n = a.d + 1;
+  const int64_t U = (int64_t)(1 + a.scan_out[a.d * C]);
+  if (blockIdx.x == 0 && threadIdx.x == 0) a.u_out[0] = (unsigned long long)U;
+  for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < U; u += (int64_t)gridDim.x * blockDim.x) {
+    if (u == 0) {
+      a.parent[0] = kInf;
+      a.frame[0] = 0;
+      a.depth[0] = 0;
+      const bool empty_path = a.d > 0 && a.plen[a.order[0]] == 0;
+      for (int j = 0; j < m; ++j) {
+        a.excl[j] = empty_path ? a.psums[(int64_t)a.order[0] * m + j] : 0;
+        a.incl[j] = a.scan_out[a.d * C + 1 + j];
+      }
+      continue;
+    }
+    const int64_t i = a.node_path[u];
+    const uint32_t pid = a.order[i];
+    const uint32_t L = a.lcp[i], len = a.plen[pid];
+    const uint64_t b = node_base(a, i);
+    const uint32_t l = L + 1 + (uint32_t)(u - b);
+    a.parent[u] = u == (int64_t)b ? a.chain_parent[i] : (uint32_t)(u - 1);
+    a.frame[u] = a.pframes[a.pstart[pid] + l - 1];
+    a.depth[u] = l;
+    const int64_t e = (i + 1 == a.d || l > a.lcp[i + 1]) ? i + 1 : next_smaller(a, n, i + 2, l);
+    const uint64_t *si = a.scan_out + i * C, *se = a.scan_out + e * C;
+    for (int j = 0; j < m; ++j) {
+      a.excl[u * m + j] = l == len ? a.psums[(int64_t)pid * m + j] : 0;
+      a.incl[u * m + j] = se[1 + j] - si[1 + j];
+    }
+  }
+}
+
+inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
+
+}  // namespace
+
+void launch_sort(CanonArgs &a, hipStream_t s) {
+  if (a.d <= 0) return;
+  uint32_t *src = a.order, *dst = a.order_tmp;
+  hipLaunchKernelGGL(sort_block_kernel, dim3(blocks_for(a.d, kSortBlock)), dim3(512), 0, s, a, src);
+  for (int64_t run = kSortBlock; run < a.d; run *= 2) {
+    hipLaunchKernelGGL(merge_pass_kernel, dim3(blocks_for((a.d + kMergeItems - 1) / kMergeItems, 256)), dim3(256),
+                       0, s, a, src, dst, run);
+    uint32_t *t = src; src = dst; dst = t;
+  }
+  a.order = src;
+  a.order_tmp = dst;
+}
+
+void launch_canon(const CanonArgs &a, hipStream_t s) {
+  const int C = 1 + a.m;
+  const int64_t n = a.d + 1;
+  hipLaunchKernelGGL(lcp_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, a);
+  if (a.d > 0) {
+    const int64_t nblk = (a.d + kScanRows - 1) / kScanRows;
+    hipLaunchKernelGGL(scan_reduce_kernel, dim3((unsigned)nblk), dim3(256), 0, s, a.scan_in, a.d, C, a.scan_blk);
+    hipLaunchKernelGGL(scan_blocks_kernel, dim3(1), dim3(256), 0, s, a.scan_blk, nblk, C, a.scan_out, a.d);
+    hipLaunchKernelGGL(scan_final_kernel, dim3((unsigned)nblk), dim3(256), 0, s, a.scan_in, a.d, C, a.scan_blk,
+                       a.scan_out);
+  } else {
+    (void)hipMemsetAsync(a.scan_out, 0, sizeof(uint64_t) * C, s);
+  }
+  // level 0 of the range-minimum table is lcp itself
+  (void)hipMemcpyAsync(a.sparse, a.lcp, sizeof(uint32_t) * n, hipMemcpyDeviceToDevice, s);
+  for (int k = 1; k < a.levels; ++k)
+    hipLaunchKernelGGL(sparse_level_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, a.sparse, n, k);
+  if (a.d > 0) hipLaunchKernelGGL(chain_kernel, dim3(blocks_for(a.d, 256)), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(emit_kernel, dim3(a.grid_nodes), dim3(256), 0, s, a);
+}
+
+}  // namespace cct

@@ -1,0 +1,170 @@
+// Internal definitions shared by the HIP kernels and the host runtime of libcct.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cct {
+
+// ---- unique-path table -------------------------------------------------------
+// One 64-bit word per slot: (tag << 32) | ref.  ref is a path id of the tree's path
+// store, or kEventRef | event index for a path first seen in the current call.
+constexpr uint64_t kEmptySlot = ~0ull;
+constexpr uint32_t kEventRef = 0x80000000u;
+constexpr uint32_t kRefMask = 0x7FFFFFFFu;
+
+// ---- ingest tiling -------------------------------------------------------------
+constexpr int kIngestThreads = 256;     // 4 waves of 64
+constexpr int kTileEvents = 256;        // max events per tile
+constexpr int kTileFrames = 6144;       // LDS staging capacity (frames) of one tile
+constexpr int kMapWords = 2048;         // LDS aggregation map: uint64 sums
+constexpr int kMapKeys = 2048;          // LDS aggregation map: slot keys (>= entries)
+
+// ---- counters written by the ingest kernel --------------------------------------
+enum Counter { kCtrNew = 0, kCtrNewFrames = 1, kCtrError = 2, kCtrOverflow = 3, kCtrCount = 8 };
+enum ErrorBits { kErrOffsets = 1 };
+
+// ---- path hashing ----------------------------------------------------------------
+// A path's hash is a sum over its frames of a position-dependent term, so partial
+// sums over any split of the path combine by addition; a murmur3-style finalizer
+// mixes in the length.  Correctness never depends on the hash: every match is
+// verified frame by frame.
+__host__ __device__ inline uint64_t frame_term(uint32_t f, uint32_t k) {
+  uint32_t x = f + k * 0x9E3779B9u;
+  uint32_t y = (f ^ 0x5BD1E995u) + k * 0x85EBCA6Bu;
+  return (uint64_t)x * (uint64_t)(y | 1u);
+}
+__host__ __device__ inline uint64_t finish_hash(uint64_t s, uint64_t len) {
+  uint64_t h = s + len * 0x9E3779B97F4A7C15ull;
+  h ^= h >> 33;
+  h *= 0xFF51AFD7ED558CCDull;
+  h ^= h >> 33;
+  h *= 0xC4CEB9FE1A85EC53ull;
+  h ^= h >> 33;
+  return h;
+}
+
+__device__ inline uint32_t hash32(uint32_t x) {
+  x ^= x >> 16;
+  x *= 0x7FEB352Du;
+  x ^= x >> 15;
+  x *= 0x846CA68Bu;
+  x ^= x >> 16;
+  return x;
+}
+
+// ---- arguments -----------------------------------------------------------------------
+struct IngestArgs {
+  // input batch
+  const int64_t *off;
+  const uint32_t *fr;
+  const uint64_t *w;
+  int64_t n_events, n_frames;
+  int32_t m;
+  int32_t tile_events;  // events per tile
+  int64_t n_tiles;
+  // unique-path table
+  uint64_t *slot;
+  uint64_t cap_mask;
+  uint64_t hash_mask;   // all ones, except under a forced-collision test setting
+  uint64_t *delta;      // [cap][m] per-call sums
+  uint32_t *new_slots;  // slots claimed in this call, [max_new]
+  uint64_t max_new;
+  // the tree's path store (for paths seen in earlier calls)
+  const uint32_t *pframes;
+  const int64_t *pstart;
+  const uint32_t *plen;
+  // counters [kCtrCount]
+  unsigned long long *ctr;
+};
+
+// Host-side launch wrappers (one translation unit per kernel family).
+void launch_ingest(const IngestArgs &a, int grid, hipStream_t s);
+
+// Path store: path d occupies frames [pstart[d], pstart[d] + round16(plen[d])) of
+// pframes (pstart is a multiple of kStoreAlign, the tail is zero-filled), and its
+// checkpoint hashes cp[pstart[d] / kStoreAlign + b] = hash of its prefix of length
+// kStoreAlign * (b + 1), for every full block b.
+constexpr int kStoreAlign = 16;
+__host__ __device__ inline int64_t round_store(int64_t len) {
+  return (len + kStoreAlign - 1) / kStoreAlign * kStoreAlign;
+}
+
+struct PublishArgs {
+  const int64_t *off;        // batch offsets (frames of new paths come from the batch)
+  const uint32_t *fr;
+  uint64_t *slot;
+  const uint32_t *new_slots;
+  int64_t n_new;
+  int64_t d_old;
+  int32_t m;
+  const uint64_t *delta;     // [cap][m]
+  uint32_t *pframes;
+  uint64_t *pcp;             // checkpoint hashes
+  int64_t *pstart;
+  uint32_t *plen;
+  uint32_t *pslot;
+  uint64_t *psums;           // [D][m]
+  int64_t store_used;        // frames already used in the store
+  unsigned long long *cursor;  // frame cursor of this call (device, zeroed)
+};
+void launch_publish(const PublishArgs &a, hipStream_t s);
+void launch_fold_old(int64_t d_old, int32_t m, const uint32_t *pslot, const uint64_t *delta, uint64_t *psums,
+                     hipStream_t s);
+void launch_unclaim(uint64_t *slot, uint64_t cap, hipStream_t s);
+void launch_rehash(const uint32_t *pframes, const int64_t *pstart, const uint32_t *plen, int64_t d,
+                   uint64_t *slot, uint64_t cap_mask, uint64_t hash_mask, uint32_t *pslot, hipStream_t s);
+
+struct CanonArgs {
+  int64_t d;             // number of distinct full paths
+  int32_t m;
+  int32_t exact;         // 1: compare frames only (no checkpoint-hash shortcut)
+  const uint32_t *pframes;
+  const uint64_t *pcp;
+  const int64_t *pstart;
+  const uint32_t *plen;
+  const uint64_t *psums; // [D][m]
+  // outputs / scratch
+  uint32_t *order;       // [D] path ids in lexicographic order
+  uint32_t *order_tmp;   // [D]
+  uint32_t *lcp;         // [D+1] lcp with the previous path in order; lcp[D] = 0
+  uint64_t *scan_in;     // [D][1+m] new-node counts and sums in order
+  uint64_t *scan_out;    // [D+1][1+m] exclusive prefix sums (+ totals at row D)
+  uint64_t *scan_blk;    // block partials
+  int64_t scan_blocks;
+  uint32_t *sparse;      // [levels][D] range minima of lcp
+  int32_t levels;
+  uint32_t *chain_parent; // [D]
+  uint32_t *node_path;   // [U_max] path index (in order) of each node
+  int64_t u_max;
+  // node arrays
+  uint32_t *parent, *frame, *depth;
+  uint64_t *excl, *incl;
+  unsigned long long *u_out;  // device: [0] node count, [1] order-violation flag
+  int grid_nodes;
+};
+void launch_sort(CanonArgs &a, hipStream_t s);        // leaves the result in a.order
+void launch_canon(const CanonArgs &a, hipStream_t s);  // lcp, scans, sparse table, emission
+
+struct QueryArgs {
+  int64_t q;
+  int64_t qn_frames;
+  const int64_t *qoff;
+  const uint32_t *qfr;
+  int64_t d;
+  int64_t u;                 // node count (ids are < u)
+  int32_t m;
+  const uint32_t *pframes;
+  const int64_t *pstart;
+  const uint32_t *plen;
+  const uint32_t *order;
+  const uint32_t *lcp;       // [D+1]
+  const uint64_t *scan_out;  // column 0 holds the node-id bases
+  const uint64_t *excl, *incl;
+  int64_t *node_ids;
+  uint64_t *qexcl, *qincl;
+  unsigned long long *err;
+};
+void launch_query(const QueryArgs &a, hipStream_t s);
+
+}  // namespace cct

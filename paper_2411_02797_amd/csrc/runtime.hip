@@ -1,0 +1,580 @@
+// Host runtime of libcct: argument checks, the tree handle, a caching device-memory
+// pool, and the orchestration of ingest -> publish -> canonical ordering -> emission
+// on the caller's stream.  See include/cct.h for the contract.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <unordered_map>
+#include <vector>
+
+#include "../../include/cct.h"
+#include "common.h"
+
+using namespace cct;
+
+namespace {
+
+thread_local std::string g_error;
+thread_local double g_timings[5] = {0, 0, 0, 0, 0};
+thread_local int g_alloc_countdown = 0;  // test hook: >0 makes the n-th allocation of a call fail
+
+cct_status fail(cct_status s, const char *msg) {
+  g_error = msg;
+  return s;
+}
+
+// ---- caching device-memory pool --------------------------------------------------
+struct Pool {
+  std::mutex mu;
+  std::multimap<std::pair<int, size_t>, void *> cache;  // (device, bytes) -> block
+  std::unordered_map<void *, std::pair<int, size_t>> live;
+};
+Pool &pool() {
+  static Pool *p = new Pool;  // never destroyed: blocks may outlive static destructors
+  return *p;
+}
+
+size_t round_bytes(size_t b) {
+  if (b < 256) return 256;
+  if (b < (1u << 20)) return (b + 255) & ~(size_t)255;
+  return (b + (1u << 20) - 1) & ~(size_t)((1u << 20) - 1);
+}
+
+void *pool_alloc(size_t bytes) {
+  if (g_alloc_countdown > 0 && --g_alloc_countdown == 0) return nullptr;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return nullptr;
+  const size_t want = round_bytes(bytes);
+  Pool &P = pool();
+  {
+    std::lock_guard<std::mutex> lk(P.mu);
+    auto it = P.cache.lower_bound({dev, want});
+    if (it != P.cache.end() && it->first.first == dev && it->first.second <= 2 * want) {
+      void *p = it->second;
+      P.live[p] = it->first;
+      P.cache.erase(it);
+      return p;
+    }
+  }
+  void *p = nullptr;
+  if (hipMalloc(&p, want) != hipSuccess) {
+    (void)hipGetLastError();
+    cct_release_cached_memory();
+    if (hipMalloc(&p, want) != hipSuccess) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+  }
+  std::lock_guard<std::mutex> lk(P.mu);
+  P.live[p] = {dev, want};
+  return p;
+}
+
+void pool_free(void *p) {
+  if (!p) return;
+  Pool &P = pool();
+  std::lock_guard<std::mutex> lk(P.mu);
+  auto it = P.live.find(p);
+  if (it == P.live.end()) return;
+  P.cache.emplace(it->second, p);
+  P.live.erase(it);
+}
+
+// An owned device buffer from the pool.
+struct Buf {
+  void *p = nullptr;
+  size_t bytes = 0;
+  Buf() = default;
+  Buf(const Buf &) = delete;
+  Buf &operator=(const Buf &) = delete;
+  Buf(Buf &&o) noexcept : p(o.p), bytes(o.bytes) { o.p = nullptr; o.bytes = 0; }
+  Buf &operator=(Buf &&o) noexcept {
+    if (this != &o) { release(); p = o.p; bytes = o.bytes; o.p = nullptr; o.bytes = 0; }
+    return *this;
+  }
+  ~Buf() { release(); }
+  bool alloc(size_t n) {
+    release();
+    p = pool_alloc(n ? n : 1);
+    bytes = p ? n : 0;
+    return p != nullptr;
+  }
+  void release() { pool_free(p); p = nullptr; bytes = 0; }
+  template <class T> T *as() const { return static_cast<T *>(p); }
+};
+
+int cu_count() {
+  static int cached[64] = {0};
+  int dev = 0;
+  (void)hipGetDevice(&dev);
+  if (dev < 0 || dev >= 64) return 256;
+  if (!cached[dev]) {
+    hipDeviceProp_t prop;
+    cached[dev] = hipGetDeviceProperties(&prop, dev) == hipSuccess ? prop.multiProcessorCount : 256;
+  }
+  return cached[dev];
+}
+
+// pinned host staging for small device -> host reads
+unsigned long long *host_scratch() {
+  thread_local unsigned long long *h = nullptr;
+  if (!h && hipHostMalloc((void **)&h, 64 * sizeof(unsigned long long), hipHostMallocDefault) != hipSuccess) {
+    (void)hipGetLastError();
+    h = nullptr;
+  }
+  return h;
+}
+
+int64_t env_int(const char *name, int64_t dflt) {
+  const char *v = std::getenv(name);
+  if (!v || !*v) return dflt;
+  return std::strtoll(v, nullptr, 10);
+}
+
+uint64_t pow2_at_least(uint64_t x) {
+  uint64_t p = 1;
+  while (p < x) p <<= 1;
+  return p;
+}
+
+int floor_log2(uint64_t x) {
+  int l = 0;
+  while ((x >> 1) >= 1 && x > 1) { x >>= 1; ++l; }
+  return l;
+}
+
+}  // namespace
+
+// ---- the tree ------------------------------------------------------------------------
+struct cct_tree {
+  int device = 0;
+  int32_t m = 1;
+  // unique-path table (slot words); sums live per path in psums
+  uint64_t cap = 0;
+  Buf slot;
+  // path store
+  int64_t d = 0, dcap = 0;
+  int64_t store_used = 0, store_cap = 0, sum_len = 0;
+  Buf pframes, pcp, pstart, plen, pslot, psums;
+  // canonical arrays
+  int64_t u = 0;
+  Buf parent, frame, depth, excl, incl;
+  // canonical metadata kept for queries
+  Buf order, lcp, scan_out;
+};
+
+namespace {
+
+#define HIP_TRY(x)                                              \
+  do {                                                          \
+    hipError_t e_ = (x);                                        \
+    if (e_ != hipSuccess) {                                     \
+      (void)hipGetLastError();                                  \
+      return fail(CCT_EDEVICE, hipGetErrorString(e_));          \
+    }                                                           \
+  } while (0)
+
+cct_status check_paths(const cct_paths *p, bool need_metrics) {
+  if (!p) return fail(CCT_EINVAL, "paths is NULL");
+  if (p->n_events < 0 || p->n_frames < 0) return fail(CCT_EINVAL, "negative size");
+  if (p->n_events > CCT_MAX_EVENTS) return fail(CCT_EOVERFLOW, "too many events in one call");
+  if (p->n_metrics < 1 || p->n_metrics > CCT_MAX_METRICS) return fail(CCT_EINVAL, "n_metrics out of range");
+  if (!p->offsets) return fail(CCT_EINVAL, "offsets is NULL");
+  if (p->n_frames > 0 && !p->frames) return fail(CCT_EINVAL, "frames is NULL");
+  if (need_metrics && p->n_events > 0 && !p->metrics) return fail(CCT_EINVAL, "metrics is NULL");
+  if (((uintptr_t)p->offsets & 7) || ((uintptr_t)p->frames & 3) || ((uintptr_t)p->metrics & 7))
+    return fail(CCT_EINVAL, "misaligned pointer");
+  return CCT_OK;
+}
+
+// Grow a device array to hold `need` bytes, keeping the first `keep` bytes.
+cct_status grow(Buf &b, size_t need, size_t keep, hipStream_t s) {
+  if (b.p && b.bytes >= need) return CCT_OK;
+  Buf nb;
+  if (!nb.alloc(need)) return fail(CCT_ENOMEM, "device allocation failed");
+  if (keep) HIP_TRY(hipMemcpyAsync(nb.p, b.p, keep, hipMemcpyDeviceToDevice, s));
+  b = std::move(nb);
+  return CCT_OK;
+}
+
+// HIP events on the call's stream: 0 call start, 1/2 around the ingest kernel, 3 after
+// publish, 4 after the sort, 5 after node emission.
+struct Timer {
+  hipEvent_t ev[6] = {nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
+  bool ok = true;
+  Timer() {
+    for (auto &e : ev)
+      if (hipEventCreate(&e) != hipSuccess) { ok = false; (void)hipGetLastError(); }
+  }
+  ~Timer() {
+    for (auto &e : ev)
+      if (e) (void)hipEventDestroy(e);
+  }
+  void mark(int i, hipStream_t s) {
+    if (ok) (void)hipEventRecord(ev[i], s);
+  }
+  float span(int a, int b) {
+    float ms = 0;
+    if (hipEventElapsedTime(&ms, ev[a], ev[b]) != hipSuccess) { (void)hipGetLastError(); return 0; }
+    return ms;
+  }
+  // timings: ingest kernel, publish, sort, emission, whole call
+  void collect(bool ingested) {
+    for (int i = 0; i < 5; ++i) g_timings[i] = 0;
+    if (!ok) return;
+    if (ingested) g_timings[0] = span(1, 2);
+    g_timings[1] = span(2, 3);
+    g_timings[2] = span(3, 4);
+    g_timings[3] = span(4, 5);
+    g_timings[4] = span(0, 5);
+  }
+};
+
+// Re-insert the tree's stored paths into a fresh table of capacity `cap`.
+cct_status rehash(cct_tree *t, uint64_t cap, uint64_t hash_mask, hipStream_t s) {
+  Buf ns;
+  if (!ns.alloc(cap * 8)) return fail(CCT_ENOMEM, "device allocation failed");
+  HIP_TRY(hipMemsetAsync(ns.p, 0xFF, cap * 8, s));
+  Buf np;
+  if (t->d > 0) {
+    if (!np.alloc(t->dcap * 4)) return fail(CCT_ENOMEM, "device allocation failed");
+    launch_rehash(t->pframes.as<uint32_t>(), t->pstart.as<int64_t>(), t->plen.as<uint32_t>(), t->d,
+                  ns.as<uint64_t>(), cap - 1, hash_mask, np.as<uint32_t>(), s);
+    HIP_TRY(hipGetLastError());
+    t->pslot = std::move(np);
+  }
+  t->slot = std::move(ns);
+  t->cap = cap;
+  return CCT_OK;
+}
+
+// Aggregate one batch into `t` (fresh or existing).  Strong guarantee: on error the
+// tree's table, path store, sums and node arrays are as before.
+cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
+  const int32_t m = t->m;
+  const int64_t N = p->n_events;
+  g_alloc_countdown = (int)env_int("CCT_TEST_FAIL_ALLOC", 0);
+  const int hash_bits = (int)env_int("CCT_TEST_HASH_BITS", 64);
+  const uint64_t hash_mask = hash_bits >= 64 ? ~0ull : ((1ull << (hash_bits < 0 ? 0 : hash_bits)) - 1);
+  unsigned long long *hs = host_scratch();
+  if (!hs) return fail(CCT_ENOMEM, "pinned host allocation failed");
+  Timer tm;
+  tm.mark(0, s);
+
+  Buf ctr;
+  if (!ctr.alloc(kCtrCount * 8 + 64)) return fail(CCT_ENOMEM, "device allocation failed");
+  unsigned long long *dctr = ctr.as<unsigned long long>();
+
+  if (N == 0) {
+    // nothing to insert; offsets[0] must still be 0 and n_frames 0
+    if (p->n_frames != 0) return fail(CCT_EINVAL, "n_frames != offsets[N]");
+    HIP_TRY(hipMemcpyAsync(hs, p->offsets, 8, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    if (hs[0] != 0) return fail(CCT_EINVAL, "offsets[0] != 0");
+    if (t->parent.p) return CCT_OK;
+    tm.mark(1, s);
+    tm.mark(2, s);
+  }
+
+  // ---- A1-A3: ingest (retry with a larger table on overflow) -------------------------
+  Buf delta, new_slots;
+  uint64_t n_new = 0, new_frames = 0;
+  if (N > 0) {
+    for (int attempt = 0;; ++attempt) {
+      if (attempt > 12) return fail(CCT_EOVERFLOW, "unique-path table cannot grow further");
+      const uint64_t max_new = t->cap / 2 > (uint64_t)t->d ? t->cap / 2 - (uint64_t)t->d : 0;
+      if (max_new == 0) {
+        cct_status st = rehash(t, t->cap * 4, hash_mask, s);
+        if (st) return st;
+        continue;
+      }
+      if (!delta.alloc(t->cap * m * 8) || !new_slots.alloc(max_new * 4))
+        return fail(CCT_ENOMEM, "device allocation failed");
+      HIP_TRY(hipMemsetAsync(delta.p, 0, t->cap * m * 8, s));
+      HIP_TRY(hipMemsetAsync(dctr, 0, kCtrCount * 8, s));
+      IngestArgs a{};
+      a.off = p->offsets; a.fr = p->frames; a.w = p->metrics;
+      a.n_events = N; a.n_frames = p->n_frames; a.m = m;
+      const double mean = std::max(1.0, (double)p->n_frames / (double)N);
+      a.tile_events = (int32_t)std::max(1.0, std::min((double)kTileEvents, 0.75 * kTileFrames / mean));
+      a.n_tiles = (N + a.tile_events - 1) / a.tile_events;
+      a.slot = t->slot.as<uint64_t>(); a.cap_mask = t->cap - 1; a.hash_mask = hash_mask;
+      a.delta = delta.as<uint64_t>(); a.new_slots = new_slots.as<uint32_t>(); a.max_new = max_new;
+      a.pframes = t->pframes.as<uint32_t>(); a.pstart = t->pstart.as<int64_t>(); a.plen = t->plen.as<uint32_t>();
+      a.ctr = dctr;
+      const int grid = (int)std::min<int64_t>(a.n_tiles, (int64_t)cu_count() * 2);
+      tm.mark(1, s);
+      launch_ingest(a, grid, s);
+      tm.mark(2, s);
+      HIP_TRY(hipGetLastError());
+      HIP_TRY(hipMemcpyAsync(hs, dctr, kCtrCount * 8, hipMemcpyDeviceToHost, s));
+      HIP_TRY(hipStreamSynchronize(s));
+      if (hs[kCtrError] || hs[kCtrOverflow]) {
+        launch_unclaim(t->slot.as<uint64_t>(), t->cap, s);
+        HIP_TRY(hipGetLastError());
+        if (hs[kCtrError]) {
+          HIP_TRY(hipStreamSynchronize(s));
+          return fail(CCT_EINVAL, "malformed offsets");
+        }
+        cct_status st = rehash(t, t->cap * 4, hash_mask, s);
+        if (st) return st;
+        continue;
+      }
+      n_new = hs[kCtrNew];
+      new_frames = hs[kCtrNewFrames];
+      break;
+    }
+  }
+
+  // ---- allocate everything the rest of the call needs (rollback possible until here)
+  const int64_t D = t->d + (int64_t)n_new;
+  const int64_t sum_len = t->sum_len + (int64_t)new_frames;
+  auto rollback = [&](cct_status st) {
+    if (n_new) launch_unclaim(t->slot.as<uint64_t>(), t->cap, s);
+    (void)hipStreamSynchronize(s);
+    return st;
+  };
+  if (sum_len + 1 > (int64_t)0xFFFFFFFE) return rollback(fail(CCT_EOVERFLOW, "tree would exceed 2^32-2 nodes"));
+  const int64_t store_need = t->store_used + (int64_t)new_frames + (int64_t)(kStoreAlign - 1) * (int64_t)n_new;
+  const int64_t dneed = std::max<int64_t>(D, 1);
+  cct_tree old_arrays_holder;  // receives replaced buffers, released on return
+  {
+    cct_status st = CCT_OK;
+    if (store_need > t->store_cap || !t->pframes.p) {
+      const int64_t ncap = std::max<int64_t>(store_need + store_need / 2, 1024);
+      Buf f2, c2;
+      if (!f2.alloc(ncap * 4) || !c2.alloc((ncap / kStoreAlign + 1) * 8)) return rollback(fail(CCT_ENOMEM, "device allocation failed"));
+      if (t->store_used) {
+        if (hipMemcpyAsync(f2.p, t->pframes.p, t->store_used * 4, hipMemcpyDeviceToDevice, s) != hipSuccess ||
+            hipMemcpyAsync(c2.p, t->pcp.p, (t->store_used / kStoreAlign) * 8, hipMemcpyDeviceToDevice, s) != hipSuccess)
+          return rollback(fail(CCT_EDEVICE, "copy failed"));
+      }
+      old_arrays_holder.pframes = std::move(t->pframes);
+      old_arrays_holder.pcp = std::move(t->pcp);
+      t->pframes = std::move(f2);
+      t->pcp = std::move(c2);
+      t->store_cap = ncap;
+    }
+    if (dneed > t->dcap || !t->pstart.p) {
+      const int64_t ncap = std::max<int64_t>(dneed + dneed / 2, 256);
+      Buf a1, a2, a3, a4;
+      if (!a1.alloc(ncap * 8) || !a2.alloc(ncap * 4) || !a3.alloc(ncap * 4) || !a4.alloc(ncap * m * 8))
+        return rollback(fail(CCT_ENOMEM, "device allocation failed"));
+      if (t->d) {
+        if (hipMemcpyAsync(a1.p, t->pstart.p, t->d * 8, hipMemcpyDeviceToDevice, s) != hipSuccess ||
+            hipMemcpyAsync(a2.p, t->plen.p, t->d * 4, hipMemcpyDeviceToDevice, s) != hipSuccess ||
+            hipMemcpyAsync(a3.p, t->pslot.p, t->d * 4, hipMemcpyDeviceToDevice, s) != hipSuccess ||
+            hipMemcpyAsync(a4.p, t->psums.p, t->d * m * 8, hipMemcpyDeviceToDevice, s) != hipSuccess)
+          return rollback(fail(CCT_EDEVICE, "copy failed"));
+      }
+      old_arrays_holder.pstart = std::move(t->pstart);
+      old_arrays_holder.plen = std::move(t->plen);
+      old_arrays_holder.pslot = std::move(t->pslot);
+      old_arrays_holder.psums = std::move(t->psums);
+      t->pstart = std::move(a1); t->plen = std::move(a2); t->pslot = std::move(a3); t->psums = std::move(a4);
+      t->dcap = ncap;
+    }
+    (void)st;
+  }
+  const int C = 1 + m;
+  const int64_t n1 = D + 1;
+  const int levels = floor_log2((uint64_t)n1) + 1;
+  const int64_t nblk = (D + 1023) / 1024 + 1;
+  const int64_t u_max = sum_len + 1;
+  Buf order, order_tmp, lcp, scan_in, scan_out, scan_blk, sparse, chain, node_path, cursor;
+  Buf n_parent, n_frame, n_depth, n_excl, n_incl;
+  if (!order.alloc(dneed * 4) || !order_tmp.alloc(dneed * 4) || !lcp.alloc(n1 * 4) || !scan_in.alloc(dneed * C * 8) ||
+      !scan_out.alloc(n1 * C * 8) || !scan_blk.alloc(nblk * C * 8) || !sparse.alloc((int64_t)levels * n1 * 4) ||
+      !chain.alloc(dneed * 4) || !node_path.alloc(u_max * 4) || !cursor.alloc(64) || !n_parent.alloc(u_max * 4) ||
+      !n_frame.alloc(u_max * 4) || !n_depth.alloc(u_max * 4) || !n_excl.alloc(u_max * m * 8) ||
+      !n_incl.alloc(u_max * m * 8))
+    return rollback(fail(CCT_ENOMEM, "device allocation failed"));
+
+  // ---- publish new paths, fold this call's sums into the old ones -----------------------
+  HIP_TRY(hipMemsetAsync(cursor.p, 0, 64, s));
+  if (n_new) {
+    PublishArgs pa{};
+    pa.off = p->offsets; pa.fr = p->frames; pa.slot = t->slot.as<uint64_t>();
+    pa.new_slots = new_slots.as<uint32_t>(); pa.n_new = (int64_t)n_new; pa.d_old = t->d; pa.m = m;
+    pa.delta = delta.as<uint64_t>(); pa.pframes = t->pframes.as<uint32_t>(); pa.pcp = t->pcp.as<uint64_t>();
+    pa.pstart = t->pstart.as<int64_t>(); pa.plen = t->plen.as<uint32_t>(); pa.pslot = t->pslot.as<uint32_t>();
+    pa.psums = t->psums.as<uint64_t>(); pa.store_used = t->store_used; pa.cursor = cursor.as<unsigned long long>();
+    launch_publish(pa, s);
+  }
+  if (N > 0) launch_fold_old(t->d, m, t->pslot.as<uint32_t>(), delta.as<uint64_t>(), t->psums.as<uint64_t>(), s);
+  HIP_TRY(hipGetLastError());
+  tm.mark(3, s);
+
+  // ---- A5-A9: canonical order and node arrays ------------------------------------------
+  CanonArgs ca{};
+  ca.d = D; ca.m = m; ca.exact = env_int("CCT_TEST_EXACT_SORT", 0) ? 1 : 0;
+  ca.pframes = t->pframes.as<uint32_t>(); ca.pcp = t->pcp.as<uint64_t>(); ca.pstart = t->pstart.as<int64_t>();
+  ca.plen = t->plen.as<uint32_t>(); ca.psums = t->psums.as<uint64_t>();
+  ca.order = order.as<uint32_t>(); ca.order_tmp = order_tmp.as<uint32_t>(); ca.lcp = lcp.as<uint32_t>();
+  ca.scan_in = scan_in.as<uint64_t>(); ca.scan_out = scan_out.as<uint64_t>(); ca.scan_blk = scan_blk.as<uint64_t>();
+  ca.scan_blocks = nblk; ca.sparse = sparse.as<uint32_t>(); ca.levels = levels;
+  ca.chain_parent = chain.as<uint32_t>(); ca.node_path = node_path.as<uint32_t>(); ca.u_max = u_max;
+  ca.parent = n_parent.as<uint32_t>(); ca.frame = n_frame.as<uint32_t>(); ca.depth = n_depth.as<uint32_t>();
+  ca.excl = n_excl.as<uint64_t>(); ca.incl = n_incl.as<uint64_t>();
+  ca.u_out = cursor.as<unsigned long long>() + 2;
+  ca.grid_nodes = (int)std::max<int64_t>(1, std::min<int64_t>((u_max + 255) / 256, (int64_t)cu_count() * 16));
+  for (int pass = 0; pass < 2; ++pass) {
+    CanonArgs run = ca;
+    launch_sort(run, s);
+    tm.mark(4, s);
+    launch_canon(run, s);
+    HIP_TRY(hipGetLastError());
+    tm.mark(5, s);
+    HIP_TRY(hipMemcpyAsync(hs, cursor.p, 64, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    if (!hs[3]) {  // order verified strictly increasing
+      if (run.order != ca.order) std::swap(order, order_tmp);
+      break;
+    }
+    if (pass == 1 || ca.exact) return fail(CCT_EDEVICE, "canonical order failed exact verification");
+    ca.exact = 1;  // a checkpoint-hash collision misled the sort: redo with exact compares
+    HIP_TRY(hipMemsetAsync(cursor.as<unsigned long long>() + 2, 0, 16, s));
+  }
+  tm.collect(N > 0);
+
+  // ---- commit -------------------------------------------------------------------------------
+  t->store_used += (int64_t)hs[0];
+  t->d = D;
+  t->sum_len = sum_len;
+  t->u = (int64_t)hs[2];
+  t->parent = std::move(n_parent); t->frame = std::move(n_frame); t->depth = std::move(n_depth);
+  t->excl = std::move(n_excl); t->incl = std::move(n_incl);
+  t->order = std::move(order); t->lcp = std::move(lcp); t->scan_out = std::move(scan_out);
+  return CCT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+cct_status cct_build(const cct_paths *events, void *hip_stream, cct_tree **out) {
+  g_error.clear();
+  if (!out) return fail(CCT_EINVAL, "out is NULL");
+  cct_status st = check_paths(events, true);
+  if (st) return st;
+  hipStream_t s = (hipStream_t)hip_stream;
+  cct_tree *t = new (std::nothrow) cct_tree;
+  if (!t) return fail(CCT_ENOMEM, "host allocation failed");
+  (void)hipGetDevice(&t->device);
+  t->m = events->n_metrics;
+  const int64_t N = events->n_events;
+  int64_t cap = env_int("CCT_TEST_TABLE_CAP", 0);
+  if (cap <= 0) cap = (int64_t)std::min<uint64_t>(pow2_at_least((uint64_t)std::max<int64_t>(2 * N, 1024)), 1ull << 21);
+  cap = (int64_t)pow2_at_least((uint64_t)std::max<int64_t>(cap, 16));
+  if (!t->slot.alloc(cap * 8)) { delete t; return fail(CCT_ENOMEM, "device allocation failed"); }
+  t->cap = (uint64_t)cap;
+  if (hipMemsetAsync(t->slot.p, 0xFF, cap * 8, s) != hipSuccess) {
+    (void)hipGetLastError();
+    delete t;
+    return fail(CCT_EDEVICE, "memset failed");
+  }
+  st = aggregate(t, events, s);
+  if (st) { delete t; return st; }
+  *out = t;
+  return CCT_OK;
+}
+
+cct_status cct_merge(cct_tree *tree, const cct_paths *chunk, void *hip_stream) {
+  g_error.clear();
+  if (!tree) return fail(CCT_EINVAL, "tree is NULL");
+  cct_status st = check_paths(chunk, true);
+  if (st) return st;
+  if (chunk->n_metrics != tree->m) return fail(CCT_EMISMATCH, "metric count differs from the tree's");
+  int dev = 0;
+  (void)hipGetDevice(&dev);
+  if (dev != tree->device) return fail(CCT_EINVAL, "tree belongs to another device");
+  return aggregate(tree, chunk, (hipStream_t)hip_stream);
+}
+
+cct_status cct_query(const cct_tree *tree, const cct_paths *q, void *hip_stream, int64_t *node_ids, uint64_t *excl,
+                     uint64_t *incl) {
+  g_error.clear();
+  if (!tree || !q) return fail(CCT_EINVAL, "NULL argument");
+  if (q->n_events < 0 || q->n_frames < 0 || !q->offsets || (q->n_frames > 0 && !q->frames))
+    return fail(CCT_EINVAL, "bad query batch");
+  if (q->n_events > CCT_MAX_EVENTS) return fail(CCT_EOVERFLOW, "too many queries in one call");
+  if (q->n_events > 0 && !node_ids) return fail(CCT_EINVAL, "node_ids is NULL");
+  if (q->n_events == 0) return CCT_OK;
+  hipStream_t s = (hipStream_t)hip_stream;
+  unsigned long long *hs = host_scratch();
+  if (!hs) return fail(CCT_ENOMEM, "pinned host allocation failed");
+  g_alloc_countdown = 0;
+  Buf err;
+  if (!err.alloc(8)) return fail(CCT_ENOMEM, "device allocation failed");
+  HIP_TRY(hipMemsetAsync(err.p, 0, 8, s));
+  QueryArgs a{};
+  a.q = q->n_events; a.qn_frames = q->n_frames; a.qoff = q->offsets; a.qfr = q->frames;
+  a.d = tree->d; a.u = tree->u; a.m = tree->m;
+  a.pframes = tree->pframes.as<uint32_t>(); a.pstart = tree->pstart.as<int64_t>(); a.plen = tree->plen.as<uint32_t>();
+  a.order = tree->order.as<uint32_t>(); a.lcp = tree->lcp.as<uint32_t>(); a.scan_out = tree->scan_out.as<uint64_t>();
+  a.excl = tree->excl.as<uint64_t>(); a.incl = tree->incl.as<uint64_t>();
+  a.node_ids = node_ids; a.qexcl = excl; a.qincl = incl; a.err = err.as<unsigned long long>();
+  launch_query(a, s);
+  HIP_TRY(hipGetLastError());
+  HIP_TRY(hipMemcpyAsync(hs, err.p, 8, hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  if (hs[0] & 2) return fail(CCT_EDEVICE, "query found an inconsistent tree");
+  if (hs[0]) return fail(CCT_EINVAL, "malformed query offsets");
+  return CCT_OK;
+}
+
+cct_status cct_info(const cct_tree *tree, int64_t *n_nodes, int32_t *n_metrics, int64_t *n_paths) {
+  if (!tree) return fail(CCT_EINVAL, "tree is NULL");
+  if (n_nodes) *n_nodes = tree->u;
+  if (n_metrics) *n_metrics = tree->m;
+  if (n_paths) *n_paths = tree->d;
+  return CCT_OK;
+}
+
+cct_status cct_export(const cct_tree *tree, void *hip_stream, uint32_t *parent, uint32_t *frame, uint32_t *depth,
+                      uint64_t *excl, uint64_t *incl) {
+  g_error.clear();
+  if (!tree) return fail(CCT_EINVAL, "tree is NULL");
+  hipStream_t s = (hipStream_t)hip_stream;
+  const size_t U = (size_t)tree->u, m = (size_t)tree->m;
+  if (parent) HIP_TRY(hipMemcpyAsync(parent, tree->parent.p, U * 4, hipMemcpyDefault, s));
+  if (frame) HIP_TRY(hipMemcpyAsync(frame, tree->frame.p, U * 4, hipMemcpyDefault, s));
+  if (depth) HIP_TRY(hipMemcpyAsync(depth, tree->depth.p, U * 4, hipMemcpyDefault, s));
+  if (excl) HIP_TRY(hipMemcpyAsync(excl, tree->excl.p, U * m * 8, hipMemcpyDefault, s));
+  if (incl) HIP_TRY(hipMemcpyAsync(incl, tree->incl.p, U * m * 8, hipMemcpyDefault, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  return CCT_OK;
+}
+
+void cct_free(cct_tree *tree) { delete tree; }
+
+void cct_release_cached_memory(void) {
+  Pool &P = pool();
+  std::lock_guard<std::mutex> lk(P.mu);
+  int cur = 0;
+  (void)hipGetDevice(&cur);
+  for (auto &kv : P.cache) {
+    (void)hipSetDevice(kv.first.first);
+    (void)hipFree(kv.second);
+  }
+  P.cache.clear();
+  (void)hipSetDevice(cur);
+  (void)hipGetLastError();
+}
+
+const char *cct_last_error(void) { return g_error.c_str(); }
+
+int cct_last_timings(double *ms, int n) {
+  if (!ms || n <= 0) return 0;
+  const int k = n < 5 ? n : 5;
+  for (int i = 0; i < k; ++i) ms[i] = g_timings[i];
+  return k;
+}
+
+}  // extern "C"

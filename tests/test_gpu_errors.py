@@ -1,0 +1,107 @@
+"""Error paths of the C ABI, forced from the host; every kernel still exits normally."""
+import numpy as np
+import pytest
+
+import oracle
+import tracegen
+from gpu_util import assert_same, gpu_tree, to_dev, torch_or_skip
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    torch_or_skip()
+
+
+def _status(fn):
+    import paper_2411_02797_amd as cct
+    with pytest.raises(cct.CctError) as ei:
+        fn()
+    return ei.value.name
+
+
+@pytest.mark.parametrize("kind", ["first_nonzero", "decreasing", "last_mismatch", "huge"])
+def test_malformed_offsets(kind):
+    import paper_2411_02797_amd as cct
+    torch = torch_or_skip()
+    o, f, w = tracegen.random_paths(5000, 30, 10, 1, seed=1)
+    to, tf, tw = to_dev(o, f, w)
+    bad = to.clone()
+    if kind == "first_nonzero":
+        bad[0] = 1
+    elif kind == "decreasing":
+        bad[2500] = bad[2499] - 1
+    elif kind == "last_mismatch":
+        bad[-1] = bad[-1] - 1
+    else:
+        bad[1000] = 2**40
+    assert _status(lambda: cct.build(bad, tf, tw)) == "CCT_EINVAL"
+
+
+def test_merge_failure_leaves_tree_unchanged():
+    import paper_2411_02797_amd as cct
+    o, f, w = tracegen.random_paths(4000, 60, 10, 2, seed=2)
+    tree = cct.build(*to_dev(o, f, w))
+    before = tree.to_numpy()
+    o2, f2, w2 = tracegen.random_paths(3000, 60, 10, 2, seed=3)
+    to2, tf2, tw2 = to_dev(o2, f2, w2)
+    bad = to2.clone()
+    bad[1500] = bad[1499] - 1
+    assert _status(lambda: tree.merge(bad, tf2, tw2)) == "CCT_EINVAL"
+    assert_same(tree.to_numpy(), before, "after failed merge")
+    _, _, tw3 = to_dev(o2, f2, np.zeros((3000, 3), np.uint64))
+    assert _status(lambda: tree.merge(to2, tf2, tw3)) == "CCT_EMISMATCH"
+    tree.merge(to2, tf2, tw2)  # still usable
+    orc = oracle.Oracle(2)
+    orc.ingest(o, f, w)
+    orc.ingest(o2, f2, w2)
+    assert_same(tree.to_numpy(), orc.tree(), "merge after failures")
+    tree.free()
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 5, 8, 12, 20])
+def test_allocation_failure(monkeypatch, k):
+    import paper_2411_02797_amd as cct
+    o, f, w = tracegen.random_paths(3000, 40, 10, 1, seed=k)
+    tree = cct.build(*to_dev(o, f, w))
+    before = tree.to_numpy()
+    o2, f2, w2 = tracegen.random_paths(2000, 80, 10, 1, seed=100 + k)
+    d2 = to_dev(o2, f2, w2)
+    monkeypatch.setenv("CCT_TEST_FAIL_ALLOC", str(k))
+    try:
+        tree.merge(*d2)
+        merged = True
+    except cct.CctError as e:
+        assert e.name == "CCT_ENOMEM"
+        merged = False
+    monkeypatch.delenv("CCT_TEST_FAIL_ALLOC")
+    if merged:
+        orc = oracle.Oracle(1)
+        orc.ingest(o, f, w)
+        orc.ingest(o2, f2, w2)
+        assert_same(tree.to_numpy(), orc.tree(), "merged")
+    else:
+        assert_same(tree.to_numpy(), before, "unchanged after ENOMEM")
+    tree.free()
+    monkeypatch.setenv("CCT_TEST_FAIL_ALLOC", str(k))
+    try:
+        t = gpu_tree(o, f, w)
+        assert_same(t, oracle.build_tree(o, f, w))
+    except cct.CctError as e:
+        assert e.name == "CCT_ENOMEM"
+
+
+def test_bad_tensor_arguments():
+    import paper_2411_02797_amd as cct
+    torch = torch_or_skip()
+    o, f, w = tracegen.random_paths(10, 5, 4, 1, seed=1)
+    to, tf, tw = to_dev(o, f, w)
+    with pytest.raises(ValueError):
+        cct.build(to.to(torch.int32), tf, tw)
+    with pytest.raises(ValueError):
+        cct.build(to, tf, tw[:5])
+    with pytest.raises(ValueError):
+        cct.build(to, tf, torch.zeros((10, 9), dtype=torch.int64, device=to.device)[:, ::2])
+    assert _status(lambda: cct.build(to, tf, torch.zeros((10, 9), dtype=torch.int64, device=to.device))) \
+        == "CCT_EINVAL"
