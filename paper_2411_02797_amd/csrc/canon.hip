@@ -341,19 +341,22 @@ void launch_sort(CanonArgs &a, hipStream_t s) {
   a.order_tmp = dst;
 }
 
+void launch_scan(const uint64_t *in, int64_t rows, int C, uint64_t *blk, uint64_t *out, hipStream_t s) {
+  if (rows > 0) {
+    const int64_t nblk = (rows + kScanRows - 1) / kScanRows;
+    hipLaunchKernelGGL(scan_reduce_kernel, dim3((unsigned)nblk), dim3(256), 0, s, in, rows, C, blk);
+    hipLaunchKernelGGL(scan_blocks_kernel, dim3(1), dim3(256), 0, s, blk, nblk, C, out, rows);
+    hipLaunchKernelGGL(scan_final_kernel, dim3((unsigned)nblk), dim3(256), 0, s, in, rows, C, blk, out);
+  } else {
+    (void)hipMemsetAsync(out, 0, sizeof(uint64_t) * C, s);
+  }
+}
+
 void launch_canon(const CanonArgs &a, hipStream_t s) {
   const int C = 1 + a.m;
   const int64_t n = a.d + 1;
   hipLaunchKernelGGL(lcp_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, a);
-  if (a.d > 0) {
-    const int64_t nblk = (a.d + kScanRows - 1) / kScanRows;
-    hipLaunchKernelGGL(scan_reduce_kernel, dim3((unsigned)nblk), dim3(256), 0, s, a.scan_in, a.d, C, a.scan_blk);
-    hipLaunchKernelGGL(scan_blocks_kernel, dim3(1), dim3(256), 0, s, a.scan_blk, nblk, C, a.scan_out, a.d);
-    hipLaunchKernelGGL(scan_final_kernel, dim3((unsigned)nblk), dim3(256), 0, s, a.scan_in, a.d, C, a.scan_blk,
-                       a.scan_out);
-  } else {
-    (void)hipMemsetAsync(a.scan_out, 0, sizeof(uint64_t) * C, s);
-  }
+  launch_scan(a.scan_in, a.d, C, a.scan_blk, a.scan_out, s);
   // level 0 of the range-minimum table is lcp itself
   (void)hipMemcpyAsync(a.sparse, a.lcp, sizeof(uint32_t) * n, hipMemcpyDeviceToDevice, s);
   for (int k = 1; k < a.levels; ++k)

@@ -14,11 +14,11 @@ constexpr uint32_t kEventRef = 0x80000000u;
 constexpr uint32_t kRefMask = 0x7FFFFFFFu;
 
 // ---- ingest tiling -------------------------------------------------------------
-constexpr int kIngestThreads = 256;     // 4 waves of 64
-constexpr int kTileEvents = 256;        // max events per tile
-constexpr int kTileFrames = 6144;       // LDS staging capacity (frames) of one tile
-constexpr int kMapWords = 2048;         // LDS aggregation map: uint64 sums
-constexpr int kMapKeys = 2048;          // LDS aggregation map: slot keys (>= entries)
+constexpr int kIngestThreads = 1024;    // 16 waves of 64, each with its own tile loop
+constexpr int kWaveEvents = 63;         // max events per wave tile (lane j holds offset j, j <= 63)
+constexpr int kWaveFrames = 64 * 16;    // frames of a wave tile (16 per lane)
+constexpr int kCacheEntries = 1024;     // LDS resolved-path cache entries per workgroup
+constexpr int kCacheWords = 2048;       // LDS resolved-path cache: uint64 sums
 
 // ---- counters written by the ingest kernel --------------------------------------
 enum Counter { kCtrNew = 0, kCtrNewFrames = 1, kCtrError = 2, kCtrOverflow = 3, kCtrCount = 8 };
@@ -61,7 +61,7 @@ struct IngestArgs {
   const uint64_t *w;
   int64_t n_events, n_frames;
   int32_t m;
-  int32_t tile_events;  // events per tile
+  int32_t tile_events;  // events per wave tile (<= kWaveEvents)
   int64_t n_tiles;
   // unique-path table
   uint64_t *slot;
@@ -106,9 +106,14 @@ struct PublishArgs {
   uint32_t *pslot;
   uint64_t *psums;           // [D][m]
   int64_t store_used;        // frames already used in the store
-  unsigned long long *cursor;  // frame cursor of this call (device, zeroed)
+  const uint64_t *starts;    // [n_new] exclusive prefix sums of the padded lengths
 };
+void launch_new_lengths(const int64_t *off, const uint64_t *slot, const uint32_t *new_slots, int64_t n,
+                        uint64_t *out, hipStream_t s);
 void launch_publish(const PublishArgs &a, hipStream_t s);
+// Exclusive prefix sums of `rows` rows of C uint64 columns (mod 2^64) into out[0..rows),
+// totals into out row `rows`; blk holds (rows / 1024 + 1) * C scratch words.
+void launch_scan(const uint64_t *in, int64_t rows, int C, uint64_t *blk, uint64_t *out, hipStream_t s);
 void launch_fold_old(int64_t d_old, int32_t m, const uint32_t *pslot, const uint64_t *delta, uint64_t *psums,
                      hipStream_t s);
 void launch_unclaim(uint64_t *slot, uint64_t cap, hipStream_t s);

@@ -9,47 +9,72 @@
 // iff their paths are equal frame by frame, which is exactly when the paper's tree
 // insertion would end them on the same node.
 //
-// Layout per workgroup (256 threads, persistent over tiles of consecutive events):
-//   - a tile's frames are staged in LDS with 16-byte loads (coalesced HBM stream);
-//   - each thread hashes a run of an odd number of consecutive staged frames
-//     (odd stride: conflict-free LDS banks) and adds partial sums per event with LDS
-//     atomics; the hash is a sum of position-dependent terms, so partial sums over
-//     any split of a path combine by addition;
-//   - one thread per event probes the table (linear probing, one 64-bit CAS to claim
-//     an empty slot); a tag match is verified frame by frame by one wave per event
-//     against the candidate's frames (L2/MALL resident: hot paths are few);
-//   - metrics go into an LDS map keyed by slot and are flushed to HBM with 64-bit
-//     atomics once per workgroup, so a hot path costs one global atomic per
-//     workgroup rather than one per event.
+// Work decomposition: one workgroup of 16 waves per CU, persistent.  Every wave owns a
+// contiguous range of events and cuts it into tiles that fill its 1024-frame LDS
+// slice (at most 63 events: lane j holds offset j), without workgroup barriers, so a
+// CU keeps 16 tiles in flight.  While a wave resolves tile t, the frames of tile t+1
+// stream into registers.  Lane l holds the 16-byte groups l, l + 64, l + 128,
+// l + 192 of a tile, so every load instruction reads 1 KiB of consecutive frames
+// (fully coalesced HBM stream) and every LDS access of a wave hits distinct banks.
+//   - hash: each lane sums a position-dependent term over its four runs of four
+//     frames; partial sums per event meet in LDS (64-bit LDS atomics).  The hash is a
+//     sum of terms, so partial sums over any split of a path combine by adding.  The
+//     walk also records each frame's event.
+//   - dedup: lane j resolves event j: a path with the same hash and length already
+//     resolved in this workgroup (LDS cache), else the table (linear probing, one
+//     64-bit CAS claims an empty slot).  Every candidate is verified frame by frame:
+//     lane l compares staged frames l, l + 64, ... with the candidate's frames, so
+//     each load instruction reads 64 consecutive frames (L2/MALL resident: hot paths
+//     are few).
+//   - metrics: summed into the cache entry of the path (LDS atomics) and flushed to
+//     HBM with 64-bit atomics once per workgroup; paths outside the cache add to HBM
+//     directly.
 #include "common.h"
 
 namespace cct {
 
 namespace {
 
-constexpr uint32_t kEmptyKey = 0xFFFFFFFFu;
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 enum : int32_t { kProbing = 0, kCandidate = 1, kResolved = 2, kFailed = 3 };
+enum : int32_t { kTileFast = 0, kTileSlow = 1, kTileBad = 2, kTileNone = 3 };
 
-struct alignas(16) IngestShared {
-  uint32_t fr[kTileFrames + 16];     // staged frames, slot j <-> global frame g0 - lead + j
-  uint64_t msum[kMapWords];          // LDS aggregation map sums [entries][m]
-  uint32_t mkey[kMapKeys];           // LDS aggregation map keys (table slot ids)
-  int64_t off[kTileEvents + 1];      // tile offsets (global)
-  uint64_t h[kTileEvents];           // per-event hash accumulator, then final hash
-  int64_t repbase[kTileEvents];      // first frame of the candidate's path
-  uint32_t probe[kTileEvents];       // current probe slot
-  uint32_t steps[kTileEvents];       // slots probed so far (bounded by the capacity)
-  int32_t ls[kTileEvents + 1];       // tile-local starts
-  int32_t state[kTileEvents];
-  int32_t from_store[kTileEvents];   // candidate frames live in the path store
-  int32_t mapidx[kTileEvents];
-  int32_t flag;
+constexpr int kWaves = kIngestThreads / 64;
+constexpr uint32_t kNotReady = 0xFFFFFFFFu;
+constexpr uint64_t kInStore = 1ull << 63;   // cache cbase: frames live in the path store
+
+struct WaveShared {
+  uint32_t fr[kWaveFrames];        // staged frames: slot x <-> relative position x - lead
+  uint8_t evt[kWaveFrames];        // event of each staged slot
+  int32_t ls[kWaveEvents + 1];     // event starts relative to the tile's first frame
+  int32_t bad[kWaveEvents + 1];    // verification found a differing frame
+  uint64_t hacc[kWaveEvents + 1];  // hash partial sums
+  uint64_t vaddr[kWaveEvents + 1]; // byte address of the candidate frame at relative position 0, or 0
 };
 
-__device__ inline int map_entries(int m) {
-  int e = kMapWords / m;
-  if (e > kMapKeys) e = kMapKeys;
+// Per-workgroup cache of resolved paths, keyed by (hash, length): the table slot,
+// where that slot's frames live (to verify against) and this workgroup's metric sums
+// for it.  Hot paths cost no table access after their first resolution in a
+// workgroup, and one global atomic per metric per workgroup at the end.
+struct IngestShared {
+  uint64_t ckey[kCacheEntries];    // hash (0: empty / not cacheable)
+  uint64_t cbase[kCacheEntries];   // first frame (kInStore: in the path store)
+  uint32_t clen[kCacheEntries];
+  uint32_t cslot[kCacheEntries];   // kNotReady until the entry is filled in
+  uint64_t csum[kCacheWords];      // [entries][m]
+  WaveShared wv[kWaves];
+};
+
+__device__ inline void wave_sync() {
+  // orders this wave's LDS accesses: every lane's earlier LDS writes are visible to
+  // every lane's later LDS reads
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+}
+
+__device__ inline int cache_entries(int m) {
+  int e = kCacheWords / m;
+  if (e > kCacheEntries) e = kCacheEntries;
   int p = 1;
   while (p * 2 <= e) p *= 2;
   return p;
@@ -63,284 +88,398 @@ __device__ inline uint64_t wave_sum_u64(uint64_t v) {
   return v;
 }
 
-// Length of the candidate path referenced by `ref` and where its frames live.
-__device__ inline void candidate_frames(const IngestArgs &a, uint32_t ref, int64_t *len, int64_t *base,
-                                        int32_t *store) {
-  if (ref & kEventRef) {
-    int64_t e = ref & kRefMask;
-    int64_t s = a.off[e];
-    *len = a.off[e + 1] - s;
-    *base = s;
-    *store = 0;
-  } else {
-    *len = a.plen[ref];
-    *base = a.pstart[ref];
-    *store = 1;
+// wave-uniform values kept in scalar registers
+__device__ inline int64_t uniform64(int64_t v) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)v >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+__device__ inline int64_t shfl_i64(int64_t v, int src) {
+  uint32_t lo = __shfl((uint32_t)v, src, 64), hi = __shfl((uint32_t)((uint64_t)v >> 32), src, 64);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// A tile: events [e0, e0 + ne) of the wave's range, wave-uniform.
+struct Tile {
+  int64_t e0, g0;
+  int32_t ne, span, lead, kind;
+};
+
+// Offsets window at event e (lane j holds offsets[e + j], j <= min(63, end - e)).
+__device__ inline int64_t load_window(const IngestArgs &a, int64_t e, int64_t end, int lane) {
+  return e < end && lane <= end - e ? a.off[e + lane] : 0;
+}
+
+// Validate the window and cut the next tile: as many events as fit in the staging
+// slice.  Every offset is validated here, before any frame is read.
+__device__ inline Tile make_tile(const IngestArgs &a, int64_t e, int64_t end, int64_t o, int lane) {
+  Tile t{};
+  if (e >= end) { t.kind = kTileNone; return t; }
+  t.e0 = e;
+  const int jmax = (int)min((int64_t)kWaveEvents, end - e);
+  const int64_t onext = shfl_i64(o, lane + 1 < 64 ? lane + 1 : 63);
+  bool bad = lane < jmax && onext < o;
+  if (lane <= jmax) bad |= o < 0 || o > a.n_frames;
+  if (lane == 0) bad |= e == 0 && o != 0;
+  if (lane == jmax) bad |= e + jmax == a.n_events && o != a.n_frames;
+  if (__any(bad)) { t.kind = kTileBad; return t; }
+  t.g0 = uniform64(shfl_i64(o, 0));
+  t.lead = (int)(((uintptr_t)a.fr >> 2) + (uint64_t)t.g0) & 3;
+  const uint64_t fit = __ballot(lane >= 1 && lane <= jmax && o - t.g0 + t.lead <= kWaveFrames);
+  if (fit == 0) {  // a single path longer than the slice
+    t.ne = 1;
+    t.kind = kTileSlow;
+    return t;
+  }
+  t.ne = 63 - __builtin_clzll(fit);  // offsets are non-decreasing: the fitting lanes are 1..ne
+  t.span = (int)(uniform64(shfl_i64(o, t.ne)) - t.g0);
+  t.kind = kTileFast;
+  return t;
+}
+
+// This lane's frames of a fast tile: 16-byte groups q * 64 + lane (slots
+// 256 q + 4 lane .. + 4), at 16-byte aligned addresses; elements outside the tile are
+// left zero.
+__device__ inline void load_frames(const IngestArgs &a, const Tile &t, int lane, u32x4 nf[4]) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int r = q * 256 + lane * 4 - t.lead;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (t.kind == kTileFast && r + 4 > 0 && r < t.span) {
+      const int64_t gi = t.g0 + r;
+      if (gi >= 0 && gi + 4 <= a.n_frames) {
+        v = __builtin_nontemporal_load((const u32x4 *)(a.fr + gi));
+      } else {
+        for (int e = 0; e < 4; ++e)
+          if (r + e >= 0 && r + e < t.span) v[e] = a.fr[gi + e];
+      }
+    }
+    nf[q] = v;
   }
 }
 
-// Walk the probe sequence of one event until it claims an empty slot (resolved, new
-// path) or meets a slot whose tag and length match (candidate, needs verification).
-__device__ void probe_event(const IngestArgs &a, IngestShared &S, int i, int64_t ev, int64_t len) {
-  const uint64_t h = S.h[i];
-  const uint32_t tag = (uint32_t)(h >> 32);
-  uint64_t s = S.probe[i];
+// Per-event resolution state, held by the lane that owns the event.
+struct Probe {
+  uint64_t h;        // final hash (masked)
+  uint64_t cbase;    // frames of the candidate / resolved path (kInStore bit: path store)
+  uint32_t slot;     // current probe slot (capacity <= 2^31)
+  uint32_t steps;    // slots probed so far
+  uint32_t len;      // staged events are shorter than a tile
+  int32_t state;
+};
+
+// Walk the probe sequence until the event claims an empty slot (resolved, new path)
+// or meets a slot whose tag and length match (candidate, needs verification).
+// Every event probes at most `capacity` slots over all its rounds: past the load
+// limit the table may be full, and the event then gives up (overflow).  Slot words
+// are read through the caches: a stale empty word only leads to a CAS, which sees the
+// true word.
+__device__ __forceinline__ void probe(const IngestArgs &a, Probe &p, int64_t ev, int64_t ev_start, int64_t len) {
+  const uint32_t tag = (uint32_t)(p.h >> 32);
   for (;;) {
-    // every event probes at most `capacity` slots over all its rounds: past the load
-    // limit the table may be full, and the event then gives up (overflow)
-    if ((uint64_t)S.steps[i]++ > a.cap_mask) {
+    if ((uint64_t)p.steps++ > a.cap_mask) {
       atomicOr(&a.ctr[kCtrOverflow], 1ull);
-      S.state[i] = kFailed;
+      p.state = kFailed;
       return;
     }
-    uint64_t w = __atomic_load_n(&a.slot[s], __ATOMIC_RELAXED);
+    uint64_t w = a.slot[p.slot];
     if (w == kEmptySlot) {
       const uint64_t mine = ((uint64_t)tag << 32) | (kEventRef | (uint32_t)ev);
-      uint64_t prev = atomicCAS((unsigned long long *)&a.slot[s], (unsigned long long)kEmptySlot,
-                                (unsigned long long)mine);
+      const uint64_t prev = atomicCAS((unsigned long long *)&a.slot[p.slot], (unsigned long long)kEmptySlot,
+                                      (unsigned long long)mine);
       if (prev == kEmptySlot) {
-        unsigned long long k = atomicAdd(&a.ctr[kCtrNew], 1ull);
-        if (k < a.max_new) {
-          a.new_slots[k] = (uint32_t)s;
-        } else {
-          atomicOr(&a.ctr[kCtrOverflow], 1ull);
-        }
+        const unsigned long long k = atomicAdd(&a.ctr[kCtrNew], 1ull);
+        if (k < a.max_new) a.new_slots[k] = (uint32_t)p.slot;
+        else atomicOr(&a.ctr[kCtrOverflow], 1ull);
         atomicAdd(&a.ctr[kCtrNewFrames], (unsigned long long)len);
-        S.probe[i] = (uint32_t)s;
-        S.state[i] = kResolved;
+        p.cbase = (uint64_t)ev_start;
+        p.state = kResolved;
         return;
       }
       w = prev;
     }
     if ((uint32_t)(w >> 32) == tag) {
-      int64_t clen, cbase;
-      int32_t store;
-      candidate_frames(a, (uint32_t)w, &clen, &cbase, &store);
+      const uint32_t ref = (uint32_t)w;
+      int64_t clen;
+      uint64_t cbase;
+      if (ref & kEventRef) {
+        const int64_t e = ref & kRefMask;
+        const int64_t s = a.off[e];
+        clen = a.off[e + 1] - s;
+        cbase = (uint64_t)s;
+      } else {
+        clen = a.plen[ref];
+        cbase = (uint64_t)a.pstart[ref] | kInStore;
+      }
       if (clen == len) {
-        S.probe[i] = (uint32_t)s;
-        if (len == 0) {
-          S.state[i] = kResolved;
-        } else {
-          S.repbase[i] = cbase;
-          S.from_store[i] = store;
-          S.state[i] = kCandidate;
-        }
+        p.cbase = cbase;
+        p.state = len == 0 ? kResolved : kCandidate;
         return;
       }
     }
-    s = (s + 1) & a.cap_mask;
+    p.slot = (uint32_t)((p.slot + 1) & a.cap_mask);
   }
 }
 
-// Add one event's metrics into the LDS map (or straight to HBM when the map is full).
-__device__ inline int map_insert(IngestShared &S, uint32_t slot, int entries) {
-  uint32_t k = hash32(slot) & (uint32_t)(entries - 1);
+// Cache entry holding a resolved path with this hash and length, or -1.
+__device__ inline int cache_find(const IngestShared &S, uint64_t h, uint32_t len, int entries) {
+  if (h == 0) return -1;
+  uint32_t k = (uint32_t)h & (uint32_t)(entries - 1);
   for (int t = 0; t < 8; ++t) {
-    uint32_t prev = atomicCAS(&S.mkey[k], kEmptyKey, slot);
-    if (prev == kEmptyKey || prev == slot) return (int)k;
+    const uint64_t key = S.ckey[k];
+    if (key == 0) return -1;
+    if (key == h && S.cslot[k] != kNotReady && S.clen[k] == len) return (int)k;
     k = (k + 1) & (uint32_t)(entries - 1);
   }
   return -1;
 }
 
-// Tiles whose frames exceed the LDS staging buffer: one event at a time, the whole
-// workgroup striding over its frames in HBM.
-__device__ void slow_tile(const IngestArgs &a, IngestShared &S, int64_t e0, int ne, int entries) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  for (int i = 0; i < ne; ++i) {
-    const int64_t gs = S.off[i], len = S.off[i + 1] - gs;
-    uint64_t acc = 0;
-    for (int64_t k = tid; k < len; k += kIngestThreads) acc += frame_term(a.fr[gs + k], (uint32_t)k);
-    acc = wave_sum_u64(acc);
-    if (tid == 0) S.h[0] = 0;
-    __syncthreads();
-    if (lane == 0) atomicAdd((unsigned long long *)&S.h[0], (unsigned long long)acc);
-    __syncthreads();
-    if (tid == 0) {
-      S.h[0] = finish_hash(S.h[0], (uint64_t)len) & a.hash_mask;
-      S.probe[0] = (uint32_t)(S.h[0] & a.cap_mask);
-      S.steps[0] = 0;
-      S.state[0] = kProbing;
+// Cache entry for a path just resolved to `slot`: the existing entry for it, a new
+// one, or -1 (window full, or an entry for the same hash is not ready / names
+// another slot: the caller then adds its metrics straight to HBM).
+__device__ inline int cache_insert(IngestShared &S, uint64_t h, uint32_t len, uint32_t slot, uint64_t cbase,
+                                   int entries) {
+  if (h == 0) return -1;
+  uint32_t k = (uint32_t)h & (uint32_t)(entries - 1);
+  for (int t = 0; t < 8; ++t) {
+    const uint64_t prev = atomicCAS((unsigned long long *)&S.ckey[k], 0ull, (unsigned long long)h);
+    if (prev == 0) {
+      S.cbase[k] = cbase;
+      S.clen[k] = len;
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+      S.cslot[k] = slot;
+      return (int)k;
     }
-    __syncthreads();
+    if (prev == h) {
+      const uint32_t cs = S.cslot[k];
+      if (cs == kNotReady) return -1;
+      if (cs == slot) return (int)k;
+      if (S.clen[k] == len) return -1;  // same hash and length, another path
+    }
+    k = (k + 1) & (uint32_t)(entries - 1);
+  }
+  return -1;
+}
+
+// Add one event's metric into its cache entry or straight into HBM.
+__device__ inline void add_metric(const IngestArgs &a, IngestShared &S, int ci, uint64_t slot, int c, uint64_t v) {
+  if (ci >= 0) atomicAdd((unsigned long long *)&S.csum[ci * a.m + c], (unsigned long long)v);
+  else atomicAdd((unsigned long long *)&a.delta[slot * a.m + c], (unsigned long long)v);
+}
+
+// Tiles whose frames exceed a wave's staging capacity: one event at a time, the
+// wave striding over its frames in HBM.
+__device__ __forceinline__ void slow_wave_tile(const IngestArgs &a, int64_t e0, int ne, int64_t o) {
+  const int lane = threadIdx.x & 63;
+  for (int j = 0; j < ne; ++j) {
+    const int64_t gs = shfl_i64(o, j), len = shfl_i64(o, j + 1) - gs;
+    uint64_t acc = 0;
+    for (int64_t k = lane; k < len; k += 64) acc += frame_term(a.fr[gs + k], (uint32_t)k);
+    acc = wave_sum_u64(acc);
+    Probe p{};
+    p.h = finish_hash(acc, (uint64_t)len) & a.hash_mask;
+    p.slot = (uint32_t)(p.h & a.cap_mask);
+    p.len = (uint32_t)len;  // compared with candidate lengths below as 64-bit
+    p.state = kProbing;
     for (;;) {
-      if (tid == 0) probe_event(a, S, 0, e0 + i, len);
-      __syncthreads();
-      if (S.state[0] != kCandidate) break;
-      const uint32_t *src = S.from_store[0] ? a.pframes : a.fr;
-      const int64_t cb = S.repbase[0];
+      if (lane == 0) probe(a, p, e0 + j, gs, len);
+      const int state = __shfl(p.state, 0, 64);
+      if (state != kCandidate) { p.state = state; break; }
+      const uint64_t cb = (uint64_t)shfl_i64((int64_t)p.cbase, 0);
+      const uint32_t *src = (cb & kInStore) ? a.pframes + (cb & ~kInStore) : a.fr + cb;
       bool mism = false;
-      for (int64_t k = tid; k < len; k += kIngestThreads) mism |= a.fr[gs + k] != src[cb + k];
-      mism = __syncthreads_or(mism);
-      if (!mism) {
-        if (tid == 0) S.state[0] = kResolved;
-        __syncthreads();
+      for (int64_t k = lane; k < len; k += 64) mism |= a.fr[gs + k] != src[k];
+      if (__any(mism)) {
+        if (lane == 0) { p.slot = (uint32_t)((p.slot + 1) & a.cap_mask); p.state = kProbing; }
+      } else {
+        p.state = kResolved;
         break;
       }
-      if (tid == 0) { S.probe[0] = (uint32_t)((S.probe[0] + 1) & a.cap_mask); S.state[0] = kProbing; }
-      __syncthreads();
     }
-    if (S.state[0] == kResolved) {
-      const uint32_t slot = S.probe[0];
-      if (tid == 0) S.mapidx[0] = map_insert(S, slot, entries);
-      __syncthreads();
-      const int mi = S.mapidx[0];
-      if (tid < a.m) {
-        const uint64_t v = a.w[(e0 + i) * a.m + tid];
-        if (mi >= 0) atomicAdd((unsigned long long *)&S.msum[mi * a.m + tid], (unsigned long long)v);
-        else atomicAdd((unsigned long long *)&a.delta[(uint64_t)slot * a.m + tid], (unsigned long long)v);
-      }
+    if (p.state == kResolved) {
+      const uint64_t slot = (uint64_t)shfl_i64((int64_t)p.slot, 0);
+      if (lane < a.m) atomicAdd((unsigned long long *)&a.delta[slot * a.m + lane],
+                                (unsigned long long)a.w[(e0 + j) * a.m + lane]);
     }
-    __syncthreads();
-    (void)wave;
   }
+}
+
+// Event j containing relative position r (largest j with ls[j] <= r; ls[ne] > r).
+__device__ inline int event_at(const WaveShared &W, int ne, int r) {
+  int lo = 0, hi = ne;
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (W.ls[mid] <= r) lo = mid; else hi = mid;
+  }
+  return lo;
 }
 
 __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
   __shared__ IngestShared S;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  WaveShared &W = S.wv[wave];
   const int m = a.m;
-  const int entries = map_entries(m);
-  for (int i = tid; i < kMapKeys; i += kIngestThreads) S.mkey[i] = kEmptyKey;
-  for (int i = tid; i < kMapWords; i += kIngestThreads) S.msum[i] = 0;
+  const int entries = cache_entries(m);
+  for (int i = tid; i < kCacheEntries; i += kIngestThreads) { S.ckey[i] = 0; S.cslot[i] = kNotReady; }
+  for (int i = tid; i < kCacheWords; i += kIngestThreads) S.csum[i] = 0;
   __syncthreads();
 
-  for (int64_t tile = blockIdx.x; tile < a.n_tiles; tile += gridDim.x) {
-    if (tid == 0) S.flag = (int)__atomic_load_n(&a.ctr[kCtrOverflow], __ATOMIC_RELAXED);
-    __syncthreads();
-    if (S.flag) break;
-    const int64_t e0 = tile * a.tile_events;
-    const int ne = (int)min((int64_t)a.tile_events, a.n_events - e0);
+  // this wave's events
+  const int64_t waves_total = (int64_t)gridDim.x * kWaves, w = (int64_t)blockIdx.x * kWaves + wave;
+  const int64_t end = (w + 1) * a.n_events / waves_total;
+  int64_t e_cur = w * a.n_events / waves_total;
+  int64_t o_cur = load_window(a, e_cur, end, lane);
+  Tile t = make_tile(a, e_cur, end, o_cur, lane);
+  u32x4 nf[4];
+  load_frames(a, t, lane, nf);
 
-    // A1: offsets of the tile, validated before any frame is read
-    for (int i = tid; i <= ne; i += kIngestThreads) S.off[i] = a.off[e0 + i];
-    __syncthreads();
-    bool bad = false;
-    for (int i = tid; i < ne; i += kIngestThreads) bad |= S.off[i + 1] < S.off[i];
-    if (tid == 0) {
-      bad |= S.off[0] < 0 || S.off[ne] > a.n_frames;
-      if (e0 == 0) bad |= S.off[0] != 0;
-      if (e0 + ne == a.n_events) bad |= S.off[ne] != a.n_frames;
+  for (int iter = 0; t.kind != kTileNone; ++iter) {
+    // early exit after a table overflow (the host retries); checked now and then, as
+    // every check is an uncached read of one hot address
+    if ((iter & 63) == 63 && __atomic_load_n(&a.ctr[kCtrOverflow], __ATOMIC_RELAXED)) break;
+    if (t.kind == kTileBad) {
+      if (lane == 0) atomicOr(&a.ctr[kCtrError], (unsigned long long)kErrOffsets);
+      break;  // the call fails; this wave's range cannot be cut further
     }
-    if (__syncthreads_or(bad)) {
-      if (tid == 0) atomicOr(&a.ctr[kCtrError], (unsigned long long)kErrOffsets);
+    const int64_t e_nxt = t.e0 + t.ne;
+    if (t.kind == kTileSlow) {
+      slow_wave_tile(a, t.e0, t.ne, o_cur);
+      e_cur = e_nxt;
+      o_cur = load_window(a, e_cur, end, lane);
+      t = make_tile(a, e_cur, end, o_cur, lane);
+      load_frames(a, t, lane, nf);
       continue;
     }
-    const int64_t g0 = S.off[0];
-    const int64_t span64 = S.off[ne] - g0;
-    if (span64 > kTileFrames) {
-      slow_tile(a, S, e0, ne, entries);
-      continue;
-    }
-    const int span = (int)span64;
-    for (int i = tid; i <= ne; i += kIngestThreads) S.ls[i] = (int32_t)(S.off[i] - g0);
-    for (int i = tid; i < ne; i += kIngestThreads) S.h[i] = 0;
+    const int ne = t.ne, span = t.span, lead = t.lead;
+    const int64_t e0 = t.e0;
+    const int nm = ne * m;
+    // stage the current frames; the next offsets window and this tile's metrics are
+    // on their way while the tile is hashed
+#pragma unroll
+    for (int q = 0; q < 4; ++q) *(u32x4 *)&W.fr[q * 256 + lane * 4] = nf[q];
+    if (lane <= ne) W.ls[lane] = (int32_t)(o_cur - t.g0);
+    if (lane < ne) W.hacc[lane] = 0;
+    const int64_t o_nxt = load_window(a, e_nxt, end, lane);
+    const uint64_t mv0 = lane < nm ? a.w[e0 * m + lane] : 0;
+    const uint64_t mv1 = lane + 64 < nm ? a.w[e0 * m + lane + 64] : 0;
+    wave_sync();
 
-    // stage the tile's frames: 16-byte groups aligned in memory and in LDS
-    const int lead = (int)(((uintptr_t)a.fr >> 2) + (uint64_t)g0) & 3;
-    const uint32_t *gbase = (const uint32_t *)((uintptr_t)a.fr + (uintptr_t)((g0 - lead) * 4));
-    const int nq = (lead + span + 3) >> 2;
-    for (int q = tid; q < nq; q += kIngestThreads) {
-      const int lo = q * 4;
-      if (lo >= lead && lo + 4 <= lead + span) {
-        const u32x4 v = __builtin_nontemporal_load((const u32x4 *)(gbase + lo));
-        *(u32x4 *)&S.fr[lo] = v;
-      } else {
-        for (int x = 0; x < 4; ++x) {
-          const int j = lo + x;
-          if (j >= lead && j < lead + span) S.fr[j] = gbase[j];
-        }
-      }
-    }
-    __syncthreads();
-
-    // A2: hash.  Thread runs of R (odd) consecutive frames, partial sums per event.
-    if (span > 0) {
-      const int R = ((span + kIngestThreads - 1) / kIngestThreads) | 1;
-      const int p0 = tid * R, p1 = min(span, p0 + R);
-      if (p0 < p1) {
-        int lo = 0, hi = ne;  // largest i with ls[i] <= p0 (ls[ne] = span > p0)
-        while (hi - lo > 1) {
-          const int mid = (lo + hi) >> 1;
-          if (S.ls[mid] <= p0) lo = mid; else hi = mid;
-        }
-        int cur = lo, cs = S.ls[cur], nx = S.ls[cur + 1];
+    // A2: hash.  Four runs of four frames per lane: slots 256 q + 4 lane .. + 4.
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int r0 = q * 256 + lane * 4 - lead;
+      if (r0 + 4 > 0 && r0 < span) {
+        const u32x4 v = *(const u32x4 *)&W.fr[q * 256 + lane * 4];
+        int cur = event_at(W, ne, r0 < 0 ? 0 : r0), cs = W.ls[cur], nx = W.ls[cur + 1];
         uint64_t acc = 0;
-        for (int p = p0; p < p1; ++p) {
-          if (p >= nx) {
-            atomicAdd((unsigned long long *)&S.h[cur], (unsigned long long)acc);
+        uint32_t ev4 = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int r = r0 + i;
+          const bool valid = r >= 0 && r < span;
+          if (valid && r >= nx) {
+            atomicAdd((unsigned long long *)&W.hacc[cur], (unsigned long long)acc);
             acc = 0;
-            do { ++cur; } while (S.ls[cur + 1] <= p);
-            cs = S.ls[cur];
-            nx = S.ls[cur + 1];
+            do { ++cur; } while (W.ls[cur + 1] <= r);
+            cs = W.ls[cur];
+            nx = W.ls[cur + 1];
           }
-          acc += frame_term(S.fr[lead + p], (uint32_t)(p - cs));
+          if (valid) acc += frame_term(v[i], (uint32_t)(r - cs));
+          ev4 |= (uint32_t)cur << (8 * i);
         }
-        atomicAdd((unsigned long long *)&S.h[cur], (unsigned long long)acc);
+        atomicAdd((unsigned long long *)&W.hacc[cur], (unsigned long long)acc);
+        *(uint32_t *)&W.evt[q * 256 + lane * 4] = ev4;
       }
     }
-    __syncthreads();
+    // the next tile's frames stream in while this tile resolves
+    const Tile tn = make_tile(a, e_nxt, end, o_nxt, lane);
+    load_frames(a, tn, lane, nf);
+    wave_sync();
 
-    // A3: exact dedup.  Probe, verify candidates a wave per event, repeat.
-    for (int i = tid; i < ne; i += kIngestThreads) {
-      const int64_t len = S.ls[i + 1] - S.ls[i];
-      const uint64_t h = finish_hash(S.h[i], (uint64_t)len) & a.hash_mask;
-      S.h[i] = h;
-      S.probe[i] = (uint32_t)(h & a.cap_mask);
-      S.steps[i] = 0;
-      S.state[i] = kProbing;
+    // A3: exact dedup.  Lane j resolves event j: a cached resolution of the same hash
+    // and length, else the table; every candidate is verified by all lanes.
+    Probe p{};
+    p.state = kResolved;
+    int ci = -1;  // cache entry of the candidate (-2: a cached candidate failed)
+    if (lane < ne) {
+      p.len = (uint32_t)(W.ls[lane + 1] - W.ls[lane]);
+      p.h = finish_hash(W.hacc[lane], (uint64_t)p.len) & a.hash_mask;
+      p.slot = (uint32_t)(p.h & a.cap_mask);
+      p.state = kProbing;
+      ci = cache_find(S, p.h, p.len, entries);
+      if (ci >= 0) {
+        p.slot = S.cslot[ci];
+        p.cbase = S.cbase[ci];
+        p.state = p.len == 0 ? kResolved : kCandidate;
+      }
     }
-    __syncthreads();
     for (;;) {
-      for (int i = tid; i < ne; i += kIngestThreads)
-        if (S.state[i] == kProbing) probe_event(a, S, i, e0 + i, S.ls[i + 1] - S.ls[i]);
-      __syncthreads();
-      bool any = false;
-      for (int i = tid; i < ne; i += kIngestThreads) any |= S.state[i] == kCandidate;
-      if (!__syncthreads_or(any)) break;
-      for (int i = wave; i < ne; i += kIngestThreads / 64) {
-        if (S.state[i] != kCandidate) continue;  // uniform across the wave
-        const int len = S.ls[i + 1] - S.ls[i];
-        const uint32_t *mine = &S.fr[lead + S.ls[i]];
-        const uint32_t *src = (S.from_store[i] ? a.pframes : a.fr) + S.repbase[i];
-        bool mism = false;
-        for (int k = lane; k < len; k += 64) mism |= mine[k] != src[k];
-        mism = __any(mism);
-        if (lane == 0) {
-          if (mism) {
-            S.probe[i] = (uint32_t)((S.probe[i] + 1) & a.cap_mask);
-            S.state[i] = kProbing;
-          } else {
-            S.state[i] = kResolved;
-          }
+      if (p.state == kProbing) probe(a, p, e0 + lane, o_cur, (int64_t)p.len);
+      if (!__any(p.state == kCandidate)) break;
+      if (lane < ne) {
+        uint64_t va = 0;
+        if (p.state == kCandidate) {
+          const uint32_t *src = (p.cbase & kInStore) ? a.pframes + (p.cbase & ~kInStore) : a.fr + p.cbase;
+          va = (uint64_t)(uintptr_t)src - 4ull * (uint64_t)W.ls[lane];
+        }
+        W.vaddr[lane] = va;
+        W.bad[lane] = 0;
+      }
+      wave_sync();
+      // lane l checks staged slots l, l + 64, ...: 64 consecutive frames per load
+#pragma unroll
+      for (int i = 0; i < kWaveFrames / 64; ++i) {
+        const int x = i * 64 + lane, r = x - lead;
+        if (r >= 0 && r < span) {
+          const int e = W.evt[x];
+          const uint64_t va = W.vaddr[e];
+          if (va && *(const uint32_t *)(uintptr_t)(va + 4ull * (uint64_t)r) != W.fr[x]) W.bad[e] = 1;
         }
       }
-      __syncthreads();
+      wave_sync();
+      if (p.state == kCandidate) {
+        if (W.bad[lane]) {
+          p.slot = (uint32_t)((p.slot + 1) & a.cap_mask);
+          p.state = kProbing;
+          ci = -2;
+        } else {
+          p.state = kResolved;
+        }
+      }
+      wave_sync();
     }
 
-    // exclusive aggregation: LDS map keyed by slot, HBM atomics when the map is full
-    for (int i = tid; i < ne; i += kIngestThreads)
-      S.mapidx[i] = S.state[i] == kResolved ? map_insert(S, S.probe[i], entries) : -2;
-    __syncthreads();
-    for (int t = tid; t < ne * m; t += kIngestThreads) {
-      const int i = t / m, j = t - i * m;
-      const int mi = S.mapidx[i];
-      if (mi == -2) continue;
-      const uint64_t v = a.w[(e0 + i) * m + j];
-      if (mi >= 0) atomicAdd((unsigned long long *)&S.msum[mi * m + j], (unsigned long long)v);
-      else atomicAdd((unsigned long long *)&a.delta[(uint64_t)S.probe[i] * m + j], (unsigned long long)v);
+    // exclusive aggregation into the cache entry of the path (HBM atomics when none)
+    int mi = -3;  // -3: nothing to add
+    if (lane < ne && p.state == kResolved) {
+      if (ci == -1) ci = cache_insert(S, p.h, p.len, p.slot, p.cbase, entries);
+      mi = ci < 0 ? -1 : ci;
     }
-    __syncthreads();
+    const uint32_t myslot = p.slot;
+    for (int q0 = 0; q0 < nm; q0 += 64) {  // uniform trip count: every lane takes part in the shuffles
+      const int q = q0 + lane;
+      const int j = min(q / m, ne - 1), c = q - j * m;
+      const int mj = __shfl(mi, j, 64);
+      const uint64_t sj = __shfl(myslot, j, 64);
+      if (q < nm && mj != -3) {
+        const uint64_t v = q < 64 ? mv0 : q < 128 ? mv1 : a.w[e0 * m + q];
+        add_metric(a, S, mj, sj, c, v);
+      }
+    }
+    e_cur = e_nxt;
+    o_cur = o_nxt;
+    t = tn;
   }
 
-  // flush the LDS map
+  // flush the cached sums
   __syncthreads();
   for (int k = tid; k < entries; k += kIngestThreads) {
-    const uint32_t key = S.mkey[k];
-    if (key == kEmptyKey) continue;
+    const uint32_t slot = S.cslot[k];
+    if (S.ckey[k] == 0 || slot == kNotReady) continue;
     for (int j = 0; j < m; ++j) {
-      const uint64_t v = S.msum[k * m + j];
-      if (v) atomicAdd((unsigned long long *)&a.delta[(uint64_t)key * m + j], (unsigned long long)v);
+      const uint64_t v = S.csum[k * m + j];
+      if (v) atomicAdd((unsigned long long *)&a.delta[(uint64_t)slot * m + j], (unsigned long long)v);
     }
   }
 }
@@ -358,9 +497,7 @@ __global__ __launch_bounds__(256) void publish_kernel(PublishArgs a) {
   const int64_t e = (int64_t)((uint32_t)w & kRefMask);
   const int64_t src = a.off[e], len = a.off[e + 1] - src;
   const int64_t rl = round_store(len);
-  int64_t start = 0;
-  if (lane == 0) start = a.store_used + (int64_t)atomicAdd(a.cursor, (unsigned long long)rl);
-  start = __shfl(start, 0, 64);
+  const int64_t start = a.store_used + (int64_t)a.starts[i];
   const int64_t id = a.d_old + i;
   for (int64_t k = lane; k < rl; k += 64) a.pframes[start + k] = k < len ? a.fr[src + k] : 0u;
   // checkpoint hashes: lane b sums block b of 16 frames; a wave prefix scan then
@@ -391,6 +528,15 @@ __global__ __launch_bounds__(256) void publish_kernel(PublishArgs a) {
     a.slot[s] = (w & 0xFFFFFFFF00000000ull) | (uint64_t)id;
   }
   if (lane < a.m) a.psums[id * a.m + lane] = a.delta[(uint64_t)s * a.m + lane];
+}
+
+// Padded store length of every new path (input of the scan that places them).
+__global__ void new_lengths_kernel(const int64_t *off, const uint64_t *slot, const uint32_t *new_slots, int64_t n,
+                                   uint64_t *out) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int64_t e = (int64_t)((uint32_t)slot[new_slots[i]] & kRefMask);
+  out[i] = (uint64_t)round_store(off[e + 1] - off[e]);
 }
 
 __global__ void fold_old_kernel(int64_t d_old, int32_t m, const uint32_t *pslot, const uint64_t *delta,
@@ -434,6 +580,11 @@ inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1)
 
 void launch_ingest(const IngestArgs &a, int grid, hipStream_t s) {
   hipLaunchKernelGGL(ingest_kernel, dim3(grid), dim3(kIngestThreads), 0, s, a);
+}
+void launch_new_lengths(const int64_t *off, const uint64_t *slot, const uint32_t *new_slots, int64_t n,
+                        uint64_t *out, hipStream_t s) {
+  if (n <= 0) return;
+  hipLaunchKernelGGL(new_lengths_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, off, slot, new_slots, n, out);
 }
 void launch_publish(const PublishArgs &a, hipStream_t s) {
   if (a.n_new <= 0) return;

@@ -13,7 +13,7 @@
 #include <unordered_map>
 #include <vector>
 
-#include "../../include/cct.h"
+#include "cct.h"
 #include "common.h"
 
 using namespace cct;
@@ -301,14 +301,15 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
       IngestArgs a{};
       a.off = p->offsets; a.fr = p->frames; a.w = p->metrics;
       a.n_events = N; a.n_frames = p->n_frames; a.m = m;
-      const double mean = std::max(1.0, (double)p->n_frames / (double)N);
-      a.tile_events = (int32_t)std::max(1.0, std::min((double)kTileEvents, 0.75 * kTileFrames / mean));
-      a.n_tiles = (N + a.tile_events - 1) / a.tile_events;
+      a.tile_events = kWaveEvents;
+      a.n_tiles = (N + kWaveEvents - 1) / kWaveEvents;  // upper bound of the tile count
       a.slot = t->slot.as<uint64_t>(); a.cap_mask = t->cap - 1; a.hash_mask = hash_mask;
       a.delta = delta.as<uint64_t>(); a.new_slots = new_slots.as<uint32_t>(); a.max_new = max_new;
       a.pframes = t->pframes.as<uint32_t>(); a.pstart = t->pstart.as<int64_t>(); a.plen = t->plen.as<uint32_t>();
       a.ctr = dctr;
-      const int grid = (int)std::min<int64_t>(a.n_tiles, (int64_t)cu_count() * 2);
+      // one workgroup per CU; every wave owns an equal share of the events
+      const int64_t wg_needed = (N + kIngestThreads / 64 - 1) / (kIngestThreads / 64);
+      const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(wg_needed, (int64_t)cu_count()));
       tm.mark(1, s);
       launch_ingest(a, grid, s);
       tm.mark(2, s);
@@ -387,24 +388,30 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   const int levels = floor_log2((uint64_t)n1) + 1;
   const int64_t nblk = (D + 1023) / 1024 + 1;
   const int64_t u_max = sum_len + 1;
-  Buf order, order_tmp, lcp, scan_in, scan_out, scan_blk, sparse, chain, node_path, cursor;
+  Buf order, order_tmp, lcp, scan_in, scan_out, scan_blk, sparse, chain, node_path, cursor, nlen, nstart, nblkbuf;
   Buf n_parent, n_frame, n_depth, n_excl, n_incl;
   if (!order.alloc(dneed * 4) || !order_tmp.alloc(dneed * 4) || !lcp.alloc(n1 * 4) || !scan_in.alloc(dneed * C * 8) ||
       !scan_out.alloc(n1 * C * 8) || !scan_blk.alloc(nblk * C * 8) || !sparse.alloc((int64_t)levels * n1 * 4) ||
       !chain.alloc(dneed * 4) || !node_path.alloc(u_max * 4) || !cursor.alloc(64) || !n_parent.alloc(u_max * 4) ||
       !n_frame.alloc(u_max * 4) || !n_depth.alloc(u_max * 4) || !n_excl.alloc(u_max * m * 8) ||
-      !n_incl.alloc(u_max * m * 8))
+      !n_incl.alloc(u_max * m * 8) || !nlen.alloc((n_new + 1) * 8) || !nstart.alloc((n_new + 1) * 8) ||
+      !nblkbuf.alloc(((int64_t)n_new / 1024 + 2) * 8))
     return rollback(fail(CCT_ENOMEM, "device allocation failed"));
 
   // ---- publish new paths, fold this call's sums into the old ones -----------------------
   HIP_TRY(hipMemsetAsync(cursor.p, 0, 64, s));
   if (n_new) {
+    // place the new paths in the store: exclusive scan of their padded lengths
+    launch_new_lengths(p->offsets, t->slot.as<uint64_t>(), new_slots.as<uint32_t>(), (int64_t)n_new,
+                       nlen.as<uint64_t>(), s);
+    launch_scan(nlen.as<uint64_t>(), (int64_t)n_new, 1, nblkbuf.as<uint64_t>(), nstart.as<uint64_t>(), s);
+    HIP_TRY(hipMemcpyAsync(cursor.p, nstart.as<uint64_t>() + n_new, 8, hipMemcpyDeviceToDevice, s));
     PublishArgs pa{};
     pa.off = p->offsets; pa.fr = p->frames; pa.slot = t->slot.as<uint64_t>();
     pa.new_slots = new_slots.as<uint32_t>(); pa.n_new = (int64_t)n_new; pa.d_old = t->d; pa.m = m;
     pa.delta = delta.as<uint64_t>(); pa.pframes = t->pframes.as<uint32_t>(); pa.pcp = t->pcp.as<uint64_t>();
     pa.pstart = t->pstart.as<int64_t>(); pa.plen = t->plen.as<uint32_t>(); pa.pslot = t->pslot.as<uint32_t>();
-    pa.psums = t->psums.as<uint64_t>(); pa.store_used = t->store_used; pa.cursor = cursor.as<unsigned long long>();
+    pa.psums = t->psums.as<uint64_t>(); pa.store_used = t->store_used; pa.starts = nstart.as<uint64_t>();
     launch_publish(pa, s);
   }
   if (N > 0) launch_fold_old(t->d, m, t->pslot.as<uint32_t>(), delta.as<uint64_t>(), t->psums.as<uint64_t>(), s);

@@ -11,6 +11,7 @@ OUT = os.path.join(HERE, "libcct.so")
 SOURCES = ["ingest.hip", "canon.hip", "query.hip", "runtime.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
+         "-I", os.path.join(os.path.dirname(HERE), "include"),
          # packed FP32 instructions are kept out of every code object
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
