@@ -7,22 +7,37 @@
 namespace cct {
 
 // ---- unique-path table -------------------------------------------------------
-// One 64-bit word per slot: (tag << 32) | ref.  ref is a path id of the tree's path
-// store, or kEventRef | event index for a path first seen in the current call.
+// One 16-byte entry per slot.  word = (tag << 32) | ref, where ref is a path id of the
+// tree's path store, or kEventRef | event index for a path first seen in the current
+// call; it is claimed with one 64-bit CAS.  info tells where the slot's frames live and
+// how many there are, so a lookup needs one memory round trip: written by the claimer
+// right after its CAS (readers that still see kEmptyInfo fall back to ref).
+struct Slot {
+  uint64_t word;
+  uint64_t info;
+};
 constexpr uint64_t kEmptySlot = ~0ull;
+constexpr uint64_t kEmptyInfo = ~0ull;
 constexpr uint32_t kEventRef = 0x80000000u;
 constexpr uint32_t kRefMask = 0x7FFFFFFFu;
+// info = (first frame << 24) | (in path store << 23) | length; lengths >= kInfoLongLen
+// are stored as kInfoLongLen (their exact length is then read through ref).
+constexpr uint64_t kInfoLongLen = 0x7FFFFF;
+__host__ __device__ inline uint64_t make_info(uint64_t base, bool store, uint64_t len) {
+  return (base << 24) | ((uint64_t)store << 23) | (len < kInfoLongLen ? len : kInfoLongLen);
+}
 
 // ---- ingest tiling -------------------------------------------------------------
 constexpr int kIngestThreads = 1024;    // 16 waves of 64, each with its own tile loop
 constexpr int kWaveEvents = 63;         // max events per wave tile (lane j holds offset j, j <= 63)
 constexpr int kWaveFrames = 64 * 16;    // frames of a wave tile (16 per lane)
-constexpr int kCacheEntries = 1024;     // LDS resolved-path cache entries per workgroup
-constexpr int kCacheWords = 2048;       // LDS resolved-path cache: uint64 sums
+constexpr int kCacheEntries = 2048;     // LDS resolved-path cache entries per workgroup
 
-// ---- counters written by the ingest kernel --------------------------------------
-enum Counter { kCtrNew = 0, kCtrNewFrames = 1, kCtrError = 2, kCtrOverflow = 3, kCtrCount = 8 };
+// ---- counters written by the ingest kernels --------------------------------------
+enum Counter { kCtrNew = 0, kCtrNewFrames = 1, kCtrError = 2, kCtrOverflow = 3, kCtrNewLen = 4,
+               kCtrCount = 8 };
 enum ErrorBits { kErrOffsets = 1 };
+constexpr uint32_t kNoSlot = 0xFFFFFFFFu;  // event not resolved (the call fails or retries)
 
 // ---- path hashing ----------------------------------------------------------------
 // A path's hash is a sum over its frames of a position-dependent term, so partial
@@ -58,18 +73,12 @@ struct IngestArgs {
   // input batch
   const int64_t *off;
   const uint32_t *fr;
-  const uint64_t *w;
   int64_t n_events, n_frames;
-  int32_t m;
-  int32_t tile_events;  // events per wave tile (<= kWaveEvents)
-  int64_t n_tiles;
   // unique-path table
-  uint64_t *slot;
+  Slot *slot;
   uint64_t cap_mask;
   uint64_t hash_mask;   // all ones, except under a forced-collision test setting
-  uint64_t *delta;      // [cap][m] per-call sums
-  uint32_t *new_slots;  // slots claimed in this call, [max_new]
-  uint64_t max_new;
+  uint32_t *slot_of;    // [N] output: table slot of every event
   // the tree's path store (for paths seen in earlier calls)
   const uint32_t *pframes;
   const int64_t *pstart;
@@ -80,6 +89,16 @@ struct IngestArgs {
 
 // Host-side launch wrappers (one translation unit per kernel family).
 void launch_ingest(const IngestArgs &a, int grid, hipStream_t s);
+// Sum metrics [N][m] into delta[slot_of[e]][m] (LDS-privatized per workgroup).
+void launch_aggregate(const uint32_t *slot_of, const uint64_t *w, int64_t n, int32_t m, uint64_t *delta, int grid,
+                      hipStream_t s);
+// List the slots claimed in this call (word ref with kEventRef): new_slots, and into
+// ctr: kCtrNew (count), kCtrNewFrames (sum of padded store lengths), kCtrNewLen (sum
+// of lengths).
+// part: 2 * collect_blocks(cap) words of scratch.
+int64_t collect_blocks(uint64_t cap);
+void launch_collect_new(const Slot *slot, uint64_t cap, const int64_t *off, uint32_t *new_slots,
+                        unsigned long long *ctr, unsigned long long *part, hipStream_t s);
 
 // Path store: path d occupies frames [pstart[d], pstart[d] + round16(plen[d])) of
 // pframes (pstart is a multiple of kStoreAlign, the tail is zero-filled), and its
@@ -93,7 +112,7 @@ __host__ __device__ inline int64_t round_store(int64_t len) {
 struct PublishArgs {
   const int64_t *off;        // batch offsets (frames of new paths come from the batch)
   const uint32_t *fr;
-  uint64_t *slot;
+  Slot *slot;
   const uint32_t *new_slots;
   int64_t n_new;
   int64_t d_old;
@@ -108,7 +127,7 @@ struct PublishArgs {
   int64_t store_used;        // frames already used in the store
   const uint64_t *starts;    // [n_new] exclusive prefix sums of the padded lengths
 };
-void launch_new_lengths(const int64_t *off, const uint64_t *slot, const uint32_t *new_slots, int64_t n,
+void launch_new_lengths(const int64_t *off, const Slot *slot, const uint32_t *new_slots, int64_t n,
                         uint64_t *out, hipStream_t s);
 void launch_publish(const PublishArgs &a, hipStream_t s);
 // Exclusive prefix sums of `rows` rows of C uint64 columns (mod 2^64) into out[0..rows),
@@ -116,9 +135,9 @@ void launch_publish(const PublishArgs &a, hipStream_t s);
 void launch_scan(const uint64_t *in, int64_t rows, int C, uint64_t *blk, uint64_t *out, hipStream_t s);
 void launch_fold_old(int64_t d_old, int32_t m, const uint32_t *pslot, const uint64_t *delta, uint64_t *psums,
                      hipStream_t s);
-void launch_unclaim(uint64_t *slot, uint64_t cap, hipStream_t s);
+void launch_unclaim(Slot *slot, uint64_t cap, hipStream_t s);
 void launch_rehash(const uint32_t *pframes, const int64_t *pstart, const uint32_t *plen, int64_t d,
-                   uint64_t *slot, uint64_t cap_mask, uint64_t hash_mask, uint32_t *pslot, hipStream_t s);
+                   Slot *slot, uint64_t cap_mask, uint64_t hash_mask, uint32_t *pslot, hipStream_t s);
 
 struct CanonArgs {
   int64_t d;             // number of distinct full paths

@@ -1,34 +1,34 @@
 // Ingest: one HBM pass over a CSR batch of call paths that validates the offsets,
-// hashes every path, maps it exactly onto its distinct full path in the unique-path
-// table, and sums its metrics into that path's exclusive sums.
+// hashes every path and maps it exactly onto its distinct full path in the
+// unique-path table (one table slot per distinct path), then a second, light pass
+// sums every event's metrics into its slot.
 //
 // This is the "insert call paths, collapse frames that refer to the same location"
 // and "aggregate metrics within the same context" step of the profiler (Design,
 // "Profiler", "Calling Context Tree"; Overview), done once per distinct full path
-// instead of once per event and per frame: two events land on the same table entry
-// iff their paths are equal frame by frame, which is exactly when the paper's tree
+// instead of once per event and per frame: two events land on the same slot iff
+// their paths are equal frame by frame, which is exactly when the paper's tree
 // insertion would end them on the same node.
 //
-// Work decomposition: one workgroup of 16 waves per CU, persistent.  Every wave owns a
-// contiguous range of events and cuts it into tiles that fill its 1024-frame LDS
-// slice (at most 63 events: lane j holds offset j), without workgroup barriers, so a
-// CU keeps 16 tiles in flight.  While a wave resolves tile t, the frames of tile t+1
-// stream into registers.  Lane l holds the 16-byte groups l, l + 64, l + 128,
-// l + 192 of a tile, so every load instruction reads 1 KiB of consecutive frames
-// (fully coalesced HBM stream) and every LDS access of a wave hits distinct banks.
+// Work decomposition of the hashing pass: one workgroup of 16 waves per CU,
+// persistent.  Every wave owns a contiguous range of events and cuts it into tiles
+// that fill its 1024-frame LDS slice (at most 63 events: lane j holds offset j),
+// without workgroup barriers, so a CU keeps 16 tiles in flight.  While a wave
+// resolves tile t, the frames of tile t+1 stream into registers.  Lane l holds the
+// 16-byte groups l, l + 64, l + 128, l + 192 of a tile, so every load instruction
+// reads 1 KiB of consecutive frames (a fully coalesced HBM stream) and every LDS
+// access of a wave hits distinct banks.
 //   - hash: each lane sums a position-dependent term over its four runs of four
 //     frames; partial sums per event meet in LDS (64-bit LDS atomics).  The hash is a
 //     sum of terms, so partial sums over any split of a path combine by adding.  The
 //     walk also records each frame's event.
 //   - dedup: lane j resolves event j: a path with the same hash and length already
-//     resolved in this workgroup (LDS cache), else the table (linear probing, one
+//     resolved in this workgroup (LDS cache), else the table (linear probing over
+//     16-byte slots that carry the candidate's location, so one round trip; one
 //     64-bit CAS claims an empty slot).  Every candidate is verified frame by frame:
 //     lane l compares staged frames l, l + 64, ... with the candidate's frames, so
 //     each load instruction reads 64 consecutive frames (L2/MALL resident: hot paths
 //     are few).
-//   - metrics: summed into the cache entry of the path (LDS atomics) and flushed to
-//     HBM with 64-bit atomics once per workgroup; paths outside the cache add to HBM
-//     directly.
 #include "common.h"
 
 namespace cct {
@@ -41,43 +41,38 @@ enum : int32_t { kTileFast = 0, kTileSlow = 1, kTileBad = 2, kTileNone = 3 };
 
 constexpr int kWaves = kIngestThreads / 64;
 constexpr uint32_t kNotReady = 0xFFFFFFFFu;
-constexpr uint64_t kInStore = 1ull << 63;   // cache cbase: frames live in the path store
+constexpr uint64_t kInStore = 1ull << 63;   // candidate base: frames live in the path store
+constexpr uint64_t kRelVerify = 1ull << 62, kRelStore = 1ull << 61, kRelBias = kWaveFrames;
+constexpr uint64_t kRelMask = kRelStore - 1;
 
 struct WaveShared {
   uint32_t fr[kWaveFrames];        // staged frames: slot x <-> relative position x - lead
   uint8_t evt[kWaveFrames];        // event of each staged slot
+  uint8_t gmap[kWaveFrames / 4];   // event containing the first position of each 4-slot group
   int32_t ls[kWaveEvents + 1];     // event starts relative to the tile's first frame
   int32_t bad[kWaveEvents + 1];    // verification found a differing frame
   uint64_t hacc[kWaveEvents + 1];  // hash partial sums
-  uint64_t vaddr[kWaveEvents + 1]; // byte address of the candidate frame at relative position 0, or 0
+  uint64_t vrel[kWaveEvents + 1];  // candidate frame index at relative position 0 (+ kRelBias), with
+                                   // kRelVerify / kRelStore flags; 0: nothing to verify
 };
 
-// Per-workgroup cache of resolved paths, keyed by (hash, length): the table slot,
-// where that slot's frames live (to verify against) and this workgroup's metric sums
-// for it.  Hot paths cost no table access after their first resolution in a
-// workgroup, and one global atomic per metric per workgroup at the end.
+// Per-workgroup cache of resolved paths, keyed by (hash, length): the table slot and
+// where that slot's frames live (to verify against).  Hot paths cost no table access
+// after their first resolution in a workgroup.
 struct IngestShared {
   uint64_t ckey[kCacheEntries];    // hash (0: empty / not cacheable)
   uint64_t cbase[kCacheEntries];   // first frame (kInStore: in the path store)
   uint32_t clen[kCacheEntries];
   uint32_t cslot[kCacheEntries];   // kNotReady until the entry is filled in
-  uint64_t csum[kCacheWords];      // [entries][m]
   WaveShared wv[kWaves];
 };
 
+// Orders this wave's LDS accesses: every lane's earlier LDS writes are visible to
+// every lane's later LDS reads.  Waits for LDS operations only (lgkmcnt), so global
+// loads in flight keep streaming.
 __device__ inline void wave_sync() {
-  // orders this wave's LDS accesses: every lane's earlier LDS writes are visible to
-  // every lane's later LDS reads
-  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
   __builtin_amdgcn_wave_barrier();
-}
-
-__device__ inline int cache_entries(int m) {
-  int e = kCacheWords / m;
-  if (e > kCacheEntries) e = kCacheEntries;
-  int p = 1;
-  while (p * 2 <= e) p *= 2;
-  return p;
 }
 
 __device__ inline uint64_t wave_sum_u64(uint64_t v) {
@@ -171,10 +166,10 @@ struct Probe {
 
 // Walk the probe sequence until the event claims an empty slot (resolved, new path)
 // or meets a slot whose tag and length match (candidate, needs verification).
-// Every event probes at most `capacity` slots over all its rounds: past the load
-// limit the table may be full, and the event then gives up (overflow).  Slot words
-// are read through the caches: a stale empty word only leads to a CAS, which sees the
-// true word.
+// Every event probes at most `capacity` slots over all its rounds: a full table makes
+// the event give up (overflow; the host retries with a larger table).  Slots are read
+// through the caches: a stale empty word only leads to a CAS, which sees the true
+// word.
 __device__ __forceinline__ void probe(const IngestArgs &a, Probe &p, int64_t ev, int64_t ev_start, int64_t len) {
   const uint32_t tag = (uint32_t)(p.h >> 32);
   for (;;) {
@@ -183,34 +178,38 @@ __device__ __forceinline__ void probe(const IngestArgs &a, Probe &p, int64_t ev,
       p.state = kFailed;
       return;
     }
-    uint64_t w = a.slot[p.slot];
+    Slot *sl = a.slot + p.slot;
+    uint64_t w = sl->word, info = sl->info;
     if (w == kEmptySlot) {
       const uint64_t mine = ((uint64_t)tag << 32) | (kEventRef | (uint32_t)ev);
-      const uint64_t prev = atomicCAS((unsigned long long *)&a.slot[p.slot], (unsigned long long)kEmptySlot,
+      const uint64_t prev = atomicCAS((unsigned long long *)&sl->word, (unsigned long long)kEmptySlot,
                                       (unsigned long long)mine);
       if (prev == kEmptySlot) {
-        const unsigned long long k = atomicAdd(&a.ctr[kCtrNew], 1ull);
-        if (k < a.max_new) a.new_slots[k] = (uint32_t)p.slot;
-        else atomicOr(&a.ctr[kCtrOverflow], 1ull);
-        atomicAdd(&a.ctr[kCtrNewFrames], (unsigned long long)len);
+        sl->info = make_info((uint64_t)ev_start, false, (uint64_t)len);
         p.cbase = (uint64_t)ev_start;
         p.state = kResolved;
         return;
       }
       w = prev;
+      info = kEmptyInfo;
     }
     if ((uint32_t)(w >> 32) == tag) {
-      const uint32_t ref = (uint32_t)w;
       int64_t clen;
       uint64_t cbase;
-      if (ref & kEventRef) {
-        const int64_t e = ref & kRefMask;
-        const int64_t s = a.off[e];
-        clen = a.off[e + 1] - s;
-        cbase = (uint64_t)s;
+      if (info != kEmptyInfo && (info & kInfoLongLen) != kInfoLongLen) {
+        clen = (int64_t)(info & kInfoLongLen);
+        cbase = (info >> 24) | (((info >> 23) & 1) ? kInStore : 0);
       } else {
-        clen = a.plen[ref];
-        cbase = (uint64_t)a.pstart[ref] | kInStore;
+        const uint32_t ref = (uint32_t)w;
+        if (ref & kEventRef) {
+          const int64_t e = ref & kRefMask;
+          const int64_t s = a.off[e];
+          clen = a.off[e + 1] - s;
+          cbase = (uint64_t)s;
+        } else {
+          clen = a.plen[ref];
+          cbase = (uint64_t)a.pstart[ref] | kInStore;
+        }
       }
       if (clen == len) {
         p.cbase = cbase;
@@ -223,49 +222,38 @@ __device__ __forceinline__ void probe(const IngestArgs &a, Probe &p, int64_t ev,
 }
 
 // Cache entry holding a resolved path with this hash and length, or -1.
-__device__ inline int cache_find(const IngestShared &S, uint64_t h, uint32_t len, int entries) {
+__device__ inline int cache_find(const IngestShared &S, uint64_t h, uint32_t len) {
   if (h == 0) return -1;
-  uint32_t k = (uint32_t)h & (uint32_t)(entries - 1);
+  uint32_t k = (uint32_t)h & (uint32_t)(kCacheEntries - 1);
   for (int t = 0; t < 8; ++t) {
     const uint64_t key = S.ckey[k];
     if (key == 0) return -1;
     if (key == h && S.cslot[k] != kNotReady && S.clen[k] == len) return (int)k;
-    k = (k + 1) & (uint32_t)(entries - 1);
+    k = (k + 1) & (uint32_t)(kCacheEntries - 1);
   }
   return -1;
 }
 
-// Cache entry for a path just resolved to `slot`: the existing entry for it, a new
-// one, or -1 (window full, or an entry for the same hash is not ready / names
-// another slot: the caller then adds its metrics straight to HBM).
-__device__ inline int cache_insert(IngestShared &S, uint64_t h, uint32_t len, uint32_t slot, uint64_t cbase,
-                                   int entries) {
-  if (h == 0) return -1;
-  uint32_t k = (uint32_t)h & (uint32_t)(entries - 1);
+// Remember a path just resolved to `slot` (unless its probe window is full, or an
+// entry for the same hash and length names another path).
+__device__ inline void cache_insert(IngestShared &S, uint64_t h, uint32_t len, uint32_t slot, uint64_t cbase) {
+  if (h == 0) return;
+  uint32_t k = (uint32_t)h & (uint32_t)(kCacheEntries - 1);
   for (int t = 0; t < 8; ++t) {
     const uint64_t prev = atomicCAS((unsigned long long *)&S.ckey[k], 0ull, (unsigned long long)h);
     if (prev == 0) {
       S.cbase[k] = cbase;
       S.clen[k] = len;
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // payload before the ready slot id
       S.cslot[k] = slot;
-      return (int)k;
+      return;
     }
     if (prev == h) {
       const uint32_t cs = S.cslot[k];
-      if (cs == kNotReady) return -1;
-      if (cs == slot) return (int)k;
-      if (S.clen[k] == len) return -1;  // same hash and length, another path
+      if (cs == kNotReady || cs == slot || S.clen[k] == len) return;
     }
-    k = (k + 1) & (uint32_t)(entries - 1);
+    k = (k + 1) & (uint32_t)(kCacheEntries - 1);
   }
-  return -1;
-}
-
-// Add one event's metric into its cache entry or straight into HBM.
-__device__ inline void add_metric(const IngestArgs &a, IngestShared &S, int ci, uint64_t slot, int c, uint64_t v) {
-  if (ci >= 0) atomicAdd((unsigned long long *)&S.csum[ci * a.m + c], (unsigned long long)v);
-  else atomicAdd((unsigned long long *)&a.delta[slot * a.m + c], (unsigned long long)v);
 }
 
 // Tiles whose frames exceed a wave's staging capacity: one event at a time, the
@@ -280,7 +268,6 @@ __device__ __forceinline__ void slow_wave_tile(const IngestArgs &a, int64_t e0, 
     Probe p{};
     p.h = finish_hash(acc, (uint64_t)len) & a.hash_mask;
     p.slot = (uint32_t)(p.h & a.cap_mask);
-    p.len = (uint32_t)len;  // compared with candidate lengths below as 64-bit
     p.state = kProbing;
     for (;;) {
       if (lane == 0) probe(a, p, e0 + j, gs, len);
@@ -297,11 +284,8 @@ __device__ __forceinline__ void slow_wave_tile(const IngestArgs &a, int64_t e0, 
         break;
       }
     }
-    if (p.state == kResolved) {
-      const uint64_t slot = (uint64_t)shfl_i64((int64_t)p.slot, 0);
-      if (lane < a.m) atomicAdd((unsigned long long *)&a.delta[slot * a.m + lane],
-                                (unsigned long long)a.w[(e0 + j) * a.m + lane]);
-    }
+    const uint32_t slot = (uint32_t)__shfl((int)p.slot, 0, 64);
+    if (lane == 0) a.slot_of[e0 + j] = p.state == kResolved ? slot : kNoSlot;
   }
 }
 
@@ -319,20 +303,18 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
   __shared__ IngestShared S;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   WaveShared &W = S.wv[wave];
-  const int m = a.m;
-  const int entries = cache_entries(m);
   for (int i = tid; i < kCacheEntries; i += kIngestThreads) { S.ckey[i] = 0; S.cslot[i] = kNotReady; }
-  for (int i = tid; i < kCacheWords; i += kIngestThreads) S.csum[i] = 0;
   __syncthreads();
 
-  // this wave's events
+  // this wave's events.  Pipeline: the offsets window of tile t+1 is loaded during
+  // tile t-1, so tile t+1's frames can be requested as soon as tile t starts.
   const int64_t waves_total = (int64_t)gridDim.x * kWaves, w = (int64_t)blockIdx.x * kWaves + wave;
   const int64_t end = (w + 1) * a.n_events / waves_total;
-  int64_t e_cur = w * a.n_events / waves_total;
-  int64_t o_cur = load_window(a, e_cur, end, lane);
-  Tile t = make_tile(a, e_cur, end, o_cur, lane);
+  int64_t o_cur = load_window(a, w * a.n_events / waves_total, end, lane);
+  Tile t = make_tile(a, w * a.n_events / waves_total, end, o_cur, lane);
   u32x4 nf[4];
   load_frames(a, t, lane, nf);
+  int64_t o_nxt = t.kind == kTileFast || t.kind == kTileSlow ? load_window(a, t.e0 + t.ne, end, lane) : 0;
 
   for (int iter = 0; t.kind != kTileNone; ++iter) {
     // early exit after a table overflow (the host retries); checked now and then, as
@@ -345,24 +327,47 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
     const int64_t e_nxt = t.e0 + t.ne;
     if (t.kind == kTileSlow) {
       slow_wave_tile(a, t.e0, t.ne, o_cur);
-      e_cur = e_nxt;
-      o_cur = load_window(a, e_cur, end, lane);
-      t = make_tile(a, e_cur, end, o_cur, lane);
+      o_cur = o_nxt;
+      t = make_tile(a, e_nxt, end, o_cur, lane);
       load_frames(a, t, lane, nf);
+      o_nxt = t.kind == kTileFast || t.kind == kTileSlow ? load_window(a, t.e0 + t.ne, end, lane) : 0;
       continue;
     }
     const int ne = t.ne, span = t.span, lead = t.lead;
     const int64_t e0 = t.e0;
-    const int nm = ne * m;
-    // stage the current frames; the next offsets window and this tile's metrics are
-    // on their way while the tile is hashed
 #pragma unroll
     for (int q = 0; q < 4; ++q) *(u32x4 *)&W.fr[q * 256 + lane * 4] = nf[q];
+    // event starts, and the group map: the event containing the first position of
+    // every 4-slot group.  Event j is written to the first group that starts at or
+    // after it, by the last event to map there (one writer per byte); a running max
+    // then fills the groups in between.
+    *(uint32_t *)&W.gmap[lane * 4] = 0;
     if (lane <= ne) W.ls[lane] = (int32_t)(o_cur - t.g0);
-    if (lane < ne) W.hacc[lane] = 0;
-    const int64_t o_nxt = load_window(a, e_nxt, end, lane);
-    const uint64_t mv0 = lane < nm ? a.w[e0 * m + lane] : 0;
-    const uint64_t mv1 = lane + 64 < nm ? a.w[e0 * m + lane + 64] : 0;
+    {
+      const int g = ((int)(o_cur - t.g0) + lead + 3) >> 2;
+      const int gn = __shfl_down(g, 1, 64);
+      wave_sync();
+      if (lane < ne) {
+        W.hacc[lane] = 0;
+        if (g < kWaveFrames / 4 && (lane == ne - 1 || gn != g)) W.gmap[g] = (uint8_t)lane;
+      }
+    }
+    wave_sync();
+    {
+      const uint32_t pk = *(const uint32_t *)&W.gmap[lane * 4];
+      uint32_t b0 = pk & 0xFF, b1 = max(b0, (pk >> 8) & 0xFF), b2 = max(b1, (pk >> 16) & 0xFF),
+               b3 = max(b2, pk >> 24);
+      uint32_t run = b3;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t u = __shfl_up(run, o, 64);
+        if (lane >= o) run = max(run, u);
+      }
+      uint32_t before = __shfl_up(run, 1, 64);
+      if (lane == 0) before = 0;
+      b0 = max(b0, before); b1 = max(b1, before); b2 = max(b2, before); b3 = max(b3, before);
+      *(uint32_t *)&W.gmap[lane * 4] = b0 | b1 << 8 | b2 << 16 | b3 << 24;
+    }
     wave_sync();
 
     // A2: hash.  Four runs of four frames per lane: slots 256 q + 4 lane .. + 4.
@@ -371,7 +376,7 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
       const int r0 = q * 256 + lane * 4 - lead;
       if (r0 + 4 > 0 && r0 < span) {
         const u32x4 v = *(const u32x4 *)&W.fr[q * 256 + lane * 4];
-        int cur = event_at(W, ne, r0 < 0 ? 0 : r0), cs = W.ls[cur], nx = W.ls[cur + 1];
+        int cur = W.gmap[q * 64 + lane], cs = W.ls[cur], nx = W.ls[cur + 1];
         uint64_t acc = 0;
         uint32_t ev4 = 0;
 #pragma unroll
@@ -392,49 +397,66 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
         *(uint32_t *)&W.evt[q * 256 + lane * 4] = ev4;
       }
     }
-    // the next tile's frames stream in while this tile resolves
+    wave_sync();
+
+    // the next tile's frames, and the offsets window after it, stream in while this
+    // tile resolves
     const Tile tn = make_tile(a, e_nxt, end, o_nxt, lane);
     load_frames(a, tn, lane, nf);
-    wave_sync();
+    const int64_t o_nn = tn.kind == kTileFast || tn.kind == kTileSlow ? load_window(a, tn.e0 + tn.ne, end, lane) : 0;
 
     // A3: exact dedup.  Lane j resolves event j: a cached resolution of the same hash
     // and length, else the table; every candidate is verified by all lanes.
     Probe p{};
     p.state = kResolved;
-    int ci = -1;  // cache entry of the candidate (-2: a cached candidate failed)
+    bool cached = false;  // the candidate came from the cache (no re-insert needed)
     if (lane < ne) {
       p.len = (uint32_t)(W.ls[lane + 1] - W.ls[lane]);
       p.h = finish_hash(W.hacc[lane], (uint64_t)p.len) & a.hash_mask;
       p.slot = (uint32_t)(p.h & a.cap_mask);
       p.state = kProbing;
-      ci = cache_find(S, p.h, p.len, entries);
+      const int ci = cache_find(S, p.h, p.len);
       if (ci >= 0) {
         p.slot = S.cslot[ci];
         p.cbase = S.cbase[ci];
         p.state = p.len == 0 ? kResolved : kCandidate;
+        cached = true;
       }
     }
     for (;;) {
       if (p.state == kProbing) probe(a, p, e0 + lane, o_cur, (int64_t)p.len);
       if (!__any(p.state == kCandidate)) break;
       if (lane < ne) {
-        uint64_t va = 0;
-        if (p.state == kCandidate) {
-          const uint32_t *src = (p.cbase & kInStore) ? a.pframes + (p.cbase & ~kInStore) : a.fr + p.cbase;
-          va = (uint64_t)(uintptr_t)src - 4ull * (uint64_t)W.ls[lane];
-        }
-        W.vaddr[lane] = va;
+        uint64_t v = 0;
+        if (p.state == kCandidate)
+          v = kRelVerify | ((p.cbase & kInStore) ? kRelStore : 0) |
+              ((p.cbase & ~kInStore) + kRelBias - (uint64_t)W.ls[lane]);
+        W.vrel[lane] = v;
         W.bad[lane] = 0;
       }
       wave_sync();
-      // lane l checks staged slots l, l + 64, ...: 64 consecutive frames per load
+      // lane l checks staged slots l, l + 64, ...: every load instruction reads 64
+      // consecutive frames.  Addresses are formed without branches and the loads are
+      // issued in two batches of eight, so a tile costs two round trips.
 #pragma unroll
-      for (int i = 0; i < kWaveFrames / 64; ++i) {
-        const int x = i * 64 + lane, r = x - lead;
-        if (r >= 0 && r < span) {
-          const int e = W.evt[x];
-          const uint64_t va = W.vaddr[e];
-          if (va && *(const uint32_t *)(uintptr_t)(va + 4ull * (uint64_t)r) != W.fr[x]) W.bad[e] = 1;
+      for (int h = 0; h < 4; ++h) {
+        uint32_t cand[4];
+        uint32_t act = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int x = (h * 4 + i) * 64 + lane, r = x - lead;
+          const bool in = r >= 0 && r < span;
+          const uint64_t v = W.vrel[W.evt[x] & kWaveEvents];  // slots outside the span hold stale events
+          const bool chk = in && (v & kRelVerify);
+          const uint32_t *src = (v & kRelStore) ? a.pframes : a.fr;
+          cand[i] = 0;
+          if (chk) cand[i] = src[(v & kRelMask) - kRelBias + (uint64_t)r];
+          act |= (uint32_t)chk << i;
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int x = (h * 4 + i) * 64 + lane;
+          if (((act >> i) & 1u) && cand[i] != W.fr[x]) W.bad[W.evt[x]] = 1;
         }
       }
       wave_sync();
@@ -442,58 +464,151 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
         if (W.bad[lane]) {
           p.slot = (uint32_t)((p.slot + 1) & a.cap_mask);
           p.state = kProbing;
-          ci = -2;
+          cached = true;  // resolved past a cached path with the same hash: not cacheable
         } else {
           p.state = kResolved;
         }
       }
       wave_sync();
     }
-
-    // exclusive aggregation into the cache entry of the path (HBM atomics when none)
-    int mi = -3;  // -3: nothing to add
-    if (lane < ne && p.state == kResolved) {
-      if (ci == -1) ci = cache_insert(S, p.h, p.len, p.slot, p.cbase, entries);
-      mi = ci < 0 ? -1 : ci;
+    if (lane < ne) {
+      if (p.state == kResolved && !cached) cache_insert(S, p.h, p.len, p.slot, p.cbase);
+      a.slot_of[e0 + lane] = p.state == kResolved ? p.slot : kNoSlot;
     }
-    const uint32_t myslot = p.slot;
-    for (int q0 = 0; q0 < nm; q0 += 64) {  // uniform trip count: every lane takes part in the shuffles
-      const int q = q0 + lane;
-      const int j = min(q / m, ne - 1), c = q - j * m;
-      const int mj = __shfl(mi, j, 64);
-      const uint64_t sj = __shfl(myslot, j, 64);
-      if (q < nm && mj != -3) {
-        const uint64_t v = q < 64 ? mv0 : q < 128 ? mv1 : a.w[e0 * m + q];
-        add_metric(a, S, mj, sj, c, v);
-      }
-    }
-    e_cur = e_nxt;
     o_cur = o_nxt;
+    o_nxt = o_nn;
     t = tn;
   }
+}
 
-  // flush the cached sums
+// Metric sums per slot: one persistent workgroup per CU walks a contiguous event
+// range and sums into an LDS map keyed by slot (a hot path costs one HBM atomic per
+// metric per workgroup), falling back to HBM atomics when a key's probe window is
+// full.  A key already in the map is found with plain LDS reads (broadcast), so hot
+// keys cost no atomic compare-and-swap.
+constexpr int kAggThreads = 1024;
+constexpr int kAggWords = 16384;  // LDS sums (128 KiB)
+constexpr int kAggKeys = 8192;
+constexpr uint32_t kEmptyKey = 0xFFFFFFFFu;
+
+__global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const uint32_t *slot_of, const uint64_t *w, int64_t n,
+                                                                int32_t m, uint64_t *delta) {
+  __shared__ uint32_t key[kAggKeys];
+  __shared__ uint64_t sum[kAggWords];
+  const int tid = threadIdx.x;
+  int entries = kAggWords / m;
+  if (entries > kAggKeys) entries = kAggKeys;
+  int p2 = 1;
+  while (p2 * 2 <= entries) p2 *= 2;
+  entries = p2;
+  for (int i = tid; i < kAggKeys; i += kAggThreads) key[i] = kEmptyKey;
+  for (int i = tid; i < kAggWords; i += kAggThreads) sum[i] = 0;
   __syncthreads();
-  for (int k = tid; k < entries; k += kIngestThreads) {
-    const uint32_t slot = S.cslot[k];
-    if (S.ckey[k] == 0 || slot == kNotReady) continue;
+  const int64_t b = blockIdx.x, nb = gridDim.x;
+  const int64_t lo = b * n / nb, hi = (b + 1) * n / nb;
+  for (int64_t e = lo + tid; e < hi; e += kAggThreads) {
+    const uint32_t s = slot_of[e];
+    if (s == kNoSlot) continue;
+    uint32_t k = hash32(s) & (uint32_t)(entries - 1);
+    int mi = -1;
+    for (int t = 0; t < 8; ++t) {
+      uint32_t cur = key[k];
+      if (cur == kEmptyKey) cur = atomicCAS(&key[k], kEmptyKey, s);
+      if (cur == kEmptyKey || cur == s) { mi = (int)k; break; }
+      k = (k + 1) & (uint32_t)(entries - 1);
+    }
     for (int j = 0; j < m; ++j) {
-      const uint64_t v = S.csum[k * m + j];
-      if (v) atomicAdd((unsigned long long *)&a.delta[(uint64_t)slot * m + j], (unsigned long long)v);
+      const uint64_t v = w[e * m + j];
+      if (mi >= 0) atomicAdd((unsigned long long *)&sum[mi * m + j], (unsigned long long)v);
+      else atomicAdd((unsigned long long *)&delta[(uint64_t)s * m + j], (unsigned long long)v);
+    }
+  }
+  __syncthreads();
+  for (int k = tid; k < entries; k += kAggThreads) {
+    const uint32_t s = key[k];
+    if (s == kEmptyKey) continue;
+    for (int j = 0; j < m; ++j) {
+      const uint64_t v = sum[k * m + j];
+      if (v) atomicAdd((unsigned long long *)&delta[(uint64_t)s * m + j], (unsigned long long)v);
     }
   }
 }
 
+// Slots claimed in this call: a block of 1024 threads scans 4096 slots, counts its
+// claims, reserves list positions with one atomic, and writes them (the list order
+// is irrelevant: paths get their canonical ids later).  Lengths come from the slot's
+// info word; per-block sums of padded and exact lengths go to part[block][2].
+constexpr int kCollectThreads = 1024, kCollectPerThread = 4;
+__global__ __launch_bounds__(kCollectThreads) void collect_new_kernel(const Slot *slot, uint64_t cap,
+                                                                      const int64_t *off, uint32_t *new_slots,
+                                                                      unsigned long long *ctr,
+                                                                      unsigned long long *part) {
+  __shared__ uint32_t cnt;
+  __shared__ unsigned long long base, frames, lens;
+  if (threadIdx.x == 0) { cnt = 0; frames = 0; lens = 0; }
+  __syncthreads();
+  uint32_t found[kCollectPerThread], pos[kCollectPerThread];
+  uint64_t my_frames = 0, my_lens = 0;
+  int nf = 0;
+  for (int r = 0; r < kCollectPerThread; ++r) {
+    const uint64_t s = ((uint64_t)blockIdx.x * kCollectPerThread + r) * kCollectThreads + threadIdx.x;
+    if (s >= cap) break;
+    const Slot sl = slot[s];
+    if (sl.word != kEmptySlot && ((uint32_t)sl.word & kEventRef)) {
+      int64_t len;
+      if (sl.info != kEmptyInfo && (sl.info & kInfoLongLen) != kInfoLongLen) {
+        len = (int64_t)(sl.info & kInfoLongLen);
+      } else {
+        const int64_t e = (int64_t)((uint32_t)sl.word & kRefMask);
+        len = off[e + 1] - off[e];
+      }
+      found[nf] = (uint32_t)s;
+      pos[nf] = atomicAdd(&cnt, 1u);
+      ++nf;
+      my_frames += (uint64_t)round_store(len);
+      my_lens += (uint64_t)len;
+    }
+  }
+  if (nf) {
+    atomicAdd(&frames, (unsigned long long)my_frames);
+    atomicAdd(&lens, (unsigned long long)my_lens);
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    base = cnt ? atomicAdd(&ctr[kCtrNew], (unsigned long long)cnt) : 0;
+    part[blockIdx.x * 2] = frames;
+    part[blockIdx.x * 2 + 1] = lens;
+  }
+  __syncthreads();
+  for (int i = 0; i < nf; ++i) new_slots[base + pos[i]] = found[i];
+}
+
+// Totals of the per-block length sums into ctr (one block).
+__global__ __launch_bounds__(256) void collect_sum_kernel(const unsigned long long *part, int64_t nblk,
+                                                          unsigned long long *ctr) {
+  __shared__ unsigned long long sf[256], sl[256];
+  unsigned long long f = 0, l = 0;
+  for (int64_t i = threadIdx.x; i < nblk; i += 256) { f += part[i * 2]; l += part[i * 2 + 1]; }
+  sf[threadIdx.x] = f;
+  sl[threadIdx.x] = l;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if ((int)threadIdx.x < o) { sf[threadIdx.x] += sf[threadIdx.x + o]; sl[threadIdx.x] += sl[threadIdx.x + o]; }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) { ctr[kCtrNewFrames] = sf[0]; ctr[kCtrNewLen] = sl[0]; }
+}
+
 // Publish the paths first seen in this call: give each a path id, copy its frames
 // into the tree's path store (16-frame aligned, zero tail), write its checkpoint
-// hashes and exclusive sums, and point its table slot at the path id.  One wave per
-// path.
+// hashes and exclusive sums, and point its table slot at the path id and the stored
+// frames.  One wave per path.
 __global__ __launch_bounds__(256) void publish_kernel(PublishArgs a) {
   const int lane = threadIdx.x & 63;
   const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   if (i >= a.n_new) return;
   const uint32_t s = a.new_slots[i];
-  const uint64_t w = a.slot[s];
+  const uint64_t w = a.slot[s].word;
   const int64_t e = (int64_t)((uint32_t)w & kRefMask);
   const int64_t src = a.off[e], len = a.off[e + 1] - src;
   const int64_t rl = round_store(len);
@@ -525,17 +640,18 @@ __global__ __launch_bounds__(256) void publish_kernel(PublishArgs a) {
     a.pstart[id] = start;
     a.plen[id] = (uint32_t)len;
     a.pslot[id] = s;
-    a.slot[s] = (w & 0xFFFFFFFF00000000ull) | (uint64_t)id;
+    a.slot[s].word = (w & 0xFFFFFFFF00000000ull) | (uint64_t)id;
+    a.slot[s].info = make_info((uint64_t)start, true, (uint64_t)len);
   }
   if (lane < a.m) a.psums[id * a.m + lane] = a.delta[(uint64_t)s * a.m + lane];
 }
 
 // Padded store length of every new path (input of the scan that places them).
-__global__ void new_lengths_kernel(const int64_t *off, const uint64_t *slot, const uint32_t *new_slots, int64_t n,
+__global__ void new_lengths_kernel(const int64_t *off, const Slot *slot, const uint32_t *new_slots, int64_t n,
                                    uint64_t *out) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
-  const int64_t e = (int64_t)((uint32_t)slot[new_slots[i]] & kRefMask);
+  const int64_t e = (int64_t)((uint32_t)slot[new_slots[i]].word & kRefMask);
   out[i] = (uint64_t)round_store(off[e + 1] - off[e]);
 }
 
@@ -548,17 +664,20 @@ __global__ void fold_old_kernel(int64_t d_old, int32_t m, const uint32_t *pslot,
 }
 
 // Roll back every slot claimed in the current call (after an error or overflow).
-__global__ void unclaim_kernel(uint64_t *slot, uint64_t cap) {
+__global__ void unclaim_kernel(Slot *slot, uint64_t cap) {
   const uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= cap) return;
-  const uint64_t w = slot[t];
-  if (w != kEmptySlot && ((uint32_t)w & kEventRef)) slot[t] = kEmptySlot;
+  const uint64_t w = slot[t].word;
+  if (w != kEmptySlot && ((uint32_t)w & kEventRef)) {
+    slot[t].word = kEmptySlot;
+    slot[t].info = kEmptyInfo;
+  }
 }
 
 // Re-insert the stored paths into a larger, empty table (distinct paths: no
 // verification needed, each claims the first empty slot of its probe sequence).
 __global__ void rehash_kernel(const uint32_t *pframes, const int64_t *pstart, const uint32_t *plen, int64_t d,
-                              uint64_t *slot, uint64_t cap_mask, uint64_t hash_mask, uint32_t *pslot) {
+                              Slot *slot, uint64_t cap_mask, uint64_t hash_mask, uint32_t *pslot) {
   const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (id >= d) return;
   const int64_t st = pstart[id];
@@ -568,9 +687,10 @@ __global__ void rehash_kernel(const uint32_t *pframes, const int64_t *pstart, co
   const uint64_t h = finish_hash(acc, len) & hash_mask;
   const uint64_t word = (h & 0xFFFFFFFF00000000ull) | (uint64_t)id;
   uint64_t s = h & cap_mask;
-  while (atomicCAS((unsigned long long *)&slot[s], (unsigned long long)kEmptySlot, (unsigned long long)word) !=
+  while (atomicCAS((unsigned long long *)&slot[s].word, (unsigned long long)kEmptySlot, (unsigned long long)word) !=
          kEmptySlot)
     s = (s + 1) & cap_mask;
+  slot[s].info = make_info((uint64_t)st, true, len);
   pslot[id] = (uint32_t)s;
 }
 
@@ -581,8 +701,22 @@ inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1)
 void launch_ingest(const IngestArgs &a, int grid, hipStream_t s) {
   hipLaunchKernelGGL(ingest_kernel, dim3(grid), dim3(kIngestThreads), 0, s, a);
 }
-void launch_new_lengths(const int64_t *off, const uint64_t *slot, const uint32_t *new_slots, int64_t n,
-                        uint64_t *out, hipStream_t s) {
+void launch_aggregate(const uint32_t *slot_of, const uint64_t *w, int64_t n, int32_t m, uint64_t *delta, int grid,
+                      hipStream_t s) {
+  if (n <= 0) return;
+  hipLaunchKernelGGL(aggregate_kernel, dim3(grid), dim3(kAggThreads), 0, s, slot_of, w, n, m, delta);
+}
+int64_t collect_blocks(uint64_t cap) { return (int64_t)((cap + kCollectThreads * kCollectPerThread - 1) /
+                                                         (kCollectThreads * kCollectPerThread)); }
+void launch_collect_new(const Slot *slot, uint64_t cap, const int64_t *off, uint32_t *new_slots,
+                        unsigned long long *ctr, unsigned long long *part, hipStream_t s) {
+  const int64_t nb = collect_blocks(cap);
+  hipLaunchKernelGGL(collect_new_kernel, dim3((unsigned)nb), dim3(kCollectThreads), 0, s, slot, cap, off, new_slots,
+                     ctr, part);
+  hipLaunchKernelGGL(collect_sum_kernel, dim3(1), dim3(256), 0, s, part, nb, ctr);
+}
+void launch_new_lengths(const int64_t *off, const Slot *slot, const uint32_t *new_slots, int64_t n, uint64_t *out,
+                        hipStream_t s) {
   if (n <= 0) return;
   hipLaunchKernelGGL(new_lengths_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, off, slot, new_slots, n, out);
 }
@@ -596,11 +730,11 @@ void launch_fold_old(int64_t d_old, int32_t m, const uint32_t *pslot, const uint
   hipLaunchKernelGGL(fold_old_kernel, dim3(blocks_for(d_old * m, 256)), dim3(256), 0, s, d_old, m, pslot, delta,
                      psums);
 }
-void launch_unclaim(uint64_t *slot, uint64_t cap, hipStream_t s) {
+void launch_unclaim(Slot *slot, uint64_t cap, hipStream_t s) {
   hipLaunchKernelGGL(unclaim_kernel, dim3(blocks_for((int64_t)cap, 256)), dim3(256), 0, s, slot, cap);
 }
-void launch_rehash(const uint32_t *pframes, const int64_t *pstart, const uint32_t *plen, int64_t d,
-                   uint64_t *slot, uint64_t cap_mask, uint64_t hash_mask, uint32_t *pslot, hipStream_t s) {
+void launch_rehash(const uint32_t *pframes, const int64_t *pstart, const uint32_t *plen, int64_t d, Slot *slot,
+                   uint64_t cap_mask, uint64_t hash_mask, uint32_t *pslot, hipStream_t s) {
   if (d <= 0) return;
   hipLaunchKernelGGL(rehash_kernel, dim3(blocks_for(d, 256)), dim3(256), 0, s, pframes, pstart, plen, d, slot,
                      cap_mask, hash_mask, pslot);

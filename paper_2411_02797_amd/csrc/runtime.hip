@@ -239,13 +239,13 @@ struct Timer {
 // Re-insert the tree's stored paths into a fresh table of capacity `cap`.
 cct_status rehash(cct_tree *t, uint64_t cap, uint64_t hash_mask, hipStream_t s) {
   Buf ns;
-  if (!ns.alloc(cap * 8)) return fail(CCT_ENOMEM, "device allocation failed");
-  HIP_TRY(hipMemsetAsync(ns.p, 0xFF, cap * 8, s));
+  if (!ns.alloc(cap * sizeof(Slot))) return fail(CCT_ENOMEM, "device allocation failed");
+  HIP_TRY(hipMemsetAsync(ns.p, 0xFF, cap * sizeof(Slot), s));
   Buf np;
   if (t->d > 0) {
     if (!np.alloc(t->dcap * 4)) return fail(CCT_ENOMEM, "device allocation failed");
     launch_rehash(t->pframes.as<uint32_t>(), t->pstart.as<int64_t>(), t->plen.as<uint32_t>(), t->d,
-                  ns.as<uint64_t>(), cap - 1, hash_mask, np.as<uint32_t>(), s);
+                  ns.as<Slot>(), cap - 1, hash_mask, np.as<uint32_t>(), s);
     HIP_TRY(hipGetLastError());
     t->pslot = std::move(np);
   }
@@ -283,28 +283,27 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   }
 
   // ---- A1-A3: ingest (retry with a larger table on overflow) -------------------------
-  Buf delta, new_slots;
-  uint64_t n_new = 0, new_frames = 0;
+  // keep the table at most half full before inserting
+  if ((uint64_t)t->d * 2 > t->cap) {
+    cct_status st = rehash(t, pow2_at_least((uint64_t)t->d * 4), hash_mask, s);
+    if (st) return st;
+  }
+  Buf delta, new_slots, slot_of, cpart;
+  uint64_t n_new = 0, new_frames = 0, new_store = 0;
   if (N > 0) {
+    if (!slot_of.alloc((size_t)N * 4)) return fail(CCT_ENOMEM, "device allocation failed");
     for (int attempt = 0;; ++attempt) {
       if (attempt > 12) return fail(CCT_EOVERFLOW, "unique-path table cannot grow further");
-      const uint64_t max_new = t->cap / 2 > (uint64_t)t->d ? t->cap / 2 - (uint64_t)t->d : 0;
-      if (max_new == 0) {
-        cct_status st = rehash(t, t->cap * 4, hash_mask, s);
-        if (st) return st;
-        continue;
-      }
-      if (!delta.alloc(t->cap * m * 8) || !new_slots.alloc(max_new * 4))
+      if (!delta.alloc(t->cap * m * 8) || !new_slots.alloc(t->cap * 4) ||
+          !cpart.alloc((size_t)collect_blocks(t->cap) * 16))
         return fail(CCT_ENOMEM, "device allocation failed");
       HIP_TRY(hipMemsetAsync(delta.p, 0, t->cap * m * 8, s));
       HIP_TRY(hipMemsetAsync(dctr, 0, kCtrCount * 8, s));
       IngestArgs a{};
-      a.off = p->offsets; a.fr = p->frames; a.w = p->metrics;
-      a.n_events = N; a.n_frames = p->n_frames; a.m = m;
-      a.tile_events = kWaveEvents;
-      a.n_tiles = (N + kWaveEvents - 1) / kWaveEvents;  // upper bound of the tile count
-      a.slot = t->slot.as<uint64_t>(); a.cap_mask = t->cap - 1; a.hash_mask = hash_mask;
-      a.delta = delta.as<uint64_t>(); a.new_slots = new_slots.as<uint32_t>(); a.max_new = max_new;
+      a.off = p->offsets; a.fr = p->frames;
+      a.n_events = N; a.n_frames = p->n_frames;
+      a.slot = t->slot.as<Slot>(); a.cap_mask = t->cap - 1; a.hash_mask = hash_mask;
+      a.slot_of = slot_of.as<uint32_t>();
       a.pframes = t->pframes.as<uint32_t>(); a.pstart = t->pstart.as<int64_t>(); a.plen = t->plen.as<uint32_t>();
       a.ctr = dctr;
       // one workgroup per CU; every wave owns an equal share of the events
@@ -313,11 +312,15 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
       tm.mark(1, s);
       launch_ingest(a, grid, s);
       tm.mark(2, s);
+      launch_aggregate(a.slot_of, p->metrics, N, m, delta.as<uint64_t>(),
+                       (int)std::max<int64_t>(1, std::min<int64_t>((N + 8191) / 8192, (int64_t)cu_count())), s);
+      launch_collect_new(t->slot.as<Slot>(), t->cap, p->offsets, new_slots.as<uint32_t>(), dctr,
+                         cpart.as<unsigned long long>(), s);
       HIP_TRY(hipGetLastError());
       HIP_TRY(hipMemcpyAsync(hs, dctr, kCtrCount * 8, hipMemcpyDeviceToHost, s));
       HIP_TRY(hipStreamSynchronize(s));
       if (hs[kCtrError] || hs[kCtrOverflow]) {
-        launch_unclaim(t->slot.as<uint64_t>(), t->cap, s);
+        launch_unclaim(t->slot.as<Slot>(), t->cap, s);
         HIP_TRY(hipGetLastError());
         if (hs[kCtrError]) {
           HIP_TRY(hipStreamSynchronize(s));
@@ -328,7 +331,8 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
         continue;
       }
       n_new = hs[kCtrNew];
-      new_frames = hs[kCtrNewFrames];
+      new_frames = hs[kCtrNewLen];
+      new_store = hs[kCtrNewFrames];
       break;
     }
   }
@@ -337,12 +341,12 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   const int64_t D = t->d + (int64_t)n_new;
   const int64_t sum_len = t->sum_len + (int64_t)new_frames;
   auto rollback = [&](cct_status st) {
-    if (n_new) launch_unclaim(t->slot.as<uint64_t>(), t->cap, s);
+    if (n_new) launch_unclaim(t->slot.as<Slot>(), t->cap, s);
     (void)hipStreamSynchronize(s);
     return st;
   };
   if (sum_len + 1 > (int64_t)0xFFFFFFFE) return rollback(fail(CCT_EOVERFLOW, "tree would exceed 2^32-2 nodes"));
-  const int64_t store_need = t->store_used + (int64_t)new_frames + (int64_t)(kStoreAlign - 1) * (int64_t)n_new;
+  const int64_t store_need = t->store_used + (int64_t)new_store;
   const int64_t dneed = std::max<int64_t>(D, 1);
   cct_tree old_arrays_holder;  // receives replaced buffers, released on return
   {
@@ -402,12 +406,12 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   HIP_TRY(hipMemsetAsync(cursor.p, 0, 64, s));
   if (n_new) {
     // place the new paths in the store: exclusive scan of their padded lengths
-    launch_new_lengths(p->offsets, t->slot.as<uint64_t>(), new_slots.as<uint32_t>(), (int64_t)n_new,
+    launch_new_lengths(p->offsets, t->slot.as<Slot>(), new_slots.as<uint32_t>(), (int64_t)n_new,
                        nlen.as<uint64_t>(), s);
     launch_scan(nlen.as<uint64_t>(), (int64_t)n_new, 1, nblkbuf.as<uint64_t>(), nstart.as<uint64_t>(), s);
     HIP_TRY(hipMemcpyAsync(cursor.p, nstart.as<uint64_t>() + n_new, 8, hipMemcpyDeviceToDevice, s));
     PublishArgs pa{};
-    pa.off = p->offsets; pa.fr = p->frames; pa.slot = t->slot.as<uint64_t>();
+    pa.off = p->offsets; pa.fr = p->frames; pa.slot = t->slot.as<Slot>();
     pa.new_slots = new_slots.as<uint32_t>(); pa.n_new = (int64_t)n_new; pa.d_old = t->d; pa.m = m;
     pa.delta = delta.as<uint64_t>(); pa.pframes = t->pframes.as<uint32_t>(); pa.pcp = t->pcp.as<uint64_t>();
     pa.pstart = t->pstart.as<int64_t>(); pa.plen = t->plen.as<uint32_t>(); pa.pslot = t->pslot.as<uint32_t>();
@@ -479,9 +483,9 @@ cct_status cct_build(const cct_paths *events, void *hip_stream, cct_tree **out) 
   int64_t cap = env_int("CCT_TEST_TABLE_CAP", 0);
   if (cap <= 0) cap = (int64_t)std::min<uint64_t>(pow2_at_least((uint64_t)std::max<int64_t>(2 * N, 1024)), 1ull << 21);
   cap = (int64_t)pow2_at_least((uint64_t)std::max<int64_t>(cap, 16));
-  if (!t->slot.alloc(cap * 8)) { delete t; return fail(CCT_ENOMEM, "device allocation failed"); }
+  if (!t->slot.alloc(cap * sizeof(Slot))) { delete t; return fail(CCT_ENOMEM, "device allocation failed"); }
   t->cap = (uint64_t)cap;
-  if (hipMemsetAsync(t->slot.p, 0xFF, cap * 8, s) != hipSuccess) {
+  if (hipMemsetAsync(t->slot.p, 0xFF, cap * sizeof(Slot), s) != hipSuccess) {
     (void)hipGetLastError();
     delete t;
     return fail(CCT_EDEVICE, "memset failed");
