@@ -82,13 +82,25 @@ def main():
     ap.add_argument("--workload", default="layered_16m", choices=sorted(DESCRIPTIONS))
     ap.add_argument("--cpu-sample", type=int, default=1 << 21, help="events timed on the oracle")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibrate", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB five times (the reference kernel that "
+                         "scales the HBM byte counters) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU; multi-GPU sharding is a design note only",
+        print(json.dumps({"error": "bench.py measures one GPU; sharding across GPUs is a design only, nothing here runs on several",
                           "n_gpus": args.gpus}))
         sys.exit(2)
 
     import torch
+    if args.copy_calibrate:
+        n = args.copy_calibrate << 20
+        src = torch.ones(n // 4, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 5}))
+        return
     import tracegen
     import paper_2411_02797_amd as cct
 
@@ -123,10 +135,12 @@ def main():
     log(f"timed {args.steps} steps: {ms:.3f} ms/step; mean phases(ms) ingest/publish/sort/emit/total = "
         f"{['%.3f' % x for x in ph.mean(axis=0)]}")
 
-    # algorithmic bytes: what the method must move (inputs once, every output once)
-    b_in = 8 * (N + 1) + 4 * F + 8 * M * N
-    b_alg = b_in + U * (12 + 16 * M)
-    achieved = b_in / (ingest_ms * 1e-3) / 1e9
+    # algorithmic bytes.  The dominant kernel (ingest: validate, hash, exact dedup) must
+    # read the offsets and every frame once; the whole call must in addition read the
+    # metrics once and write every output array once.
+    b_ingest = 8 * (N + 1) + 4 * F
+    b_alg = b_ingest + 8 * M * N + U * (12 + 16 * M)
+    achieved = b_ingest / (ingest_ms * 1e-3) / 1e9
     traffic = measured_traffic(args.workload)
     line = {
         "metric": METRIC,
@@ -145,8 +159,8 @@ def main():
                    "metrics": M, "distinct_paths": D, "nodes": U},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic,
-                     "kernel": "ingest_kernel (hash + exact dedup + exclusive sums)",
-                     "bytes_per_launch": b_in, "avg_launch_ms": ingest_ms},
+                     "kernel": "ingest_kernel (validate offsets, hash paths, exact dedup into the table)",
+                     "bytes_per_launch": b_ingest, "avg_launch_ms": ingest_ms},
         "effective_hbm_gbps": b_alg / (ms * 1e-3) / 1e9,
         "effective_frac_of_peak": b_alg / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
         "phase_ms": {"ingest": ingest_ms, "publish": float(ph[:, 1].mean()), "sort": float(ph[:, 2].mean()),

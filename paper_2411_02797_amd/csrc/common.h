@@ -31,7 +31,7 @@ __host__ __device__ inline uint64_t make_info(uint64_t base, bool store, uint64_
 constexpr int kIngestThreads = 1024;    // 16 waves of 64, each with its own tile loop
 constexpr int kWaveEvents = 63;         // max events per wave tile (lane j holds offset j, j <= 63)
 constexpr int kWaveFrames = 64 * 16;    // frames of a wave tile (16 per lane)
-constexpr int kCacheEntries = 2048;     // LDS resolved-path cache entries per workgroup
+constexpr int kCacheEntries = 4096;     // LDS resolved-path cache entries per workgroup
 
 // ---- counters written by the ingest kernels --------------------------------------
 enum Counter { kCtrNew = 0, kCtrNewFrames = 1, kCtrError = 2, kCtrOverflow = 3, kCtrNewLen = 4,
@@ -40,13 +40,16 @@ enum ErrorBits { kErrOffsets = 1 };
 constexpr uint32_t kNoSlot = 0xFFFFFFFFu;  // event not resolved (the call fails or retries)
 
 // ---- path hashing ----------------------------------------------------------------
-// A path's hash is a sum over its frames of a position-dependent term, so partial
+// A path's hash is a sum over its frames of a term of (frame, position), so partial
 // sums over any split of the path combine by addition; a murmur3-style finalizer
-// mixes in the length.  Correctness never depends on the hash: every match is
-// verified frame by frame.
+// mixes in the length.  The term is one 32 x 32 -> 64-bit product of two
+// position-dependent mixes of the frame (one multiply-add on CDNA); both factors
+// move with the position, so paths over a few small frame ids still spread.
+// Correctness never depends on the hash: every match is verified frame by frame.
+constexpr uint32_t kTermMulX = 0x9E3779B9u, kTermMulY = 0x85EBCA6Bu, kTermXorY = 0x5BD1E995u;
 __host__ __device__ inline uint64_t frame_term(uint32_t f, uint32_t k) {
-  uint32_t x = f + k * 0x9E3779B9u;
-  uint32_t y = (f ^ 0x5BD1E995u) + k * 0x85EBCA6Bu;
+  const uint32_t x = f + k * kTermMulX;
+  const uint32_t y = (f ^ kTermXorY) + k * kTermMulY;
   return (uint64_t)x * (uint64_t)(y | 1u);
 }
 __host__ __device__ inline uint64_t finish_hash(uint64_t s, uint64_t len) {

@@ -12,23 +12,23 @@
 //
 // Work decomposition of the hashing pass: one workgroup of 16 waves per CU,
 // persistent.  Every wave owns a contiguous range of events and cuts it into tiles
-// that fill its 1024-frame LDS slice (at most 63 events: lane j holds offset j),
-// without workgroup barriers, so a CU keeps 16 tiles in flight.  While a wave
-// resolves tile t, the frames of tile t+1 stream into registers.  Lane l holds the
-// 16-byte groups l, l + 64, l + 128, l + 192 of a tile, so every load instruction
-// reads 1 KiB of consecutive frames (a fully coalesced HBM stream) and every LDS
-// access of a wave hits distinct banks.
-//   - hash: each lane sums a position-dependent term over its four runs of four
-//     frames; partial sums per event meet in LDS (64-bit LDS atomics).  The hash is a
-//     sum of terms, so partial sums over any split of a path combine by adding.  The
-//     walk also records each frame's event.
+// of at most 63 events whose paths, cut into blocks of 16 frames, fill at most its 64
+// lanes: lane l holds one block (16 consecutive frames of one event) in registers,
+// loaded with four 16-byte buffer loads (the buffer's range check makes reads past
+// the end of the batch return zero).  Consecutive lanes hold consecutive blocks, so
+// a wave's loads cover a contiguous stretch of the batch.  Workgroups need no
+// barriers, so a CU keeps 16 tiles in flight; while a wave resolves tile t, the
+// frames of tile t+1 stream into registers.
+//   - hash: a path's hash is a sum over its frames of a term of (frame, position in
+//     the path); a lane sums its block, and the block sums of an event meet in LDS.
+//     A block knows its position in the path, so no lane ever looks for an event
+//     boundary.
 //   - dedup: lane j resolves event j: a path with the same hash and length already
 //     resolved in this workgroup (LDS cache), else the table (linear probing over
 //     16-byte slots that carry the candidate's location, so one round trip; one
 //     64-bit CAS claims an empty slot).  Every candidate is verified frame by frame:
-//     lane l compares staged frames l, l + 64, ... with the candidate's frames, so
-//     each load instruction reads 64 consecutive frames (L2/MALL resident: hot paths
-//     are few).
+//     each block lane compares its 16 frames with the candidate's (16-byte loads; hot
+//     candidates are L2 resident).
 #include "common.h"
 
 namespace cct {
@@ -36,24 +36,25 @@ namespace cct {
 namespace {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef u32x4 u32x4_a4 __attribute__((aligned(4)));
+// global-memory pointers (address space 1), so candidate loads are global loads
+typedef const uint32_t __attribute__((address_space(1))) *gptr;
+typedef const u32x4_a4 __attribute__((address_space(1))) *gptr4;
 enum : int32_t { kProbing = 0, kCandidate = 1, kResolved = 2, kFailed = 3 };
 enum : int32_t { kTileFast = 0, kTileSlow = 1, kTileBad = 2, kTileNone = 3 };
 
 constexpr int kWaves = kIngestThreads / 64;
+constexpr int kBlock = 16;                      // frames per lane block
+constexpr int kMaxBlocks = kWaveFrames / kBlock;  // 64: one block per lane
 constexpr uint32_t kNotReady = 0xFFFFFFFFu;
 constexpr uint64_t kInStore = 1ull << 63;   // candidate base: frames live in the path store
-constexpr uint64_t kRelVerify = 1ull << 62, kRelStore = 1ull << 61, kRelBias = kWaveFrames;
-constexpr uint64_t kRelMask = kRelStore - 1;
 
 struct WaveShared {
-  uint32_t fr[kWaveFrames];        // staged frames: slot x <-> relative position x - lead
-  uint8_t evt[kWaveFrames];        // event of each staged slot
-  uint8_t gmap[kWaveFrames / 4];   // event containing the first position of each 4-slot group
-  int32_t ls[kWaveEvents + 1];     // event starts relative to the tile's first frame
-  int32_t bad[kWaveEvents + 1];    // verification found a differing frame
-  uint64_t hacc[kWaveEvents + 1];  // hash partial sums
-  uint64_t vrel[kWaveEvents + 1];  // candidate frame index at relative position 0 (+ kRelBias), with
-                                   // kRelVerify / kRelStore flags; 0: nothing to verify
+  uint64_t hacc[64];  // hash sums per event
+  uint64_t vptr[64];  // global address of the candidate's first frame; 0: nothing to verify
+  uint32_t vlim[64];  // frames readable from vptr (the path, padded in the path store)
+  uint8_t bad[64];    // verification found a differing frame
+  uint8_t first[64];  // event whose first block is at lane l (0 if none)
 };
 
 // Per-workgroup cache of resolved paths, keyed by (hash, length): the table slot and
@@ -83,6 +84,19 @@ __device__ inline uint64_t wave_sum_u64(uint64_t v) {
   return v;
 }
 
+// Inclusive scans over the 64 lanes (DPP row shifts, then row broadcasts).
+template <bool kMax>
+__device__ inline int wave_scan(int v) {
+  auto op = [](int x, int y) { return kMax ? max(x, y) : x + y; };
+  v = op(v, __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, true));  // row_shr:1
+  v = op(v, __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, true));  // row_shr:2
+  v = op(v, __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, true));  // row_shr:4
+  v = op(v, __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, true));  // row_shr:8
+  v = op(v, __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false)); // row_bcast:15
+  v = op(v, __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, false)); // row_bcast:31
+  return v;
+}
+
 // wave-uniform values kept in scalar registers
 __device__ inline int64_t uniform64(int64_t v) {
   const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
@@ -97,8 +111,14 @@ __device__ inline int64_t shfl_i64(int64_t v, int src) {
 
 // A tile: events [e0, e0 + ne) of the wave's range, wave-uniform.
 struct Tile {
-  int64_t e0, g0;
-  int32_t ne, span, lead, kind;
+  int64_t e0, g0;  // first event and its first frame
+  int32_t ne, kind;
+};
+
+// This lane's block of a tile: frames [16 m, 16 m + rem) of event ev (ev = -1: idle
+// lane), at byte offset voff from the tile's first frame.
+struct Blk {
+  int32_t ev, m, rem, voff;
 };
 
 // Offsets window at event e (lane j holds offsets[e + j], j <= min(63, end - e)).
@@ -106,10 +126,15 @@ __device__ inline int64_t load_window(const IngestArgs &a, int64_t e, int64_t en
   return e < end && lane <= end - e ? a.off[e + lane] : 0;
 }
 
-// Validate the window and cut the next tile: as many events as fit in the staging
-// slice.  Every offset is validated here, before any frame is read.
-__device__ inline Tile make_tile(const IngestArgs &a, int64_t e, int64_t end, int64_t o, int lane) {
+// Validate the window and cut the next tile: as many events as fit in 64 blocks; map
+// every lane to its block.  Every offset is validated here, before any frame is read.
+__device__ inline Tile make_tile(const IngestArgs &a, WaveShared &W, int64_t e, int64_t end, int64_t o, int lane,
+                                 Blk &b) {
   Tile t{};
+  b.ev = -1;
+  b.m = 0;
+  b.rem = 0;
+  b.voff = 0;
   if (e >= end) { t.kind = kTileNone; return t; }
   t.e0 = e;
   const int jmax = (int)min((int64_t)kWaveEvents, end - e);
@@ -120,37 +145,65 @@ __device__ inline Tile make_tile(const IngestArgs &a, int64_t e, int64_t end, in
   if (lane == jmax) bad |= e + jmax == a.n_events && o != a.n_frames;
   if (__any(bad)) { t.kind = kTileBad; return t; }
   t.g0 = uniform64(shfl_i64(o, 0));
-  t.lead = (int)(((uintptr_t)a.fr >> 2) + (uint64_t)t.g0) & 3;
-  const uint64_t fit = __ballot(lane >= 1 && lane <= jmax && o - t.g0 + t.lead <= kWaveFrames);
-  if (fit == 0) {  // a single path longer than the slice
+  // blocks per event (kMaxBlocks + 1: does not fit), inclusive prefix over events
+  const int64_t len = lane < jmax ? onext - o : 0;
+  const int nb = len > kWaveFrames ? kMaxBlocks + 1 : (int)((len + kBlock - 1) / kBlock);
+  const int incl = wave_scan<false>(nb);
+  const uint64_t fit = __ballot(lane < jmax && incl <= kMaxBlocks);
+  t.ne = __popcll(fit);  // block counts are non-negative: the fitting events are a prefix
+  if (t.ne == 0) {       // a single path longer than a tile
     t.ne = 1;
     t.kind = kTileSlow;
     return t;
   }
-  t.ne = 63 - __builtin_clzll(fit);  // offsets are non-decreasing: the fitting lanes are 1..ne
-  t.span = (int)(uniform64(shfl_i64(o, t.ne)) - t.g0);
   t.kind = kTileFast;
+  // lane -> block: event j's blocks are lanes [incl - nb, incl)
+  const int nblk = __shfl(incl, t.ne - 1, 64);
+  const int excl = incl - nb;
+  W.first[lane] = 0;
+  wave_sync();
+  if (lane < t.ne && nb > 0) W.first[excl] = (uint8_t)lane;
+  wave_sync();
+  const int ev = wave_scan<true>(W.first[lane]);
+  const int ev_excl = __shfl(excl, ev, 64);
+  const int ev_len = __shfl((int)len, ev, 64);
+  const int ev_start = __shfl((int)(o - t.g0), ev, 64);
+  const int m = lane - ev_excl;
+  if (lane < nblk && m >= 0 && m * kBlock < ev_len) {
+    b.ev = ev;
+    b.m = m;
+    b.rem = ev_len - m * kBlock;
+    b.voff = (ev_start + m * kBlock) * 4;
+  }
   return t;
 }
 
-// This lane's frames of a fast tile: 16-byte groups q * 64 + lane (slots
-// 256 q + 4 lane .. + 4), at 16-byte aligned addresses; elements outside the tile are
-// left zero.
-__device__ inline void load_frames(const IngestArgs &a, const Tile &t, int lane, u32x4 nf[4]) {
+// Buffer resource over the batch's frames from the tile's first frame on: loads past
+// the end of the batch return zero.
+__device__ inline __amdgpu_buffer_rsrc_t tile_rsrc(const IngestArgs &a, const Tile &t) {
+  const int64_t avail = a.n_frames - t.g0;
+  const int bytes = (int)(avail < (1 << 28) ? avail * 4 : (1 << 30));
+  return __builtin_amdgcn_make_buffer_rsrc((void *)(a.fr + t.g0), (short)0, bytes, 0x00020000);
+}
+
+// This lane's block: four 16-byte loads; a 16-byte load that would reach past the end
+// of the batch is split into 4-byte loads (each range checked).  Frames past the
+// block's event are left as loaded (never used).
+__device__ inline void load_block(const IngestArgs &a, const Tile &t, const Blk &b, u32x4 nf[4]) {
+  const __amdgpu_buffer_rsrc_t r = tile_rsrc(a, t);
+  const int64_t lim = (a.n_frames - t.g0) * 4;
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int r = q * 256 + lane * 4 - t.lead;
+  for (int j = 0; j < 4; ++j) {
     u32x4 v = {0u, 0u, 0u, 0u};
-    if (t.kind == kTileFast && r + 4 > 0 && r < t.span) {
-      const int64_t gi = t.g0 + r;
-      if (gi >= 0 && gi + 4 <= a.n_frames) {
-        v = __builtin_nontemporal_load((const u32x4 *)(a.fr + gi));
+    if (t.kind == kTileFast && 4 * j < b.rem) {
+      if (b.voff + 16 * j + 16 <= lim) {
+        v = __builtin_amdgcn_raw_buffer_load_b128(r, b.voff + 16 * j, 0, 0);
       } else {
-        for (int e = 0; e < 4; ++e)
-          if (r + e >= 0 && r + e < t.span) v[e] = a.fr[gi + e];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) v[k] = __builtin_amdgcn_raw_buffer_load_b32(r, b.voff + 16 * j + 4 * k, 0, 0);
       }
     }
-    nf[q] = v;
+    nf[j] = v;
   }
 }
 
@@ -289,15 +342,6 @@ __device__ __forceinline__ void slow_wave_tile(const IngestArgs &a, int64_t e0, 
   }
 }
 
-// Event j containing relative position r (largest j with ls[j] <= r; ls[ne] > r).
-__device__ inline int event_at(const WaveShared &W, int ne, int r) {
-  int lo = 0, hi = ne;
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    if (W.ls[mid] <= r) lo = mid; else hi = mid;
-  }
-  return lo;
-}
 
 __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
   __shared__ IngestShared S;
@@ -307,13 +351,14 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
   __syncthreads();
 
   // this wave's events.  Pipeline: the offsets window of tile t+1 is loaded during
-  // tile t-1, so tile t+1's frames can be requested as soon as tile t starts.
+  // tile t-1, so tile t+1's frames can be requested while tile t resolves.
   const int64_t waves_total = (int64_t)gridDim.x * kWaves, w = (int64_t)blockIdx.x * kWaves + wave;
   const int64_t end = (w + 1) * a.n_events / waves_total;
   int64_t o_cur = load_window(a, w * a.n_events / waves_total, end, lane);
-  Tile t = make_tile(a, w * a.n_events / waves_total, end, o_cur, lane);
+  Blk b;
+  Tile t = make_tile(a, W, w * a.n_events / waves_total, end, o_cur, lane, b);
   u32x4 nf[4];
-  load_frames(a, t, lane, nf);
+  load_block(a, t, b, nf);
   int64_t o_nxt = t.kind == kTileFast || t.kind == kTileSlow ? load_window(a, t.e0 + t.ne, end, lane) : 0;
 
   for (int iter = 0; t.kind != kTileNone; ++iter) {
@@ -328,90 +373,46 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
     if (t.kind == kTileSlow) {
       slow_wave_tile(a, t.e0, t.ne, o_cur);
       o_cur = o_nxt;
-      t = make_tile(a, e_nxt, end, o_cur, lane);
-      load_frames(a, t, lane, nf);
+      t = make_tile(a, W, e_nxt, end, o_cur, lane, b);
+      load_block(a, t, b, nf);
       o_nxt = t.kind == kTileFast || t.kind == kTileSlow ? load_window(a, t.e0 + t.ne, end, lane) : 0;
       continue;
     }
-    const int ne = t.ne, span = t.span, lead = t.lead;
+    const int ne = t.ne;
     const int64_t e0 = t.e0;
+    uint32_t f[kBlock];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) *(u32x4 *)&W.fr[q * 256 + lane * 4] = nf[q];
-    // event starts, and the group map: the event containing the first position of
-    // every 4-slot group.  Event j is written to the first group that starts at or
-    // after it, by the last event to map there (one writer per byte); a running max
-    // then fills the groups in between.
-    *(uint32_t *)&W.gmap[lane * 4] = 0;
-    if (lane <= ne) W.ls[lane] = (int32_t)(o_cur - t.g0);
-    {
-      const int g = ((int)(o_cur - t.g0) + lead + 3) >> 2;
-      const int gn = __shfl_down(g, 1, 64);
-      wave_sync();
-      if (lane < ne) {
-        W.hacc[lane] = 0;
-        if (g < kWaveFrames / 4 && (lane == ne - 1 || gn != g)) W.gmap[g] = (uint8_t)lane;
-      }
-    }
-    wave_sync();
-    {
-      const uint32_t pk = *(const uint32_t *)&W.gmap[lane * 4];
-      uint32_t b0 = pk & 0xFF, b1 = max(b0, (pk >> 8) & 0xFF), b2 = max(b1, (pk >> 16) & 0xFF),
-               b3 = max(b2, pk >> 24);
-      uint32_t run = b3;
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t u = __shfl_up(run, o, 64);
-        if (lane >= o) run = max(run, u);
-      }
-      uint32_t before = __shfl_up(run, 1, 64);
-      if (lane == 0) before = 0;
-      b0 = max(b0, before); b1 = max(b1, before); b2 = max(b2, before); b3 = max(b3, before);
-      *(uint32_t *)&W.gmap[lane * 4] = b0 | b1 << 8 | b2 << 16 | b3 << 24;
-    }
-    wave_sync();
+      for (int k = 0; k < 4; ++k) f[4 * j + k] = nf[j][k];
+    const Blk cb = b;
 
-    // A2: hash.  Four runs of four frames per lane: slots 256 q + 4 lane .. + 4.
+    // A2: hash.  The block's sum of frame_term(frame, 16 m + i) over its frames.
+    W.hacc[lane] = 0;
+    wave_sync();
+    if (cb.ev >= 0) {
+      const uint32_t kx = (uint32_t)(cb.m * kBlock) * kTermMulX, ky = (uint32_t)(cb.m * kBlock) * kTermMulY;
+      uint64_t acc = 0;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int r0 = q * 256 + lane * 4 - lead;
-      if (r0 + 4 > 0 && r0 < span) {
-        const u32x4 v = *(const u32x4 *)&W.fr[q * 256 + lane * 4];
-        int cur = W.gmap[q * 64 + lane], cs = W.ls[cur], nx = W.ls[cur + 1];
-        uint64_t acc = 0;
-        uint32_t ev4 = 0;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int r = r0 + i;
-          const bool valid = r >= 0 && r < span;
-          if (valid && r >= nx) {
-            atomicAdd((unsigned long long *)&W.hacc[cur], (unsigned long long)acc);
-            acc = 0;
-            do { ++cur; } while (W.ls[cur + 1] <= r);
-            cs = W.ls[cur];
-            nx = W.ls[cur + 1];
-          }
-          if (valid) acc += frame_term(v[i], (uint32_t)(r - cs));
-          ev4 |= (uint32_t)cur << (8 * i);
-        }
-        atomicAdd((unsigned long long *)&W.hacc[cur], (unsigned long long)acc);
-        *(uint32_t *)&W.evt[q * 256 + lane * 4] = ev4;
+      for (int i = 0; i < kBlock; ++i) {  // frame_term(f[i], 16 m + i), zero past the path
+        const uint32_t x = f[i] + kx + (uint32_t)i * kTermMulX;
+        const uint32_t y = (f[i] ^ kTermXorY) + ky + (uint32_t)i * kTermMulY;
+        acc += (uint64_t)x * (uint64_t)(i < cb.rem ? y | 1u : 0u);
       }
+      atomicAdd((unsigned long long *)&W.hacc[cb.ev], (unsigned long long)acc);
     }
     wave_sync();
-
-    // the next tile's frames, and the offsets window after it, stream in while this
-    // tile resolves
-    const Tile tn = make_tile(a, e_nxt, end, o_nxt, lane);
-    load_frames(a, tn, lane, nf);
-    const int64_t o_nn = tn.kind == kTileFast || tn.kind == kTileSlow ? load_window(a, tn.e0 + tn.ne, end, lane) : 0;
 
     // A3: exact dedup.  Lane j resolves event j: a cached resolution of the same hash
-    // and length, else the table; every candidate is verified by all lanes.
+    // and length, else the table; every candidate is verified by the event's blocks.
+    // (cross-lane reads with every lane active: a disabled source lane reads as zero)
+    const int64_t o_end = shfl_i64(o_cur, lane + 1 < 64 ? lane + 1 : 63);
     Probe p{};
     p.state = kResolved;
-    bool cached = false;  // the candidate came from the cache (no re-insert needed)
+    bool cached = false;      // resolved through the cache or past a colliding path: not re-inserted
+    bool from_cache = false;  // the current candidate came from the cache
     if (lane < ne) {
-      p.len = (uint32_t)(W.ls[lane + 1] - W.ls[lane]);
+      p.len = (uint32_t)(o_end - o_cur);
       p.h = finish_hash(W.hacc[lane], (uint64_t)p.len) & a.hash_mask;
       p.slot = (uint32_t)(p.h & a.cap_mask);
       p.state = kProbing;
@@ -421,53 +422,80 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
         p.cbase = S.cbase[ci];
         p.state = p.len == 0 ? kResolved : kCandidate;
         cached = true;
+        from_cache = true;
       }
     }
+
+    // the next tile's frames, and the offsets window after it, stream in while this
+    // tile resolves
+    const Tile tn = make_tile(a, W, e_nxt, end, o_nxt, lane, b);
+    load_block(a, tn, b, nf);
+    const int64_t o_nn = tn.kind == kTileFast || tn.kind == kTileSlow ? load_window(a, tn.e0 + tn.ne, end, lane) : 0;
+
     for (;;) {
       if (p.state == kProbing) probe(a, p, e0 + lane, o_cur, (int64_t)p.len);
       if (!__any(p.state == kCandidate)) break;
       if (lane < ne) {
-        uint64_t v = 0;
-        if (p.state == kCandidate)
-          v = kRelVerify | ((p.cbase & kInStore) ? kRelStore : 0) |
-              ((p.cbase & ~kInStore) + kRelBias - (uint64_t)W.ls[lane]);
-        W.vrel[lane] = v;
+        uint64_t vp = 0;
+        uint32_t lim = 0;
+        if (p.state == kCandidate) {
+          const uint64_t fi = p.cbase & ~kInStore;
+          if (p.cbase & kInStore) {
+            vp = (uint64_t)(uintptr_t)(a.pframes + fi);
+            lim = (uint32_t)round_store(p.len);
+          } else {
+            vp = (uint64_t)(uintptr_t)(a.fr + fi);
+            const int64_t av = a.n_frames - (int64_t)fi;
+            lim = (uint32_t)(av < (int64_t)kWaveFrames ? av : kWaveFrames);
+          }
+        }
+        W.vptr[lane] = vp;
+        W.vlim[lane] = lim;
         W.bad[lane] = 0;
       }
       wave_sync();
-      // lane l checks staged slots l, l + 64, ...: every load instruction reads 64
-      // consecutive frames.  Addresses are formed without branches and the loads are
-      // issued in two batches of eight, so a tile costs two round trips.
+      // every block of a candidate compares its frames with the candidate's: 16-byte
+      // loads, except where a load would reach past what is readable there
+      if (cb.ev >= 0) {
+        const uint64_t vp = W.vptr[cb.ev];
+        if (vp != 0) {
+          const int avail = (int)W.vlim[cb.ev] - cb.m * kBlock;
+          const gptr cp = (gptr)vp + cb.m * kBlock;
+          uint32_t c[kBlock];
 #pragma unroll
-      for (int h = 0; h < 4; ++h) {
-        uint32_t cand[4];
-        uint32_t act = 0;
+          for (int j = 0; j < 4; ++j) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int x = (h * 4 + i) * 64 + lane, r = x - lead;
-          const bool in = r >= 0 && r < span;
-          const uint64_t v = W.vrel[W.evt[x] & kWaveEvents];  // slots outside the span hold stale events
-          const bool chk = in && (v & kRelVerify);
-          const uint32_t *src = (v & kRelStore) ? a.pframes : a.fr;
-          cand[i] = 0;
-          if (chk) cand[i] = src[(v & kRelMask) - kRelBias + (uint64_t)r];
-          act |= (uint32_t)chk << i;
-        }
+            for (int k = 0; k < 4; ++k) c[4 * j + k] = f[4 * j + k];
+            if (4 * j < cb.rem) {
+              if (4 * j + 4 <= avail) {
+                const u32x4 v = *(gptr4)(cp + 4 * j);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int x = (h * 4 + i) * 64 + lane;
-          if (((act >> i) & 1u) && cand[i] != W.fr[x]) W.bad[W.evt[x]] = 1;
+                for (int k = 0; k < 4; ++k) c[4 * j + k] = v[k];
+              } else {
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                  if (4 * j + k < cb.rem) c[4 * j + k] = cp[4 * j + k];
+              }
+            }
+          }
+          bool mism = false;
+#pragma unroll
+          for (int i = 0; i < kBlock; ++i) mism |= i < cb.rem && c[i] != f[i];
+          if (mism) W.bad[cb.ev] = 1;
         }
       }
       wave_sync();
       if (p.state == kCandidate) {
         if (W.bad[lane]) {
-          p.slot = (uint32_t)((p.slot + 1) & a.cap_mask);
+          // a table candidate was reached along the probe sequence, so the path is
+          // further on; a cached one says nothing about the slots before it
+          p.slot = (uint32_t)((from_cache ? p.h : p.slot + 1) & a.cap_mask);
           p.state = kProbing;
-          cached = true;  // resolved past a cached path with the same hash: not cacheable
+          cached = true;  // another path has the same hash and length: not cacheable
         } else {
           p.state = kResolved;
         }
+        from_cache = false;
       }
       wave_sync();
     }

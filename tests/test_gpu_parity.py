@@ -130,6 +130,16 @@ def test_forced_hash_collisions(monkeypatch, bits):
     assert_same(gpu_tree(o, f, w), oracle.build_tree(o, f, w), f"bits={bits}")
 
 
+@pytest.mark.parametrize("bits", [5, 9])
+def test_forced_collisions_through_cache(monkeypatch, bits):
+    # many events per distinct path, so workgroup caches hold paths whose hash and
+    # length collide with others: a cached candidate that differs must not make an
+    # event skip the slots before it on the probe sequence
+    monkeypatch.setenv("CCT_TEST_HASH_BITS", str(bits))
+    o, f, w = tracegen.random_small(20_000, 4, 7, 2, seed=40 + bits)
+    assert_same(gpu_tree(o, f, w), oracle.build_tree(o, f, w), f"bits={bits}")
+
+
 def test_forced_table_overflow_regrows(monkeypatch):
     monkeypatch.setenv("CCT_TEST_TABLE_CAP", "16")
     o, f, w = tracegen.random_paths(5000, 500, 12, 1, seed=9)
