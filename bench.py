@@ -80,7 +80,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="layered_16m", choices=sorted(DESCRIPTIONS))
-    ap.add_argument("--cpu-sample", type=int, default=1 << 21, help="events timed on the oracle")
+    ap.add_argument("--cpu-sample", type=int, default=1 << 24, help="events timed on the oracle")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibrate", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times (the reference kernel that "
