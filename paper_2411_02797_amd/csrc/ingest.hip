@@ -44,8 +44,8 @@ enum : int32_t { kProbing = 0, kCandidate = 1, kResolved = 2, kFailed = 3 };
 enum : int32_t { kTileFast = 0, kTileSlow = 1, kTileBad = 2, kTileNone = 3 };
 
 constexpr int kWaves = kIngestThreads / 64;
-constexpr int kBlock = 16;                      // frames per lane block
-constexpr int kMaxBlocks = kWaveFrames / kBlock;  // 64: one block per lane
+constexpr int kBlock = 16;                        // frames per lane block
+constexpr int kTileBlocks = kWaveFrames / kBlock;   // blocks per wave tile: kLaneBlocks per lane
 constexpr uint32_t kNotReady = 0xFFFFFFFFu;
 constexpr uint64_t kInStore = 1ull << 63;   // candidate base: frames live in the path store
 
@@ -54,7 +54,7 @@ struct WaveShared {
   uint64_t vptr[64];  // global address of the candidate's first frame; 0: nothing to verify
   uint32_t vlim[64];  // frames readable from vptr (the path, padded in the path store)
   uint8_t bad[64];    // verification found a differing frame
-  uint8_t first[64];  // event whose first block is at lane l (0 if none)
+  uint8_t first[kTileBlocks];  // event whose first block is block b (0 if none)
 };
 
 // Per-workgroup cache of resolved paths, keyed by (hash, length): the table slot and
@@ -113,10 +113,12 @@ __device__ inline int64_t shfl_i64(int64_t v, int src) {
 struct Tile {
   int64_t e0, g0;  // first event and its first frame
   int32_t ne, kind;
+  int32_t span;    // frames of the tile's events
 };
 
-// This lane's block of a tile: frames [16 m, 16 m + rem) of event ev (ev = -1: idle
-// lane), at byte offset voff from the tile's first frame.
+// One of this lane's blocks of a tile: frames [16 m, 16 m + rem) of event ev (ev = -1:
+// no block), at byte offset voff from the tile's first frame.  Lane l holds blocks
+// l + 64 q, q < kLaneBlocks.
 struct Blk {
   int32_t ev, m, rem, voff;
 };
@@ -126,15 +128,14 @@ __device__ inline int64_t load_window(const IngestArgs &a, int64_t e, int64_t en
   return e < end && lane <= end - e ? a.off[e + lane] : 0;
 }
 
-// Validate the window and cut the next tile: as many events as fit in 64 blocks; map
-// every lane to its block.  Every offset is validated here, before any frame is read.
+// Validate the window and cut the next tile: as many events as fit in the tile's
+// blocks; map every lane to its blocks.  Every offset is validated here, before any
+// frame is read.
 __device__ inline Tile make_tile(const IngestArgs &a, WaveShared &W, int64_t e, int64_t end, int64_t o, int lane,
-                                 Blk &b) {
+                                 Blk (&b)[kLaneBlocks]) {
   Tile t{};
-  b.ev = -1;
-  b.m = 0;
-  b.rem = 0;
-  b.voff = 0;
+#pragma unroll
+  for (int q = 0; q < kLaneBlocks; ++q) b[q] = Blk{-1, 0, 0, 0};
   if (e >= end) { t.kind = kTileNone; return t; }
   t.e0 = e;
   const int jmax = (int)min((int64_t)kWaveEvents, end - e);
@@ -145,11 +146,11 @@ __device__ inline Tile make_tile(const IngestArgs &a, WaveShared &W, int64_t e, 
   if (lane == jmax) bad |= e + jmax == a.n_events && o != a.n_frames;
   if (__any(bad)) { t.kind = kTileBad; return t; }
   t.g0 = uniform64(shfl_i64(o, 0));
-  // blocks per event (kMaxBlocks + 1: does not fit), inclusive prefix over events
+  // blocks per event (kTileBlocks + 1: does not fit), inclusive prefix over events
   const int64_t len = lane < jmax ? onext - o : 0;
-  const int nb = len > kWaveFrames ? kMaxBlocks + 1 : (int)((len + kBlock - 1) / kBlock);
+  const int nb = len > kWaveFrames ? kTileBlocks + 1 : (int)((len + kBlock - 1) / kBlock);
   const int incl = wave_scan<false>(nb);
-  const uint64_t fit = __ballot(lane < jmax && incl <= kMaxBlocks);
+  const uint64_t fit = __ballot(lane < jmax && incl <= kTileBlocks);
   t.ne = __popcll(fit);  // block counts are non-negative: the fitting events are a prefix
   if (t.ne == 0) {       // a single path longer than a tile
     t.ne = 1;
@@ -157,23 +158,26 @@ __device__ inline Tile make_tile(const IngestArgs &a, WaveShared &W, int64_t e, 
     return t;
   }
   t.kind = kTileFast;
-  // lane -> block: event j's blocks are lanes [incl - nb, incl)
-  const int nblk = __shfl(incl, t.ne - 1, 64);
+  t.span = (int)(uniform64(shfl_i64(o, t.ne)) - t.g0);
+  // block -> event: event j's blocks are [incl - nb, incl)
+  const int nblk = __builtin_amdgcn_readlane(incl, t.ne - 1);
   const int excl = incl - nb;
-  W.first[lane] = 0;
+  const int rel = (int)(o - t.g0);
+#pragma unroll
+  for (int q = 0; q < kLaneBlocks; ++q) W.first[q * 64 + lane] = 0;
   wave_sync();
   if (lane < t.ne && nb > 0) W.first[excl] = (uint8_t)lane;
   wave_sync();
-  const int ev = wave_scan<true>(W.first[lane]);
-  const int ev_excl = __shfl(excl, ev, 64);
-  const int ev_len = __shfl((int)len, ev, 64);
-  const int ev_start = __shfl((int)(o - t.g0), ev, 64);
-  const int m = lane - ev_excl;
-  if (lane < nblk && m >= 0 && m * kBlock < ev_len) {
-    b.ev = ev;
-    b.m = m;
-    b.rem = ev_len - m * kBlock;
-    b.voff = (ev_start + m * kBlock) * 4;
+  int carry = 0;
+#pragma unroll
+  for (int q = 0; q < kLaneBlocks; ++q) {
+    const int ev = max(wave_scan<true>(W.first[q * 64 + lane]), carry);
+    carry = __builtin_amdgcn_readlane(ev, 63);
+    const int ev_excl = __shfl(excl, ev, 64);
+    const int ev_len = __shfl((int)len, ev, 64);
+    const int ev_start = __shfl(rel, ev, 64);
+    const int bi = q * 64 + lane, m = bi - ev_excl;
+    if (bi < nblk && m >= 0 && m * kBlock < ev_len) b[q] = Blk{ev, m, ev_len - m * kBlock, (ev_start + m * kBlock) * 4};
   }
   return t;
 }
@@ -186,24 +190,39 @@ __device__ inline __amdgpu_buffer_rsrc_t tile_rsrc(const IngestArgs &a, const Ti
   return __builtin_amdgcn_make_buffer_rsrc((void *)(a.fr + t.g0), (short)0, bytes, 0x00020000);
 }
 
-// This lane's block: four 16-byte loads; a 16-byte load that would reach past the end
-// of the batch is split into 4-byte loads (each range checked).  Frames past the
+// This lane's blocks: four 16-byte loads each; a 16-byte load that would reach past
+// the end of the batch is split into 4-byte loads (each range checked).  Frames past a
 // block's event are left as loaded (never used).
-__device__ inline void load_block(const IngestArgs &a, const Tile &t, const Blk &b, u32x4 nf[4]) {
+__device__ inline void load_blocks(const IngestArgs &a, const Tile &t, const Blk (&b)[kLaneBlocks],
+                                   u32x4 (&nf)[kLaneBlocks][4]) {
+  if (t.kind != kTileFast) return;
   const __amdgpu_buffer_rsrc_t r = tile_rsrc(a, t);
   const int64_t lim = (a.n_frames - t.g0) * 4;
+  if ((int64_t)t.span * 4 + 64 <= lim) {
+    // every load of the tile ends inside the batch: no per-lane conditions (idle
+    // lanes and frames past a block's event read frames that are never used)
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    u32x4 v = {0u, 0u, 0u, 0u};
-    if (t.kind == kTileFast && 4 * j < b.rem) {
-      if (b.voff + 16 * j + 16 <= lim) {
-        v = __builtin_amdgcn_raw_buffer_load_b128(r, b.voff + 16 * j, 0, 0);
-      } else {
+    for (int q = 0; q < kLaneBlocks; ++q)
 #pragma unroll
-        for (int k = 0; k < 4; ++k) v[k] = __builtin_amdgcn_raw_buffer_load_b32(r, b.voff + 16 * j + 4 * k, 0, 0);
+      for (int j = 0; j < 4; ++j) nf[q][j] = __builtin_amdgcn_raw_buffer_load_b128(r, b[q].voff + 16 * j, 0, 0);
+    return;
+  }
+#pragma unroll
+  for (int q = 0; q < kLaneBlocks; ++q) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (4 * j < b[q].rem) {
+        if (b[q].voff + 16 * j + 16 <= lim) {
+          v = __builtin_amdgcn_raw_buffer_load_b128(r, b[q].voff + 16 * j, 0, 0);
+        } else {
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+            v[k] = __builtin_amdgcn_raw_buffer_load_b32(r, b[q].voff + 16 * j + 4 * k, 0, 0);
+        }
       }
+      nf[q][j] = v;
     }
-    nf[j] = v;
   }
 }
 
@@ -355,10 +374,10 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
   const int64_t waves_total = (int64_t)gridDim.x * kWaves, w = (int64_t)blockIdx.x * kWaves + wave;
   const int64_t end = (w + 1) * a.n_events / waves_total;
   int64_t o_cur = load_window(a, w * a.n_events / waves_total, end, lane);
-  Blk b;
+  Blk b[kLaneBlocks];
   Tile t = make_tile(a, W, w * a.n_events / waves_total, end, o_cur, lane, b);
-  u32x4 nf[4];
-  load_block(a, t, b, nf);
+  u32x4 nf[kLaneBlocks][4];
+  load_blocks(a, t, b, nf);
   int64_t o_nxt = t.kind == kTileFast || t.kind == kTileSlow ? load_window(a, t.e0 + t.ne, end, lane) : 0;
 
   for (int iter = 0; t.kind != kTileNone; ++iter) {
@@ -374,32 +393,39 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
       slow_wave_tile(a, t.e0, t.ne, o_cur);
       o_cur = o_nxt;
       t = make_tile(a, W, e_nxt, end, o_cur, lane, b);
-      load_block(a, t, b, nf);
+      load_blocks(a, t, b, nf);
       o_nxt = t.kind == kTileFast || t.kind == kTileSlow ? load_window(a, t.e0 + t.ne, end, lane) : 0;
       continue;
     }
     const int ne = t.ne;
     const int64_t e0 = t.e0;
-    uint32_t f[kBlock];
+    uint32_t f[kLaneBlocks][kBlock];
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int q = 0; q < kLaneBlocks; ++q)
 #pragma unroll
-      for (int k = 0; k < 4; ++k) f[4 * j + k] = nf[j][k];
-    const Blk cb = b;
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) f[q][4 * j + k] = nf[q][j][k];
+    Blk cb[kLaneBlocks];
+#pragma unroll
+    for (int q = 0; q < kLaneBlocks; ++q) cb[q] = b[q];
 
-    // A2: hash.  The block's sum of frame_term(frame, 16 m + i) over its frames.
+    // A2: hash.  Each block's sum of frame_term(frame, 16 m + i) over its frames.
     W.hacc[lane] = 0;
     wave_sync();
-    if (cb.ev >= 0) {
-      const uint32_t kx = (uint32_t)(cb.m * kBlock) * kTermMulX, ky = (uint32_t)(cb.m * kBlock) * kTermMulY;
-      uint64_t acc = 0;
 #pragma unroll
-      for (int i = 0; i < kBlock; ++i) {  // frame_term(f[i], 16 m + i), zero past the path
-        const uint32_t x = f[i] + kx + (uint32_t)i * kTermMulX;
-        const uint32_t y = (f[i] ^ kTermXorY) + ky + (uint32_t)i * kTermMulY;
-        acc += (uint64_t)x * (uint64_t)(i < cb.rem ? y | 1u : 0u);
+    for (int q = 0; q < kLaneBlocks; ++q) {
+      if (cb[q].ev >= 0) {
+        const uint32_t kx = (uint32_t)(cb[q].m * kBlock) * kTermMulX, ky = (uint32_t)(cb[q].m * kBlock) * kTermMulY;
+        uint64_t acc = 0;
+#pragma unroll
+        for (int i = 0; i < kBlock; ++i) {  // frame_term(f, 16 m + i), zero past the path
+          const uint32_t x = f[q][i] + kx + (uint32_t)i * kTermMulX;
+          const uint32_t y = (f[q][i] ^ kTermXorY) + ky + (uint32_t)i * kTermMulY;
+          acc += (uint64_t)x * (uint64_t)(i < cb[q].rem ? y | 1u : 0u);
+        }
+        atomicAdd((unsigned long long *)&W.hacc[cb[q].ev], (unsigned long long)acc);
       }
-      atomicAdd((unsigned long long *)&W.hacc[cb.ev], (unsigned long long)acc);
     }
     wave_sync();
 
@@ -429,7 +455,7 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
     // the next tile's frames, and the offsets window after it, stream in while this
     // tile resolves
     const Tile tn = make_tile(a, W, e_nxt, end, o_nxt, lane, b);
-    load_block(a, tn, b, nf);
+    load_blocks(a, tn, b, nf);
     const int64_t o_nn = tn.kind == kTileFast || tn.kind == kTileSlow ? load_window(a, tn.e0 + tn.ne, end, lane) : 0;
 
     for (;;) {
@@ -454,34 +480,41 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
         W.bad[lane] = 0;
       }
       wave_sync();
-      // every block of a candidate compares its frames with the candidate's: 16-byte
-      // loads, except where a load would reach past what is readable there
-      if (cb.ev >= 0) {
-        const uint64_t vp = W.vptr[cb.ev];
-        if (vp != 0) {
-          const int avail = (int)W.vlim[cb.ev] - cb.m * kBlock;
-          const gptr cp = (gptr)vp + cb.m * kBlock;
-          uint32_t c[kBlock];
+      // every block of a candidate compares its frames with the candidate's: four
+      // 16-byte loads, or 4-byte loads where a 16-byte load would reach past what is
+      // readable at the candidate
+      {
+        uint32_t c[kLaneBlocks][kBlock];
+        bool chk[kLaneBlocks];
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
+        for (int q = 0; q < kLaneBlocks; ++q) {
+          const uint64_t vp = cb[q].ev >= 0 ? W.vptr[cb[q].ev] : 0;
+          chk[q] = vp != 0;
+          const int avail = chk[q] ? (int)W.vlim[cb[q].ev] - cb[q].m * kBlock : 0;
+          const gptr cp = (gptr)vp + cb[q].m * kBlock;
 #pragma unroll
-            for (int k = 0; k < 4; ++k) c[4 * j + k] = f[4 * j + k];
-            if (4 * j < cb.rem) {
-              if (4 * j + 4 <= avail) {
+          for (int i = 0; i < kBlock; ++i) c[q][i] = f[q][i];
+          if (chk[q]) {
+            if (avail >= kBlock) {
+#pragma unroll
+              for (int j = 0; j < 4; ++j) {
                 const u32x4 v = *(gptr4)(cp + 4 * j);
 #pragma unroll
-                for (int k = 0; k < 4; ++k) c[4 * j + k] = v[k];
-              } else {
-#pragma unroll
-                for (int k = 0; k < 4; ++k)
-                  if (4 * j + k < cb.rem) c[4 * j + k] = cp[4 * j + k];
+                for (int k = 0; k < 4; ++k) c[q][4 * j + k] = v[k];
               }
+            } else {
+#pragma unroll
+              for (int i = 0; i < kBlock; ++i)
+                if (i < cb[q].rem) c[q][i] = cp[i];
             }
           }
-          bool mism = false;
+        }
 #pragma unroll
-          for (int i = 0; i < kBlock; ++i) mism |= i < cb.rem && c[i] != f[i];
-          if (mism) W.bad[cb.ev] = 1;
+        for (int q = 0; q < kLaneBlocks; ++q) {
+          uint32_t d = 0;
+#pragma unroll
+          for (int i = 0; i < kBlock; ++i) d |= i < cb[q].rem ? c[q][i] ^ f[q][i] : 0u;
+          if (chk[q] && d != 0) W.bad[cb[q].ev] = 1;
         }
       }
       wave_sync();
