@@ -172,6 +172,48 @@ struct CanonArgs {
   int grid_nodes;
 };
 void launch_sort(CanonArgs &a, hipStream_t s);        // leaves the result in a.order
+
+// Lexicographic order of the D distinct paths through a trie of 16-frame blocks (see
+// trie.hip).  Scratch sizes: nblocks = store blocks in use (sum of ceil(len / 16)),
+// cap = power of two >= 2 * nblocks.
+struct TrieArgs {
+  int64_t d;
+  int64_t nblocks;
+  uint64_t cap;                // node table capacity (power of two)
+  const uint32_t *pframes;
+  const uint64_t *pcp;
+  const int64_t *pstart;
+  const uint32_t *plen;
+  uint64_t *tkey;              // [cap] node keys (0: empty)
+  uint64_t *tinfo;             // [cap] (representative block << 32) | depth
+  uint32_t *pblk;              // [nblocks] path of each store block
+  uint32_t *occ;               // [nblocks] node of each store block
+  uint32_t *nparent;           // [cap] parent node (cap: the root)
+  uint32_t *ncount;            // [cap] distinct paths through the node
+  uint32_t *nend;              // [cap + 1] a path ends at the node (cap: the root)
+  uint64_t *hist;              // [cap + 1] children per node
+  uint64_t *gstart;            // [cap + 2] exclusive prefix sums of hist
+  uint32_t *cidx;              // [cap] index of each node among its siblings (root's children:
+                               //        (link workgroup << 22) | index within the workgroup)
+  uint32_t *rootbase;          // [1024] first index of each link workgroup's root children
+  uint32_t *grouped;           // [nblocks] nodes grouped by parent, siblings in order
+  uint32_t *grouped2;          // [nblocks] scratch
+  uint32_t *posof;             // [cap] position of each node in grouped
+  uint64_t *cnt;               // [nblocks] path counts in grouped order
+  uint64_t *cnt_scan;          // [nblocks + 1] their exclusive prefix sums
+  uint64_t *scan_blk;          // scan scratch: (nblocks / 1024 + 2) words
+  uint64_t *lists;             // [3][list_cap] (start << 32 | size): buckets of up to 64, larger
+                               // buckets, groups of more than 1024 siblings
+  int64_t list_cap;
+  int64_t large_cap;           // groups of more than 1024 siblings that can be listed
+  uint32_t *lgroup;            // [cap + 1] list index of a large group, by parent node
+  uint32_t *spl;               // [large_cap][256] splitters (node ids)
+  uint32_t *bcnt;              // [large_cap][256] bucket sizes
+  unsigned long long *ctr;     // [8]: [0..2] list counts, [3] failure
+  uint32_t *order;             // [D] out: path ids in lexicographic order
+};
+// ctr[3] != 0 after the call: the trie could not be used (the caller sorts another way).
+void launch_trie_sort(const TrieArgs &a, hipStream_t s);
 void launch_canon(const CanonArgs &a, hipStream_t s);  // lcp, scans, sparse table, emission
 
 struct QueryArgs {

@@ -1,0 +1,595 @@
+// Lexicographic order of the distinct full paths through a trie of 16-frame blocks.
+//
+// The canonical node ids are the lexicographic ranks of the paths (the paper's tree
+// has no ids; see canon.hip).  Sorting variable-length paths by comparison needs long
+// chains of dependent memory reads (paths share long prefixes), so the rank of each
+// path is computed instead:
+//   - every path of the path store is a chain of blocks of 16 frames (the last one
+//     possibly shorter).  A block node is a distinct prefix ending at a block
+//     boundary or at a path's end; nodes are deduplicated by hashing (the 16-frame
+//     checkpoint hashes the store already holds) and then verified exactly: a node's
+//     occurrences must share the parent node and the block's frames, which proves by
+//     induction over the depth that equal nodes are equal prefixes;
+//   - siblings (nodes with the same parent) are ordered by their blocks (frames
+//     compared as unsigned, a shorter block first when it is a prefix of the other);
+//   - with count(X) the number of paths through node X, the paths before path p are
+//     those that leave p's chain X_1 .. X_n at an earlier sibling of some X_k, plus
+//     the paths ending exactly at some X_{k-1} (proper prefixes of p):
+//       rank(p) = sum_k [ sum of count(S) over siblings S < X_k  +  ends(X_{k-1}) ].
+// A failed verification (a hash collision) or an oversized sibling group raises a
+// flag, and the caller falls back to the comparison sort; the order is in any case
+// re-verified frame by frame before it is used.
+#include "common.h"
+
+namespace cct {
+
+namespace {
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+constexpr int kBlk = kStoreAlign;           // frames per block
+constexpr int kChunk = 1024;                // groups up to this size are sorted by chunk
+constexpr int kMedium = 2048;               // LDS sort capacity of one workgroup
+constexpr uint64_t kRootSeed = 0x5851F42D4C957F2Dull;
+constexpr uint16_t kNone = 0xFFFFu;
+enum { kListSmall = 0, kListMedium = 1, kListLarge = 2, kFail = 3 };
+
+__device__ inline void fail(const TrieArgs &a) { atomicOr(&a.ctr[kFail], 1ull); }
+
+// Orders this wave's LDS accesses (every lane's earlier LDS writes before any lane's
+// later LDS reads).
+__device__ inline void wave_sync() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_wave_barrier();
+}
+
+// block s of the store (frames [16 s, 16 s + 16)): its path d, index k in the path,
+// depth (prefix length at its end) and the path's length
+struct BlockPos {
+  uint32_t d, k, depth, len;
+};
+__device__ inline BlockPos block_pos(const TrieArgs &a, int64_t s) {
+  BlockPos b;
+  b.d = a.pblk[s];
+  b.k = (uint32_t)(s - a.pstart[b.d] / kBlk);
+  b.len = a.plen[b.d];
+  b.depth = min((b.k + 1) * (uint32_t)kBlk, b.len);
+  return b;
+}
+// frames in a node's block (1..16), from its depth
+__device__ inline uint32_t block_frames(uint32_t depth) { return ((depth - 1) & (kBlk - 1)) + 1; }
+
+__global__ void fill_kernel(TrieArgs a) {
+  const int64_t d = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (d >= a.d) return;
+  a.order[d] = (uint32_t)d;
+  const uint32_t len = a.plen[d];
+  if (len == 0) {
+    a.nend[a.cap] = 1;  // the empty path ends at the root
+    return;
+  }
+  const int64_t b0 = a.pstart[d] / kBlk, nb = (len + kBlk - 1) / kBlk;
+  for (int64_t k = 0; k < nb; ++k) a.pblk[b0 + k] = (uint32_t)d;
+}
+
+// Node of every block: open addressing on the prefix hash (claimed by CAS).
+__global__ void insert_kernel(TrieArgs a) {
+  const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (s >= a.nblocks) return;
+  const BlockPos b = block_pos(a, s);
+  uint64_t key;
+  if (b.depth == (b.k + 1) * kBlk) {
+    key = a.pcp[s];  // full block: the checkpoint hash of the prefix
+  } else {           // a path's last, partial block: hash it onto the previous checkpoint
+    const uint32_t *f = a.pframes + s * kBlk;
+    uint64_t acc = 0;
+    for (uint32_t i = 0; i < b.depth - b.k * kBlk; ++i) acc += frame_term(f[i], b.k * kBlk + i);
+    key = finish_hash(acc + (b.k ? a.pcp[s - 1] : kRootSeed) * 0x9E3779B97F4A7C15ull, b.depth);
+  }
+  if (key == 0) key = 1;
+  const uint64_t mask = a.cap - 1;
+  uint64_t slot = key & mask;
+  for (uint64_t step = 0; step < a.cap; ++step) {
+    uint64_t cur = a.tkey[slot];
+    if (cur == 0) {
+      cur = atomicCAS((unsigned long long *)&a.tkey[slot], 0ull, (unsigned long long)key);
+      if (cur == 0) {
+        a.tinfo[slot] = ((uint64_t)s << 32) | b.depth;
+        a.occ[s] = (uint32_t)slot;
+        return;
+      }
+    }
+    if (cur == key) {
+      a.occ[s] = (uint32_t)slot;
+      return;
+    }
+    slot = (slot + 1) & mask;
+  }
+  a.occ[s] = 0;
+  fail(a);
+}
+
+// Verify every occurrence against its node's representative (same depth, same parent
+// node, same frames), link parents, count children per parent, paths per node (summed
+// in an LDS map per workgroup first: nodes near the root are on many paths) and path
+// ends.
+constexpr int kLinkThreads = 1024, kLinkMap = 8192;
+constexpr uint32_t kMapEmpty = 0xFFFFFFFFu;
+
+__global__ __launch_bounds__(kLinkThreads) void link_kernel(TrieArgs a) {
+  __shared__ uint32_t mkey[kLinkMap];
+  __shared__ uint32_t mval[kLinkMap];
+  __shared__ unsigned long long root_children;
+  for (int i = threadIdx.x; i < kLinkMap; i += kLinkThreads) { mkey[i] = kMapEmpty; mval[i] = 0; }
+  if (threadIdx.x == 0) root_children = 0;
+  __syncthreads();
+  const int64_t lo = (int64_t)blockIdx.x * a.nblocks / gridDim.x, hi = (int64_t)(blockIdx.x + 1) * a.nblocks / gridDim.x;
+  for (int64_t s = lo + threadIdx.x; s < hi; s += kLinkThreads) {
+    const BlockPos b = block_pos(a, s);
+    const uint32_t X = a.occ[s];
+    const uint64_t info = a.tinfo[X];
+    const int64_t rep = (int64_t)(info >> 32);
+    const uint32_t P = b.k ? a.occ[s - 1] : (uint32_t)a.cap;
+    // the representative links the node and takes its index among its siblings (the
+    // root's children, many, take theirs with one LDS atomic per wave)
+    const bool is_rep = rep == s, to_root = P == (uint32_t)a.cap;
+    const uint64_t rm = __ballot(is_rep && to_root);
+    if (rm) {
+      const int lane = threadIdx.x & 63, leader = __builtin_ctzll(rm);
+      unsigned long long base = 0;
+      if (lane == leader) base = atomicAdd(&root_children, (unsigned long long)__popcll(rm));
+      base = __shfl(base, leader, 64);
+      // (workgroup << 22) | index among this workgroup's root children
+      if (is_rep && to_root) a.cidx[X] = (blockIdx.x << 22) | (uint32_t)(base + __popcll(rm & ((1ull << lane) - 1)));
+    }
+    if (is_rep) {
+      a.nparent[X] = P;
+      if (!to_root) a.cidx[X] = (uint32_t)atomicAdd((unsigned long long *)&a.hist[P], 1ull);
+    } else {
+      bool ok = (uint32_t)info == b.depth && rep < a.nblocks;
+      if (ok) {
+        const BlockPos r = block_pos(a, rep);
+        const uint32_t RP = r.k ? a.occ[rep - 1] : (uint32_t)a.cap;
+        ok = RP == P && r.k == b.k;
+        if (ok) {
+          const u32x4 *x = (const u32x4 *)(a.pframes + s * kBlk), *y = (const u32x4 *)(a.pframes + rep * kBlk);
+          const uint32_t nf = b.depth - b.k * kBlk;
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            const u32x4 vx = x[c], vy = y[c];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if ((uint32_t)(4 * c + e) < nf && vx[e] != vy[e]) ok = false;
+          }
+        }
+      }
+      if (!ok) fail(a);
+    }
+    uint32_t h = hash32(X) & (kLinkMap - 1);
+    bool done = false;
+    for (int t = 0; t < 16 && !done; ++t) {
+      uint32_t cur = mkey[h];
+      if (cur == kMapEmpty) cur = atomicCAS(&mkey[h], kMapEmpty, X);
+      if (cur == kMapEmpty || cur == X) {
+        atomicAdd(&mval[h], 1u);
+        done = true;
+      } else {
+        h = (h + 1) & (kLinkMap - 1);
+      }
+    }
+    if (!done) atomicAdd(&a.ncount[X], 1u);
+    if (b.depth == b.len) a.nend[X] = 1;
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < kLinkMap; i += kLinkThreads)
+    if (mkey[i] != kMapEmpty) atomicAdd(&a.ncount[mkey[i]], mval[i]);
+  // the root's children: this workgroup's block of indices (the root is one hot counter)
+  if (threadIdx.x == 0)
+    a.rootbase[blockIdx.x] = (uint32_t)(root_children ? atomicAdd((unsigned long long *)&a.hist[a.cap], root_children) : 0);
+}
+
+// Nodes grouped by parent: position = start of the parent's group (prefix sums of the
+// child counts) + the node's index among its siblings.  Groups too large to be sorted
+// by chunk are listed.
+__global__ __launch_bounds__(256) void scatter_kernel(TrieArgs a) {
+  const int64_t X = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (X >= (int64_t)a.cap || a.tkey[X] == 0) return;
+  const uint32_t P = a.nparent[X], ci = a.cidx[X];
+  const uint64_t c = P == (uint32_t)a.cap ? a.rootbase[ci >> 22] + (ci & ((1u << 22) - 1)) : ci;
+  const uint64_t g0 = a.gstart[P], n = a.hist[P];
+  const uint64_t pos = g0 + c;
+  a.grouped[pos] = (uint32_t)X;
+  a.posof[X] = (uint32_t)pos;
+  if (c == 0 && n > (uint64_t)kChunk) {
+    const unsigned long long i = atomicAdd(&a.ctr[kListLarge], 1ull);
+    if ((int64_t)i < a.large_cap) {
+      a.lists[kListLarge * a.list_cap + i] = (g0 << 32) | n;
+      a.lgroup[P] = (uint32_t)i;
+    } else {
+      fail(a);
+    }
+  }
+}
+
+// ---- sibling order ------------------------------------------------------------------
+// a node's block: frames at the representative's store block, and their number
+__device__ inline void node_block(const TrieArgs &a, uint32_t X, u32x4 (&v)[4], uint32_t &nf) {
+  const uint64_t info = a.tinfo[X];
+  const u32x4 *p = (const u32x4 *)(a.pframes + (info >> 32) * kBlk);
+#pragma unroll
+  for (int c = 0; c < 4; ++c) v[c] = p[c];
+  nf = block_frames((uint32_t)info);
+}
+
+// block x < block y (LDS rows of 16 frames)
+__device__ inline bool block_less(const uint32_t *x, uint32_t nx, const uint32_t *y, uint32_t ny) {
+  const uint32_t n = min(nx, ny);
+  for (uint32_t c = 0; c < 4 * 4; c += 4) {
+    const u32x4 vx = *(const u32x4 *)(x + c), vy = *(const u32x4 *)(y + c);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (c + e >= n) return nx < ny;
+      if (vx[e] != vy[e]) return vx[e] < vy[e];
+    }
+  }
+  return nx < ny;
+}
+
+// Bitonic sort of n <= 2048 LDS entries: si holds entry indices, padded with kNone
+// (+inf); lt(p, q) orders two entries.
+template <class Less>
+__device__ inline void lds_bitonic(uint16_t *si, int n, Less lt) {
+  int n2 = 1;
+  while (n2 < n) n2 <<= 1;
+  for (int i = threadIdx.x; i < n2; i += blockDim.x) si[i] = i < n ? (uint16_t)i : kNone;
+  __syncthreads();
+  for (int k = 2; k <= n2; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int t = threadIdx.x; t < n2 / 2; t += blockDim.x) {
+        const int i0 = 2 * j * (t / j) + (t % j), i1 = i0 + j;
+        const uint16_t x = si[i0], y = si[i1];
+        auto less = [&](uint16_t p, uint16_t q) { return p != kNone && (q == kNone || lt(p, q)); };
+        // ascending where (i0 & k) == 0, else descending
+        if ((i0 & k) == 0 ? less(y, x) : less(x, y)) { si[i0] = y; si[i1] = x; }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+constexpr int kMedThreads = 1024;
+struct MedShared {
+  uint32_t sb[kMedium][kBlk];
+  uint8_t sn[kMedium];
+  uint16_t si[kMedium];
+};
+
+// Groups of 2 .. 1024 siblings, by chunk: workgroup c orders every such group whose
+// start lies in positions [1024 c, 1024 c + 1024) -- at most 2047 consecutive
+// positions.  Their members (singleton groups skipped) are staged in LDS and sorted
+// together by (group start, block) with one bitonic sort.
+struct ChunkShared {
+  MedShared m;
+  uint32_t gkey[kMedium];  // group start of each staged member
+  uint16_t pos[kMedium];   // its chunk-local position
+  uint32_t first, last_end, count;
+};
+
+__global__ __launch_bounds__(kMedThreads) void chunk_kernel(TrieArgs a) {
+  __shared__ ChunkShared C;
+  const uint64_t nodes = a.gstart[a.cap + 1];
+  const uint64_t lo = (uint64_t)blockIdx.x * kChunk;
+  if (lo >= nodes) return;
+  if (threadIdx.x == 0) { C.first = 0xFFFFFFFFu; C.last_end = 0; C.count = 0; }
+  __syncthreads();
+  {
+    const uint64_t p = lo + threadIdx.x;
+    if (threadIdx.x < kChunk && p < nodes) {
+      const uint32_t P = a.nparent[a.grouped[p]];
+      const uint64_t g0 = a.gstart[P], n = a.hist[P];
+      if (g0 == p && n >= 2 && n <= (uint64_t)kChunk) {
+        atomicMin(&C.first, (uint32_t)p);
+        atomicMax(&C.last_end, (uint32_t)(p + n));
+      }
+    }
+  }
+  __syncthreads();
+  if (C.first == 0xFFFFFFFFu) return;
+  const uint32_t first = C.first, m = C.last_end - first;
+  for (uint32_t i = threadIdx.x; i < m; i += kMedThreads) {
+    const uint32_t X = a.grouped[first + i];
+    const uint32_t P = a.nparent[X];
+    if (a.hist[P] < 2) continue;
+    const uint32_t k = atomicAdd(&C.count, 1u);
+    u32x4 v[4];
+    uint32_t nf;
+    node_block(a, X, v, nf);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) *(u32x4 *)&C.m.sb[k][4 * c] = v[c];
+    C.m.sn[k] = (uint8_t)nf;
+    C.gkey[k] = (uint32_t)a.gstart[P];
+    C.pos[k] = (uint16_t)i;
+  }
+  __syncthreads();
+  const uint32_t cnt = C.count;
+  lds_bitonic(C.m.si, (int)cnt, [&](uint16_t p, uint16_t q) {
+    return C.gkey[p] != C.gkey[q] ? C.gkey[p] < C.gkey[q] : block_less(C.m.sb[p], C.m.sn[p], C.m.sb[q], C.m.sn[q]);
+  });
+  // a member of rank r in the sorted order goes to its group's start + (r - the rank of
+  // the group's first member); every original position is read before any write
+  uint32_t Xs[kMedium / kMedThreads];
+  for (uint32_t r = threadIdx.x, q = 0; r < cnt; r += kMedThreads, ++q) Xs[q] = a.grouped[first + C.pos[C.m.si[r]]];
+  __syncthreads();
+  for (uint32_t r = threadIdx.x, q = 0; r < cnt; r += kMedThreads, ++q) {
+    const uint32_t G = C.gkey[C.m.si[r]];
+    uint32_t lo2 = 0, hi2 = r;
+    while (lo2 < hi2) {
+      const uint32_t mid = (lo2 + hi2) >> 1;
+      if (C.gkey[C.m.si[mid]] < G) lo2 = mid + 1; else hi2 = mid;
+    }
+    const uint32_t pos = G + (r - lo2);
+    a.grouped[pos] = Xs[q];
+    a.posof[Xs[q]] = pos;
+  }
+}
+
+// Buckets of large groups (2 .. 2048 siblings): one workgroup each, blocks in LDS.
+__global__ __launch_bounds__(kMedThreads) void medium_kernel(TrieArgs a) {
+  __shared__ MedShared S;
+  const uint64_t ng = min((uint64_t)a.ctr[kListMedium], (uint64_t)a.list_cap);
+  for (uint64_t g = blockIdx.x; g < ng; g += gridDim.x) {
+    const uint64_t e = a.lists[kListMedium * a.list_cap + g];
+    const uint32_t start = (uint32_t)(e >> 32), n = (uint32_t)e;
+    for (uint32_t i = threadIdx.x; i < n; i += kMedThreads) {
+      u32x4 v[4];
+      uint32_t nf;
+      node_block(a, a.grouped[start + i], v, nf);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) *(u32x4 *)&S.sb[i][4 * c] = v[c];
+      S.sn[i] = (uint8_t)nf;
+    }
+    __syncthreads();
+    lds_bitonic(S.si, (int)n, [&](uint16_t p, uint16_t q) { return block_less(S.sb[p], S.sn[p], S.sb[q], S.sn[q]); });
+    // grouped[start + i] still holds the unsorted members (read before any write)
+    uint32_t Xs[kMedium / kMedThreads];
+    for (uint32_t i = threadIdx.x, q = 0; i < n; i += kMedThreads, ++q) Xs[q] = a.grouped[start + S.si[i]];
+    __syncthreads();
+    for (uint32_t i = threadIdx.x, q = 0; i < n; i += kMedThreads, ++q) {
+      a.grouped[start + i] = Xs[q];
+      a.posof[Xs[q]] = start + i;
+    }
+    __syncthreads();
+  }
+}
+
+// Groups of more than 1024 siblings are cut into ordered buckets: splitters from a
+// sorted sample (4 per bucket, aiming at buckets of about 32), every member's bucket
+// by binary search over the splitters, the group reordered by bucket; every bucket is
+// then a group of its own, ordered by one wave (up to 64) or one workgroup.
+constexpr int kMaxBuckets = 256, kOversample = 4, kBucketTarget = 32;
+
+__device__ inline int buckets_for(uint32_t n) {
+  int nb = 2;
+  while (nb < kMaxBuckets && (uint32_t)nb * kBucketTarget < n) nb <<= 1;
+  return nb;
+}
+
+// one workgroup per large group: sorted sample -> splitters (node ids)
+__global__ __launch_bounds__(kMedThreads) void split_kernel(TrieArgs a) {
+  __shared__ MedShared S;
+  const uint64_t ng = min((uint64_t)a.ctr[kListLarge], (uint64_t)a.large_cap);
+  for (uint64_t g = blockIdx.x; g < ng; g += gridDim.x) {
+    const uint64_t e = a.lists[kListLarge * a.list_cap + g];
+    const uint32_t start = (uint32_t)(e >> 32), n = (uint32_t)e;
+    const int nb = buckets_for(n), ns = nb * kOversample;
+    for (int i = threadIdx.x; i < ns; i += kMedThreads) {
+      const uint32_t X = a.grouped[start + (uint64_t)i * n / ns];
+      u32x4 v[4];
+      uint32_t nf;
+      node_block(a, X, v, nf);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) *(u32x4 *)&S.sb[i][4 * c] = v[c];
+      S.sn[i] = (uint8_t)nf;
+    }
+    __syncthreads();
+    lds_bitonic(S.si, ns, [&](uint16_t p, uint16_t q) { return block_less(S.sb[p], S.sn[p], S.sb[q], S.sn[q]); });
+    // splitter j (j = 0 .. nb - 2) is the sample at sorted position (j + 1) * kOversample
+    for (int j = threadIdx.x; j < nb - 1; j += kMedThreads)
+      a.spl[g * kMaxBuckets + j] = a.grouped[start + (uint64_t)S.si[(j + 1) * kOversample] * n / ns];
+    __syncthreads();
+  }
+}
+
+// every member of a large group: its bucket (number of splitters below it), kept in
+// posof until the member's position is known; bucket sizes counted per group
+struct ClassShared {
+  uint32_t sb[2][kMaxBuckets][kBlk];
+  uint8_t sn[2][kMaxBuckets];
+  uint32_t grp[2];
+};
+__global__ __launch_bounds__(kMedThreads) void classify_kernel(TrieArgs a) {
+  __shared__ ClassShared C;
+  const uint64_t nodes = a.gstart[a.cap + 1];
+  const uint64_t lo = (uint64_t)blockIdx.x * kChunk;
+  if (lo >= nodes) return;
+  const uint64_t p = lo + threadIdx.x;
+  uint32_t X = 0, P = 0, g = 0xFFFFFFFFu;
+  if (threadIdx.x < kChunk && p < nodes) {
+    X = a.grouped[p];
+    P = a.nparent[X];
+    if (a.hist[P] > (uint64_t)kChunk) {
+      g = a.lgroup[P];  // listed large group (an unlisted one has already failed the call)
+      if ((uint64_t)g >= min((uint64_t)a.ctr[kListLarge], (uint64_t)a.large_cap)) g = 0xFFFFFFFFu;
+    }
+  }
+  // at most two large groups overlap 1024 consecutive positions: the first and last
+  // position's
+  if (threadIdx.x == 0) { C.grp[0] = 0xFFFFFFFFu; C.grp[1] = 0xFFFFFFFFu; }
+  __syncthreads();
+  const uint64_t last = min(lo + kChunk, nodes) - 1;
+  if (p == lo) C.grp[0] = g;
+  if (p == last) C.grp[1] = g;
+  __syncthreads();
+  for (int h = 0; h < 2; ++h) {
+    const uint32_t gh = C.grp[h];
+    if (gh == 0xFFFFFFFFu) continue;
+    const uint64_t e = a.lists[kListLarge * a.list_cap + gh];
+    const int nb = buckets_for((uint32_t)e);
+    for (int j = threadIdx.x; j < nb - 1; j += kMedThreads) {
+      u32x4 v[4];
+      uint32_t nf;
+      node_block(a, a.spl[gh * kMaxBuckets + j], v, nf);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) *(u32x4 *)&C.sb[h][j][4 * c] = v[c];
+      C.sn[h][j] = (uint8_t)nf;
+    }
+  }
+  __syncthreads();
+  if (g == 0xFFFFFFFFu) return;
+  const int h = g == C.grp[0] ? 0 : 1;
+  const int nb = buckets_for((uint32_t)a.lists[kListLarge * a.list_cap + g]);
+  u32x4 v[4];
+  uint32_t nf;
+  node_block(a, X, v, nf);
+  uint32_t x[kBlk];
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) x[4 * c + q] = v[c][q];
+  int blo = 0, bhi = nb - 1;
+  while (blo < bhi) {
+    const int mid = (blo + bhi) >> 1;
+    if (block_less(C.sb[h][mid], C.sn[h][mid], x, nf)) blo = mid + 1; else bhi = mid;
+  }
+  a.posof[X] = (uint32_t)blo;
+  atomicAdd(&a.bcnt[g * kMaxBuckets + blo], 1u);
+}
+
+// one workgroup per large group: reorder by bucket, list the buckets
+struct ReorderShared {
+  uint32_t bstart[kMaxBuckets], bcur[kMaxBuckets];
+};
+__global__ __launch_bounds__(kMedThreads) void reorder_kernel(TrieArgs a) {
+  __shared__ ReorderShared R;
+  const uint64_t ng = min((uint64_t)a.ctr[kListLarge], (uint64_t)a.large_cap);
+  for (uint64_t g = blockIdx.x; g < ng; g += gridDim.x) {
+    const uint64_t e = a.lists[kListLarge * a.list_cap + g];
+    const uint32_t start = (uint32_t)(e >> 32), n = (uint32_t)e;
+    const int nb = buckets_for(n);
+    if (threadIdx.x == 0) {
+      uint32_t run = 0;
+      for (int j = 0; j < nb; ++j) { R.bstart[j] = run; run += a.bcnt[g * kMaxBuckets + j]; }
+    }
+    for (int j = threadIdx.x; j < nb; j += kMedThreads) R.bcur[j] = 0;
+    __syncthreads();
+    for (uint32_t i = threadIdx.x; i < n; i += kMedThreads) {
+      const uint32_t X = a.grouped[start + i];
+      const uint32_t bk = a.posof[X];
+      a.grouped2[start + R.bstart[bk] + atomicAdd(&R.bcur[bk], 1u)] = X;
+    }
+    __syncthreads();
+    for (uint32_t i = threadIdx.x; i < n; i += kMedThreads) {
+      const uint32_t X = a.grouped2[start + i];
+      a.grouped[start + i] = X;
+      a.posof[X] = start + i;
+    }
+    for (int j = threadIdx.x; j < nb; j += kMedThreads) {
+      const uint32_t c = a.bcnt[g * kMaxBuckets + j];
+      if (c < 2) continue;
+      if (c > (uint32_t)kMedium) { fail(a); continue; }
+      const int cls = c <= 64 ? kListSmall : kListMedium;
+      const unsigned long long i = atomicAdd(&a.ctr[cls], 1ull);
+      if ((int64_t)i < a.list_cap) a.lists[cls * a.list_cap + i] = ((uint64_t)(start + R.bstart[j]) << 32) | c;
+      else fail(a);
+    }
+    __syncthreads();
+  }
+}
+
+// buckets of up to 64: one wave each, every member counts the members before it
+constexpr int kBucketWaves = 4;
+__global__ __launch_bounds__(64 * kBucketWaves) void bucket_kernel(TrieArgs a) {
+  __shared__ uint32_t sb[kBucketWaves][64][kBlk];
+  __shared__ uint32_t sn[kBucketWaves][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const uint64_t ng = min((uint64_t)a.ctr[kListSmall], (uint64_t)a.list_cap);
+  for (uint64_t g = (uint64_t)blockIdx.x * kBucketWaves + w; g < ng; g += (uint64_t)gridDim.x * kBucketWaves) {
+    const uint64_t e = a.lists[kListSmall * a.list_cap + g];
+    const uint32_t start = (uint32_t)(e >> 32), n = (uint32_t)e;
+    uint32_t X = 0;
+    if (lane < (int)n) {
+      X = a.grouped[start + lane];
+      u32x4 v[4];
+      uint32_t nf;
+      node_block(a, X, v, nf);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) *(u32x4 *)&sb[w][lane][4 * c] = v[c];
+      sn[w][lane] = nf;
+    }
+    wave_sync();
+    if (lane < (int)n) {
+      uint32_t rank = 0;
+      for (uint32_t j = 0; j < n; ++j)
+        if (j != (uint32_t)lane && block_less(sb[w][j], sn[w][j], sb[w][lane], sn[w][lane])) ++rank;
+      a.grouped[start + rank] = X;
+      a.posof[X] = start + rank;
+    }
+    wave_sync();
+  }
+}
+
+// path counts in grouped order (zero past the last node)
+__global__ void counts_kernel(TrieArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= a.nblocks) return;
+  const uint64_t nodes = a.gstart[a.cap + 1];
+  a.cnt[i] = (uint64_t)i < nodes ? a.ncount[a.grouped[i]] : 0;
+}
+
+__global__ void rank_kernel(TrieArgs a) {
+  const int64_t d = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (d >= a.d) return;
+  const uint32_t len = a.plen[d];
+  uint64_t rank = 0;
+  uint32_t prev = (uint32_t)a.cap;
+  const int64_t b0 = a.pstart[d] / kBlk, nb = (len + kBlk - 1) / kBlk;
+  for (int64_t k = 0; k < nb; ++k) {
+    const uint32_t X = a.occ[b0 + k];
+    rank += a.cnt_scan[a.posof[X]] - a.cnt_scan[a.gstart[a.nparent[X]]] + a.nend[prev];
+    prev = X;
+  }
+  if (rank < (uint64_t)a.d) a.order[rank] = (uint32_t)d;
+  else fail(a);
+}
+
+inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
+
+}  // namespace
+
+void launch_trie_sort(const TrieArgs &a, hipStream_t s) {
+  if (a.d <= 0) return;
+  (void)hipMemsetAsync(a.ctr, 0, 8 * sizeof(unsigned long long), s);
+  (void)hipMemsetAsync(a.tkey, 0, a.cap * 8, s);
+  (void)hipMemsetAsync(a.ncount, 0, a.cap * 4, s);
+  (void)hipMemsetAsync(a.nend, 0, (a.cap + 1) * 4, s);
+  (void)hipMemsetAsync(a.hist, 0, (a.cap + 1) * 8, s);
+  (void)hipMemsetAsync(a.bcnt, 0, (size_t)a.large_cap * kMaxBuckets * 4, s);
+  hipLaunchKernelGGL(fill_kernel, dim3(blocks_for(a.d, 256)), dim3(256), 0, s, a);
+  if (a.nblocks > 0) {
+    hipLaunchKernelGGL(insert_kernel, dim3(blocks_for(a.nblocks, 256)), dim3(256), 0, s, a);
+    const int64_t link_grid = std::max<int64_t>(1, std::min<int64_t>(blocks_for(a.nblocks, 4096), 1024));
+    hipLaunchKernelGGL(link_kernel, dim3((unsigned)link_grid), dim3(kLinkThreads), 0, s, a);
+    launch_scan(a.hist, (int64_t)a.cap + 1, 1, a.scan_blk, a.gstart, s);
+    hipLaunchKernelGGL(scatter_kernel, dim3(blocks_for((int64_t)a.cap, 256)), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(chunk_kernel, dim3(blocks_for(a.nblocks, kChunk)), dim3(kMedThreads), 0, s, a);
+    hipLaunchKernelGGL(split_kernel, dim3(256), dim3(kMedThreads), 0, s, a);
+    hipLaunchKernelGGL(classify_kernel, dim3(blocks_for(a.nblocks, kChunk)), dim3(kMedThreads), 0, s, a);
+    hipLaunchKernelGGL(reorder_kernel, dim3(256), dim3(kMedThreads), 0, s, a);
+    hipLaunchKernelGGL(bucket_kernel, dim3(1024), dim3(64 * kBucketWaves), 0, s, a);
+    hipLaunchKernelGGL(medium_kernel, dim3(256), dim3(kMedThreads), 0, s, a);
+    hipLaunchKernelGGL(counts_kernel, dim3(blocks_for(a.nblocks, 256)), dim3(256), 0, s, a);
+    launch_scan(a.cnt, a.nblocks, 1, a.scan_blk, a.cnt_scan, s);
+  }
+  hipLaunchKernelGGL(rank_kernel, dim3(blocks_for(a.d, 256)), dim3(256), 0, s, a);
+}
+
+}  // namespace cct

@@ -140,6 +140,35 @@ def test_forced_collisions_through_cache(monkeypatch, bits):
     assert_same(gpu_tree(o, f, w), oracle.build_tree(o, f, w), f"bits={bits}")
 
 
+@pytest.mark.parametrize("case", ["tiny", "layered_1m_part", "deep_part", "random_small", "random_paths", "long"])
+def test_block_trie_order(monkeypatch, case):
+    # the block-trie ranking must be usable (no fallback) and agree with the oracle and
+    # with the comparison sort
+    if case == "tiny":
+        o, f, w = tracegen.generate("tiny")
+    elif case == "layered_1m_part":
+        o, f, w = tracegen.generate("layered_1m", n_events=200_000)
+    elif case == "deep_part":
+        o, f, w = tracegen.generate("deep_recursion", n_events=30_000)
+    elif case == "random_small":
+        o, f, w = tracegen.random_small(5000, 16, 9, 1, seed=77)
+    elif case == "random_paths":
+        o, f, w = tracegen.random_paths(20_000, 40, 70, 2, seed=78)
+    else:  # paths of every length 0..300 over 3 frame ids: many full and partial blocks
+        lens = np.arange(301)
+        rng = np.random.default_rng(79)
+        o = np.zeros(lens.size + 1, np.int64)
+        o[1:] = np.cumsum(lens)
+        f = rng.integers(0, 3, int(o[-1])).astype(np.uint32)
+        w = rng.integers(0, 1000, (lens.size, 1)).astype(np.uint64)
+    want = oracle.build_tree(o, f, w)
+    monkeypatch.setenv("CCT_TEST_REQUIRE_TRIE", "1")
+    assert_same(gpu_tree(o, f, w), want, f"{case} trie")
+    monkeypatch.delenv("CCT_TEST_REQUIRE_TRIE")
+    monkeypatch.setenv("CCT_TEST_MERGE_SORT", "1")
+    assert_same(gpu_tree(o, f, w), want, f"{case} comparison sort")
+
+
 def test_forced_table_overflow_regrows(monkeypatch):
     monkeypatch.setenv("CCT_TEST_TABLE_CAP", "16")
     o, f, w = tracegen.random_paths(5000, 500, 12, 1, seed=9)
