@@ -27,10 +27,12 @@ namespace {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kBlk = kStoreAlign;           // frames per block
-constexpr int kChunk = 1024;                // groups up to this size are sorted by chunk
+constexpr int kChunk = 512;                 // groups up to this size are sorted by chunk
+constexpr int kChunkCap = 2 * kChunk;       // staged members of one chunk (at most 2 kChunk - 1)
 constexpr int kMedium = 2048;               // LDS sort capacity of one workgroup
 constexpr uint64_t kRootSeed = 0x5851F42D4C957F2Dull;
 constexpr uint16_t kNone = 0xFFFFu;
+constexpr int kMaxBuckets = 256, kOversample = 2, kBucketTarget = 32;  // large groups (split_kernel)
 enum { kListSmall = 0, kListMedium = 1, kListLarge = 2, kFail = 3 };
 
 __device__ inline void fail(const TrieArgs &a) { atomicOr(&a.ctr[kFail], 1ull); }
@@ -57,6 +59,18 @@ __device__ inline BlockPos block_pos(const TrieArgs &a, int64_t s) {
 }
 // frames in a node's block (1..16), from its depth
 __device__ inline uint32_t block_frames(uint32_t depth) { return ((depth - 1) & (kBlk - 1)) + 1; }
+
+// zero the node table, counts, end flags, child counts, bucket counts and counters
+__global__ void clear_kernel(TrieArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i <= (int64_t)a.cap) {
+    if (i < (int64_t)a.cap) { a.tkey[i] = 0; a.ncount[i] = 0; }
+    a.nend[i] = 0;
+    a.hist[i] = 0;
+  }
+  if (i < a.large_cap * kMaxBuckets) a.bcnt[i] = 0;
+  if (i < 8) a.ctr[i] = 0;
+}
 
 __global__ void fill_kernel(TrieArgs a) {
   const int64_t d = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -263,18 +277,21 @@ struct MedShared {
   uint16_t si[kMedium];
 };
 
-// Groups of 2 .. 1024 siblings, by chunk: workgroup c orders every such group whose
-// start lies in positions [1024 c, 1024 c + 1024) -- at most 2047 consecutive
+// Groups of 2 .. 512 siblings, by chunk: workgroup c orders every such group whose
+// start lies in positions [512 c, 512 c + 512) -- at most 1023 consecutive
 // positions.  Their members (singleton groups skipped) are staged in LDS and sorted
 // together by (group start, block) with one bitonic sort.
 struct ChunkShared {
-  MedShared m;
-  uint32_t gkey[kMedium];  // group start of each staged member
-  uint16_t pos[kMedium];   // its chunk-local position
+  uint32_t sb[kChunkCap][kBlk];
+  uint8_t sn[kChunkCap];
+  uint16_t si[kChunkCap];
+  uint32_t gkey[kChunkCap];  // group start of each staged member
+  uint16_t pos[kChunkCap];   // its chunk-local position
   uint32_t first, last_end, count;
 };
 
-__global__ __launch_bounds__(kMedThreads) void chunk_kernel(TrieArgs a) {
+constexpr int kChunkThreads = 512;
+__global__ __launch_bounds__(kChunkThreads) void chunk_kernel(TrieArgs a) {
   __shared__ ChunkShared C;
   const uint64_t nodes = a.gstart[a.cap + 1];
   const uint64_t lo = (uint64_t)blockIdx.x * kChunk;
@@ -295,7 +312,7 @@ __global__ __launch_bounds__(kMedThreads) void chunk_kernel(TrieArgs a) {
   __syncthreads();
   if (C.first == 0xFFFFFFFFu) return;
   const uint32_t first = C.first, m = C.last_end - first;
-  for (uint32_t i = threadIdx.x; i < m; i += kMedThreads) {
+  for (uint32_t i = threadIdx.x; i < m; i += kChunkThreads) {
     const uint32_t X = a.grouped[first + i];
     const uint32_t P = a.nparent[X];
     if (a.hist[P] < 2) continue;
@@ -304,27 +321,27 @@ __global__ __launch_bounds__(kMedThreads) void chunk_kernel(TrieArgs a) {
     uint32_t nf;
     node_block(a, X, v, nf);
 #pragma unroll
-    for (int c = 0; c < 4; ++c) *(u32x4 *)&C.m.sb[k][4 * c] = v[c];
-    C.m.sn[k] = (uint8_t)nf;
+    for (int c = 0; c < 4; ++c) *(u32x4 *)&C.sb[k][4 * c] = v[c];
+    C.sn[k] = (uint8_t)nf;
     C.gkey[k] = (uint32_t)a.gstart[P];
     C.pos[k] = (uint16_t)i;
   }
   __syncthreads();
   const uint32_t cnt = C.count;
-  lds_bitonic(C.m.si, (int)cnt, [&](uint16_t p, uint16_t q) {
-    return C.gkey[p] != C.gkey[q] ? C.gkey[p] < C.gkey[q] : block_less(C.m.sb[p], C.m.sn[p], C.m.sb[q], C.m.sn[q]);
+  lds_bitonic(C.si, (int)cnt, [&](uint16_t p, uint16_t q) {
+    return C.gkey[p] != C.gkey[q] ? C.gkey[p] < C.gkey[q] : block_less(C.sb[p], C.sn[p], C.sb[q], C.sn[q]);
   });
   // a member of rank r in the sorted order goes to its group's start + (r - the rank of
   // the group's first member); every original position is read before any write
-  uint32_t Xs[kMedium / kMedThreads];
-  for (uint32_t r = threadIdx.x, q = 0; r < cnt; r += kMedThreads, ++q) Xs[q] = a.grouped[first + C.pos[C.m.si[r]]];
+  uint32_t Xs[kChunkCap / kChunkThreads];
+  for (uint32_t r = threadIdx.x, q = 0; r < cnt; r += kChunkThreads, ++q) Xs[q] = a.grouped[first + C.pos[C.si[r]]];
   __syncthreads();
-  for (uint32_t r = threadIdx.x, q = 0; r < cnt; r += kMedThreads, ++q) {
-    const uint32_t G = C.gkey[C.m.si[r]];
+  for (uint32_t r = threadIdx.x, q = 0; r < cnt; r += kChunkThreads, ++q) {
+    const uint32_t G = C.gkey[C.si[r]];
     uint32_t lo2 = 0, hi2 = r;
     while (lo2 < hi2) {
       const uint32_t mid = (lo2 + hi2) >> 1;
-      if (C.gkey[C.m.si[mid]] < G) lo2 = mid + 1; else hi2 = mid;
+      if (C.gkey[C.si[mid]] < G) lo2 = mid + 1; else hi2 = mid;
     }
     const uint32_t pos = G + (r - lo2);
     a.grouped[pos] = Xs[q];
@@ -361,11 +378,10 @@ __global__ __launch_bounds__(kMedThreads) void medium_kernel(TrieArgs a) {
   }
 }
 
-// Groups of more than 1024 siblings are cut into ordered buckets: splitters from a
-// sorted sample (4 per bucket, aiming at buckets of about 32), every member's bucket
+// Groups of more than 512 siblings are cut into ordered buckets: splitters from a
+// sorted sample (2 per bucket, aiming at buckets of about 32), every member's bucket
 // by binary search over the splitters, the group reordered by bucket; every bucket is
 // then a group of its own, ordered by one wave (up to 64) or one workgroup.
-constexpr int kMaxBuckets = 256, kOversample = 4, kBucketTarget = 32;
 
 __device__ inline int buckets_for(uint32_t n) {
   int nb = 2;
@@ -567,12 +583,7 @@ inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1)
 
 void launch_trie_sort(const TrieArgs &a, hipStream_t s) {
   if (a.d <= 0) return;
-  (void)hipMemsetAsync(a.ctr, 0, 8 * sizeof(unsigned long long), s);
-  (void)hipMemsetAsync(a.tkey, 0, a.cap * 8, s);
-  (void)hipMemsetAsync(a.ncount, 0, a.cap * 4, s);
-  (void)hipMemsetAsync(a.nend, 0, (a.cap + 1) * 4, s);
-  (void)hipMemsetAsync(a.hist, 0, (a.cap + 1) * 8, s);
-  (void)hipMemsetAsync(a.bcnt, 0, (size_t)a.large_cap * kMaxBuckets * 4, s);
+  hipLaunchKernelGGL(clear_kernel, dim3(blocks_for((int64_t)a.cap + 1, 256)), dim3(256), 0, s, a);
   hipLaunchKernelGGL(fill_kernel, dim3(blocks_for(a.d, 256)), dim3(256), 0, s, a);
   if (a.nblocks > 0) {
     hipLaunchKernelGGL(insert_kernel, dim3(blocks_for(a.nblocks, 256)), dim3(256), 0, s, a);
@@ -580,7 +591,7 @@ void launch_trie_sort(const TrieArgs &a, hipStream_t s) {
     hipLaunchKernelGGL(link_kernel, dim3((unsigned)link_grid), dim3(kLinkThreads), 0, s, a);
     launch_scan(a.hist, (int64_t)a.cap + 1, 1, a.scan_blk, a.gstart, s);
     hipLaunchKernelGGL(scatter_kernel, dim3(blocks_for((int64_t)a.cap, 256)), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(chunk_kernel, dim3(blocks_for(a.nblocks, kChunk)), dim3(kMedThreads), 0, s, a);
+    hipLaunchKernelGGL(chunk_kernel, dim3(blocks_for(a.nblocks, kChunk)), dim3(kChunkThreads), 0, s, a);
     hipLaunchKernelGGL(split_kernel, dim3(256), dim3(kMedThreads), 0, s, a);
     hipLaunchKernelGGL(classify_kernel, dim3(blocks_for(a.nblocks, kChunk)), dim3(kMedThreads), 0, s, a);
     hipLaunchKernelGGL(reorder_kernel, dim3(256), dim3(kMedThreads), 0, s, a);
