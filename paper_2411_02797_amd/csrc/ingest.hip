@@ -10,15 +10,15 @@
 // their paths are equal frame by frame, which is exactly when the paper's tree
 // insertion would end them on the same node.
 //
-// Work decomposition of the hashing pass: one workgroup of 16 waves per CU,
+// Work decomposition of the hashing pass: one workgroup of 12 waves per CU,
 // persistent.  Every wave owns a contiguous range of events and cuts it into tiles
-// of at most 63 events whose paths, cut into blocks of 16 frames, fill at most its 64
-// lanes: lane l holds one block (16 consecutive frames of one event) in registers,
-// loaded with four 16-byte buffer loads (the buffer's range check makes reads past
-// the end of the batch return zero).  Consecutive lanes hold consecutive blocks, so
-// a wave's loads cover a contiguous stretch of the batch.  Workgroups need no
-// barriers, so a CU keeps 16 tiles in flight; while a wave resolves tile t, the
-// frames of tile t+1 stream into registers.
+// of at most 63 events whose paths, cut into blocks of 16 frames, fill at most 128
+// blocks: lane l holds blocks l and l + 64 (16 consecutive frames of one event each)
+// in registers, loaded with four 16-byte buffer loads per block (the buffer's range
+// check makes reads past the end of the batch return zero).  Consecutive lanes hold
+// consecutive blocks, so a wave's loads cover a contiguous stretch of the batch.
+// Waves need no barriers, so a CU keeps 12 tiles in flight; a wave requests tile
+// t+1's frames once tile t's table and candidate loads have returned.
 //   - hash: a path's hash is a sum over its frames of a term of (frame, position in
 //     the path); a lane sums its block, and the block sums of an event meet in LDS.
 //     A block knows its position in the path, so no lane ever looks for an event
@@ -184,10 +184,14 @@ __device__ inline Tile make_tile(const IngestArgs &a, WaveShared &W, int64_t e, 
 
 // Buffer resource over the batch's frames from the tile's first frame on: loads past
 // the end of the batch return zero.
+// The descriptor is wave-uniform; its words are read from the first lane so that the
+// compiler keeps it in scalar registers (a descriptor it believes divergent costs a
+// loop around every load).
 __device__ inline __amdgpu_buffer_rsrc_t tile_rsrc(const IngestArgs &a, const Tile &t) {
-  const int64_t avail = a.n_frames - t.g0;
-  const int bytes = (int)(avail < (1 << 28) ? avail * 4 : (1 << 30));
-  return __builtin_amdgcn_make_buffer_rsrc((void *)(a.fr + t.g0), (short)0, bytes, 0x00020000);
+  const int64_t g0 = uniform64(t.g0);
+  const int64_t avail = a.n_frames - g0;
+  const int bytes = __builtin_amdgcn_readfirstlane((int)(avail < (1 << 28) ? avail * 4 : (1 << 30)));
+  return __builtin_amdgcn_make_buffer_rsrc((void *)(a.fr + g0), (short)0, bytes, 0x00020000);
 }
 
 // This lane's blocks: four 16-byte loads each; a 16-byte load that would reach past
@@ -370,7 +374,7 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
   __syncthreads();
 
   // this wave's events.  Pipeline: the offsets window of tile t+1 is loaded during
-  // tile t-1, so tile t+1's frames can be requested while tile t resolves.
+  // tile t-1, so tile t+1 can be cut as soon as tile t has resolved.
   const int64_t waves_total = (int64_t)gridDim.x * kWaves, w = (int64_t)blockIdx.x * kWaves + wave;
   const int64_t end = (w + 1) * a.n_events / waves_total;
   int64_t o_cur = load_window(a, w * a.n_events / waves_total, end, lane);
@@ -452,12 +456,6 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
       }
     }
 
-    // the next tile's frames, and the offsets window after it, stream in while this
-    // tile resolves
-    const Tile tn = make_tile(a, W, e_nxt, end, o_nxt, lane, b);
-    load_blocks(a, tn, b, nf);
-    const int64_t o_nn = tn.kind == kTileFast || tn.kind == kTileSlow ? load_window(a, tn.e0 + tn.ne, end, lane) : 0;
-
     for (;;) {
       if (p.state == kProbing) probe(a, p, e0 + lane, o_cur, (int64_t)p.len);
       if (!__any(p.state == kCandidate)) break;
@@ -532,6 +530,12 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
       }
       wave_sync();
     }
+    // the next tile's frames, and the offsets window after it, are requested only now:
+    // vector-memory loads retire in order, so a table or candidate load issued after
+    // them would wait for the whole next tile to arrive
+    const Tile tn = make_tile(a, W, e_nxt, end, o_nxt, lane, b);
+    load_blocks(a, tn, b, nf);
+    const int64_t o_nn = tn.kind == kTileFast || tn.kind == kTileSlow ? load_window(a, tn.e0 + tn.ne, end, lane) : 0;
     if (lane < ne) {
       if (p.state == kResolved && !cached) cache_insert(S, p.h, p.len, p.slot, p.cbase);
       a.slot_of[e0 + lane] = p.state == kResolved ? p.slot : kNoSlot;
@@ -546,51 +550,72 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
 // range and sums into an LDS map keyed by slot (a hot path costs one HBM atomic per
 // metric per workgroup), falling back to HBM atomics when a key's probe window is
 // full.  A key already in the map is found with plain LDS reads (broadcast), so hot
-// keys cost no atomic compare-and-swap.
+// keys cost no atomic compare-and-swap.  Every thread takes kAggUnroll events per
+// round and issues all their loads (slot, then the metric row) before touching LDS,
+// so a wave keeps kAggUnroll rows in flight.  M is a template parameter: the row is
+// loaded as M consecutive 8-byte words, which the compiler merges into wide loads.
 constexpr int kAggThreads = 1024;
+constexpr int kAggUnroll = 4;
 constexpr int kAggWords = 16384;  // LDS sums (128 KiB)
 constexpr int kAggKeys = 8192;
 constexpr uint32_t kEmptyKey = 0xFFFFFFFFu;
 
-__global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const uint32_t *slot_of, const uint64_t *w, int64_t n,
-                                                                int32_t m, uint64_t *delta) {
-  __shared__ uint32_t key[kAggKeys];
-  __shared__ uint64_t sum[kAggWords];
-  const int tid = threadIdx.x;
-  int entries = kAggWords / m;
-  if (entries > kAggKeys) entries = kAggKeys;
+constexpr int agg_entries(int m) {
+  int e = kAggWords / m < kAggKeys ? kAggWords / m : kAggKeys;
   int p2 = 1;
-  while (p2 * 2 <= entries) p2 *= 2;
-  entries = p2;
-  for (int i = tid; i < kAggKeys; i += kAggThreads) key[i] = kEmptyKey;
-  for (int i = tid; i < kAggWords; i += kAggThreads) sum[i] = 0;
+  while (p2 * 2 <= e) p2 *= 2;
+  return p2;
+}
+
+template <int M>
+__global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const uint32_t *slot_of, const uint64_t *w, int64_t n,
+                                                                uint64_t *delta) {
+  constexpr int kEntries = agg_entries(M);
+  __shared__ uint32_t key[kEntries];
+  __shared__ uint64_t sum[kEntries * M];
+  const int tid = threadIdx.x;
+  for (int i = tid; i < kEntries; i += kAggThreads) key[i] = kEmptyKey;
+  for (int i = tid; i < kEntries * M; i += kAggThreads) sum[i] = 0;
   __syncthreads();
   const int64_t b = blockIdx.x, nb = gridDim.x;
   const int64_t lo = b * n / nb, hi = (b + 1) * n / nb;
-  for (int64_t e = lo + tid; e < hi; e += kAggThreads) {
-    const uint32_t s = slot_of[e];
-    if (s == kNoSlot) continue;
-    uint32_t k = hash32(s) & (uint32_t)(entries - 1);
-    int mi = -1;
-    for (int t = 0; t < 8; ++t) {
-      uint32_t cur = key[k];
-      if (cur == kEmptyKey) cur = atomicCAS(&key[k], kEmptyKey, s);
-      if (cur == kEmptyKey || cur == s) { mi = (int)k; break; }
-      k = (k + 1) & (uint32_t)(entries - 1);
+  for (int64_t e0 = lo + tid; e0 < hi; e0 += (int64_t)kAggThreads * kAggUnroll) {
+    uint32_t s[kAggUnroll];
+    uint64_t v[kAggUnroll][M];
+#pragma unroll
+    for (int u = 0; u < kAggUnroll; ++u) {
+      const int64_t e = e0 + (int64_t)u * kAggThreads;
+      const bool in = e < hi;
+      s[u] = in ? slot_of[e] : kNoSlot;
+#pragma unroll
+      for (int j = 0; j < M; ++j) v[u][j] = in ? w[e * M + j] : 0;
     }
-    for (int j = 0; j < m; ++j) {
-      const uint64_t v = w[e * m + j];
-      if (mi >= 0) atomicAdd((unsigned long long *)&sum[mi * m + j], (unsigned long long)v);
-      else atomicAdd((unsigned long long *)&delta[(uint64_t)s * m + j], (unsigned long long)v);
+#pragma unroll
+    for (int u = 0; u < kAggUnroll; ++u) {
+      if (s[u] == kNoSlot) continue;
+      uint32_t k = hash32(s[u]) & (uint32_t)(kEntries - 1);
+      int mi = -1;
+      for (int t = 0; t < 8; ++t) {
+        uint32_t cur = key[k];
+        if (cur == kEmptyKey) cur = atomicCAS(&key[k], kEmptyKey, s[u]);
+        if (cur == kEmptyKey || cur == s[u]) { mi = (int)k; break; }
+        k = (k + 1) & (uint32_t)(kEntries - 1);
+      }
+#pragma unroll
+      for (int j = 0; j < M; ++j) {
+        if (mi >= 0) atomicAdd((unsigned long long *)&sum[mi * M + j], (unsigned long long)v[u][j]);
+        else atomicAdd((unsigned long long *)&delta[(uint64_t)s[u] * M + j], (unsigned long long)v[u][j]);
+      }
     }
   }
   __syncthreads();
-  for (int k = tid; k < entries; k += kAggThreads) {
-    const uint32_t s = key[k];
-    if (s == kEmptyKey) continue;
-    for (int j = 0; j < m; ++j) {
-      const uint64_t v = sum[k * m + j];
-      if (v) atomicAdd((unsigned long long *)&delta[(uint64_t)s * m + j], (unsigned long long)v);
+  for (int k = tid; k < kEntries; k += kAggThreads) {
+    const uint32_t sk = key[k];
+    if (sk == kEmptyKey) continue;
+#pragma unroll
+    for (int j = 0; j < M; ++j) {
+      const uint64_t v = sum[k * M + j];
+      if (v) atomicAdd((unsigned long long *)&delta[(uint64_t)sk * M + j], (unsigned long long)v);
     }
   }
 }
@@ -765,7 +790,14 @@ void launch_ingest(const IngestArgs &a, int grid, hipStream_t s) {
 void launch_aggregate(const uint32_t *slot_of, const uint64_t *w, int64_t n, int32_t m, uint64_t *delta, int grid,
                       hipStream_t s) {
   if (n <= 0) return;
-  hipLaunchKernelGGL(aggregate_kernel, dim3(grid), dim3(kAggThreads), 0, s, slot_of, w, n, m, delta);
+  switch (m) {
+#define CCT_AGG_CASE(M)                                                                                      \
+  case M: hipLaunchKernelGGL(aggregate_kernel<M>, dim3(grid), dim3(kAggThreads), 0, s, slot_of, w, n, delta); break;
+    CCT_AGG_CASE(1) CCT_AGG_CASE(2) CCT_AGG_CASE(3) CCT_AGG_CASE(4)
+    CCT_AGG_CASE(5) CCT_AGG_CASE(6) CCT_AGG_CASE(7) CCT_AGG_CASE(8)
+#undef CCT_AGG_CASE
+    default: break;
+  }
 }
 int64_t collect_blocks(uint64_t cap) { return (int64_t)((cap + kCollectThreads * kCollectPerThread - 1) /
                                                          (kCollectThreads * kCollectPerThread)); }
