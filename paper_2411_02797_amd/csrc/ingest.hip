@@ -339,7 +339,11 @@ __device__ __forceinline__ void slow_wave_tile(const IngestArgs &a, int64_t e0, 
   for (int j = 0; j < ne; ++j) {
     const int64_t gs = shfl_i64(o, j), len = shfl_i64(o, j + 1) - gs;
     uint64_t acc = 0;
-    for (int64_t k = lane; k < len; k += 64) acc += frame_term(a.fr[gs + k], (uint32_t)k);
+    for (int64_t p = lane; 2 * p < len; p += 64) {  // pairs of the zero-padded path (padding pairs added below)
+      const uint32_t f0 = a.fr[gs + 2 * p], f1 = 2 * p + 1 < len ? a.fr[gs + 2 * p + 1] : 0u;
+      acc += pair_term(f0, f1, (uint32_t)p);
+    }
+    for (int64_t p = (len + 1) / 2 + lane; p < round_store(len) / 2; p += 64) acc += pair_term(0u, 0u, (uint32_t)p);
     acc = wave_sum_u64(acc);
     Probe p{};
     p.h = finish_hash(acc, (uint64_t)len) & a.hash_mask;
@@ -414,19 +418,23 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
 #pragma unroll
     for (int q = 0; q < kLaneBlocks; ++q) cb[q] = b[q];
 
-    // A2: hash.  Each block's sum of frame_term(frame, 16 m + i) over its frames.
+    // A2: hash.  Each block sums pair_term over its 8 pairs (pair index 8 m + i) with
+    // frames past the path read as zero: the hash covers the zero-padded block.
     W.hacc[lane] = 0;
     wave_sync();
 #pragma unroll
     for (int q = 0; q < kLaneBlocks; ++q) {
       if (cb[q].ev >= 0) {
-        const uint32_t kx = (uint32_t)(cb[q].m * kBlock) * kTermMulX, ky = (uint32_t)(cb[q].m * kBlock) * kTermMulY;
+        const uint32_t pb = (uint32_t)(cb[q].m * (kBlock / 2));
+        const uint32_t kx = pb * kPairMulX + kPairAddX, ky = pb * kPairMulY + kPairAddY;
         uint64_t acc = 0;
 #pragma unroll
-        for (int i = 0; i < kBlock; ++i) {  // frame_term(f, 16 m + i), zero past the path
-          const uint32_t x = f[q][i] + kx + (uint32_t)i * kTermMulX;
-          const uint32_t y = (f[q][i] ^ kTermXorY) + ky + (uint32_t)i * kTermMulY;
-          acc += (uint64_t)x * (uint64_t)(i < cb[q].rem ? y | 1u : 0u);
+        for (int i = 0; i < kBlock / 2; ++i) {
+          const uint32_t f0 = 2 * i < cb[q].rem ? f[q][2 * i] : 0u;
+          const uint32_t f1 = 2 * i + 1 < cb[q].rem ? f[q][2 * i + 1] : 0u;
+          const uint32_t x = f0 + kx + (uint32_t)i * kPairMulX;
+          const uint32_t y = f1 + ky + (uint32_t)i * kPairMulY;
+          acc += (uint64_t)x * (uint64_t)y + (((uint64_t)f1 << 32) | f0);
         }
         atomicAdd((unsigned long long *)&W.hacc[cb[q].ev], (unsigned long long)acc);
       }
@@ -490,8 +498,6 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
           chk[q] = vp != 0;
           const int avail = chk[q] ? (int)W.vlim[cb[q].ev] - cb[q].m * kBlock : 0;
           const gptr cp = (gptr)vp + cb[q].m * kBlock;
-#pragma unroll
-          for (int i = 0; i < kBlock; ++i) c[q][i] = f[q][i];
           if (chk[q]) {
             if (avail >= kBlock) {
 #pragma unroll
@@ -502,17 +508,20 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
               }
             } else {
 #pragma unroll
-              for (int i = 0; i < kBlock; ++i)
-                if (i < cb[q].rem) c[q][i] = cp[i];
+              for (int i = 0; i < kBlock; ++i) c[q][i] = i < cb[q].rem ? cp[i] : 0u;
             }
           }
         }
+        // frames inside the path must match
 #pragma unroll
         for (int q = 0; q < kLaneBlocks; ++q) {
-          uint32_t d = 0;
+          if (chk[q]) {
+            uint32_t d = 0;
 #pragma unroll
-          for (int i = 0; i < kBlock; ++i) d |= i < cb[q].rem ? c[q][i] ^ f[q][i] : 0u;
-          if (chk[q] && d != 0) W.bad[cb[q].ev] = 1;
+            for (int i = 0; i < kBlock; ++i) d |= i < cb[q].rem ? c[q][i] ^ f[q][i] : 0u;
+            const bool ne = d != 0;
+            if (ne) W.bad[cb[q].ev] = 1;
+          }
         }
       }
       wave_sync();
@@ -768,8 +777,8 @@ __global__ void rehash_kernel(const uint32_t *pframes, const int64_t *pstart, co
   if (id >= d) return;
   const int64_t st = pstart[id];
   const uint32_t len = plen[id];
-  uint64_t acc = 0;
-  for (uint32_t k = 0; k < len; ++k) acc += frame_term(pframes[st + k], k);
+  uint64_t acc = 0;  // the stored path is zero-padded to a multiple of 16 frames
+  for (uint32_t p = 0; 2 * p < (uint32_t)round_store(len); ++p) acc += pair_term(pframes[st + 2 * p], pframes[st + 2 * p + 1], p);
   const uint64_t h = finish_hash(acc, len) & hash_mask;
   const uint64_t word = (h & 0xFFFFFFFF00000000ull) | (uint64_t)id;
   uint64_t s = h & cap_mask;
