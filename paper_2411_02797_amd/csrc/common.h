@@ -106,9 +106,25 @@ struct IngestArgs {
 
 // Host-side launch wrappers (one translation unit per kernel family).
 void launch_ingest(const IngestArgs &a, int grid, hipStream_t s);
-// Sum metrics [N][m] into delta[slot_of[e]][m] (LDS-privatized per workgroup).
-void launch_aggregate(const uint32_t *slot_of, const uint64_t *w, int64_t n, int32_t m, uint64_t *delta, int grid,
-                      hipStream_t s);
+// Sum metrics [N][m] into delta[slot_of[e]][m] (delta starts zeroed).  Every workgroup
+// sums its event range into an LDS map keyed by slot; the maps are flushed into
+// staging buckets (bucket = slot >> bshift, plain stores, one counter atomic per
+// bucket and workgroup), and one workgroup per bucket then adds the bucket's staged
+// sums into delta.  Entries that find no room (LDS map full, bucket full) are added
+// to delta with atomics.
+struct AggStage {
+  int32_t bshift;        // bucket of slot s: s >> bshift (agg_bucket_shift(m))
+  int64_t nbuckets;      // 0: no staging (maps flushed with atomics)
+  int64_t bucket_cap;    // staged entries per bucket
+  uint32_t *count;       // [nbuckets], zeroed before the launch
+  uint32_t *keys;        // [nbuckets][bucket_cap]
+  uint64_t *sums;        // [nbuckets][bucket_cap][m]
+};
+int agg_bucket_shift(int32_t m);
+int64_t agg_max_buckets();
+int64_t agg_map_entries(int32_t m);
+void launch_aggregate(const uint32_t *slot_of, const uint64_t *w, int64_t n, int32_t m, uint64_t *delta,
+                      uint64_t cap, int grid, const AggStage &st, hipStream_t s);
 // List the slots claimed in this call (word ref with kEventRef): new_slots, and into
 // ctr: kCtrNew (count), kCtrNewFrames (sum of padded store lengths), kCtrNewLen (sum
 // of lengths).

@@ -556,32 +556,46 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
 }
 
 // Metric sums per slot: one persistent workgroup per CU walks a contiguous event
-// range and sums into an LDS map keyed by slot (a hot path costs one HBM atomic per
-// metric per workgroup), falling back to HBM atomics when a key's probe window is
-// full.  A key already in the map is found with plain LDS reads (broadcast), so hot
-// keys cost no atomic compare-and-swap.  Every thread takes kAggUnroll events per
-// round and issues all their loads (slot, then the metric row) before touching LDS,
-// so a wave keeps kAggUnroll rows in flight.  M is a template parameter: the row is
-// loaded as M consecutive 8-byte words, which the compiler merges into wide loads.
+// range and sums into an LDS map keyed by slot (a hot path costs one map entry per
+// workgroup), falling back to HBM atomics when a key's probe window is full.  A key
+// already in the map is found with plain LDS reads (broadcast), so hot keys cost no
+// atomic compare-and-swap.  Every thread takes kAggUnroll events per round and issues
+// all their loads (slot, then the metric row) before touching LDS, so a wave keeps
+// kAggUnroll rows in flight.  M is a template parameter: the row is loaded as M
+// consecutive 8-byte words, which the compiler merges into wide loads.
+//
+// The maps are flushed into staging buckets by slot range rather than with one HBM
+// atomic per entry and metric (a few million device-scope atomics): a workgroup
+// counts its entries per bucket in LDS, reserves room in each bucket with one atomic,
+// and writes its entries with plain stores; agg_reduce_kernel then sums every bucket
+// in LDS and adds it into delta, each slot owned by one workgroup.
 constexpr int kAggThreads = 1024;
 constexpr int kAggUnroll = 4;
-constexpr int kAggWords = 16384;  // LDS sums (128 KiB)
-constexpr int kAggKeys = 8192;
+constexpr int kAggHist = 2048;                            // most buckets a flush can count in LDS
+constexpr int kAggLdsBytes = 163840 - kAggHist * 4 - 256;  // map keys and sums
 constexpr uint32_t kEmptyKey = 0xFFFFFFFFu;
+constexpr int kBucketWords = 8192;                         // LDS sums of one bucket (64 KiB)
 
 constexpr int agg_entries(int m) {
-  int e = kAggWords / m < kAggKeys ? kAggWords / m : kAggKeys;
-  int p2 = 1;
-  while (p2 * 2 <= e) p2 *= 2;
-  return p2;
+  int e = kAggLdsBytes / (4 + 8 * m);
+  if (e > 8192) e = 8192;
+  return e & ~255;
 }
+constexpr int agg_bucket_slots(int m) {
+  int b = 1;
+  while (b * 2 * m <= kBucketWords) b *= 2;
+  return b;
+}
+constexpr int ilog2(int x) { return x <= 1 ? 0 : 1 + ilog2(x / 2); }
 
 template <int M>
 __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const uint32_t *slot_of, const uint64_t *w, int64_t n,
-                                                                uint64_t *delta) {
+                                                                uint64_t *delta, AggStage st) {
   constexpr int kEntries = agg_entries(M);
+  constexpr int kPer = (kEntries + kAggThreads - 1) / kAggThreads;
   __shared__ uint32_t key[kEntries];
   __shared__ uint64_t sum[kEntries * M];
+  __shared__ uint32_t hist[kAggHist];
   const int tid = threadIdx.x;
   for (int i = tid; i < kEntries; i += kAggThreads) key[i] = kEmptyKey;
   for (int i = tid; i < kEntries * M; i += kAggThreads) sum[i] = 0;
@@ -602,13 +616,13 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const uint32_t *
 #pragma unroll
     for (int u = 0; u < kAggUnroll; ++u) {
       if (s[u] == kNoSlot) continue;
-      uint32_t k = hash32(s[u]) & (uint32_t)(kEntries - 1);
+      uint32_t k = __umulhi(hash32(s[u]), (uint32_t)kEntries);
       int mi = -1;
       for (int t = 0; t < 8; ++t) {
         uint32_t cur = key[k];
         if (cur == kEmptyKey) cur = atomicCAS(&key[k], kEmptyKey, s[u]);
         if (cur == kEmptyKey || cur == s[u]) { mi = (int)k; break; }
-        k = (k + 1) & (uint32_t)(kEntries - 1);
+        k = k + 1 == (uint32_t)kEntries ? 0 : k + 1;
       }
 #pragma unroll
       for (int j = 0; j < M; ++j) {
@@ -618,14 +632,83 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_kernel(const uint32_t *
     }
   }
   __syncthreads();
-  for (int k = tid; k < kEntries; k += kAggThreads) {
+  const int nbk = (int)st.nbuckets;
+  if (nbk == 0 || nbk > kAggHist) {
+    for (int k = tid; k < kEntries; k += kAggThreads) {
+      const uint32_t sk = key[k];
+      if (sk == kEmptyKey) continue;
+#pragma unroll
+      for (int j = 0; j < M; ++j) {
+        const uint64_t v = sum[k * M + j];
+        if (v) atomicAdd((unsigned long long *)&delta[(uint64_t)sk * M + j], (unsigned long long)v);
+      }
+    }
+    return;
+  }
+  // staged flush: rank of every entry within its bucket, then one reservation per bucket
+  for (int i = tid; i < nbk; i += kAggThreads) hist[i] = 0;
+  __syncthreads();
+  uint32_t rank[kPer];
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int k = tid + j * kAggThreads;
+    rank[j] = 0;
+    if (k < kEntries && key[k] != kEmptyKey) rank[j] = atomicAdd(&hist[key[k] >> st.bshift], 1u);
+  }
+  __syncthreads();
+  for (int i = tid; i < nbk; i += kAggThreads) {
+    const uint32_t c = hist[i];
+    hist[i] = c ? atomicAdd(&st.count[i], c) : 0u;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int k = tid + j * kAggThreads;
+    if (k >= kEntries) continue;
     const uint32_t sk = key[k];
     if (sk == kEmptyKey) continue;
+    const uint32_t bk = sk >> st.bshift;
+    const uint64_t pos = (uint64_t)hist[bk] + rank[j];
+    if (pos < (uint64_t)st.bucket_cap) {
+      const uint64_t at = (uint64_t)bk * (uint64_t)st.bucket_cap + pos;
+      st.keys[at] = sk;
 #pragma unroll
-    for (int j = 0; j < M; ++j) {
-      const uint64_t v = sum[k * M + j];
-      if (v) atomicAdd((unsigned long long *)&delta[(uint64_t)sk * M + j], (unsigned long long)v);
+      for (int jj = 0; jj < M; ++jj) st.sums[at * M + jj] = sum[k * M + jj];
+    } else {  // the bucket is full (slots far from uniform): add directly
+#pragma unroll
+      for (int jj = 0; jj < M; ++jj) {
+        const uint64_t v = sum[k * M + jj];
+        if (v) atomicAdd((unsigned long long *)&delta[(uint64_t)sk * M + jj], (unsigned long long)v);
+      }
     }
+  }
+}
+
+// One workgroup per staging bucket: sum the bucket's entries in LDS, then add them
+// into delta (this workgroup is the only writer of the bucket's slots).
+template <int M>
+__global__ __launch_bounds__(kAggThreads) void agg_reduce_kernel(AggStage st, uint64_t cap, uint64_t *delta) {
+  constexpr int kSlots = agg_bucket_slots(M);
+  __shared__ uint64_t dense[kSlots * M];
+  const int tid = threadIdx.x;
+  const uint64_t bk = blockIdx.x;
+  for (int i = tid; i < kSlots * M; i += kAggThreads) dense[i] = 0;
+  __syncthreads();
+  const uint64_t cnt = st.count[bk];
+  const uint64_t n = cnt < (uint64_t)st.bucket_cap ? cnt : (uint64_t)st.bucket_cap;
+  const uint64_t base = bk * (uint64_t)st.bucket_cap;
+  for (uint64_t i = tid; i < n; i += kAggThreads) {
+    const uint32_t local = st.keys[base + i] - (uint32_t)(bk << st.bshift);
+#pragma unroll
+    for (int j = 0; j < M; ++j)
+      atomicAdd((unsigned long long *)&dense[local * M + j], (unsigned long long)st.sums[(base + i) * M + j]);
+  }
+  __syncthreads();
+  const uint64_t s0 = bk << st.bshift;
+  for (int i = tid; i < kSlots * M; i += kAggThreads) {
+    const uint64_t slot = s0 + (uint64_t)(i / M);
+    const uint64_t v = dense[i];
+    if (slot < cap && v) delta[slot * M + (i % M)] += v;
   }
 }
 
@@ -796,12 +879,40 @@ inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1)
 void launch_ingest(const IngestArgs &a, int grid, hipStream_t s) {
   hipLaunchKernelGGL(ingest_kernel, dim3(grid), dim3(kIngestThreads), 0, s, a);
 }
-void launch_aggregate(const uint32_t *slot_of, const uint64_t *w, int64_t n, int32_t m, uint64_t *delta, int grid,
-                      hipStream_t s) {
-  if (n <= 0) return;
+int agg_bucket_shift(int32_t m) {
   switch (m) {
-#define CCT_AGG_CASE(M)                                                                                      \
-  case M: hipLaunchKernelGGL(aggregate_kernel<M>, dim3(grid), dim3(kAggThreads), 0, s, slot_of, w, n, delta); break;
+    case 1: return ilog2(agg_bucket_slots(1));
+    case 2: return ilog2(agg_bucket_slots(2));
+    case 3: return ilog2(agg_bucket_slots(3));
+    case 4: return ilog2(agg_bucket_slots(4));
+    default: return ilog2(agg_bucket_slots(8));
+  }
+}
+int64_t agg_max_buckets() { return kAggHist; }
+int64_t agg_map_entries(int32_t m) {
+  switch (m) {
+    case 1: return agg_entries(1);
+    case 2: return agg_entries(2);
+    case 3: return agg_entries(3);
+    case 4: return agg_entries(4);
+    case 5: return agg_entries(5);
+    case 6: return agg_entries(6);
+    case 7: return agg_entries(7);
+    default: return agg_entries(8);
+  }
+}
+void launch_aggregate(const uint32_t *slot_of, const uint64_t *w, int64_t n, int32_t m, uint64_t *delta,
+                      uint64_t cap, int grid, const AggStage &st, hipStream_t s) {
+  if (n <= 0) return;
+  const bool staged = st.nbuckets > 0 && st.nbuckets <= kAggHist;
+  switch (m) {
+#define CCT_AGG_CASE(M)                                                                                       \
+  case M:                                                                                                     \
+    hipLaunchKernelGGL(aggregate_kernel<M>, dim3(grid), dim3(kAggThreads), 0, s, slot_of, w, n, delta, st);  \
+    if (staged)                                                                                               \
+      hipLaunchKernelGGL(agg_reduce_kernel<M>, dim3((unsigned)st.nbuckets), dim3(kAggThreads), 0, s, st, cap, \
+                         delta);                                                                              \
+    break;
     CCT_AGG_CASE(1) CCT_AGG_CASE(2) CCT_AGG_CASE(3) CCT_AGG_CASE(4)
     CCT_AGG_CASE(5) CCT_AGG_CASE(6) CCT_AGG_CASE(7) CCT_AGG_CASE(8)
 #undef CCT_AGG_CASE

@@ -288,7 +288,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     cct_status st = rehash(t, pow2_at_least((uint64_t)t->d * 4), hash_mask, s);
     if (st) return st;
   }
-  Buf delta, new_slots, slot_of, cpart;
+  Buf delta, new_slots, slot_of, cpart, agg_count, agg_keys, agg_sums;
   uint64_t n_new = 0, new_frames = 0, new_store = 0;
   if (N > 0) {
     if (!slot_of.alloc((size_t)N * 4)) return fail(CCT_ENOMEM, "device allocation failed");
@@ -312,8 +312,24 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
       tm.mark(1, s);
       launch_ingest(a, grid, s);
       tm.mark(2, s);
-      launch_aggregate(a.slot_of, p->metrics, N, m, delta.as<uint64_t>(),
-                       (int)std::max<int64_t>(1, std::min<int64_t>((N + 8191) / 8192, (int64_t)cu_count())), s);
+      // metric sums: per-workgroup LDS maps, flushed through staging buckets of slots
+      const int agg_grid = (int)std::max<int64_t>(1, std::min<int64_t>((N + 8191) / 8192, (int64_t)cu_count()));
+      AggStage stg{};
+      stg.bshift = agg_bucket_shift(m);
+      const int64_t nbk = std::max<int64_t>(1, (int64_t)(t->cap >> stg.bshift));
+      if (nbk <= agg_max_buckets()) {
+        const int64_t total = (int64_t)agg_grid * agg_map_entries(m);
+        stg.nbuckets = nbk;
+        stg.bucket_cap = 2 * ((total + nbk - 1) / nbk) + 256;  // twice the even share (slots are hashed)
+        if (!agg_count.alloc(nbk * 4) || !agg_keys.alloc(nbk * stg.bucket_cap * 4) ||
+            !agg_sums.alloc(nbk * stg.bucket_cap * m * 8))
+          return fail(CCT_ENOMEM, "device allocation failed");
+        HIP_TRY(hipMemsetAsync(agg_count.p, 0, nbk * 4, s));
+        stg.count = agg_count.as<uint32_t>();
+        stg.keys = agg_keys.as<uint32_t>();
+        stg.sums = agg_sums.as<uint64_t>();
+      }
+      launch_aggregate(a.slot_of, p->metrics, N, m, delta.as<uint64_t>(), t->cap, agg_grid, stg, s);
       launch_collect_new(t->slot.as<Slot>(), t->cap, p->offsets, new_slots.as<uint32_t>(), dctr,
                          cpart.as<unsigned long long>(), s);
       HIP_TRY(hipGetLastError());
