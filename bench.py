@@ -4,6 +4,10 @@ One step = one cct_build (ingest, exact dedup, exclusive aggregation, publish,
 canonical sort, node emission with exclusive and inclusive sums) of the whole batch,
 inputs already resident in HBM, followed by cct_free.  Prints one JSON line.
 
+With --workload merge, one step = the 32 cct_merge calls that fold 32 chunks of
+2,097,152 events into a tree built (untimed) from an 8,388,608-event base; the rate
+is chunk events per second of merge time.
+
     python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload layered_16m]
 """
 import argparse
@@ -27,6 +31,8 @@ DESCRIPTIONS = {
     "deep_recursion": "4,194,304 events, 20,000 frame ids, depth 256-512 recursion of a 12-frame cycle, "
                       "1 uint64 metric",
     "tiny": "10,000 events on a random call-site tree, 1 uint64 metric",
+    "merge": "8,388,608-event base (layered_16m program, 60% of its paths) + 32 merged chunks of 2,097,152 events "
+             "(20% from paths new to the chunk), 4 uint64 metrics (one full-range)",
 }
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ingest_traffic.json")
 
@@ -107,6 +113,8 @@ def main():
     cct.load_library()
     dev = torch.device("cuda", 0)
     t0 = time.perf_counter()
+    if args.workload == "merge":
+        return bench_merge(args, torch, tracegen, cct, dev)
     o, f, w = tracegen.generate(args.workload)
     N, F, M = o.size - 1, f.size, w.shape[1]
     log(f"generated {args.workload}: N={N:,} F={F:,} M={M} in {time.perf_counter() - t0:.1f}s")
@@ -168,6 +176,65 @@ def main():
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(o, f, w, args.cpu_sample)
+    print(json.dumps(line), flush=True)
+
+
+def bench_merge(args, torch, tracegen, cct, dev):
+    def to_dev(o, f, w):
+        return (torch.from_numpy(o).to(dev), torch.from_numpy(f.view(np.int32)).to(dev),
+                torch.from_numpy(w.view(np.int64)).to(dev))
+    t0 = time.perf_counter()
+    base = to_dev(*tracegen.generate("merge_base"))
+    chunks = []
+    n_chunk_events = n_chunk_frames = 0
+    for c in range(32):
+        o, f, w = tracegen.generate("merge_chunk", chunk=c)
+        n_chunk_events += o.size - 1
+        n_chunk_frames += f.size
+        chunks.append(to_dev(o, f, w))
+    M = chunks[0][2].shape[1]
+    torch.cuda.synchronize()
+    log(f"generated merge: base N={base[0].numel() - 1:,}, 32 chunks N={n_chunk_events:,} "
+        f"F={n_chunk_frames:,} in {time.perf_counter() - t0:.1f}s")
+    merge_ms, phases, base_ms = [], [], []
+    U = D = 0
+    for step in range(args.warmup + args.steps):
+        tree = cct.build(*base)
+        base_ms.append(cct.last_timings()[4])
+        torch.cuda.synchronize()
+        t_seq = time.perf_counter()
+        ph = []
+        for ch in chunks:
+            tree.merge(*ch)
+            ph.append(cct.last_timings())
+        torch.cuda.synchronize()
+        wall = (time.perf_counter() - t_seq) * 1000.0
+        U, _, D = tree._info()
+        tree.free()
+        if step >= args.warmup:
+            merge_ms.append(wall)
+            phases.extend(ph)
+        log(f"{'warmup' if step < args.warmup else 'step'} {step}: 32 merges {wall:.2f} ms, U={U:,} D={D:,}")
+    ms = float(np.mean(merge_ms))
+    ph = np.array(phases)
+    ingest_ms = float(ph[:, 0].mean())
+    b_ingest = 8 * (n_chunk_events // 32 + 1) + 4 * (n_chunk_frames // 32)
+    achieved = b_ingest / (ingest_ms * 1e-3) / 1e9
+    line = {
+        "metric": METRIC, "value": n_chunk_events / (ms * 1e-3), "unit": "events/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "u64", "data": "synthetic",
+        "config": {"workload": f"merge: {DESCRIPTIONS['merge']}", "chunk_events": n_chunk_events,
+                   "chunk_frames": n_chunk_frames, "metrics": M, "distinct_paths": D, "nodes": U,
+                   "base_build_ms": float(np.mean(base_ms))},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                     "kernel": "ingest_kernel of one merge (validate, hash, exact dedup against the tree)",
+                     "bytes_per_launch": b_ingest, "avg_launch_ms": ingest_ms},
+        "phase_ms_per_merge": {"ingest": ingest_ms, "publish": float(ph[:, 1].mean()),
+                               "sort": float(ph[:, 2].mean()), "emit": float(ph[:, 3].mean()),
+                               "call": float(ph[:, 4].mean())},
+    }
     print(json.dumps(line), flush=True)
 
 

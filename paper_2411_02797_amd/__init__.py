@@ -15,7 +15,8 @@ from __future__ import annotations
 import ctypes
 import os
 
-__all__ = ["build", "Tree", "CctError", "library_path", "load_library", "EXPORTED_SYMBOLS", "NO_PARENT"]
+__all__ = ["build", "Tree", "CctError", "library_path", "load_library", "last_timings", "release_cached_memory",
+           "EXPORTED_SYMBOLS", "NO_PARENT"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "libcct.so")
@@ -202,3 +203,8 @@ def last_timings():
     buf = (ctypes.c_double * 5)()
     n = load_library().cct_last_timings(buf, 5)
     return list(buf)[:n]
+
+
+def release_cached_memory():
+    """Return the library's cached device buffers to the HIP runtime (cct_release_cached_memory)."""
+    load_library().cct_release_cached_memory()
