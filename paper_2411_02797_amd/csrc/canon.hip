@@ -100,7 +100,7 @@ __global__ __launch_bounds__(512) void sort_block_kernel(CanonArgs a, uint32_t *
   __shared__ uint32_t key[kSortBlock];
   const int tid = threadIdx.x;
   const int64_t base = (int64_t)blockIdx.x * kSortBlock;
-  for (int i = tid; i < kSortBlock; i += 512) key[i] = base + i < a.d ? (uint32_t)(base + i) : kInf;
+  for (int i = tid; i < kSortBlock; i += 512) key[i] = base + i < a.d ? (uint32_t)(a.id0 + base + i) : kInf;
   __syncthreads();
   for (int k = 2; k <= kSortBlock; k <<= 1) {
     for (int j = k >> 1; j > 0; j >>= 1) {
@@ -133,6 +133,29 @@ __global__ __launch_bounds__(256) void merge_pass_kernel(CanonArgs a, const uint
   }
   int64_t ia = lo, ib = dgl - lo;
   const int64_t cnt = min((int64_t)kMergeItems, la + lb - dgl);
+  for (int64_t k = 0; k < cnt; ++k) {
+    bool take_a;
+    if (ia >= la) take_a = false;
+    else if (ib >= lb) take_a = true;
+    else take_a = !path_less(a, B[ib], A[ia]);
+    dst[o0 + k] = take_a ? A[ia++] : B[ib++];
+  }
+}
+
+// Merge of two sorted runs of different lengths (the previous order and the sorted
+// new paths): every thread finds its first output by a merge-path search, then
+// writes kMergeItems outputs.
+__global__ __launch_bounds__(256) void merge_two_kernel(CanonArgs a, const uint32_t *A, int64_t la,
+                                                        const uint32_t *B, int64_t lb, uint32_t *dst) {
+  const int64_t o0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * kMergeItems;
+  if (o0 >= la + lb) return;
+  int64_t lo = max((int64_t)0, o0 - lb), hi = min(o0, la);
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) >> 1;
+    if (path_less(a, A[mid], B[o0 - 1 - mid])) lo = mid + 1; else hi = mid;
+  }
+  int64_t ia = lo, ib = o0 - lo;
+  const int64_t cnt = min((int64_t)kMergeItems, la + lb - o0);
   for (int64_t k = 0; k < cnt; ++k) {
     bool take_a;
     if (ia >= la) take_a = false;
@@ -339,6 +362,24 @@ void launch_sort(CanonArgs &a, hipStream_t s) {
   }
   a.order = src;
   a.order_tmp = dst;
+}
+
+void launch_merge_order(CanonArgs &a, const uint32_t *old_order, int64_t d_old, hipStream_t s) {
+  const int64_t n_new = a.d - d_old;
+  const uint32_t *B = nullptr;
+  uint32_t *dst = a.order;
+  if (n_new > 0) {
+    CanonArgs r = a;
+    r.d = n_new;
+    r.id0 = d_old;
+    launch_sort(r, s);  // sorted new ids in r.order (one of the two buffers)
+    B = r.order;
+    dst = r.order_tmp;
+  }
+  hipLaunchKernelGGL(merge_two_kernel, dim3(blocks_for((a.d + kMergeItems - 1) / kMergeItems, 256)), dim3(256), 0, s,
+                     a, old_order, d_old, B, n_new, dst);
+  a.order_tmp = dst == a.order ? a.order_tmp : a.order;
+  a.order = dst;
 }
 
 void launch_scan(const uint64_t *in, int64_t rows, int C, uint64_t *blk, uint64_t *out, hipStream_t s) {

@@ -455,7 +455,10 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   // hash collision, an oversized sibling group) or its order fails the exact check,
   // pass 1 sorts by exact comparisons.  A test setting forces the comparison sort.
   const int64_t nblocks = store_need / kStoreAlign;
-  const bool use_trie = !ca.exact && !env_int("CCT_TEST_MERGE_SORT", 0) && D > 0;
+  // a merge keeps the previous order: only this call's new paths are sorted, then
+  // merged in (a test setting forces the full sort)
+  const bool incremental = t->d > 0 && t->order.p && !ca.exact && !env_int("CCT_TEST_FULL_SORT", 0);
+  const bool use_trie = !incremental && !ca.exact && !env_int("CCT_TEST_MERGE_SORT", 0) && D > 0;
   Buf tr_key, tr_info, tr_pblk, tr_occ, tr_par, tr_cnt, tr_end, tr_hist, tr_gstart, tr_cidx, tr_rb, tr_lg, tr_spl, tr_bc, tr_grp, tr_grp2, tr_pos,
       tr_c, tr_cs, tr_blk, tr_lists, tr_ctr;
   TrieArgs ta{};
@@ -485,11 +488,13 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     ta.lgroup = tr_lg.as<uint32_t>(); ta.spl = tr_spl.as<uint32_t>(); ta.bcnt = tr_bc.as<uint32_t>();
     ta.ctr = tr_ctr.as<unsigned long long>(); ta.order = ca.order;
   }
-  // 0: block trie, 1: comparison sort with checkpoint hashes, 2: exact comparisons only
-  for (int mode = use_trie ? 0 : (ca.exact ? 2 : 1);;) {
+  // 0: block trie, 1: comparison sort with checkpoint hashes, 2: exact comparisons only,
+  // 3: the previous order with this call's new paths merged in
+  for (int mode = incremental ? 3 : (use_trie ? 0 : (ca.exact ? 2 : 1));;) {
     CanonArgs run = ca;
     run.exact = mode == 2 ? 1 : 0;
     if (mode == 0) launch_trie_sort(ta, s);
+    else if (mode == 3) launch_merge_order(run, t->order.as<uint32_t>(), t->d, s);
     else launch_sort(run, s);
     tm.mark(4, s);
     launch_canon(run, s);

@@ -231,6 +231,28 @@ def test_merge_equals_one_shot():
     tree.free()
 
 
+@pytest.mark.parametrize("full_sort", [False, True])
+def test_merge_orders(monkeypatch, full_sort):
+    # a merge keeps the previous order and merges this call's new paths into it (or,
+    # forced, sorts every path again): merges that add no path, a few, and more new
+    # paths than the tree holds
+    import paper_2411_02797_amd as cct
+    if full_sort:
+        monkeypatch.setenv("CCT_TEST_FULL_SORT", "1")
+    o, f, w = tracegen.generate("merge_base", n_events=20_000)
+    tree = cct.build(*to_dev(o, f, w))
+    orc = oracle.Oracle(4)
+    orc.ingest(o, f, w)
+    batches = [(o, f, w), tracegen.generate("merge_chunk", n_events=5_000, chunk=0),
+               tracegen.random_paths(30_000, 5000, 40, 4, seed=21)]
+    for k, b in enumerate(batches):
+        tree.merge(*to_dev(*b))
+        orc.ingest(*b)
+        assert_same(tree.to_numpy(), orc.tree(), f"merge {k} (full sort {full_sort})")
+    tree.free()
+    orc.close()
+
+
 def test_merge_into_empty_and_empty_merge():
     import paper_2411_02797_amd as cct
     o, f, w = tracegen.random_paths(2000, 50, 10, 2, seed=3)
