@@ -95,6 +95,18 @@ found:
   }
 }
 
+// Sort order: (gap, path) when a gap array is given (the new paths of a merge), else
+// the path alone.
+__device__ inline bool key_less(const CanonArgs &a, uint32_t x, uint32_t y) {
+  if (x == kInf) return false;
+  if (y == kInf) return true;
+  if (a.gap) {
+    const uint32_t gx = a.gap[x - a.id0], gy = a.gap[y - a.id0];
+    if (gx != gy) return gx < gy;
+  }
+  return path_less(a, x, y);
+}
+
 // ---- sort -------------------------------------------------------------------------
 __global__ __launch_bounds__(512) void sort_block_kernel(CanonArgs a, uint32_t *out) {
   __shared__ uint32_t key[kSortBlock];
@@ -107,7 +119,7 @@ __global__ __launch_bounds__(512) void sort_block_kernel(CanonArgs a, uint32_t *
       const int i = 2 * j * (tid / j) + (tid % j), l = i + j;
       const uint32_t x = key[i], y = key[l];
       const bool up = (i & k) == 0;
-      const bool swap = up ? path_less(a, y, x) : path_less(a, x, y);
+      const bool swap = up ? key_less(a, y, x) : key_less(a, x, y);
       __syncthreads();
       if (swap) { key[i] = y; key[l] = x; }
       __syncthreads();
@@ -129,7 +141,7 @@ __global__ __launch_bounds__(256) void merge_pass_kernel(CanonArgs a, const uint
   int64_t lo = max((int64_t)0, dgl - lb), hi = min(dgl, la);
   while (lo < hi) {
     const int64_t mid = (lo + hi) >> 1;
-    if (path_less(a, A[mid], B[dgl - 1 - mid])) lo = mid + 1; else hi = mid;
+    if (key_less(a, A[mid], B[dgl - 1 - mid])) lo = mid + 1; else hi = mid;
   }
   int64_t ia = lo, ib = dgl - lo;
   const int64_t cnt = min((int64_t)kMergeItems, la + lb - dgl);
@@ -137,32 +149,47 @@ __global__ __launch_bounds__(256) void merge_pass_kernel(CanonArgs a, const uint
     bool take_a;
     if (ia >= la) take_a = false;
     else if (ib >= lb) take_a = true;
-    else take_a = !path_less(a, B[ib], A[ia]);
+    else take_a = !key_less(a, B[ib], A[ia]);
     dst[o0 + k] = take_a ? A[ia++] : B[ib++];
   }
 }
 
-// Merge of two sorted runs of different lengths (the previous order and the sorted
-// new paths): every thread finds its first output by a merge-path search, then
-// writes kMergeItems outputs.
-__global__ __launch_bounds__(256) void merge_two_kernel(CanonArgs a, const uint32_t *A, int64_t la,
-                                                        const uint32_t *B, int64_t lb, uint32_t *dst) {
-  const int64_t o0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * kMergeItems;
-  if (o0 >= la + lb) return;
-  int64_t lo = max((int64_t)0, o0 - lb), hi = min(o0, la);
+// A merge's new paths: gap[j] = number of old paths (in their sorted order) below
+// new path d_old + j, by binary search.
+__global__ __launch_bounds__(256) void gap_kernel(CanonArgs a, const uint32_t *old_order, int64_t d_old, uint32_t *gap) {
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= a.d - d_old) return;
+  const uint32_t x = (uint32_t)(d_old + j);
+  int64_t lo = 0, hi = d_old;
   while (lo < hi) {
     const int64_t mid = (lo + hi) >> 1;
-    if (path_less(a, A[mid], B[o0 - 1 - mid])) lo = mid + 1; else hi = mid;
+    if (path_less(a, old_order[mid], x)) lo = mid + 1; else hi = mid;
   }
-  int64_t ia = lo, ib = o0 - lo;
-  const int64_t cnt = min((int64_t)kMergeItems, la + lb - o0);
-  for (int64_t k = 0; k < cnt; ++k) {
-    bool take_a;
-    if (ia >= la) take_a = false;
-    else if (ib >= lb) take_a = true;
-    else take_a = !path_less(a, B[ib], A[ia]);
-    dst[o0 + k] = take_a ? A[ia++] : B[ib++];
+  gap[j] = (uint32_t)lo;
+}
+
+// Placement: the r-th new path (sorted by gap, then path) goes after its gap's old
+// paths and the r new paths before it; old path i goes after the new paths whose
+// gap is <= i.
+__global__ __launch_bounds__(256) void place_new_kernel(const uint32_t *B, int64_t n_new, int64_t d_old,
+                                                        const uint32_t *gap, uint32_t *gsorted, uint32_t *dst) {
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= n_new) return;
+  const uint32_t x = B[r];
+  const uint32_t g = gap[x - d_old];
+  gsorted[r] = g;
+  dst[g + r] = x;
+}
+__global__ __launch_bounds__(256) void place_old_kernel(const uint32_t *A, int64_t d_old, const uint32_t *gsorted,
+                                                        int64_t n_new, uint32_t *dst) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= d_old) return;
+  int64_t lo = 0, hi = n_new;  // new paths with gap <= i
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) >> 1;
+    if ((int64_t)gsorted[mid] <= i) lo = mid + 1; else hi = mid;
   }
+  dst[i + lo] = A[i];
 }
 
 // ---- exact verification, lcp, scan rows ------------------------------------------------
@@ -364,20 +391,27 @@ void launch_sort(CanonArgs &a, hipStream_t s) {
   a.order_tmp = dst;
 }
 
-void launch_merge_order(CanonArgs &a, const uint32_t *old_order, int64_t d_old, hipStream_t s) {
+void launch_merge_order(CanonArgs &a, const uint32_t *old_order, int64_t d_old, uint32_t *scratch,
+                        hipStream_t s) {
   const int64_t n_new = a.d - d_old;
+  uint32_t *gap = scratch, *gsorted = scratch + n_new;
   const uint32_t *B = nullptr;
   uint32_t *dst = a.order;
   if (n_new > 0) {
+    hipLaunchKernelGGL(gap_kernel, dim3(blocks_for(n_new, 256)), dim3(256), 0, s, a, old_order, d_old, gap);
     CanonArgs r = a;
     r.d = n_new;
     r.id0 = d_old;
-    launch_sort(r, s);  // sorted new ids in r.order (one of the two buffers)
+    r.gap = gap;
+    launch_sort(r, s);  // new ids by (gap, path), in r.order (one of the two buffers)
     B = r.order;
     dst = r.order_tmp;
+    hipLaunchKernelGGL(place_new_kernel, dim3(blocks_for(n_new, 256)), dim3(256), 0, s, B, n_new, d_old, gap,
+                       gsorted, dst);
   }
-  hipLaunchKernelGGL(merge_two_kernel, dim3(blocks_for((a.d + kMergeItems - 1) / kMergeItems, 256)), dim3(256), 0, s,
-                     a, old_order, d_old, B, n_new, dst);
+  if (d_old > 0)
+    hipLaunchKernelGGL(place_old_kernel, dim3(blocks_for(d_old, 256)), dim3(256), 0, s, old_order, d_old, gsorted,
+                       n_new, dst);
   a.order_tmp = dst == a.order ? a.order_tmp : a.order;
   a.order = dst;
 }

@@ -175,6 +175,7 @@ void launch_rehash(const uint32_t *pframes, const int64_t *pstart, const uint32_
 struct CanonArgs {
   int64_t d;             // number of distinct full paths
   int64_t id0;           // launch_sort: sorts path ids id0 .. id0 + d - 1 (0 for a full sort)
+  const uint32_t *gap;   // launch_sort with gap: orders by (gap[id - id0], path); else nullptr
   int32_t m;
   int32_t exact;         // 1: compare frames only (no checkpoint-hash shortcut)
   const uint32_t *pframes;
@@ -202,10 +203,13 @@ struct CanonArgs {
   int grid_nodes;
 };
 void launch_sort(CanonArgs &a, hipStream_t s);        // leaves the result in a.order
-// Order after a merge: the paths new in this call (ids d_old .. a.d - 1) are sorted
-// alone, then merged into the previous order (d_old ids, sorted): the old paths keep
-// their relative order.  Leaves the result in a.order.
-void launch_merge_order(CanonArgs &a, const uint32_t *old_order, int64_t d_old, hipStream_t s);
+// Order after a merge: every path new in this call (ids d_old .. a.d - 1) finds its
+// gap in the previous order (d_old ids, sorted; the old paths keep their relative
+// order) by binary search, the new paths are sorted by (gap, path), and both lists
+// are placed by integer arithmetic.  scratch: 2 (a.d - d_old) words.  Leaves the
+// result in a.order.
+void launch_merge_order(CanonArgs &a, const uint32_t *old_order, int64_t d_old, uint32_t *scratch,
+                        hipStream_t s);
 
 // Lexicographic order of the D distinct paths through a trie of 16-frame blocks (see
 // trie.hip).  Scratch sizes: nblocks = store blocks in use (sum of ceil(len / 16)),

@@ -418,6 +418,50 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
       !nblkbuf.alloc(((int64_t)n_new / 1024 + 2) * 8))
     return rollback(fail(CCT_ENOMEM, "device allocation failed"));
 
+  // sorting scratch, allocated before the tree is touched
+  const bool exact_sort = env_int("CCT_TEST_EXACT_SORT", 0) != 0;
+  // Pass 0 ranks the paths through the block trie (trie.hip); if that is not usable (a
+  // hash collision, an oversized sibling group) or its order fails the exact check,
+  // pass 1 sorts by exact comparisons.  A test setting forces the comparison sort.
+  const int64_t nblocks = store_need / kStoreAlign;
+  // a merge keeps the previous order: only this call's new paths are sorted, then
+  // merged in (a test setting forces the full sort)
+  const bool incremental = t->d > 0 && t->order.p && !exact_sort && !env_int("CCT_TEST_FULL_SORT", 0);
+  const bool use_trie = !incremental && !exact_sort && !env_int("CCT_TEST_MERGE_SORT", 0) && D > 0;
+  Buf merge_scratch;
+  if (incremental && !merge_scratch.alloc(std::max<int64_t>(2 * (int64_t)n_new, 1) * 4))
+    return rollback(fail(CCT_ENOMEM, "device allocation failed"));
+  Buf tr_key, tr_info, tr_pblk, tr_occ, tr_par, tr_cnt, tr_end, tr_hist, tr_gstart, tr_cidx, tr_rb, tr_lg, tr_spl, tr_bc, tr_grp, tr_grp2, tr_pos,
+      tr_c, tr_cs, tr_blk, tr_lists, tr_ctr;
+  TrieArgs ta{};
+  if (use_trie) {
+    const uint64_t tcap = pow2_at_least(std::max<uint64_t>(2 * (uint64_t)nblocks, 1024));
+    const int64_t nbk = std::max<int64_t>(nblocks, 1);
+    const int64_t list_cap = nbk + 1024;
+    const int64_t large_cap = nbk / 1024 + 1;  // groups of more than 1024 siblings
+    const int64_t scan_rows = std::max<int64_t>((int64_t)tcap + 1, nbk);
+    if (!tr_key.alloc(tcap * 8) || !tr_info.alloc(tcap * 8) || !tr_pblk.alloc(nbk * 4) || !tr_occ.alloc(nbk * 4) ||
+        !tr_par.alloc(tcap * 4) || !tr_cnt.alloc(tcap * 4) || !tr_end.alloc((tcap + 1) * 4) ||
+        !tr_hist.alloc((tcap + 1) * 8) || !tr_gstart.alloc((tcap + 2) * 8) || !tr_cidx.alloc(tcap * 4) ||
+        !tr_rb.alloc(1024 * 4) || !tr_lg.alloc((tcap + 1) * 4) || !tr_spl.alloc(large_cap * 256 * 4) ||
+        !tr_bc.alloc(large_cap * 256 * 4) ||
+        !tr_grp.alloc(nbk * 4) || !tr_grp2.alloc(nbk * 4) || !tr_pos.alloc(tcap * 4) || !tr_c.alloc(nbk * 8) ||
+        !tr_cs.alloc((nbk + 1) * 8) || !tr_blk.alloc((scan_rows / 1024 + 2) * 8) || !tr_lists.alloc(3 * list_cap * 8) ||
+        !tr_ctr.alloc(64))
+      return rollback(fail(CCT_ENOMEM, "device allocation failed"));
+    ta.d = D; ta.nblocks = nblocks; ta.cap = tcap;
+    ta.pframes = t->pframes.as<uint32_t>(); ta.pcp = t->pcp.as<uint64_t>(); ta.pstart = t->pstart.as<int64_t>();
+    ta.plen = t->plen.as<uint32_t>();
+    ta.tkey = tr_key.as<uint64_t>(); ta.tinfo = tr_info.as<uint64_t>(); ta.pblk = tr_pblk.as<uint32_t>();
+    ta.occ = tr_occ.as<uint32_t>(); ta.nparent = tr_par.as<uint32_t>(); ta.ncount = tr_cnt.as<uint32_t>();
+    ta.nend = tr_end.as<uint32_t>(); ta.hist = tr_hist.as<uint64_t>(); ta.gstart = tr_gstart.as<uint64_t>();
+    ta.cidx = tr_cidx.as<uint32_t>(); ta.rootbase = tr_rb.as<uint32_t>(); ta.grouped = tr_grp.as<uint32_t>(); ta.grouped2 = tr_grp2.as<uint32_t>();
+    ta.posof = tr_pos.as<uint32_t>(); ta.cnt = tr_c.as<uint64_t>(); ta.cnt_scan = tr_cs.as<uint64_t>();
+    ta.scan_blk = tr_blk.as<uint64_t>(); ta.lists = tr_lists.as<uint64_t>(); ta.list_cap = list_cap; ta.large_cap = large_cap;
+    ta.lgroup = tr_lg.as<uint32_t>(); ta.spl = tr_spl.as<uint32_t>(); ta.bcnt = tr_bc.as<uint32_t>();
+    ta.ctr = tr_ctr.as<unsigned long long>(); ta.order = order.as<uint32_t>();
+  }
+
   // ---- publish new paths, fold this call's sums into the old ones -----------------------
   HIP_TRY(hipMemsetAsync(cursor.p, 0, 64, s));
   if (n_new) {
@@ -440,7 +484,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
 
   // ---- A5-A9: canonical order and node arrays ------------------------------------------
   CanonArgs ca{};
-  ca.d = D; ca.m = m; ca.exact = env_int("CCT_TEST_EXACT_SORT", 0) ? 1 : 0;
+  ca.d = D; ca.m = m; ca.exact = exact_sort ? 1 : 0;
   ca.pframes = t->pframes.as<uint32_t>(); ca.pcp = t->pcp.as<uint64_t>(); ca.pstart = t->pstart.as<int64_t>();
   ca.plen = t->plen.as<uint32_t>(); ca.psums = t->psums.as<uint64_t>();
   ca.order = order.as<uint32_t>(); ca.order_tmp = order_tmp.as<uint32_t>(); ca.lcp = lcp.as<uint32_t>();
@@ -451,50 +495,13 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   ca.excl = n_excl.as<uint64_t>(); ca.incl = n_incl.as<uint64_t>();
   ca.u_out = cursor.as<unsigned long long>() + 2;
   ca.grid_nodes = (int)std::max<int64_t>(1, std::min<int64_t>((u_max + 255) / 256, (int64_t)cu_count() * 16));
-  // Pass 0 ranks the paths through the block trie (trie.hip); if that is not usable (a
-  // hash collision, an oversized sibling group) or its order fails the exact check,
-  // pass 1 sorts by exact comparisons.  A test setting forces the comparison sort.
-  const int64_t nblocks = store_need / kStoreAlign;
-  // a merge keeps the previous order: only this call's new paths are sorted, then
-  // merged in (a test setting forces the full sort)
-  const bool incremental = t->d > 0 && t->order.p && !ca.exact && !env_int("CCT_TEST_FULL_SORT", 0);
-  const bool use_trie = !incremental && !ca.exact && !env_int("CCT_TEST_MERGE_SORT", 0) && D > 0;
-  Buf tr_key, tr_info, tr_pblk, tr_occ, tr_par, tr_cnt, tr_end, tr_hist, tr_gstart, tr_cidx, tr_rb, tr_lg, tr_spl, tr_bc, tr_grp, tr_grp2, tr_pos,
-      tr_c, tr_cs, tr_blk, tr_lists, tr_ctr;
-  TrieArgs ta{};
-  if (use_trie) {
-    const uint64_t tcap = pow2_at_least(std::max<uint64_t>(2 * (uint64_t)nblocks, 1024));
-    const int64_t nbk = std::max<int64_t>(nblocks, 1);
-    const int64_t list_cap = nbk + 1024;
-    const int64_t large_cap = nbk / 1024 + 1;  // groups of more than 1024 siblings
-    const int64_t scan_rows = std::max<int64_t>((int64_t)tcap + 1, nbk);
-    if (!tr_key.alloc(tcap * 8) || !tr_info.alloc(tcap * 8) || !tr_pblk.alloc(nbk * 4) || !tr_occ.alloc(nbk * 4) ||
-        !tr_par.alloc(tcap * 4) || !tr_cnt.alloc(tcap * 4) || !tr_end.alloc((tcap + 1) * 4) ||
-        !tr_hist.alloc((tcap + 1) * 8) || !tr_gstart.alloc((tcap + 2) * 8) || !tr_cidx.alloc(tcap * 4) ||
-        !tr_rb.alloc(1024 * 4) || !tr_lg.alloc((tcap + 1) * 4) || !tr_spl.alloc(large_cap * 256 * 4) ||
-        !tr_bc.alloc(large_cap * 256 * 4) ||
-        !tr_grp.alloc(nbk * 4) || !tr_grp2.alloc(nbk * 4) || !tr_pos.alloc(tcap * 4) || !tr_c.alloc(nbk * 8) ||
-        !tr_cs.alloc((nbk + 1) * 8) || !tr_blk.alloc((scan_rows / 1024 + 2) * 8) || !tr_lists.alloc(3 * list_cap * 8) ||
-        !tr_ctr.alloc(64))
-      return fail(CCT_ENOMEM, "device allocation failed");
-    ta.d = D; ta.nblocks = nblocks; ta.cap = tcap;
-    ta.pframes = ca.pframes; ta.pcp = ca.pcp; ta.pstart = ca.pstart; ta.plen = ca.plen;
-    ta.tkey = tr_key.as<uint64_t>(); ta.tinfo = tr_info.as<uint64_t>(); ta.pblk = tr_pblk.as<uint32_t>();
-    ta.occ = tr_occ.as<uint32_t>(); ta.nparent = tr_par.as<uint32_t>(); ta.ncount = tr_cnt.as<uint32_t>();
-    ta.nend = tr_end.as<uint32_t>(); ta.hist = tr_hist.as<uint64_t>(); ta.gstart = tr_gstart.as<uint64_t>();
-    ta.cidx = tr_cidx.as<uint32_t>(); ta.rootbase = tr_rb.as<uint32_t>(); ta.grouped = tr_grp.as<uint32_t>(); ta.grouped2 = tr_grp2.as<uint32_t>();
-    ta.posof = tr_pos.as<uint32_t>(); ta.cnt = tr_c.as<uint64_t>(); ta.cnt_scan = tr_cs.as<uint64_t>();
-    ta.scan_blk = tr_blk.as<uint64_t>(); ta.lists = tr_lists.as<uint64_t>(); ta.list_cap = list_cap; ta.large_cap = large_cap;
-    ta.lgroup = tr_lg.as<uint32_t>(); ta.spl = tr_spl.as<uint32_t>(); ta.bcnt = tr_bc.as<uint32_t>();
-    ta.ctr = tr_ctr.as<unsigned long long>(); ta.order = ca.order;
-  }
   // 0: block trie, 1: comparison sort with checkpoint hashes, 2: exact comparisons only,
   // 3: the previous order with this call's new paths merged in
   for (int mode = incremental ? 3 : (use_trie ? 0 : (ca.exact ? 2 : 1));;) {
     CanonArgs run = ca;
     run.exact = mode == 2 ? 1 : 0;
     if (mode == 0) launch_trie_sort(ta, s);
-    else if (mode == 3) launch_merge_order(run, t->order.as<uint32_t>(), t->d, s);
+    else if (mode == 3) launch_merge_order(run, t->order.as<uint32_t>(), t->d, merge_scratch.as<uint32_t>(), s);
     else launch_sort(run, s);
     tm.mark(4, s);
     launch_canon(run, s);

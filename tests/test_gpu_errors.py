@@ -60,7 +60,7 @@ def test_merge_failure_leaves_tree_unchanged():
     tree.free()
 
 
-@pytest.mark.parametrize("k", [1, 2, 3, 5, 8, 12, 20])
+@pytest.mark.parametrize("k", [1, 2, 3, 5, 8, 12, 16, 20, 24, 28, 32, 36])
 def test_allocation_failure(monkeypatch, k):
     import paper_2411_02797_amd as cct
     o, f, w = tracegen.random_paths(3000, 40, 10, 1, seed=k)
@@ -76,13 +76,17 @@ def test_allocation_failure(monkeypatch, k):
         assert e.name == "CCT_ENOMEM"
         merged = False
     monkeypatch.delenv("CCT_TEST_FAIL_ALLOC")
+    orc = oracle.Oracle(1)
+    orc.ingest(o, f, w)
+    orc.ingest(o2, f2, w2)
     if merged:
-        orc = oracle.Oracle(1)
-        orc.ingest(o, f, w)
-        orc.ingest(o2, f2, w2)
         assert_same(tree.to_numpy(), orc.tree(), "merged")
     else:
         assert_same(tree.to_numpy(), before, "unchanged after ENOMEM")
+        # the failed call left no trace in the tree's table, path store or sums
+        tree.merge(*d2)
+        assert_same(tree.to_numpy(), orc.tree(), "merge after ENOMEM")
+    orc.close()
     tree.free()
     monkeypatch.setenv("CCT_TEST_FAIL_ALLOC", str(k))
     try:
