@@ -21,6 +21,8 @@
 //     path, which sorts first, puts its sums on the root).
 // Every step is a sort, a scan or an O(log D) search: the number of kernel launches
 // does not grow with the tree depth.
+#include <algorithm>
+
 #include "common.h"
 
 namespace cct {
@@ -197,7 +199,7 @@ __global__ void lcp_kernel(CanonArgs a) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i > a.d) return;
   const int C = 1 + a.m;
-  if (i == a.d) { a.lcp[i] = 0; return; }
+  if (i == a.d) { a.lcp[i] = 0; a.sparse[i] = 0; return; }
   const uint32_t p = a.order[i];
   uint32_t l = 0;
   if (i > 0) {
@@ -205,6 +207,7 @@ __global__ void lcp_kernel(CanonArgs a) {
     if (r >= 0) atomicOr(&a.u_out[1], 1ull);  // not strictly increasing
   }
   a.lcp[i] = l;
+  a.sparse[i] = l;  // level 0 of the range-minimum table
   uint64_t *row = a.scan_in + i * C;
   row[0] = (uint64_t)(a.plen[p] - l);
   for (int j = 0; j < a.m; ++j) row[1 + j] = a.psums[(int64_t)p * a.m + j];
@@ -300,6 +303,26 @@ __global__ void sparse_level_kernel(uint32_t *sp, int64_t n, int k) {
   uint32_t v = prev[x];
   if (x + h < n) v = min(v, prev[x + h]);
   sp[(int64_t)k * n + x] = v;
+}
+
+// Levels 1 .. kTileLevels in one pass: a workgroup takes kTileOut positions, loads
+// their lcp values and the 2^kTileLevels - 1 after them (past n: +inf) into LDS,
+// and builds every level there from the one below.
+constexpr int kTileLevels = 11, kTileOut = 2048, kTileIn = kTileOut + (1 << kTileLevels);
+__global__ __launch_bounds__(1024) void sparse_tile_kernel(uint32_t *sp, const uint32_t *lcp, int64_t n, int top) {
+  __shared__ uint32_t buf[2][kTileIn];
+  const int64_t x0 = (int64_t)blockIdx.x * kTileOut;
+  for (int i = threadIdx.x; i < kTileIn; i += 1024) buf[0][i] = x0 + i < n ? lcp[x0 + i] : 0xFFFFFFFFu;
+  __syncthreads();
+  int cur = 0;
+  for (int k = 1; k <= top; ++k) {
+    const int h = 1 << (k - 1);
+    for (int i = threadIdx.x; i + h < kTileIn; i += 1024) buf[cur ^ 1][i] = min(buf[cur][i], buf[cur][i + h]);
+    __syncthreads();
+    cur ^= 1;
+    for (int i = threadIdx.x; i < kTileOut; i += 1024)
+      if (x0 + i < n) sp[(int64_t)k * n + x0 + i] = buf[cur][i];
+  }
 }
 
 // first j >= s with lcp[j] < t (exists: lcp[D] = 0 < t for t >= 1)
@@ -432,9 +455,12 @@ void launch_canon(const CanonArgs &a, hipStream_t s) {
   const int64_t n = a.d + 1;
   hipLaunchKernelGGL(lcp_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, a);
   launch_scan(a.scan_in, a.d, C, a.scan_blk, a.scan_out, s);
-  // level 0 of the range-minimum table is lcp itself
-  (void)hipMemcpyAsync(a.sparse, a.lcp, sizeof(uint32_t) * n, hipMemcpyDeviceToDevice, s);
-  for (int k = 1; k < a.levels; ++k)
+  // range-minimum table: level 0 (lcp itself) written by lcp_kernel, levels up to
+  // kTileLevels in LDS tiles, the rest one level per launch
+  const int top = std::min(a.levels - 1, kTileLevels);
+  if (top >= 1)
+    hipLaunchKernelGGL(sparse_tile_kernel, dim3(blocks_for(n, kTileOut)), dim3(1024), 0, s, a.sparse, a.lcp, n, top);
+  for (int k = top + 1; k < a.levels; ++k)
     hipLaunchKernelGGL(sparse_level_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, a.sparse, n, k);
   if (a.d > 0) hipLaunchKernelGGL(chain_kernel, dim3(blocks_for(a.d, 256)), dim3(256), 0, s, a);
   hipLaunchKernelGGL(emit_kernel, dim3(a.grid_nodes), dim3(256), 0, s, a);

@@ -792,27 +792,35 @@ __global__ __launch_bounds__(256) void publish_kernel(PublishArgs a) {
   const int64_t rl = round_store(len);
   const int64_t start = a.store_used + (int64_t)a.starts[i];
   const int64_t id = a.d_old + i;
-  for (int64_t k = lane; k < rl; k += 64) a.pframes[start + k] = k < len ? a.fr[src + k] : 0u;
-  // checkpoint hashes: lane b sums block b of 16 frames; a wave prefix scan then
-  // gives the prefix sums at every block boundary
+  // copy the frames (zero tail) and compute the checkpoint hashes from the same
+  // coalesced loads: each group of 16 lanes holds one block of a 64-frame chunk, sums
+  // its terms with shuffles, and the blocks' prefix sums are carried across chunks
+  const int64_t full = len / kStoreAlign * kStoreAlign;  // frames of the full blocks
+  const int g = lane >> 4;
   uint64_t carry = 0;
-  const int64_t nblk = len / kStoreAlign;
-  for (int64_t b0 = 0; b0 < nblk; b0 += 64) {
-    const int64_t b = b0 + lane;
-    uint64_t v = 0;
-    if (b < nblk)
-      for (int k = 0; k < kStoreAlign; ++k) {
-        const int64_t p = b * kStoreAlign + k;
-        v += frame_term(a.fr[src + p], (uint32_t)p);
-      }
-    for (int o = 1; o < 64; o <<= 1) {  // inclusive scan across the wave
-      uint32_t lo = __shfl_up((uint32_t)v, o, 64), hi = __shfl_up((uint32_t)(v >> 32), o, 64);
-      if (lane >= o) v += ((uint64_t)hi << 32) | lo;
+  for (int64_t k0 = 0; k0 < rl; k0 += 64) {
+    const int64_t k = k0 + lane;
+    const uint32_t f = k < len ? a.fr[src + k] : 0u;
+    if (k < rl) a.pframes[start + k] = f;
+    uint64_t v = k < full ? frame_term(f, (uint32_t)k) : 0ull;
+    for (int o = 1; o < 16; o <<= 1) {  // sum over the 16 lanes of the block
+      const uint32_t lo = __shfl_xor((uint32_t)v, o, 64), hi = __shfl_xor((uint32_t)(v >> 32), o, 64);
+      v += ((uint64_t)hi << 32) | lo;
     }
-    v += carry;
-    if (b < nblk) a.pcp[start / kStoreAlign + b] = finish_hash(v, (uint64_t)(b + 1) * kStoreAlign);
-    uint32_t lo = __shfl((uint32_t)v, 63, 64), hi = __shfl((uint32_t)(v >> 32), 63, 64);
-    carry = ((uint64_t)hi << 32) | lo;
+    uint64_t bs[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t lo = __shfl((uint32_t)v, 16 * q, 64), hi = __shfl((uint32_t)(v >> 32), 16 * q, 64);
+      bs[q] = ((uint64_t)hi << 32) | lo;
+    }
+    uint64_t pre = carry;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (q <= g) pre += bs[q];
+    const int64_t b = k0 / kStoreAlign + g;  // this lane group's block
+    if ((lane & 15) == 15 && (b + 1) * kStoreAlign <= full)
+      a.pcp[start / kStoreAlign + b] = finish_hash(pre, (uint64_t)(b + 1) * kStoreAlign);
+    carry += bs[0] + bs[1] + bs[2] + bs[3];
   }
   if (lane == 0) {
     a.pstart[id] = start;

@@ -491,10 +491,25 @@ __global__ __launch_bounds__(kMedThreads) void reorder_kernel(TrieArgs a) {
     const uint64_t e = a.lists[kListLarge * a.list_cap + g];
     const uint32_t start = (uint32_t)(e >> 32), n = (uint32_t)e;
     const int nb = buckets_for(n);
-    if (threadIdx.x == 0) {
-      uint32_t run = 0;
-      for (int j = 0; j < nb; ++j) { R.bstart[j] = run; run += a.bcnt[g * kMaxBuckets + j]; }
+    // bucket starts: exclusive prefix sums of the bucket sizes (nb <= 256: four waves)
+    uint32_t c = 0, x = 0;
+    if (threadIdx.x < kMaxBuckets) {
+      const int lane = threadIdx.x & 63;
+      c = (int)threadIdx.x < nb ? a.bcnt[g * kMaxBuckets + threadIdx.x] : 0u;
+      x = c;
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t y = __shfl_up(x, o, 64);
+        if (lane >= o) x += y;
+      }
+      R.bcur[threadIdx.x] = x;  // inclusive within the wave
     }
+    __syncthreads();
+    if (threadIdx.x < kMaxBuckets) {
+      uint32_t before = 0;
+      for (int q = 0; q < (int)(threadIdx.x >> 6); ++q) before += R.bcur[64 * q + 63];
+      R.bstart[threadIdx.x] = before + x - c;
+    }
+    __syncthreads();
     for (int j = threadIdx.x; j < nb; j += kMedThreads) R.bcur[j] = 0;
     __syncthreads();
     for (uint32_t i = threadIdx.x; i < n; i += kMedThreads) {
