@@ -312,8 +312,10 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
       tm.mark(1, s);
       launch_ingest(a, grid, s);
       tm.mark(2, s);
-      // metric sums: per-workgroup LDS maps, flushed through staging buckets of slots
-      const int agg_grid = (int)std::max<int64_t>(1, std::min<int64_t>((N + 8191) / 8192, (int64_t)cu_count()));
+      // metric sums: per-workgroup LDS maps, flushed through staging buckets of slots; two
+      // workgroups per CU (run one after the other) halve the distinct slots each map
+      // must hold, so fewer events overflow into device atomics
+      const int agg_grid = (int)std::max<int64_t>(1, std::min<int64_t>((N + 8191) / 8192, (int64_t)cu_count() * 2));
       AggStage stg{};
       stg.bshift = agg_bucket_shift(m);
       const int64_t nbk = std::max<int64_t>(1, (int64_t)(t->cap >> stg.bshift));
