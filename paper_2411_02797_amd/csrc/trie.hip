@@ -27,7 +27,8 @@ namespace {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kBlk = kStoreAlign;           // frames per block
-constexpr int kChunk = 512;                 // groups up to this size are sorted by chunk
+constexpr int kChunk = 512;                 // groups up to this size are not split into buckets
+constexpr int kSmallGroup = 64;             // groups up to this size are ranked by chunk
 constexpr int kChunkCap = 2 * kChunk;       // staged members of one chunk (at most 2 kChunk - 1)
 constexpr int kMedium = 2048;               // LDS sort capacity of one workgroup
 constexpr uint64_t kRootSeed = 0x5851F42D4C957F2Dull;
@@ -221,6 +222,10 @@ __global__ __launch_bounds__(256) void scatter_kernel(TrieArgs a) {
     } else {
       fail(a);
     }
+  } else if (c == 0 && n > (uint64_t)kSmallGroup) {  // one workgroup each (medium_kernel)
+    const unsigned long long i = atomicAdd(&a.ctr[kListMedium], 1ull);
+    if ((int64_t)i < a.list_cap) a.lists[kListMedium * a.list_cap + i] = (g0 << 32) | n;
+    else fail(a);
   }
 }
 
@@ -277,17 +282,17 @@ struct MedShared {
   uint16_t si[kMedium];
 };
 
-// Groups of 2 .. 512 siblings, by chunk: workgroup c orders every such group whose
-// start lies in positions [512 c, 512 c + 512) -- at most 1023 consecutive
-// positions.  Their members (singleton groups skipped) are staged in LDS and sorted
-// together by (group start, block) with one bitonic sort.
+// Groups of 2 .. 64 siblings, by chunk: workgroup c orders every such group whose
+// start lies in positions [512 c, 512 c + 512) -- at most 575 consecutive positions,
+// staged in LDS in position order, so every group is a contiguous run.  Each member's
+// rank in its group is the number of siblings with a smaller block (siblings' blocks
+// are distinct): at most 63 comparisons per member and no barriers between them.
 struct ChunkShared {
   uint32_t sb[kChunkCap][kBlk];
   uint8_t sn[kChunkCap];
-  uint16_t si[kChunkCap];
-  uint32_t gkey[kChunkCap];  // group start of each staged member
-  uint16_t pos[kChunkCap];   // its chunk-local position
-  uint32_t first, last_end, count;
+  uint16_t gs[kChunkCap];    // chunk-local start of the member's group (kNone: not ranked here)
+  uint8_t gn[kChunkCap];     // the group's size
+  uint32_t first, last_end;
 };
 
 constexpr int kChunkThreads = 512;
@@ -296,14 +301,14 @@ __global__ __launch_bounds__(kChunkThreads) void chunk_kernel(TrieArgs a) {
   const uint64_t nodes = a.gstart[a.cap + 1];
   const uint64_t lo = (uint64_t)blockIdx.x * kChunk;
   if (lo >= nodes) return;
-  if (threadIdx.x == 0) { C.first = 0xFFFFFFFFu; C.last_end = 0; C.count = 0; }
+  if (threadIdx.x == 0) { C.first = 0xFFFFFFFFu; C.last_end = 0; }
   __syncthreads();
   {
     const uint64_t p = lo + threadIdx.x;
     if (threadIdx.x < kChunk && p < nodes) {
       const uint32_t P = a.nparent[a.grouped[p]];
       const uint64_t g0 = a.gstart[P], n = a.hist[P];
-      if (g0 == p && n >= 2 && n <= (uint64_t)kChunk) {
+      if (g0 == p && n >= 2 && n <= (uint64_t)kSmallGroup) {
         atomicMin(&C.first, (uint32_t)p);
         atomicMax(&C.last_end, (uint32_t)(p + n));
       }
@@ -312,38 +317,41 @@ __global__ __launch_bounds__(kChunkThreads) void chunk_kernel(TrieArgs a) {
   __syncthreads();
   if (C.first == 0xFFFFFFFFu) return;
   const uint32_t first = C.first, m = C.last_end - first;
-  for (uint32_t i = threadIdx.x; i < m; i += kChunkThreads) {
+  // stage: position first + i with its group's local range (small groups only)
+  constexpr int kPer = kChunkCap / kChunkThreads;
+  uint32_t Xs[kPer];
+#pragma unroll
+  for (int q = 0; q < kPer; ++q) {
+    const uint32_t i = threadIdx.x + q * kChunkThreads;
+    Xs[q] = 0;
+    if (i >= m) continue;
     const uint32_t X = a.grouped[first + i];
     const uint32_t P = a.nparent[X];
-    if (a.hist[P] < 2) continue;
-    const uint32_t k = atomicAdd(&C.count, 1u);
+    const uint64_t g0 = a.gstart[P], n = a.hist[P];
+    Xs[q] = X;
+    C.gs[i] = kNone;
+    if (n < 2 || n > (uint64_t)kSmallGroup || g0 < first || g0 + n > (uint64_t)first + m) continue;
     u32x4 v[4];
     uint32_t nf;
     node_block(a, X, v, nf);
 #pragma unroll
-    for (int c = 0; c < 4; ++c) *(u32x4 *)&C.sb[k][4 * c] = v[c];
-    C.sn[k] = (uint8_t)nf;
-    C.gkey[k] = (uint32_t)a.gstart[P];
-    C.pos[k] = (uint16_t)i;
+    for (int c = 0; c < 4; ++c) *(u32x4 *)&C.sb[i][4 * c] = v[c];
+    C.sn[i] = (uint8_t)nf;
+    C.gs[i] = (uint16_t)(g0 - first);
+    C.gn[i] = (uint8_t)n;
   }
   __syncthreads();
-  const uint32_t cnt = C.count;
-  lds_bitonic(C.si, (int)cnt, [&](uint16_t p, uint16_t q) {
-    return C.gkey[p] != C.gkey[q] ? C.gkey[p] < C.gkey[q] : block_less(C.sb[p], C.sn[p], C.sb[q], C.sn[q]);
-  });
-  // a member of rank r in the sorted order goes to its group's start + (r - the rank of
-  // the group's first member); every original position is read before any write
-  uint32_t Xs[kChunkCap / kChunkThreads];
-  for (uint32_t r = threadIdx.x, q = 0; r < cnt; r += kChunkThreads, ++q) Xs[q] = a.grouped[first + C.pos[C.si[r]]];
-  __syncthreads();
-  for (uint32_t r = threadIdx.x, q = 0; r < cnt; r += kChunkThreads, ++q) {
-    const uint32_t G = C.gkey[C.si[r]];
-    uint32_t lo2 = 0, hi2 = r;
-    while (lo2 < hi2) {
-      const uint32_t mid = (lo2 + hi2) >> 1;
-      if (C.gkey[C.si[mid]] < G) lo2 = mid + 1; else hi2 = mid;
-    }
-    const uint32_t pos = G + (r - lo2);
+  // rank within the group; every original position was read before any write, and a
+  // member's new position stays inside its group's range
+#pragma unroll
+  for (int q = 0; q < kPer; ++q) {
+    const uint32_t i = threadIdx.x + q * kChunkThreads;
+    if (i >= m || C.gs[i] == kNone) continue;
+    const uint32_t g = C.gs[i], n = C.gn[i];
+    uint32_t rank = 0;
+    for (uint32_t j = g; j < g + n; ++j)
+      if (j != i && block_less(C.sb[j], C.sn[j], C.sb[i], C.sn[i])) ++rank;
+    const uint32_t pos = first + g + rank;
     a.grouped[pos] = Xs[q];
     a.posof[Xs[q]] = pos;
   }
