@@ -440,7 +440,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     const uint64_t tcap = pow2_at_least(std::max<uint64_t>(2 * (uint64_t)nblocks, 1024));
     const int64_t nbk = std::max<int64_t>(nblocks, 1);
     const int64_t list_cap = nbk + 1024;
-    const int64_t large_cap = nbk / 1024 + 1;  // groups of more than 1024 siblings
+    const int64_t large_cap = nbk / 512 + 1;  // groups of more than 512 siblings (split into buckets)
     const int64_t scan_rows = std::max<int64_t>((int64_t)tcap + 1, nbk);
     if (!tr_key.alloc(tcap * 8) || !tr_info.alloc(tcap * 8) || !tr_pblk.alloc(nbk * 4) || !tr_occ.alloc(nbk * 4) ||
         !tr_par.alloc(tcap * 4) || !tr_cnt.alloc(tcap * 4) || !tr_end.alloc((tcap + 1) * 4) ||

@@ -488,60 +488,70 @@ __global__ __launch_bounds__(kMedThreads) void classify_kernel(TrieArgs a) {
   atomicAdd(&a.bcnt[g * kMaxBuckets + blo], 1u);
 }
 
-// one workgroup per large group: reorder by bucket, list the buckets
-struct ReorderShared {
-  uint32_t bstart[kMaxBuckets], bcur[kMaxBuckets];
-};
-__global__ __launch_bounds__(kMedThreads) void reorder_kernel(TrieArgs a) {
-  __shared__ ReorderShared R;
+// Large groups reordered by bucket, in three grid-wide steps (a large group has
+// thousands of members):
+//  - bstart_kernel, one small workgroup per large group: bucket starts (exclusive
+//    prefix sums of the bucket sizes, into spl, whose splitters are no longer needed),
+//    the buckets listed for sorting, and the sizes reset to serve as cursors;
+//  - rscatter_kernel, every member: its bucket's start + a cursor atomic, into grouped2;
+//  - rcopy_kernel, every member: back into grouped, with its position.
+__global__ __launch_bounds__(kMaxBuckets) void bstart_kernel(TrieArgs a) {
+  __shared__ uint32_t wsum[kMaxBuckets / 64];
   const uint64_t ng = min((uint64_t)a.ctr[kListLarge], (uint64_t)a.large_cap);
-  for (uint64_t g = blockIdx.x; g < ng; g += gridDim.x) {
-    const uint64_t e = a.lists[kListLarge * a.list_cap + g];
-    const uint32_t start = (uint32_t)(e >> 32), n = (uint32_t)e;
-    const int nb = buckets_for(n);
-    // bucket starts: exclusive prefix sums of the bucket sizes (nb <= 256: four waves)
-    uint32_t c = 0, x = 0;
-    if (threadIdx.x < kMaxBuckets) {
-      const int lane = threadIdx.x & 63;
-      c = (int)threadIdx.x < nb ? a.bcnt[g * kMaxBuckets + threadIdx.x] : 0u;
-      x = c;
-      for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t y = __shfl_up(x, o, 64);
-        if (lane >= o) x += y;
-      }
-      R.bcur[threadIdx.x] = x;  // inclusive within the wave
-    }
-    __syncthreads();
-    if (threadIdx.x < kMaxBuckets) {
-      uint32_t before = 0;
-      for (int q = 0; q < (int)(threadIdx.x >> 6); ++q) before += R.bcur[64 * q + 63];
-      R.bstart[threadIdx.x] = before + x - c;
-    }
-    __syncthreads();
-    for (int j = threadIdx.x; j < nb; j += kMedThreads) R.bcur[j] = 0;
-    __syncthreads();
-    for (uint32_t i = threadIdx.x; i < n; i += kMedThreads) {
-      const uint32_t X = a.grouped[start + i];
-      const uint32_t bk = a.posof[X];
-      a.grouped2[start + R.bstart[bk] + atomicAdd(&R.bcur[bk], 1u)] = X;
-    }
-    __syncthreads();
-    for (uint32_t i = threadIdx.x; i < n; i += kMedThreads) {
-      const uint32_t X = a.grouped2[start + i];
-      a.grouped[start + i] = X;
-      a.posof[X] = start + i;
-    }
-    for (int j = threadIdx.x; j < nb; j += kMedThreads) {
-      const uint32_t c = a.bcnt[g * kMaxBuckets + j];
-      if (c < 2) continue;
-      if (c > (uint32_t)kMedium) { fail(a); continue; }
-      const int cls = c <= 64 ? kListSmall : kListMedium;
-      const unsigned long long i = atomicAdd(&a.ctr[cls], 1ull);
-      if ((int64_t)i < a.list_cap) a.lists[cls * a.list_cap + i] = ((uint64_t)(start + R.bstart[j]) << 32) | c;
-      else fail(a);
-    }
-    __syncthreads();
+  const uint64_t g = blockIdx.x;
+  if (g >= ng) return;
+  const uint64_t e = a.lists[kListLarge * a.list_cap + g];
+  const uint32_t start = (uint32_t)(e >> 32), n = (uint32_t)e;
+  const int nb = buckets_for(n);
+  const int j = threadIdx.x, lane = j & 63, w = j >> 6;
+  const uint32_t c = j < nb ? a.bcnt[g * kMaxBuckets + j] : 0u;
+  uint32_t x = c;
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
   }
+  if (lane == 63) wsum[w] = x;
+  __syncthreads();
+  uint32_t before = 0;
+  for (int q = 0; q < w; ++q) before += wsum[q];
+  const uint32_t bs = before + x - c;
+  if (j >= nb) return;
+  a.spl[g * kMaxBuckets + j] = bs;
+  a.bcnt[g * kMaxBuckets + j] = 0;
+  if (c < 2) return;
+  if (c > (uint32_t)kMedium) { fail(a); return; }
+  const int cls = c <= 64 ? kListSmall : kListMedium;
+  const unsigned long long i = atomicAdd(&a.ctr[cls], 1ull);
+  if ((int64_t)i < a.list_cap) a.lists[cls * a.list_cap + i] = ((uint64_t)(start + bs) << 32) | c;
+  else fail(a);
+}
+
+// the large group of the member at position p (its bucket is in posof), or -1
+__device__ inline int64_t large_group_of(const TrieArgs &a, uint32_t X) {
+  const uint32_t P = a.nparent[X];
+  if (a.hist[P] <= (uint64_t)kChunk) return -1;
+  const uint64_t g = a.lgroup[P];
+  return g < min((uint64_t)a.ctr[kListLarge], (uint64_t)a.large_cap) ? (int64_t)g : -1;
+}
+
+__global__ void rscatter_kernel(TrieArgs a) {
+  const uint64_t p = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= a.gstart[a.cap + 1]) return;
+  const uint32_t X = a.grouped[p];
+  const int64_t g = large_group_of(a, X);
+  if (g < 0) return;
+  const uint32_t bk = a.posof[X];
+  const uint64_t dst = a.gstart[a.nparent[X]] + a.spl[g * kMaxBuckets + bk] + atomicAdd(&a.bcnt[g * kMaxBuckets + bk], 1u);
+  a.grouped2[dst] = X;
+}
+
+__global__ void rcopy_kernel(TrieArgs a) {
+  const uint64_t p = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= a.gstart[a.cap + 1]) return;
+  if (large_group_of(a, a.grouped[p]) < 0) return;
+  const uint32_t X = a.grouped2[p];
+  a.grouped[p] = X;
+  a.posof[X] = (uint32_t)p;
 }
 
 // buckets of up to 64: one wave each, every member counts the members before it
@@ -617,7 +627,9 @@ void launch_trie_sort(const TrieArgs &a, hipStream_t s) {
     hipLaunchKernelGGL(chunk_kernel, dim3(blocks_for(a.nblocks, kChunk)), dim3(kChunkThreads), 0, s, a);
     hipLaunchKernelGGL(split_kernel, dim3(256), dim3(kMedThreads), 0, s, a);
     hipLaunchKernelGGL(classify_kernel, dim3(blocks_for(a.nblocks, kChunk)), dim3(kMedThreads), 0, s, a);
-    hipLaunchKernelGGL(reorder_kernel, dim3(256), dim3(kMedThreads), 0, s, a);
+    hipLaunchKernelGGL(bstart_kernel, dim3((unsigned)a.large_cap), dim3(kMaxBuckets), 0, s, a);
+    hipLaunchKernelGGL(rscatter_kernel, dim3(blocks_for(a.nblocks, 256)), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(rcopy_kernel, dim3(blocks_for(a.nblocks, 256)), dim3(256), 0, s, a);
     hipLaunchKernelGGL(bucket_kernel, dim3(1024), dim3(64 * kBucketWaves), 0, s, a);
     hipLaunchKernelGGL(medium_kernel, dim3(256), dim3(kMedThreads), 0, s, a);
     hipLaunchKernelGGL(counts_kernel, dim3(blocks_for(a.nblocks, 256)), dim3(256), 0, s, a);
