@@ -159,8 +159,9 @@ struct PublishArgs {
   uint64_t *psums;           // [D][m]
   int64_t store_used;        // frames already used in the store
   const uint64_t *starts;    // [n_new] exclusive prefix sums of the padded lengths
+  const int64_t *src_len;    // [n_new][2] first frame in the batch and length of each new path
 };
-void launch_new_lengths(const int64_t *off, const Slot *slot, const uint32_t *new_slots, int64_t n,
+void launch_new_lengths(const int64_t *off, const Slot *slot, const uint32_t *new_slots, int64_t n, int64_t *src_len,
                         uint64_t *out, hipStream_t s);
 void launch_publish(const PublishArgs &a, hipStream_t s);
 // Exclusive prefix sums of `rows` rows of C uint64 columns (mod 2^64) into out[0..rows),

@@ -781,48 +781,66 @@ __global__ __launch_bounds__(256) void collect_sum_kernel(const unsigned long lo
 // into the tree's path store (16-frame aligned, zero tail), write its checkpoint
 // hashes and exclusive sums, and point its table slot at the path id and the stored
 // frames.  One wave per path.
+// Publish: copy every new path into the path store (zero tail up to its padded length),
+// record its checkpoint hashes, its start, length and table slot, and its sums.  One
+// wave per new path.  Its first frame and length come from new_lengths_kernel (one
+// load), and the frames of up to four 64-frame chunks are requested before any is used
+// (paths of up to 256 frames take one round trip; deeper prefetch measured slower).  Within a chunk each group of 16
+// lanes holds one block, sums its frame terms with shuffles, and the blocks' prefix sums
+// are carried across chunks.
+constexpr int kPublishChunks = 4;  // 64-frame chunks requested ahead
 __global__ __launch_bounds__(256) void publish_kernel(PublishArgs a) {
   const int lane = threadIdx.x & 63;
   const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   if (i >= a.n_new) return;
+  const int64_t src = a.src_len[2 * i], len = a.src_len[2 * i + 1];
   const uint32_t s = a.new_slots[i];
-  const uint64_t w = a.slot[s].word;
-  const int64_t e = (int64_t)((uint32_t)w & kRefMask);
-  const int64_t src = a.off[e], len = a.off[e + 1] - src;
   const int64_t rl = round_store(len);
   const int64_t start = a.store_used + (int64_t)a.starts[i];
   const int64_t id = a.d_old + i;
-  // copy the frames (zero tail) and compute the checkpoint hashes from the same
-  // coalesced loads: each group of 16 lanes holds one block of a 64-frame chunk, sums
-  // its terms with shuffles, and the blocks' prefix sums are carried across chunks
   const int64_t full = len / kStoreAlign * kStoreAlign;  // frames of the full blocks
   const int g = lane >> 4;
   uint64_t carry = 0;
+  uint32_t fq[kPublishChunks];
   for (int64_t k0 = 0; k0 < rl; k0 += 64) {
-    const int64_t k = k0 + lane;
-    const uint32_t f = k < len ? a.fr[src + k] : 0u;
-    if (k < rl) a.pframes[start + k] = f;
-    uint64_t v = k < full ? frame_term(f, (uint32_t)k) : 0ull;
-    for (int o = 1; o < 16; o <<= 1) {  // sum over the 16 lanes of the block
-      const uint32_t lo = __shfl_xor((uint32_t)v, o, 64), hi = __shfl_xor((uint32_t)(v >> 32), o, 64);
-      v += ((uint64_t)hi << 32) | lo;
-    }
-    uint64_t bs[4];
+    const int c = (int)((k0 >> 6) % kPublishChunks);
+    if (c == 0) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint32_t lo = __shfl((uint32_t)v, 16 * q, 64), hi = __shfl((uint32_t)(v >> 32), 16 * q, 64);
-      bs[q] = ((uint64_t)hi << 32) | lo;
+      for (int u = 0; u < kPublishChunks; ++u) {
+        const int64_t k = k0 + 64 * u + lane;
+        fq[u] = k < len ? a.fr[src + k] : 0u;
+      }
     }
-    uint64_t pre = carry;
+    {
+      const int64_t k = k0 + lane;
+      uint32_t f = fq[0];
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      if (q <= g) pre += bs[q];
-    const int64_t b = k0 / kStoreAlign + g;  // this lane group's block
-    if ((lane & 15) == 15 && (b + 1) * kStoreAlign <= full)
-      a.pcp[start / kStoreAlign + b] = finish_hash(pre, (uint64_t)(b + 1) * kStoreAlign);
-    carry += bs[0] + bs[1] + bs[2] + bs[3];
+      for (int u = 1; u < kPublishChunks; ++u)
+        if (c == u) f = fq[u];
+      if (k < rl) a.pframes[start + k] = f;
+      uint64_t v = k < full ? frame_term(f, (uint32_t)k) : 0ull;
+      for (int o = 1; o < 16; o <<= 1) {  // sum over the 16 lanes of the block
+        const uint32_t lo = __shfl_xor((uint32_t)v, o, 64), hi = __shfl_xor((uint32_t)(v >> 32), o, 64);
+        v += ((uint64_t)hi << 32) | lo;
+      }
+      uint64_t bs[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t lo = __shfl((uint32_t)v, 16 * q, 64), hi = __shfl((uint32_t)(v >> 32), 16 * q, 64);
+        bs[q] = ((uint64_t)hi << 32) | lo;
+      }
+      uint64_t pre = carry;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (q <= g) pre += bs[q];
+      const int64_t b = k0 / kStoreAlign + g;  // this lane group's block
+      if ((lane & 15) == 15 && (b + 1) * kStoreAlign <= full)
+        a.pcp[start / kStoreAlign + b] = finish_hash(pre, (uint64_t)(b + 1) * kStoreAlign);
+      carry += bs[0] + bs[1] + bs[2] + bs[3];
+    }
   }
   if (lane == 0) {
+    const uint64_t w = a.slot[s].word;
     a.pstart[id] = start;
     a.plen[id] = (uint32_t)len;
     a.pslot[id] = s;
@@ -832,13 +850,18 @@ __global__ __launch_bounds__(256) void publish_kernel(PublishArgs a) {
   if (lane < a.m) a.psums[id * a.m + lane] = a.delta[(uint64_t)s * a.m + lane];
 }
 
-// Padded store length of every new path (input of the scan that places them).
+// Padded store length of every new path (input of the scan that places them), and the
+// path's first frame and length in the batch (so that publish_kernel starts from one
+// load instead of the slot -> event -> offsets chain).
 __global__ void new_lengths_kernel(const int64_t *off, const Slot *slot, const uint32_t *new_slots, int64_t n,
-                                   uint64_t *out) {
+                                   int64_t *src_len, uint64_t *out) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   const int64_t e = (int64_t)((uint32_t)slot[new_slots[i]].word & kRefMask);
-  out[i] = (uint64_t)round_store(off[e + 1] - off[e]);
+  const int64_t src = off[e], len = off[e + 1] - src;
+  src_len[2 * i] = src;
+  src_len[2 * i + 1] = len;
+  out[i] = (uint64_t)round_store(len);
 }
 
 __global__ void fold_old_kernel(int64_t d_old, int32_t m, const uint32_t *pslot, const uint64_t *delta,
@@ -936,10 +959,11 @@ void launch_collect_new(const Slot *slot, uint64_t cap, const int64_t *off, uint
                      ctr, part);
   hipLaunchKernelGGL(collect_sum_kernel, dim3(1), dim3(256), 0, s, part, nb, ctr);
 }
-void launch_new_lengths(const int64_t *off, const Slot *slot, const uint32_t *new_slots, int64_t n, uint64_t *out,
-                        hipStream_t s) {
+void launch_new_lengths(const int64_t *off, const Slot *slot, const uint32_t *new_slots, int64_t n, int64_t *src_len,
+                        uint64_t *out, hipStream_t s) {
   if (n <= 0) return;
-  hipLaunchKernelGGL(new_lengths_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, off, slot, new_slots, n, out);
+  hipLaunchKernelGGL(new_lengths_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, off, slot, new_slots, n, src_len,
+                     out);
 }
 void launch_publish(const PublishArgs &a, hipStream_t s) {
   if (a.n_new <= 0) return;

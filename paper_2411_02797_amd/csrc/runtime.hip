@@ -410,14 +410,14 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   const int levels = floor_log2((uint64_t)n1) + 1;
   const int64_t nblk = (D + 1023) / 1024 + 1;
   const int64_t u_max = sum_len + 1;
-  Buf order, order_tmp, lcp, scan_in, scan_out, scan_blk, sparse, chain, node_path, cursor, nlen, nstart, nblkbuf;
+  Buf order, order_tmp, lcp, scan_in, scan_out, scan_blk, sparse, chain, node_path, cursor, nlen, nstart, nblkbuf, nsrc;
   Buf n_parent, n_frame, n_depth, n_excl, n_incl;
   if (!order.alloc(dneed * 4) || !order_tmp.alloc(dneed * 4) || !lcp.alloc(n1 * 4) || !scan_in.alloc(dneed * C * 8) ||
       !scan_out.alloc(n1 * C * 8) || !scan_blk.alloc(nblk * C * 8) || !sparse.alloc((int64_t)levels * n1 * 4) ||
       !chain.alloc(dneed * 4) || !node_path.alloc(u_max * 4) || !cursor.alloc(64) || !n_parent.alloc(u_max * 4) ||
       !n_frame.alloc(u_max * 4) || !n_depth.alloc(u_max * 4) || !n_excl.alloc(u_max * m * 8) ||
       !n_incl.alloc(u_max * m * 8) || !nlen.alloc((n_new + 1) * 8) || !nstart.alloc((n_new + 1) * 8) ||
-      !nblkbuf.alloc(((int64_t)n_new / 1024 + 2) * 8))
+      !nblkbuf.alloc(((int64_t)n_new / 1024 + 2) * 8) || !nsrc.alloc(((int64_t)n_new + 1) * 16))
     return rollback(fail(CCT_ENOMEM, "device allocation failed"));
 
   // sorting scratch, allocated before the tree is touched
@@ -469,7 +469,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   if (n_new) {
     // place the new paths in the store: exclusive scan of their padded lengths
     launch_new_lengths(p->offsets, t->slot.as<Slot>(), new_slots.as<uint32_t>(), (int64_t)n_new,
-                       nlen.as<uint64_t>(), s);
+                       nsrc.as<int64_t>(), nlen.as<uint64_t>(), s);
     launch_scan(nlen.as<uint64_t>(), (int64_t)n_new, 1, nblkbuf.as<uint64_t>(), nstart.as<uint64_t>(), s);
     HIP_TRY(hipMemcpyAsync(cursor.p, nstart.as<uint64_t>() + n_new, 8, hipMemcpyDeviceToDevice, s));
     PublishArgs pa{};
@@ -478,6 +478,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     pa.delta = delta.as<uint64_t>(); pa.pframes = t->pframes.as<uint32_t>(); pa.pcp = t->pcp.as<uint64_t>();
     pa.pstart = t->pstart.as<int64_t>(); pa.plen = t->plen.as<uint32_t>(); pa.pslot = t->pslot.as<uint32_t>();
     pa.psums = t->psums.as<uint64_t>(); pa.store_used = t->store_used; pa.starts = nstart.as<uint64_t>();
+    pa.src_len = nsrc.as<int64_t>();
     launch_publish(pa, s);
   }
   if (N > 0) launch_fold_old(t->d, m, t->pslot.as<uint32_t>(), delta.as<uint64_t>(), t->psums.as<uint64_t>(), s);
