@@ -90,6 +90,40 @@ cct_status cct_build(const cct_paths *events, void *hip_stream, cct_tree **out);
  * tree's metric count (else CCT_EMISMATCH). */
 cct_status cct_merge(cct_tree *tree, const cct_paths *chunk, void *hip_stream);
 
+/* One flush of the GPU activity buffer: record r carries the correlation ID that the
+ * profiler emitted at the GPU API callback of its activity, and the activity's metrics
+ * (Design, "Profiler", "GPU Metrics").  DEVICE pointers, borrowed for the call.
+ *   n_records  R >= 0 (R <= CCT_MAX_EVENTS)
+ *   n_metrics  M, must equal the tree's metric count (else CCT_EMISMATCH)
+ *   corr_ids   uint64[R], 8-byte aligned; any value is a legal ID
+ *   metrics    uint64[R][M] row-major, 8-byte aligned */
+typedef struct {
+  int64_t n_records;
+  int32_t n_metrics;
+  const uint64_t *corr_ids;
+  const uint64_t *metrics;
+} cct_activity;
+
+/* Merge one activity flush into `tree`, linking every record to the call path that was
+ * registered under its correlation ID (at each GPU API callback the profiler emits a
+ * unique correlation ID and associates it with the call path it retrieves there; the
+ * flushed metrics are linked to their path through that ID and aggregated: Design,
+ * "Profiler", "GPU Metrics").
+ *   registry      the call paths registered so far, CSR as in cct_paths (DEVICE; its
+ *                 n_metrics and metrics are ignored; offsets checked on the device:
+ *                 CCT_EINVAL)
+ *   reg_corr_ids  uint64[registry->n_events], DEVICE, 8-byte aligned: the correlation ID
+ *                 of each registered path; IDs must be distinct (a repeated ID is found
+ *                 on the device: CCT_EINVAL)
+ *   activity      the flushed records
+ *   n_unmatched   HOST out, may be NULL: the number of records whose ID is not registered;
+ *                 they are not merged (the caller may keep them for a later flush)
+ * The result equals cct_merge of the batch holding, for every matched record in record
+ * order, the registered path with the record's metrics.  A registered path that no
+ * record names is not inserted.  On an error the tree is unchanged. */
+cct_status cct_merge_activity(cct_tree *tree, const cct_paths *registry, const uint64_t *reg_corr_ids,
+                              const cct_activity *activity, void *hip_stream, int64_t *n_unmatched);
+
 /* Look up Q call paths (queries->offsets/frames, metrics ignored) in `tree`.
  * Writes DEVICE arrays: node_ids int64[Q] (the canonical id, or -1 if the path is
  * not a node), and, when non-NULL, excl/incl uint64[Q][M] (zeros for absent paths). */
@@ -115,11 +149,12 @@ void cct_release_cached_memory(void);
 /* Message describing the calling thread's most recent failure ("" if none). */
 const char *cct_last_error(void);
 
-/* Per-call timing of the most recent cct_build/cct_merge on the calling thread, in
- * milliseconds measured with HIP events on the call's stream: [0] ingest (hash,
- * dedup, exclusive aggregation), [1] publish of new paths, [2] canonical ordering
- * (sort, LCP, scans), [3] node emission (parents, exclusive, inclusive), [4] whole
- * call.  Returns the number of values written (<= n). */
+/* Per-call timing of the most recent cct_build/cct_merge/cct_merge_activity on the
+ * calling thread, in milliseconds measured with HIP events on the call's stream: [0]
+ * ingest (hash, dedup, exclusive aggregation), [1] publish of new paths, [2] canonical
+ * ordering (sort, LCP, scans), [3] node emission (parents, exclusive, inclusive), [4]
+ * whole merge, [5] the correlation-ID join before the merge (cct_merge_activity only;
+ * 0 otherwise).  Returns the number of values written (<= n, at most 6). */
 int cct_last_timings(double *ms, int n);
 
 #ifdef __cplusplus

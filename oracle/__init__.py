@@ -195,3 +195,43 @@ def total_metrics(metrics):
     if w.size == 0:
         return np.zeros(w.shape[1] if w.ndim == 2 else 1, np.uint64)
     return w.sum(axis=0, dtype=np.uint64)
+
+
+def join_activity(reg_offsets, reg_frames, reg_corr_ids, corr_ids, metrics):
+    """Correlation-ID join of one flush of activity records (Design, "Profiler", "GPU
+    Metrics"): at each GPU API callback the profiler emits a unique correlation ID and
+    associates it with the call path retrieved there; when the metric buffer is full,
+    every flushed record is linked through its ID to that path and aggregated.
+
+    Written from that definition: a dictionary from ID to registered path, then one
+    event per record whose ID is registered, in record order, holding the registered
+    path and the record's metrics.  Returns (offsets, frames, metrics, n_unmatched) of
+    that CSR batch; ``Oracle.ingest`` of the batch is the merge.  An ID registered
+    twice raises ValueError (the paper's IDs are unique)."""
+    ro = np.asarray(reg_offsets, np.int64)
+    rf = np.asarray(reg_frames, np.uint32)
+    path_of = {}
+    for i, c in enumerate(np.asarray(reg_corr_ids, np.uint64).tolist()):
+        if c in path_of:
+            raise ValueError(f"correlation ID {c} registered twice")
+        path_of[c] = i
+    w = np.asarray(metrics, np.uint64)
+    if w.ndim < 2:
+        w = w.reshape(-1, 1)
+    rec, reg, unmatched = [], [], 0
+    for r, c in enumerate(np.asarray(corr_ids, np.uint64).tolist()):
+        i = path_of.get(c)
+        if i is None:
+            unmatched += 1
+        else:
+            rec.append(r)
+            reg.append(i)
+    reg = np.asarray(reg, np.int64)
+    lens = ro[reg + 1] - ro[reg] if reg.size else np.zeros(0, np.int64)
+    offsets = np.zeros(reg.size + 1, np.int64)
+    np.cumsum(lens, out=offsets[1:])
+    # frames of event k: the registered path reg[k], copied in event order
+    starts = ro[reg] if reg.size else np.zeros(0, np.int64)
+    pos = np.repeat(starts - offsets[:-1], lens) + np.arange(offsets[-1], dtype=np.int64)
+    frames = rf[pos] if pos.size else np.zeros(0, np.uint32)
+    return offsets, frames, w[np.asarray(rec, np.int64)].reshape(len(rec), w.shape[1]), unmatched

@@ -7,6 +7,7 @@ to load, every call raises; there is no CPU fallback.
 
     tree = build(offsets, frames, metrics)   # int64[N+1], int32/uint32[F], int64/uint64[N, M]
     tree.merge(offsets2, frames2, metrics2)  # aggregate one more batch
+    unmatched = tree.merge_activity(reg_offsets, reg_frames, reg_corr_ids, corr_ids, metrics3)
     ids, excl, incl = tree.query(q_offsets, q_frames)
     arrays = tree.to_tensors()               # parent, frame, depth, excl, incl on the GPU
 """
@@ -24,8 +25,8 @@ _lib = None
 
 NO_PARENT = 0xFFFFFFFF
 MAX_METRICS = 8
-EXPORTED_SYMBOLS = ("cct_build", "cct_merge", "cct_query", "cct_info", "cct_export", "cct_free",
-                    "cct_release_cached_memory", "cct_last_error", "cct_last_timings")
+EXPORTED_SYMBOLS = ("cct_build", "cct_merge", "cct_merge_activity", "cct_query", "cct_info", "cct_export",
+                    "cct_free", "cct_release_cached_memory", "cct_last_error", "cct_last_timings")
 _STATUS = {0: "CCT_OK", -1: "CCT_EINVAL", -2: "CCT_ENOMEM", -3: "CCT_EDEVICE", -4: "CCT_EMISMATCH",
            -5: "CCT_EOVERFLOW"}
 
@@ -40,6 +41,11 @@ class CctError(RuntimeError):
 class _Paths(ctypes.Structure):
     _fields_ = [("n_events", ctypes.c_int64), ("n_frames", ctypes.c_int64), ("n_metrics", ctypes.c_int32),
                 ("offsets", ctypes.c_void_p), ("frames", ctypes.c_void_p), ("metrics", ctypes.c_void_p)]
+
+
+class _Activity(ctypes.Structure):
+    _fields_ = [("n_records", ctypes.c_int64), ("n_metrics", ctypes.c_int32), ("corr_ids", ctypes.c_void_p),
+                ("metrics", ctypes.c_void_p)]
 
 
 def library_path():
@@ -58,6 +64,7 @@ def load_library():
     P = ctypes.POINTER
     lib.cct_build.argtypes = [P(_Paths), vp, P(vp)]
     lib.cct_merge.argtypes = [vp, P(_Paths), vp]
+    lib.cct_merge_activity.argtypes = [vp, P(_Paths), vp, P(_Activity), vp, P(i64)]
     lib.cct_query.argtypes = [vp, P(_Paths), vp, vp, vp, vp]
     lib.cct_info.argtypes = [vp, P(i64), P(i32), P(i64)]
     lib.cct_export.argtypes = [vp, vp, vp, vp, vp, vp, vp]
@@ -67,7 +74,7 @@ def load_library():
     lib.cct_release_cached_memory.restype = None
     lib.cct_last_error.restype = ctypes.c_char_p
     lib.cct_last_timings.argtypes = [P(ctypes.c_double), ctypes.c_int]
-    for name in ("cct_build", "cct_merge", "cct_query", "cct_info", "cct_export"):
+    for name in ("cct_build", "cct_merge", "cct_merge_activity", "cct_query", "cct_info", "cct_export"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -143,6 +150,32 @@ class Tree:
         _check(load_library().cct_merge(self._h, ctypes.byref(p), _stream()))
         return self
 
+    def merge_activity(self, reg_offsets, reg_frames, reg_corr_ids, corr_ids, metrics):
+        """Merge one activity flush (cct_merge_activity): record r (correlation ID
+        corr_ids[r], metrics[r]) is linked to the registered path whose ID equals
+        corr_ids[r] (reg_offsets/reg_frames CSR, IDs reg_corr_ids).  IDs are int64 or
+        uint64 device tensors.  Returns the number of records with an unregistered ID."""
+        import torch
+        p, _ = _paths(reg_offsets, reg_frames, None, need_metrics=False)
+        for name, t in (("reg_corr_ids", reg_corr_ids), ("corr_ids", corr_ids)):
+            if not t.is_cuda or t.dtype not in (torch.int64, torch.uint64) or t.dim() != 1 or not t.is_contiguous():
+                raise ValueError(f"{name} must be a contiguous int64/uint64 device vector")
+        if reg_corr_ids.numel() != p.n_events:
+            raise ValueError("reg_corr_ids must have one ID per registered path")
+        if not metrics.is_cuda or metrics.dtype not in (torch.int64, torch.uint64) or not metrics.is_contiguous():
+            raise ValueError("metrics must be a contiguous int64/uint64 [R, M] device tensor")
+        if metrics.dim() == 1:
+            metrics = metrics.view(-1, 1)
+        r = corr_ids.numel()
+        if metrics.shape[0] != r:
+            raise ValueError("metrics must have one row per record")
+        act = _Activity(r, metrics.shape[1], corr_ids.data_ptr() if r else None, metrics.data_ptr() if r else None)
+        un = ctypes.c_int64(0)
+        _check(load_library().cct_merge_activity(self._h, ctypes.byref(p),
+                                                 reg_corr_ids.data_ptr() if p.n_events else None,
+                                                 ctypes.byref(act), _stream(), ctypes.byref(un)))
+        return un.value
+
     def query(self, offsets, frames, want_metrics=True):
         import torch
         p, _ = _paths(offsets, frames, None, need_metrics=False)
@@ -199,9 +232,10 @@ def build(offsets, frames, metrics):
 
 def last_timings():
     """Per-phase HIP-event times (ms) of this thread's last build/merge: ingest,
-    publish, sort, canonical emission, total."""
-    buf = (ctypes.c_double * 5)()
-    n = load_library().cct_last_timings(buf, 5)
+    publish, sort, canonical emission, total of the merge, and the correlation-ID join
+    of a merge_activity call (0 otherwise)."""
+    buf = (ctypes.c_double * 6)()
+    n = load_library().cct_last_timings(buf, 6)
     return list(buf)[:n]
 
 

@@ -276,4 +276,28 @@ struct QueryArgs {
 };
 void launch_query(const QueryArgs &a, hipStream_t s);
 
+// Correlation-ID join of an activity flush with the registered call paths (activity.hip)
+enum : int32_t { kActCtrError = 0, kActCtrUnmatched = 1, kActCtrCount = 2 };
+enum : uint32_t { kActBadOffsets = 1, kActRepeatedId = 2, kActTableFull = 4 };
+struct ActivityArgs {
+  int64_t n_reg;             // registered paths
+  int64_t reg_n_frames;
+  const int64_t *reg_off;    // [n_reg + 1]
+  const uint64_t *reg_corr;  // [n_reg] correlation IDs
+  uint64_t cap_mask;         // table capacity - 1 (capacity a power of two >= 2 n_reg)
+  uint32_t *claim;           // [cap] registry index + 1; 0: empty
+  uint64_t *keys;            // [cap] correlation ID of the claimed slot
+  int64_t n_rec;             // activity records
+  const uint64_t *rec_corr;  // [n_rec]
+  uint32_t *rec_reg;         // [n_rec] registry index of the record's path, kNoSlot if unmatched
+  uint32_t *ref;             // [n_reg] 1 if some record names the path
+  unsigned long long *ctr;   // [kActCtrCount]
+};
+void launch_corr_table(const ActivityArgs &a, hipStream_t s);  // validate offsets, insert, repeated IDs
+void launch_corr_join(const ActivityArgs &a, hipStream_t s);
+void launch_compact_lengths(const ActivityArgs &a, uint64_t *rows, hipStream_t s);
+void launch_compact_gather(const ActivityArgs &a, const uint32_t *reg_frames, const uint64_t *scan,
+                           const uint64_t *sums, int32_t m, int64_t *off_out, uint32_t *fr_out, uint64_t *met_out,
+                           hipStream_t s);
+
 }  // namespace cct

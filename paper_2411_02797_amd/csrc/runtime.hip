@@ -22,6 +22,7 @@ namespace {
 
 thread_local std::string g_error;
 thread_local double g_timings[5] = {0, 0, 0, 0, 0};
+thread_local double g_join_ms = 0;  // correlation-ID join of the last cct_merge_activity
 thread_local int g_alloc_countdown = 0;  // test hook: >0 makes the n-th allocation of a call fail
 
 cct_status fail(cct_status s, const char *msg) {
@@ -541,6 +542,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
 extern "C" {
 
 cct_status cct_build(const cct_paths *events, void *hip_stream, cct_tree **out) {
+  g_join_ms = 0;
   g_error.clear();
   if (!out) return fail(CCT_EINVAL, "out is NULL");
   cct_status st = check_paths(events, true);
@@ -569,6 +571,7 @@ cct_status cct_build(const cct_paths *events, void *hip_stream, cct_tree **out) 
 
 cct_status cct_merge(cct_tree *tree, const cct_paths *chunk, void *hip_stream) {
   g_error.clear();
+  g_join_ms = 0;
   if (!tree) return fail(CCT_EINVAL, "tree is NULL");
   cct_status st = check_paths(chunk, true);
   if (st) return st;
@@ -577,6 +580,103 @@ cct_status cct_merge(cct_tree *tree, const cct_paths *chunk, void *hip_stream) {
   (void)hipGetDevice(&dev);
   if (dev != tree->device) return fail(CCT_EINVAL, "tree belongs to another device");
   return aggregate(tree, chunk, (hipStream_t)hip_stream);
+}
+
+cct_status cct_merge_activity(cct_tree *tree, const cct_paths *registry, const uint64_t *reg_corr_ids,
+                              const cct_activity *act, void *hip_stream, int64_t *n_unmatched) {
+  g_error.clear();
+  g_join_ms = 0;
+  if (!tree || !registry || !act) return fail(CCT_EINVAL, "NULL argument");
+  const int64_t G = registry->n_events, R = act->n_records;
+  if (G < 0 || registry->n_frames < 0 || R < 0) return fail(CCT_EINVAL, "negative size");
+  if (G > CCT_MAX_EVENTS || R > CCT_MAX_EVENTS) return fail(CCT_EOVERFLOW, "too many paths or records in one call");
+  if (!registry->offsets || (registry->n_frames > 0 && !registry->frames) || (G > 0 && !reg_corr_ids))
+    return fail(CCT_EINVAL, "registry pointer is NULL");
+  if (act->n_metrics < 1 || act->n_metrics > CCT_MAX_METRICS) return fail(CCT_EINVAL, "n_metrics out of range");
+  if (R > 0 && (!act->corr_ids || !act->metrics)) return fail(CCT_EINVAL, "activity pointer is NULL");
+  if (((uintptr_t)registry->offsets & 7) || ((uintptr_t)registry->frames & 3) || ((uintptr_t)reg_corr_ids & 7) ||
+      ((uintptr_t)act->corr_ids & 7) || ((uintptr_t)act->metrics & 7))
+    return fail(CCT_EINVAL, "misaligned pointer");
+  if (act->n_metrics != tree->m) return fail(CCT_EMISMATCH, "metric count differs from the tree's");
+  int dev = 0;
+  (void)hipGetDevice(&dev);
+  if (dev != tree->device) return fail(CCT_EINVAL, "tree belongs to another device");
+  hipStream_t s = (hipStream_t)hip_stream;
+  const int32_t m = tree->m;
+  unsigned long long *hs = host_scratch();
+  if (!hs) return fail(CCT_ENOMEM, "pinned host allocation failed");
+  g_alloc_countdown = (int)env_int("CCT_TEST_FAIL_ALLOC", 0);
+  if (G == 0 || R == 0) {  // nothing can match: no device work
+    if (n_unmatched) *n_unmatched = R;
+    return CCT_OK;
+  }
+  Timer tm;
+  tm.mark(0, s);
+  // ---- table of registered IDs, the join, per-path sums -------------------------------
+  const uint64_t cap = pow2_at_least((uint64_t)std::max<int64_t>(2 * G, 64));
+  Buf claim, keys, rec_reg, ref, sums, ctr, rows, scan, scan_blk, agg_count, agg_keys, agg_sums;
+  const int agg_grid = (int)std::max<int64_t>(1, std::min<int64_t>((R + 8191) / 8192, (int64_t)cu_count() * 2));
+  AggStage stg{};
+  stg.bshift = agg_bucket_shift(m);
+  const int64_t nbk = std::max<int64_t>(1, (int64_t)((uint64_t)G >> stg.bshift) + 1);
+  if (!claim.alloc(cap * 4) || !keys.alloc(cap * 8) || !rec_reg.alloc((size_t)R * 4) || !ref.alloc((size_t)G * 4) ||
+      !sums.alloc((size_t)G * m * 8) || !ctr.alloc(kActCtrCount * 8) || !rows.alloc((size_t)G * 16) ||
+      !scan.alloc(((size_t)G + 1) * 16) || !scan_blk.alloc(((size_t)G / 1024 + 2) * 16))
+    return fail(CCT_ENOMEM, "device allocation failed");
+  if (nbk <= agg_max_buckets()) {
+    const int64_t total = (int64_t)agg_grid * agg_map_entries(m);
+    stg.nbuckets = nbk;
+    stg.bucket_cap = 2 * ((total + nbk - 1) / nbk) + 256;
+    if (!agg_count.alloc(nbk * 4) || !agg_keys.alloc(nbk * stg.bucket_cap * 4) ||
+        !agg_sums.alloc(nbk * stg.bucket_cap * m * 8))
+      return fail(CCT_ENOMEM, "device allocation failed");
+    HIP_TRY(hipMemsetAsync(agg_count.p, 0, nbk * 4, s));
+    stg.count = agg_count.as<uint32_t>();
+    stg.keys = agg_keys.as<uint32_t>();
+    stg.sums = agg_sums.as<uint64_t>();
+  }
+  HIP_TRY(hipMemsetAsync(claim.p, 0, cap * 4, s));
+  HIP_TRY(hipMemsetAsync(ref.p, 0, (size_t)G * 4, s));
+  HIP_TRY(hipMemsetAsync(sums.p, 0, (size_t)G * m * 8, s));
+  HIP_TRY(hipMemsetAsync(ctr.p, 0, kActCtrCount * 8, s));
+  ActivityArgs a{};
+  a.n_reg = G; a.reg_n_frames = registry->n_frames; a.reg_off = registry->offsets; a.reg_corr = reg_corr_ids;
+  a.cap_mask = cap - 1; a.claim = claim.as<uint32_t>(); a.keys = keys.as<uint64_t>();
+  a.n_rec = R; a.rec_corr = act->corr_ids; a.rec_reg = rec_reg.as<uint32_t>(); a.ref = ref.as<uint32_t>();
+  a.ctr = ctr.as<unsigned long long>();
+  launch_corr_table(a, s);
+  launch_corr_join(a, s);
+  launch_aggregate(a.rec_reg, act->metrics, R, m, sums.as<uint64_t>(), (uint64_t)G, agg_grid, stg, s);
+  launch_compact_lengths(a, rows.as<uint64_t>(), s);
+  launch_scan(rows.as<uint64_t>(), G, 2, scan_blk.as<uint64_t>(), scan.as<uint64_t>(), s);
+  HIP_TRY(hipGetLastError());
+  HIP_TRY(hipMemcpyAsync(hs, ctr.p, kActCtrCount * 8, hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipMemcpyAsync(hs + kActCtrCount, scan.as<uint64_t>() + 2 * G, 16, hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  const unsigned long long err = hs[kActCtrError], unmatched = hs[kActCtrUnmatched];
+  const int64_t n_used = (int64_t)hs[kActCtrCount], n_fr = (int64_t)hs[kActCtrCount + 1];
+  if (err & kActBadOffsets) return fail(CCT_EINVAL, "malformed registry offsets");
+  if (err & kActRepeatedId) return fail(CCT_EINVAL, "a correlation ID is registered twice");
+  if (err) return fail(CCT_EDEVICE, "correlation-ID table overflow");
+  // ---- the batch of referenced paths with their summed metrics, merged ---------------
+  Buf b_off, b_fr, b_met;
+  if (!b_off.alloc(((size_t)n_used + 1) * 8) || !b_fr.alloc((size_t)n_fr * 4) || !b_met.alloc((size_t)n_used * m * 8))
+    return fail(CCT_ENOMEM, "device allocation failed");
+  launch_compact_gather(a, registry->frames, scan.as<uint64_t>(), sums.as<uint64_t>(), m, b_off.as<int64_t>(),
+                        b_fr.as<uint32_t>(), b_met.as<uint64_t>(), s);
+  HIP_TRY(hipMemcpyAsync(b_off.as<int64_t>() + n_used, scan.as<uint64_t>() + 2 * G + 1, 8, hipMemcpyDeviceToDevice, s));
+  HIP_TRY(hipGetLastError());
+  tm.mark(1, s);
+  HIP_TRY(hipStreamSynchronize(s));
+  const double join_ms = tm.ok ? tm.span(0, 1) : 0.0;
+  cct_paths batch{};
+  batch.n_events = n_used; batch.n_frames = n_fr; batch.n_metrics = m;
+  batch.offsets = b_off.as<int64_t>(); batch.frames = b_fr.as<uint32_t>(); batch.metrics = b_met.as<uint64_t>();
+  cct_status st = aggregate(tree, &batch, s);
+  if (st) return st;
+  g_join_ms = join_ms;
+  if (n_unmatched) *n_unmatched = (int64_t)unmatched;
+  return CCT_OK;
 }
 
 cct_status cct_query(const cct_tree *tree, const cct_paths *q, void *hip_stream, int64_t *node_ids, uint64_t *excl,
@@ -654,8 +754,9 @@ const char *cct_last_error(void) { return g_error.c_str(); }
 
 int cct_last_timings(double *ms, int n) {
   if (!ms || n <= 0) return 0;
-  const int k = n < 5 ? n : 5;
-  for (int i = 0; i < k; ++i) ms[i] = g_timings[i];
+  const int k = n < 6 ? n : 6;
+  for (int i = 0; i < k && i < 5; ++i) ms[i] = g_timings[i];
+  if (k > 5) ms[5] = g_join_ms;
   return k;
 }
 

@@ -260,3 +260,70 @@ def test_checker_passes_workload_trees():
         o, f, w = tracegen.generate(name, n_events=n)
         t = oracle.build_tree(o, f, w)
         assert oracle.check(t, oracle.total_metrics(w)) == (0, 0)
+
+
+# ---- correlation-ID join (the flush step) -------------------------------------------
+# Registry: ID 100 -> [5, 7], ID 7 -> [5, 9, 2], ID 3 -> [] (the empty path).
+# Records (ID, metric): (7, 10), (999, 1), (100, 4), (7, 6), (3, 2).  By hand: record 1
+# names no registered path; the others become, in record order, the events
+# [5, 9, 2]:10, [5, 7]:4, [5, 9, 2]:6, []:2.  Their tree, by hand (ids = preorder of the
+# prefixes (), (5), (5,7), (5,9), (5,9,2)): exclusive 2 / 0 / 4 / 0 / 16 and inclusive
+# 22 / 20 / 4 / 16 / 16.
+def test_join_hand_worked():
+    o, f, w, unmatched = oracle.join_activity([0, 2, 5, 5], [5, 7, 5, 9, 2], [100, 7, 3], [7, 999, 100, 7, 3],
+                                              [[10], [1], [4], [6], [2]])
+    assert unmatched == 1
+    assert o.tolist() == [0, 3, 5, 8, 8]
+    assert f.tolist() == [5, 9, 2, 5, 7, 5, 9, 2]
+    assert w.ravel().tolist() == [10, 4, 6, 2]
+    t = oracle.build_tree(o, f, w)
+    assert t["parent"].tolist() == [oracle.NO_PARENT, 0, 1, 1, 3]
+    assert t["frame"].tolist() == [0, 5, 7, 9, 2]
+    assert t["excl"].ravel().tolist() == [2, 0, 4, 0, 16]
+    assert t["incl"].ravel().tolist() == [22, 20, 4, 16, 16]
+
+
+def test_join_rejects_a_repeated_id():
+    with pytest.raises(ValueError):
+        oracle.join_activity([0, 1, 2], [1, 2], [5, 5], [5], [[1]])
+
+
+def test_join_of_self_registered_events_is_the_trace():
+    # every event registered under its own ID and flushed once, records shuffled: the
+    # joined batch holds the trace's events (in another order), so the tree is the
+    # trace's tree
+    o, f, w = tracegen.random_paths(400, 30, 12, 2, seed=7)
+    rng = np.random.default_rng(7)
+    # distinct IDs spread over the whole uint64 range (an odd multiplier is a bijection mod 2^64)
+    ids = rng.choice(10**9, size=400, replace=False).astype(np.uint64) * np.uint64(0x9E3779B97F4A7C15)
+    perm = rng.permutation(400)
+    jo, jf, jw, unmatched = oracle.join_activity(o, f, ids, ids[perm], w[perm])
+    assert unmatched == 0
+    assert_tree_equal(oracle.build_tree(jo, jf, jw), oracle.build_tree(o, f, w), "self-registered")
+
+
+def test_join_counts_unregistered_records_by_brute_force():
+    o, f, w = tracegen.random_paths(50, 8, 6, 1, seed=3)
+    rng = np.random.default_rng(3)
+    ids = np.arange(50, dtype=np.uint64) * np.uint64(3)
+    rec = rng.integers(0, 160, size=300).astype(np.uint64)
+    rw = rng.integers(0, 2**64, size=(300, 1), dtype=np.uint64)
+    jo, jf, jw, unmatched = oracle.join_activity(o, f, ids, rec, rw)
+    registered = set(ids.tolist())
+    assert unmatched == sum(1 for c in rec.tolist() if c not in registered)
+    # brute force: the k-th matched record in order carries its registered path
+    k = 0
+    for r, c in enumerate(rec.tolist()):
+        if c in registered:
+            i = c // 3
+            assert jf[jo[k]:jo[k + 1]].tolist() == f[o[i]:o[i + 1]].tolist()
+            assert jw[k, 0] == rw[r, 0]
+            k += 1
+    assert k == jo.size - 1
+
+
+def test_join_edge_cases():
+    o, f, w, u = oracle.join_activity([0], [], [], [1, 2], [[1], [2]])
+    assert (o.tolist(), f.size, w.shape, u) == ([0], 0, (0, 1), 2)
+    o, f, w, u = oracle.join_activity([0, 2], [4, 4], [9], [], np.zeros((0, 3), np.uint64))
+    assert (o.tolist(), f.size, w.shape, u) == ([0], 0, (0, 3), 0)
