@@ -553,6 +553,11 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
     o_nxt = o_nn;
     t = tn;
   }
+  // A wave that stopped early (malformed offsets, or a table overflow the host retries)
+  // marks the rest of its range unresolved: every entry of slot_of is written once, so
+  // the aggregation that follows never reads a stale word as a slot.
+  if (t.kind != kTileNone)
+    for (int64_t e = t.e0 + lane; e < end; e += 64) a.slot_of[e] = kNoSlot;
 }
 
 // Metric sums per slot: one persistent workgroup per CU walks a contiguous event

@@ -109,3 +109,44 @@ def test_bad_tensor_arguments():
         cct.build(to, tf, torch.zeros((10, 9), dtype=torch.int64, device=to.device)[:, ::2])
     assert _status(lambda: cct.build(to, tf, torch.zeros((10, 9), dtype=torch.int64, device=to.device))) \
         == "CCT_EINVAL"
+
+
+@pytest.mark.parametrize("kind", ["first_nonzero", "decreasing", "last_mismatch", "overflow"])
+def test_early_exit_after_pool_reuse(monkeypatch, kind):
+    # Regression: a wave that stops early (malformed offsets, or a table overflow that the
+    # host retries) must still mark the rest of its events unresolved, because the
+    # aggregation reads every event's slot id.  The pool is first filled with large
+    # words (an activity merge with IDs near 2^64) so that stale memory would be out of
+    # range.
+    import paper_2411_02797_amd as cct
+    torch = torch_or_skip()
+    dev = torch.device("cuda", 0)
+    for rep in range(3):
+        n = 4000 + 1000 * rep
+        ro, rf, _ = tracegen.random_paths(n, 30, 10, 1, seed=rep)
+        ids = (np.arange(n, dtype=np.uint64) + np.uint64(2**64 - 2 * n))
+        big = torch.from_numpy(ids.view(np.int64)).to(dev)
+        t0 = cct.build(*to_dev(ro, rf, np.ones((n, 1), np.uint64)))
+        tro, trf, _ = to_dev(ro, rf, np.zeros((n, 1), np.uint64))
+        t0.merge_activity(tro, trf, big, big.flip(0).contiguous(), torch.ones((n, 1), dtype=torch.int64, device=dev))
+        t0.free()
+    o, f, w = tracegen.random_paths(5000, 30, 10, 1, seed=1)
+    to, tf, tw = to_dev(o, f, w)
+    if kind == "overflow":
+        monkeypatch.setenv("CCT_TEST_TABLE_CAP", "64")  # far fewer slots than paths: overflow, then retries
+        t = cct.build(to, tf, tw)
+        got = t.to_numpy()
+        t.free()
+        assert_same(got, oracle.build_tree(o, f, w), "after overflow retries")
+        return
+    bad = to.clone()
+    if kind == "first_nonzero":
+        bad[0] = 1
+    elif kind == "decreasing":
+        bad[2500] = bad[2499] - 1
+    else:
+        bad[-1] = bad[-1] - 1
+    assert _status(lambda: cct.build(bad, tf, tw)) == "CCT_EINVAL"
+    t = cct.build(to, tf, tw)  # the library is still usable
+    assert_same(t.to_numpy(), oracle.build_tree(o, f, w), "after EINVAL")
+    t.free()
