@@ -8,6 +8,12 @@ With --workload merge, one step = the 32 cct_merge calls that fold 32 chunks of
 2,097,152 events into a tree built (untimed) from an 8,388,608-event base; the rate
 is chunk events per second of merge time.
 
+With --workload activity, one step = 8 cct_merge_activity calls into a tree built
+(untimed) from the same base: each joins one flush of activity records (every launch
+of a 2,097,152-path registry once, in shuffled order, 10% repeated records, 2% records
+with unregistered IDs) with the registry by correlation ID and merges the result; the
+rate is records per second.
+
     python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload layered_16m]
 """
 import argparse
@@ -33,6 +39,9 @@ DESCRIPTIONS = {
     "tiny": "10,000 events on a random call-site tree, 1 uint64 metric",
     "merge": "8,388,608-event base (layered_16m program, 60% of its paths) + 32 merged chunks of 2,097,152 events "
              "(20% from paths new to the chunk), 4 uint64 metrics (one full-range)",
+    "activity": "8,388,608-event base (as merge) + 8 activity flushes, each a registry of 2,097,152 call paths "
+                "(a merge chunk) under distinct correlation IDs and 2,348,810 records (every ID once, shuffled, "
+                "+10% repeated IDs, +2% unregistered IDs), 4 uint64 metrics",
 }
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ingest_traffic.json")
 
@@ -115,6 +124,8 @@ def main():
     t0 = time.perf_counter()
     if args.workload == "merge":
         return bench_merge(args, torch, tracegen, cct, dev)
+    if args.workload == "activity":
+        return bench_activity(args, torch, tracegen, cct, dev)
     o, f, w = tracegen.generate(args.workload)
     N, F, M = o.size - 1, f.size, w.shape[1]
     log(f"generated {args.workload}: N={N:,} F={F:,} M={M} in {time.perf_counter() - t0:.1f}s")
@@ -237,6 +248,87 @@ def bench_merge(args, torch, tracegen, cct, dev):
     }
     print(json.dumps(line), flush=True)
 
+
+
+def activity_flush(tracegen, c):
+    """Flush c: the registry is merge chunk c (its call paths, registered at launch under
+    distinct IDs), the records name every registered ID once in shuffled order, plus 10%
+    repeated IDs and 2% IDs never registered."""
+    o, f, w = tracegen.generate("merge_chunk", chunk=c)
+    n, m = o.size - 1, w.shape[1]
+    rng = np.random.default_rng(1000 + c)
+    ids = (np.uint64(c + 1) << np.uint64(40)) + rng.permutation(n).astype(np.uint64)
+    order = rng.permutation(n)
+    rep = rng.integers(0, n, size=n // 10)
+    rec = np.concatenate([ids[order], ids[rep], (np.uint64(1) << np.uint64(63)) + np.arange(n // 50, dtype=np.uint64)])
+    met = np.concatenate([w[order], w[rep], w[: n // 50]])
+    perm = rng.permutation(rec.size)
+    return o, f, ids, rec[perm], np.ascontiguousarray(met[perm])
+
+
+def bench_activity(args, torch, tracegen, cct, dev):
+    def t64(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int64)).to(dev)
+    t0 = time.perf_counter()
+    bo, bf, bw = tracegen.generate("merge_base")
+    base = (torch.from_numpy(bo).to(dev), torch.from_numpy(bf.view(np.int32)).to(dev), t64(bw))
+    flushes = []
+    n_rec = n_reg = n_reg_frames = 0
+    for c in range(8):
+        o, f, ids, rec, met = activity_flush(tracegen, c)
+        n_rec += rec.size
+        n_reg += o.size - 1
+        n_reg_frames += f.size
+        flushes.append((torch.from_numpy(o).to(dev), torch.from_numpy(f.view(np.int32)).to(dev), t64(ids), t64(rec),
+                        t64(met)))
+    M = flushes[0][4].shape[1]
+    torch.cuda.synchronize()
+    log(f"generated activity: 8 flushes, {n_reg:,} registered paths ({n_reg_frames:,} frames), {n_rec:,} records "
+        f"in {time.perf_counter() - t0:.1f}s")
+    step_ms, phases = [], []
+    unmatched = U = D = 0
+    for step in range(args.warmup + args.steps):
+        tree = cct.build(*base)
+        torch.cuda.synchronize()
+        t_seq = time.perf_counter()
+        ph, un = [], 0
+        for fl in flushes:
+            un += tree.merge_activity(*fl)
+            ph.append(cct.last_timings())
+        torch.cuda.synchronize()
+        wall = (time.perf_counter() - t_seq) * 1000.0
+        U, _, D = tree._info()
+        tree.free()
+        unmatched = un
+        if step >= args.warmup:
+            step_ms.append(wall)
+            phases.extend(ph)
+        log(f"{'warmup' if step < args.warmup else 'step'} {step}: 8 flushes {wall:.2f} ms, unmatched {un:,}, "
+            f"U={U:,} D={D:,}")
+    ms = float(np.mean(step_ms))
+    ph = np.array(phases)
+    join_ms = float(ph[:, 5].mean())
+    # algorithmic bytes of the join per flush: registry offsets and IDs read, records'
+    # IDs and metrics read, the registered frames read and written once into the batch
+    per = n_reg // 8, n_rec // 8, n_reg_frames // 8
+    b_join = 8 * (per[0] + 1) + 8 * per[0] + 8 * per[1] * (1 + M) + 2 * 4 * per[2] + 8 * per[0] * (1 + M)
+    achieved = b_join / (join_ms * 1e-3) / 1e9
+    line = {
+        "metric": METRIC, "value": n_rec / (ms * 1e-3), "unit": "records/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "u64", "data": "synthetic",
+        "config": {"workload": f"activity: {DESCRIPTIONS['activity']}", "records": n_rec, "registered_paths": n_reg,
+                   "registered_frames": n_reg_frames, "unmatched_records": unmatched, "metrics": M,
+                   "distinct_paths": D, "nodes": U},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                     "kernel": "correlation-ID join of one flush (table, join, per-path sums, compaction)",
+                     "bytes_per_launch": b_join, "avg_launch_ms": join_ms},
+        "phase_ms_per_flush": {"join": join_ms, "ingest": float(ph[:, 0].mean()), "publish": float(ph[:, 1].mean()),
+                               "sort": float(ph[:, 2].mean()), "emit": float(ph[:, 3].mean()),
+                               "merge_call": float(ph[:, 4].mean())},
+    }
+    print(json.dumps(line), flush=True)
 
 if __name__ == "__main__":
     main()

@@ -277,27 +277,44 @@ struct QueryArgs {
 void launch_query(const QueryArgs &a, hipStream_t s);
 
 // Correlation-ID join of an activity flush with the registered call paths (activity.hip)
-enum : int32_t { kActCtrError = 0, kActCtrUnmatched = 1, kActCtrCount = 2 };
+enum : int32_t { kActCtrError = 0, kActCtrUnmatched = 1, kActCtrMin = 2, kActCtrMax = 3, kActCtrCount = 4 };
 enum : uint32_t { kActBadOffsets = 1, kActRepeatedId = 2, kActTableFull = 4 };
+struct alignas(16) CorrSlot {
+  uint64_t key;    // correlation ID (valid once claim != 0)
+  uint32_t claim;  // registry index + 1; 0: empty
+  uint32_t pad;
+};
 struct ActivityArgs {
   int64_t n_reg;             // registered paths
   int64_t reg_n_frames;
   const int64_t *reg_off;    // [n_reg + 1]
   const uint64_t *reg_corr;  // [n_reg] correlation IDs
-  uint64_t cap_mask;         // table capacity - 1 (capacity a power of two >= 2 n_reg)
-  uint32_t *claim;           // [cap] registry index + 1; 0: empty
-  uint64_t *keys;            // [cap] correlation ID of the claimed slot
+  // dense IDs (max - min < 4 n_reg): a direct table dtab[id - id_min] (registry index + 1,
+  // 0: not registered); otherwise the hash table
+  bool dense;
+  uint64_t id_min, id_span;  // registered IDs lie in [id_min, id_min + id_span]
+  uint32_t *dtab;            // [id_span + 1]
+  uint64_t cap_mask;         // hash table capacity - 1 (capacity a power of two >= 2 n_reg)
+  CorrSlot *table;           // [cap]
   int64_t n_rec;             // activity records
   const uint64_t *rec_corr;  // [n_rec]
   uint32_t *rec_reg;         // [n_rec] registry index of the record's path, kNoSlot if unmatched
-  uint32_t *ref;             // [n_reg] 1 if some record names the path
+  uint32_t *ref;             // [n_reg] 0, or 1 + the index of a record naming the path (its owner)
   unsigned long long *ctr;   // [kActCtrCount]
 };
+void launch_corr_range(const ActivityArgs &a, hipStream_t s);  // min and max registered ID into ctr
 void launch_corr_table(const ActivityArgs &a, hipStream_t s);  // validate offsets, insert, repeated IDs
 void launch_corr_join(const ActivityArgs &a, hipStream_t s);
+// per-path sums of the matched records; list: scratch of corr_sums_grid(n_rec) stripes
+// (n_rec + corr_sums_grid * 256 entries suffice), cnt: [corr_sums_grid(n_rec)]
+int64_t corr_sums_grid(int64_t n_rec);
+void launch_corr_sums(const ActivityArgs &a, const uint64_t *metrics, int32_t m, uint64_t *sums, uint32_t *list,
+                      uint32_t *cnt, hipStream_t s);
 void launch_compact_lengths(const ActivityArgs &a, uint64_t *rows, hipStream_t s);
+// the batch of referenced paths: offsets [n_paths + 1], frames and metrics; src_start is
+// scratch [n_paths]
 void launch_compact_gather(const ActivityArgs &a, const uint32_t *reg_frames, const uint64_t *scan,
-                           const uint64_t *sums, int32_t m, int64_t *off_out, uint32_t *fr_out, uint64_t *met_out,
-                           hipStream_t s);
+                           const uint64_t *sums, int32_t m, int64_t n_paths, int64_t n_frames, int64_t *off_out,
+                           int64_t *src_start, uint32_t *fr_out, uint64_t *met_out, hipStream_t s);
 
 }  // namespace cct

@@ -613,65 +613,67 @@ cct_status cct_merge_activity(cct_tree *tree, const cct_paths *registry, const u
   Timer tm;
   tm.mark(0, s);
   // ---- table of registered IDs, the join, per-path sums -------------------------------
-  const uint64_t cap = pow2_at_least((uint64_t)std::max<int64_t>(2 * G, 64));
-  Buf claim, keys, rec_reg, ref, sums, ctr, rows, scan, scan_blk, agg_count, agg_keys, agg_sums;
-  const int agg_grid = (int)std::max<int64_t>(1, std::min<int64_t>((R + 8191) / 8192, (int64_t)cu_count() * 2));
-  AggStage stg{};
-  stg.bshift = agg_bucket_shift(m);
-  const int64_t nbk = std::max<int64_t>(1, (int64_t)((uint64_t)G >> stg.bshift) + 1);
-  if (!claim.alloc(cap * 4) || !keys.alloc(cap * 8) || !rec_reg.alloc((size_t)R * 4) || !ref.alloc((size_t)G * 4) ||
-      !sums.alloc((size_t)G * m * 8) || !ctr.alloc(kActCtrCount * 8) || !rows.alloc((size_t)G * 16) ||
-      !scan.alloc(((size_t)G + 1) * 16) || !scan_blk.alloc(((size_t)G / 1024 + 2) * 16))
-    return fail(CCT_ENOMEM, "device allocation failed");
-  if (nbk <= agg_max_buckets()) {
-    const int64_t total = (int64_t)agg_grid * agg_map_entries(m);
-    stg.nbuckets = nbk;
-    stg.bucket_cap = 2 * ((total + nbk - 1) / nbk) + 256;
-    if (!agg_count.alloc(nbk * 4) || !agg_keys.alloc(nbk * stg.bucket_cap * 4) ||
-        !agg_sums.alloc(nbk * stg.bucket_cap * m * 8))
-      return fail(CCT_ENOMEM, "device allocation failed");
-    HIP_TRY(hipMemsetAsync(agg_count.p, 0, nbk * 4, s));
-    stg.count = agg_count.as<uint32_t>();
-    stg.keys = agg_keys.as<uint32_t>();
-    stg.sums = agg_sums.as<uint64_t>();
-  }
-  HIP_TRY(hipMemsetAsync(claim.p, 0, cap * 4, s));
-  HIP_TRY(hipMemsetAsync(ref.p, 0, (size_t)G * 4, s));
-  HIP_TRY(hipMemsetAsync(sums.p, 0, (size_t)G * m * 8, s));
-  HIP_TRY(hipMemsetAsync(ctr.p, 0, kActCtrCount * 8, s));
+  Buf table, rec_reg, ref, sums, ctr, rows, scan, scan_blk, add_list, add_cnt;
   ActivityArgs a{};
   a.n_reg = G; a.reg_n_frames = registry->n_frames; a.reg_off = registry->offsets; a.reg_corr = reg_corr_ids;
-  a.cap_mask = cap - 1; a.claim = claim.as<uint32_t>(); a.keys = keys.as<uint64_t>();
-  a.n_rec = R; a.rec_corr = act->corr_ids; a.rec_reg = rec_reg.as<uint32_t>(); a.ref = ref.as<uint32_t>();
+  a.n_rec = R; a.rec_corr = act->corr_ids;
+  // the range of the registered IDs decides between the direct and the hash table
+  if (!ctr.alloc(kActCtrCount * 8)) return fail(CCT_ENOMEM, "device allocation failed");
   a.ctr = ctr.as<unsigned long long>();
+  HIP_TRY(hipMemsetAsync(ctr.p, 0, kActCtrCount * 8, s));
+  HIP_TRY(hipMemsetAsync(a.ctr + kActCtrMin, 0xFF, 8, s));
+  launch_corr_range(a, s);
+  HIP_TRY(hipGetLastError());
+  HIP_TRY(hipMemcpyAsync(hs, a.ctr + kActCtrMin, 16, hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  a.id_min = hs[0];
+  a.id_span = hs[1] - hs[0];
+  a.dense = a.id_span < 4 * (uint64_t)G;
+  const uint64_t cap = a.dense ? a.id_span + 1 : pow2_at_least((uint64_t)std::max<int64_t>(2 * G, 64));
+  const size_t table_bytes = a.dense ? cap * 4 : cap * sizeof(CorrSlot);
+  if (!table.alloc(table_bytes) || !rec_reg.alloc((size_t)R * 4) || !ref.alloc((size_t)G * 4) ||
+      !sums.alloc((size_t)G * m * 8) || !rows.alloc((size_t)G * 16) ||
+      !scan.alloc(((size_t)G + 1) * 16) || !scan_blk.alloc(((size_t)G / 1024 + 2) * 16) ||
+      !add_list.alloc(((size_t)R + (size_t)corr_sums_grid(R) * 256) * 4) || !add_cnt.alloc((size_t)corr_sums_grid(R) * 4))
+    return fail(CCT_ENOMEM, "device allocation failed");
+  HIP_TRY(hipMemsetAsync(table.p, 0, table_bytes, s));
+  HIP_TRY(hipMemsetAsync(ref.p, 0, (size_t)G * 4, s));
+  if (a.dense) a.dtab = table.as<uint32_t>();
+  else { a.table = table.as<CorrSlot>(); a.cap_mask = cap - 1; }
+  a.rec_reg = rec_reg.as<uint32_t>(); a.ref = ref.as<uint32_t>();
   launch_corr_table(a, s);
   launch_corr_join(a, s);
-  launch_aggregate(a.rec_reg, act->metrics, R, m, sums.as<uint64_t>(), (uint64_t)G, agg_grid, stg, s);
+  launch_corr_sums(a, act->metrics, m, sums.as<uint64_t>(), add_list.as<uint32_t>(), add_cnt.as<uint32_t>(), s);
   launch_compact_lengths(a, rows.as<uint64_t>(), s);
   launch_scan(rows.as<uint64_t>(), G, 2, scan_blk.as<uint64_t>(), scan.as<uint64_t>(), s);
   HIP_TRY(hipGetLastError());
-  HIP_TRY(hipMemcpyAsync(hs, ctr.p, kActCtrCount * 8, hipMemcpyDeviceToHost, s));
-  HIP_TRY(hipMemcpyAsync(hs + kActCtrCount, scan.as<uint64_t>() + 2 * G, 16, hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipMemcpyAsync(hs, ctr.p, 2 * 8, hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipMemcpyAsync(hs + 2, scan.as<uint64_t>() + 2 * G, 16, hipMemcpyDeviceToHost, s));
   HIP_TRY(hipStreamSynchronize(s));
   const unsigned long long err = hs[kActCtrError], unmatched = hs[kActCtrUnmatched];
-  const int64_t n_used = (int64_t)hs[kActCtrCount], n_fr = (int64_t)hs[kActCtrCount + 1];
+  const int64_t n_used = (int64_t)hs[2], n_fr = (int64_t)hs[3];
   if (err & kActBadOffsets) return fail(CCT_EINVAL, "malformed registry offsets");
   if (err & kActRepeatedId) return fail(CCT_EINVAL, "a correlation ID is registered twice");
   if (err) return fail(CCT_EDEVICE, "correlation-ID table overflow");
   // ---- the batch of referenced paths with their summed metrics, merged ---------------
-  Buf b_off, b_fr, b_met;
-  if (!b_off.alloc(((size_t)n_used + 1) * 8) || !b_fr.alloc((size_t)n_fr * 4) || !b_met.alloc((size_t)n_used * m * 8))
-    return fail(CCT_ENOMEM, "device allocation failed");
-  launch_compact_gather(a, registry->frames, scan.as<uint64_t>(), sums.as<uint64_t>(), m, b_off.as<int64_t>(),
-                        b_fr.as<uint32_t>(), b_met.as<uint64_t>(), s);
-  HIP_TRY(hipMemcpyAsync(b_off.as<int64_t>() + n_used, scan.as<uint64_t>() + 2 * G + 1, 8, hipMemcpyDeviceToDevice, s));
+  // (every registered path referenced: the registry is the batch, nothing is copied)
+  cct_paths batch{};
+  batch.n_events = n_used; batch.n_frames = n_fr; batch.n_metrics = m;
+  Buf b_off, b_src, b_fr, b_met;
+  if (n_used == G) {
+    batch.offsets = registry->offsets; batch.frames = registry->frames; batch.metrics = sums.as<uint64_t>();
+  } else {
+    if (!b_off.alloc(((size_t)n_used + 1) * 8) || !b_src.alloc(((size_t)n_used + 1) * 8) ||
+        !b_fr.alloc((size_t)n_fr * 4) || !b_met.alloc((size_t)n_used * m * 8))
+      return fail(CCT_ENOMEM, "device allocation failed");
+    launch_compact_gather(a, registry->frames, scan.as<uint64_t>(), sums.as<uint64_t>(), m, n_used, n_fr,
+                          b_off.as<int64_t>(), b_src.as<int64_t>(), b_fr.as<uint32_t>(), b_met.as<uint64_t>(), s);
+    batch.offsets = b_off.as<int64_t>(); batch.frames = b_fr.as<uint32_t>(); batch.metrics = b_met.as<uint64_t>();
+  }
   HIP_TRY(hipGetLastError());
   tm.mark(1, s);
   HIP_TRY(hipStreamSynchronize(s));
   const double join_ms = tm.ok ? tm.span(0, 1) : 0.0;
-  cct_paths batch{};
-  batch.n_events = n_used; batch.n_frames = n_fr; batch.n_metrics = m;
-  batch.offsets = b_off.as<int64_t>(); batch.frames = b_fr.as<uint32_t>(); batch.metrics = b_met.as<uint64_t>();
   cct_status st = aggregate(tree, &batch, s);
   if (st) return st;
   g_join_ms = join_ms;

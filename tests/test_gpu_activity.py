@@ -186,3 +186,31 @@ def test_allocation_failure(monkeypatch, k):
     assert_same(tree.to_numpy(), orc.tree(), "merged")
     orc.close()
     tree.free()
+
+
+@pytest.mark.parametrize("seed", [21, 22])
+def test_dense_ids_with_holes(seed):
+    # registered IDs: a random 70% of a counter range (the direct table is used, with
+    # holes); records name registered IDs, holes, and IDs just below and above the range
+    m = 2
+    ro, rf, _ = tracegen.random_paths(3000, 35, 14, 1, seed=seed)
+    rng = np.random.default_rng(seed)
+    base = np.uint64(2**63 - 1000)
+    pool = np.arange(4300, dtype=np.uint64) + base
+    ids = rng.permutation(rng.choice(pool, size=3000, replace=False))
+    holes = np.setdiff1d(pool, ids)
+    rec = np.concatenate([ids[rng.integers(0, 3000, 5000)], holes[:200], base - np.arange(1, 50, dtype=np.uint64),
+                          base + np.uint64(4300) + np.arange(50, dtype=np.uint64)])
+    rec = rec[rng.permutation(rec.size)]
+    rw = rng.integers(0, 2**64, size=(rec.size, m), dtype=np.uint64)
+    other = tracegen.random_paths(2000, 35, 14, m, seed=seed + 1)
+    got, want = run_case(other, (ro, rf, ids, rec, rw), m)
+    assert_same(got, want, f"dense IDs, seed {seed}")
+    # a repeated ID inside the dense range is rejected
+    import paper_2411_02797_amd as cct
+    tree = cct.build(*to_dev(*other))
+    rep = ids.copy()
+    rep[2999] = rep[5]
+    to, tf, _ = to_dev(ro, rf, np.zeros((ro.size - 1, 1), np.uint64))
+    assert _status(lambda: tree.merge_activity(to, tf, _u64(rep), _u64(rec), _u64(rw))) == "CCT_EINVAL"
+    tree.free()
