@@ -124,6 +124,23 @@ typedef struct {
 cct_status cct_merge_activity(cct_tree *tree, const cct_paths *registry, const uint64_t *reg_corr_ids,
                               const cct_activity *activity, void *hip_stream, int64_t *n_unmatched);
 
+/* Bottom-up view of `tree`: for every distinct frame f that labels a node (the root's
+ * placeholder excluded), in ascending frame order,
+ *   excl[f][j] = sum of metric j over the events whose path ends with f (the exclusive
+ *                sums of the nodes labelled f),
+ *   incl[f][j] = sum of metric j over the events whose path contains f, each event counted
+ *                once however often f recurs on its path.
+ * The flame graph's bottom-up view aggregates the metrics of the same node across
+ * different call paths (Implementation, "GUI", "Flame Graph Visualization").
+ *   capacity   entries of the output arrays; they are written only if capacity >= K
+ *   frames     DEVICE or HOST uint32[K], or NULL
+ *   excl/incl  DEVICE or HOST uint64[K][M] row-major, or NULL
+ *   n_frames   HOST out: K
+ * Call with capacity 0 to learn K, then with arrays of K entries: the view is computed
+ * once and kept with the tree until the tree changes (cct_merge, cct_merge_activity). */
+cct_status cct_bottom_up(cct_tree *tree, void *hip_stream, int64_t capacity, uint32_t *frames, uint64_t *excl,
+                         uint64_t *incl, int64_t *n_frames);
+
 /* Look up Q call paths (queries->offsets/frames, metrics ignored) in `tree`.
  * Writes DEVICE arrays: node_ids int64[Q] (the canonical id, or -1 if the path is
  * not a node), and, when non-NULL, excl/incl uint64[Q][M] (zeros for absent paths). */
@@ -154,7 +171,9 @@ const char *cct_last_error(void);
  * ingest (hash, dedup, exclusive aggregation), [1] publish of new paths, [2] canonical
  * ordering (sort, LCP, scans), [3] node emission (parents, exclusive, inclusive), [4]
  * whole merge, [5] the correlation-ID join before the merge (cct_merge_activity only;
- * 0 otherwise).  Returns the number of values written (<= n, at most 6). */
+ * 0 otherwise), [6] the computation of the bottom-up view by the last cct_bottom_up (0
+ * when it was kept from an earlier call).  Returns the number of values written (<= n,
+ * at most 7). */
 int cct_last_timings(double *ms, int n);
 
 #ifdef __cplusplus

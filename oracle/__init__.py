@@ -62,6 +62,14 @@ def _load():
         lib.or_brute.argtypes = [i64, vp, vp, vp, i32, vp, vp, vp, vp, vp]
         lib.or_point_query.argtypes = [i64, vp, vp, vp, i32, i64, vp, vp, vp, vp, vp, ctypes.c_int]
         lib.or_check.argtypes = [i64, i32, vp, vp, vp, vp, vp, vp, vp]
+        lib.or_bottom_up.restype = vp
+        lib.or_bottom_up.argtypes = [i64, vp, vp, vp, i32]
+        lib.or_bottom_up_size.restype = i64
+        lib.or_bottom_up_size.argtypes = [vp]
+        lib.or_bottom_up_fetch.argtypes = [vp, vp, vp, vp]
+        lib.or_bottom_up_fetch.restype = None
+        lib.or_bottom_up_free.argtypes = [vp]
+        lib.or_bottom_up_free.restype = None
         _lib = lib
     return _lib
 
@@ -235,3 +243,27 @@ def join_activity(reg_offsets, reg_frames, reg_corr_ids, corr_ids, metrics):
     pos = np.repeat(starts - offsets[:-1], lens) + np.arange(offsets[-1], dtype=np.int64)
     frames = rf[pos] if pos.size else np.zeros(0, np.uint32)
     return offsets, frames, w[np.asarray(rec, np.int64)].reshape(len(rec), w.shape[1]), unmatched
+
+
+def bottom_up(offsets, frames, metrics):
+    """Bottom-up view from the events (``or_bottom_up`` in oracle.cpp): for every frame on
+    some path, ascending, (frames[K], excl[K, M], incl[K, M]) where excl sums the events
+    whose path ends with the frame and incl the events whose path contains it, each event
+    once however often the frame recurs (Implementation, "GUI": the bottom-up view
+    aggregates the metrics of the same node across different call paths)."""
+    o, f, w = _csr(offsets, frames, metrics)
+    n, m = o.size - 1, w.shape[1]
+    lib = _load()
+    h = lib.or_bottom_up(n, _p(o), _p(f), _p(w), m)
+    if not h:
+        raise ValueError("malformed offsets")
+    try:
+        K = lib.or_bottom_up_size(h)
+        fr = np.empty(max(K, 1), np.uint32)
+        ex = np.empty((max(K, 1), m), np.uint64)
+        inc = np.empty((max(K, 1), m), np.uint64)
+        lib.or_bottom_up_fetch(h, _p(fr), _p(ex), _p(inc))
+    finally:
+        lib.or_bottom_up_free(h)
+    return fr[:K], ex[:K], inc[:K]
+

@@ -15,11 +15,13 @@
 // Parity of every function here is pinned by tests against hand-worked trees,
 // brute-force prefix enumeration, closed forms and invariants; the paper itself prints
 // no tree values, so nothing here is pinned to a printed number.
+#include <algorithm>
 #include <cstdint>
 #include <cstring>
 #include <map>
 #include <set>
 #include <thread>
+#include <unordered_map>
 #include <vector>
 
 namespace {
@@ -249,5 +251,75 @@ int or_check(int64_t U, int32_t m, const uint32_t *parent, const uint32_t *frame
   }
   return 0;
 }
+
+// ---- bottom-up view, from the events (Implementation, "GUI": the bottom-up view
+// aggregates the metrics of the same node across different call paths) ----
+// For every frame f on some path, ascending: excl[f] = sum of w over the events whose path
+// ends with f; incl[f] = sum of w over the events whose path contains f, each event once
+// (its distinct frames: a sorted, de-duplicated copy of the path).
+struct BottomUp {
+  int32_t m;
+  std::vector<uint32_t> frames;
+  std::vector<uint64_t> excl, incl;
+};
+
+// Computes the view into a handle (NULL on malformed offsets); or_bottom_up_fetch copies
+// it out (frames ascending), or_bottom_up_free releases it.
+void *or_bottom_up(int64_t n, const int64_t *offsets, const uint32_t *frames, const uint64_t *metrics, int32_t m) {
+  if (!valid_offsets(n, offsets) || m < 1) return nullptr;
+  // frame -> row of the accumulators (a hash map: ordered output comes from a final sort)
+  std::unordered_map<uint32_t, size_t> row;
+  std::vector<uint64_t> ex, in;
+  auto row_of = [&](uint32_t f) {
+    auto it = row.find(f);
+    if (it != row.end()) return it->second;
+    const size_t r = row.size();
+    row.emplace(f, r);
+    ex.resize(ex.size() + m, 0);
+    in.resize(in.size() + m, 0);
+    return r;
+  };
+  std::vector<uint32_t> distinct;
+  for (int64_t i = 0; i < n; ++i) {
+    const uint32_t *f = frames + offsets[i];
+    const int64_t L = offsets[i + 1] - offsets[i];
+    if (L == 0) continue;
+    const uint64_t *w = metrics + (size_t)i * m;
+    const size_t re = row_of(f[L - 1]);
+    for (int32_t j = 0; j < m; ++j) ex[re * m + j] += w[j];
+    distinct.assign(f, f + L);
+    std::sort(distinct.begin(), distinct.end());
+    distinct.erase(std::unique(distinct.begin(), distinct.end()), distinct.end());
+    for (uint32_t x : distinct) {
+      const size_t r = row_of(x);
+      for (int32_t j = 0; j < m; ++j) in[r * m + j] += w[j];
+    }
+  }
+  const int64_t K = (int64_t)row.size();
+  std::vector<std::pair<uint32_t, size_t>> order(row.begin(), row.end());
+  std::sort(order.begin(), order.end());
+  auto *v = new BottomUp{m, std::vector<uint32_t>(K), std::vector<uint64_t>((size_t)K * m),
+                         std::vector<uint64_t>((size_t)K * m)};
+  for (int64_t k = 0; k < K; ++k) {
+    const size_t r = order[k].second;
+    v->frames[k] = order[k].first;
+    for (int32_t j = 0; j < m; ++j) {
+      v->excl[(size_t)k * m + j] = ex[r * m + j];
+      v->incl[(size_t)k * m + j] = in[r * m + j];
+    }
+  }
+  return v;
+}
+
+int64_t or_bottom_up_size(void *h) { return (int64_t)static_cast<BottomUp *>(h)->frames.size(); }
+
+void or_bottom_up_fetch(void *h, uint32_t *frames_out, uint64_t *excl_out, uint64_t *incl_out) {
+  const auto *v = static_cast<BottomUp *>(h);
+  std::copy(v->frames.begin(), v->frames.end(), frames_out);
+  std::copy(v->excl.begin(), v->excl.end(), excl_out);
+  std::copy(v->incl.begin(), v->incl.end(), incl_out);
+}
+
+void or_bottom_up_free(void *h) { delete static_cast<BottomUp *>(h); }
 
 }  // extern "C"

@@ -10,6 +10,7 @@ to load, every call raises; there is no CPU fallback.
     unmatched = tree.merge_activity(reg_offsets, reg_frames, reg_corr_ids, corr_ids, metrics3)
     ids, excl, incl = tree.query(q_offsets, q_frames)
     arrays = tree.to_tensors()               # parent, frame, depth, excl, incl on the GPU
+    view = tree.bottom_up()                  # frames, excl, incl per distinct frame
 """
 from __future__ import annotations
 
@@ -25,8 +26,8 @@ _lib = None
 
 NO_PARENT = 0xFFFFFFFF
 MAX_METRICS = 8
-EXPORTED_SYMBOLS = ("cct_build", "cct_merge", "cct_merge_activity", "cct_query", "cct_info", "cct_export",
-                    "cct_free", "cct_release_cached_memory", "cct_last_error", "cct_last_timings")
+EXPORTED_SYMBOLS = ("cct_build", "cct_merge", "cct_merge_activity", "cct_bottom_up", "cct_query", "cct_info",
+                    "cct_export", "cct_free", "cct_release_cached_memory", "cct_last_error", "cct_last_timings")
 _STATUS = {0: "CCT_OK", -1: "CCT_EINVAL", -2: "CCT_ENOMEM", -3: "CCT_EDEVICE", -4: "CCT_EMISMATCH",
            -5: "CCT_EOVERFLOW"}
 
@@ -65,6 +66,7 @@ def load_library():
     lib.cct_build.argtypes = [P(_Paths), vp, P(vp)]
     lib.cct_merge.argtypes = [vp, P(_Paths), vp]
     lib.cct_merge_activity.argtypes = [vp, P(_Paths), vp, P(_Activity), vp, P(i64)]
+    lib.cct_bottom_up.argtypes = [vp, vp, i64, vp, vp, vp, P(i64)]
     lib.cct_query.argtypes = [vp, P(_Paths), vp, vp, vp, vp]
     lib.cct_info.argtypes = [vp, P(i64), P(i32), P(i64)]
     lib.cct_export.argtypes = [vp, vp, vp, vp, vp, vp, vp]
@@ -74,7 +76,8 @@ def load_library():
     lib.cct_release_cached_memory.restype = None
     lib.cct_last_error.restype = ctypes.c_char_p
     lib.cct_last_timings.argtypes = [P(ctypes.c_double), ctypes.c_int]
-    for name in ("cct_build", "cct_merge", "cct_merge_activity", "cct_query", "cct_info", "cct_export"):
+    for name in ("cct_build", "cct_merge", "cct_merge_activity", "cct_bottom_up", "cct_query", "cct_info",
+                 "cct_export"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -190,6 +193,23 @@ class Tree:
                                         inc.data_ptr() if want_metrics and q else None))
         return ids, ex, inc
 
+    def bottom_up(self, device=None):
+        """Bottom-up view (cct_bottom_up): {"frames": int32[K] (bit patterns of uint32,
+        ascending as unsigned), "excl", "incl": int64[K, M] (bit patterns of uint64)}."""
+        import torch
+        lib = load_library()
+        k = ctypes.c_int64(0)
+        _check(lib.cct_bottom_up(self._h, _stream(), 0, None, None, None, ctypes.byref(k)))
+        u, m, _ = self._info()
+        dev = torch.device(device) if device is not None else torch.device("cuda", torch.cuda.current_device())
+        out = {"frames": torch.empty(k.value, dtype=torch.int32, device=dev),
+               "excl": torch.empty((k.value, m), dtype=torch.int64, device=dev),
+               "incl": torch.empty((k.value, m), dtype=torch.int64, device=dev)}
+        if k.value:
+            _check(lib.cct_bottom_up(self._h, _stream(), k.value, out["frames"].data_ptr(), out["excl"].data_ptr(),
+                                     out["incl"].data_ptr(), ctypes.byref(k)))
+        return out
+
     def to_tensors(self, device=None):
         """Canonical arrays as tensors: parent/frame/depth int32[U] (bit patterns of
         uint32), excl/incl int64[U, M] (bit patterns of uint64)."""
@@ -231,11 +251,12 @@ def build(offsets, frames, metrics):
 
 
 def last_timings():
-    """Per-phase HIP-event times (ms) of this thread's last build/merge: ingest,
-    publish, sort, canonical emission, total of the merge, and the correlation-ID join
-    of a merge_activity call (0 otherwise)."""
-    buf = (ctypes.c_double * 6)()
-    n = load_library().cct_last_timings(buf, 6)
+    """Per-phase HIP-event times (ms) of this thread's last calls: ingest, publish, sort,
+    canonical emission and total of the last build/merge, the correlation-ID join of a
+    merge_activity call (0 otherwise), and the bottom-up view computed by the last
+    bottom_up call (0 when it was kept from an earlier call)."""
+    buf = (ctypes.c_double * 7)()
+    n = load_library().cct_last_timings(buf, 7)
     return list(buf)[:n]
 
 

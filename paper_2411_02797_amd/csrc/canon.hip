@@ -373,6 +373,7 @@ __global__ __launch_bounds__(256) void emit_kernel(CanonArgs a) {
       a.parent[0] = kInf;
       a.frame[0] = 0;
       a.depth[0] = 0;
+      a.subend[0] = (uint32_t)U;
       const bool empty_path = a.d > 0 && a.plen[a.order[0]] == 0;
       for (int j = 0; j < m; ++j) {
         a.excl[j] = empty_path ? a.psums[(int64_t)a.order[0] * m + j] : 0;
@@ -389,6 +390,8 @@ __global__ __launch_bounds__(256) void emit_kernel(CanonArgs a) {
     a.frame[u] = a.pframes[a.pstart[pid] + l - 1];
     a.depth[u] = l;
     const int64_t e = (i + 1 == a.d || l > a.lcp[i + 1]) ? i + 1 : next_smaller(a, n, i + 2, l);
+    // the subtree is the paths i .. e-1 below depth l: ids up to the first node of path e
+    a.subend[u] = (uint32_t)node_base(a, e);
     const uint64_t *si = a.scan_out + i * C, *se = a.scan_out + e * C;
     for (int j = 0; j < m; ++j) {
       a.excl[u * m + j] = l == len ? a.psums[(int64_t)pid * m + j] : 0;

@@ -199,6 +199,7 @@ struct CanonArgs {
   int64_t u_max;
   // node arrays
   uint32_t *parent, *frame, *depth;
+  uint32_t *subend;      // [U] end of each node's subtree: its descendants are the ids (u, subend[u])
   uint64_t *excl, *incl;
   unsigned long long *u_out;  // device: [0] node count, [1] order-violation flag
   int grid_nodes;
@@ -316,5 +317,23 @@ void launch_compact_lengths(const ActivityArgs &a, uint64_t *rows, hipStream_t s
 void launch_compact_gather(const ActivityArgs &a, const uint32_t *reg_frames, const uint64_t *scan,
                            const uint64_t *sums, int32_t m, int64_t n_paths, int64_t n_frames, int64_t *off_out,
                            int64_t *src_start, uint32_t *fr_out, uint64_t *met_out, hipStream_t s);
+
+// Bottom-up view (bottomup.hip): stable radix sort of uint32 (key, value) pairs (four
+// passes; hist [256 * radix_blocks(n)], offs [256 * radix_blocks(n) + 1], scan_blk for
+// launch_scan over 256 * radix_blocks(n) rows; result back in keys / vals), exclusive
+// max-scan of uint64 (blk [maxscan_blocks(n)]), and the view's kernels.
+int64_t radix_blocks(int64_t n);
+int64_t maxscan_blocks(int64_t n);
+void launch_radix_sort(uint32_t *keys, uint32_t *vals, uint32_t *keys_tmp, uint32_t *vals_tmp, int64_t n,
+                       uint64_t *hist, uint64_t *offs, uint64_t *scan_blk, hipStream_t s);
+void launch_maxscan(const uint64_t *in, int64_t n, uint64_t *blk, uint64_t *out, hipStream_t s);
+void launch_bu_keys(const uint32_t *frame, int64_t n, uint32_t *keys, uint32_t *vals, hipStream_t s);
+void launch_bu_heads(const uint32_t *K, int64_t n, uint64_t *head, hipStream_t s);
+void launch_bu_tag(const uint32_t *V, const uint64_t *head, const uint64_t *gscan, const uint32_t *subend, int64_t n,
+                   uint64_t *tag, int64_t *gstart, hipStream_t s);
+void launch_bu_rows(const uint32_t *V, const uint64_t *head, const uint64_t *gscan, const uint64_t *mx,
+                    const uint64_t *excl, const uint64_t *incl, int32_t m, int64_t n, uint64_t *rows, hipStream_t s);
+void launch_bu_out(const uint32_t *K, const int64_t *gstart, int64_t G, const uint64_t *S, int32_t m, uint32_t *frames,
+                   uint64_t *excl, uint64_t *incl, hipStream_t s);
 
 }  // namespace cct

@@ -23,12 +23,27 @@ namespace {
 thread_local std::string g_error;
 thread_local double g_timings[5] = {0, 0, 0, 0, 0};
 thread_local double g_join_ms = 0;  // correlation-ID join of the last cct_merge_activity
+thread_local double g_view_ms = 0;  // bottom-up view computed by the last cct_bottom_up (0: cached)
 thread_local int g_alloc_countdown = 0;  // test hook: >0 makes the n-th allocation of a call fail
+
+int64_t env_int(const char *name, int64_t dflt) {
+  const char *v = std::getenv(name);
+  if (!v || !*v) return dflt;
+  return std::strtoll(v, nullptr, 10);
+}
 
 cct_status fail(cct_status s, const char *msg) {
   g_error = msg;
   return s;
 }
+
+// Arms the test hook for one public call (CCT_TEST_FAIL_ALLOC = n: the call's n-th pool
+// allocation fails) and disarms it when the call returns, so no count carries over into
+// the next call.
+struct AllocHook {
+  AllocHook() { g_alloc_countdown = (int)env_int("CCT_TEST_FAIL_ALLOC", 0); }
+  ~AllocHook() { g_alloc_countdown = 0; }
+};
 
 // ---- caching device-memory pool --------------------------------------------------
 struct Pool {
@@ -132,12 +147,6 @@ unsigned long long *host_scratch() {
   return h;
 }
 
-int64_t env_int(const char *name, int64_t dflt) {
-  const char *v = std::getenv(name);
-  if (!v || !*v) return dflt;
-  return std::strtoll(v, nullptr, 10);
-}
-
 uint64_t pow2_at_least(uint64_t x) {
   uint64_t p = 1;
   while (p < x) p <<= 1;
@@ -165,7 +174,10 @@ struct cct_tree {
   Buf pframes, pcp, pstart, plen, pslot, psums;
   // canonical arrays
   int64_t u = 0;
-  Buf parent, frame, depth, excl, incl;
+  Buf parent, frame, depth, subend, excl, incl;
+  // bottom-up view (cct_bottom_up), kept until the tree changes; bu_k < 0: not computed
+  int64_t bu_k = -1;
+  Buf bu_frames, bu_excl, bu_incl;
   // canonical metadata kept for queries
   Buf order, lcp, scan_out;
 };
@@ -260,7 +272,6 @@ cct_status rehash(cct_tree *t, uint64_t cap, uint64_t hash_mask, hipStream_t s) 
 cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   const int32_t m = t->m;
   const int64_t N = p->n_events;
-  g_alloc_countdown = (int)env_int("CCT_TEST_FAIL_ALLOC", 0);
   const int hash_bits = (int)env_int("CCT_TEST_HASH_BITS", 64);
   const uint64_t hash_mask = hash_bits >= 64 ? ~0ull : ((1ull << (hash_bits < 0 ? 0 : hash_bits)) - 1);
   unsigned long long *hs = host_scratch();
@@ -412,10 +423,10 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   const int64_t nblk = (D + 1023) / 1024 + 1;
   const int64_t u_max = sum_len + 1;
   Buf order, order_tmp, lcp, scan_in, scan_out, scan_blk, sparse, chain, node_path, cursor, nlen, nstart, nblkbuf, nsrc;
-  Buf n_parent, n_frame, n_depth, n_excl, n_incl;
+  Buf n_parent, n_frame, n_depth, n_subend, n_excl, n_incl;  // canonical arrays of the new tree
   if (!order.alloc(dneed * 4) || !order_tmp.alloc(dneed * 4) || !lcp.alloc(n1 * 4) || !scan_in.alloc(dneed * C * 8) ||
       !scan_out.alloc(n1 * C * 8) || !scan_blk.alloc(nblk * C * 8) || !sparse.alloc((int64_t)levels * n1 * 4) ||
-      !chain.alloc(dneed * 4) || !node_path.alloc(u_max * 4) || !cursor.alloc(64) || !n_parent.alloc(u_max * 4) ||
+      !chain.alloc(dneed * 4) || !node_path.alloc(u_max * 4) || !cursor.alloc(64) || !n_parent.alloc(u_max * 4) || !n_subend.alloc(u_max * 4) ||
       !n_frame.alloc(u_max * 4) || !n_depth.alloc(u_max * 4) || !n_excl.alloc(u_max * m * 8) ||
       !n_incl.alloc(u_max * m * 8) || !nlen.alloc((n_new + 1) * 8) || !nstart.alloc((n_new + 1) * 8) ||
       !nblkbuf.alloc(((int64_t)n_new / 1024 + 2) * 8) || !nsrc.alloc(((int64_t)n_new + 1) * 16))
@@ -496,6 +507,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   ca.scan_blocks = nblk; ca.sparse = sparse.as<uint32_t>(); ca.levels = levels;
   ca.chain_parent = chain.as<uint32_t>(); ca.node_path = node_path.as<uint32_t>(); ca.u_max = u_max;
   ca.parent = n_parent.as<uint32_t>(); ca.frame = n_frame.as<uint32_t>(); ca.depth = n_depth.as<uint32_t>();
+  ca.subend = n_subend.as<uint32_t>();
   ca.excl = n_excl.as<uint64_t>(); ca.incl = n_incl.as<uint64_t>();
   ca.u_out = cursor.as<unsigned long long>() + 2;
   ca.grid_nodes = (int)std::max<int64_t>(1, std::min<int64_t>((u_max + 255) / 256, (int64_t)cu_count() * 16));
@@ -532,6 +544,8 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   t->sum_len = sum_len;
   t->u = (int64_t)hs[2];
   t->parent = std::move(n_parent); t->frame = std::move(n_frame); t->depth = std::move(n_depth);
+  t->subend = std::move(n_subend);
+  t->bu_k = -1;  // the bottom-up view of the old tree is stale
   t->excl = std::move(n_excl); t->incl = std::move(n_incl);
   t->order = std::move(order); t->lcp = std::move(lcp); t->scan_out = std::move(scan_out);
   return CCT_OK;
@@ -542,6 +556,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
 extern "C" {
 
 cct_status cct_build(const cct_paths *events, void *hip_stream, cct_tree **out) {
+  AllocHook hook;
   g_join_ms = 0;
   g_error.clear();
   if (!out) return fail(CCT_EINVAL, "out is NULL");
@@ -570,6 +585,7 @@ cct_status cct_build(const cct_paths *events, void *hip_stream, cct_tree **out) 
 }
 
 cct_status cct_merge(cct_tree *tree, const cct_paths *chunk, void *hip_stream) {
+  AllocHook hook;
   g_error.clear();
   g_join_ms = 0;
   if (!tree) return fail(CCT_EINVAL, "tree is NULL");
@@ -584,6 +600,7 @@ cct_status cct_merge(cct_tree *tree, const cct_paths *chunk, void *hip_stream) {
 
 cct_status cct_merge_activity(cct_tree *tree, const cct_paths *registry, const uint64_t *reg_corr_ids,
                               const cct_activity *act, void *hip_stream, int64_t *n_unmatched) {
+  AllocHook hook;  // counts the join's and the merge's allocations together
   g_error.clear();
   g_join_ms = 0;
   if (!tree || !registry || !act) return fail(CCT_EINVAL, "NULL argument");
@@ -605,7 +622,6 @@ cct_status cct_merge_activity(cct_tree *tree, const cct_paths *registry, const u
   const int32_t m = tree->m;
   unsigned long long *hs = host_scratch();
   if (!hs) return fail(CCT_ENOMEM, "pinned host allocation failed");
-  g_alloc_countdown = (int)env_int("CCT_TEST_FAIL_ALLOC", 0);
   if (G == 0 || R == 0) {  // nothing can match: no device work
     if (n_unmatched) *n_unmatched = R;
     return CCT_OK;
@@ -681,6 +697,91 @@ cct_status cct_merge_activity(cct_tree *tree, const cct_paths *registry, const u
   return CCT_OK;
 }
 
+namespace {
+
+// The bottom-up view of `t` into t->bu_* (see bottomup.hip).  Nothing of the tree changes
+// on failure.
+cct_status compute_bottom_up(cct_tree *t, hipStream_t s) {
+  const int64_t n = t->u - 1;  // nodes other than the root
+  const int32_t m = t->m;
+  unsigned long long *hs = host_scratch();
+  if (!hs) return fail(CCT_ENOMEM, "pinned host allocation failed");
+  if (n <= 0) {
+    t->bu_k = 0;
+    return CCT_OK;
+  }
+  const int64_t rb = radix_blocks(n), hist_rows = 256 * rb;
+  const int64_t scan_rows = std::max<int64_t>(hist_rows, n);
+  Buf keys, vals, keys_t, vals_t, hist, offs, scan_blk, head, gscan, tag, mx, ms_blk, gstart, rows, S;
+  if (!keys.alloc(n * 4) || !vals.alloc(n * 4) || !keys_t.alloc(n * 4) || !vals_t.alloc(n * 4) ||
+      !hist.alloc(hist_rows * 8) || !offs.alloc((hist_rows + 1) * 8) ||
+      !scan_blk.alloc((scan_rows / 1024 + 2) * 2 * m * 8) || !head.alloc(n * 8) || !gscan.alloc((n + 1) * 8) ||
+      !tag.alloc(n * 8) || !mx.alloc(n * 8) || !ms_blk.alloc((maxscan_blocks(n) + 1) * 8) ||
+      !gstart.alloc((n + 1) * 8) || !rows.alloc(n * 2 * m * 8) || !S.alloc((n + 1) * 2 * m * 8))
+    return fail(CCT_ENOMEM, "device allocation failed");
+  Timer tm;
+  tm.mark(0, s);
+  uint32_t *K = keys.as<uint32_t>(), *V = vals.as<uint32_t>();
+  launch_bu_keys(t->frame.as<uint32_t>(), n, K, V, s);
+  launch_radix_sort(K, V, keys_t.as<uint32_t>(), vals_t.as<uint32_t>(), n, hist.as<uint64_t>(), offs.as<uint64_t>(),
+                    scan_blk.as<uint64_t>(), s);
+  launch_bu_heads(K, n, head.as<uint64_t>(), s);
+  launch_scan(head.as<uint64_t>(), n, 1, scan_blk.as<uint64_t>(), gscan.as<uint64_t>(), s);
+  launch_bu_tag(V, head.as<uint64_t>(), gscan.as<uint64_t>(), t->subend.as<uint32_t>(), n, tag.as<uint64_t>(),
+                gstart.as<int64_t>(), s);
+  launch_maxscan(tag.as<uint64_t>(), n, ms_blk.as<uint64_t>(), mx.as<uint64_t>(), s);
+  launch_bu_rows(V, head.as<uint64_t>(), gscan.as<uint64_t>(), mx.as<uint64_t>(), t->excl.as<uint64_t>(),
+                 t->incl.as<uint64_t>(), m, n, rows.as<uint64_t>(), s);
+  launch_scan(rows.as<uint64_t>(), n, 2 * m, scan_blk.as<uint64_t>(), S.as<uint64_t>(), s);
+  HIP_TRY(hipGetLastError());
+  HIP_TRY(hipMemcpyAsync(hs, gscan.as<uint64_t>() + n, 8, hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  const int64_t G = (int64_t)hs[0];
+  Buf f_out, e_out, i_out;
+  if (!f_out.alloc(G * 4) || !e_out.alloc(G * m * 8) || !i_out.alloc(G * m * 8))
+    return fail(CCT_ENOMEM, "device allocation failed");
+  launch_bu_out(K, gstart.as<int64_t>(), G, S.as<uint64_t>(), m, f_out.as<uint32_t>(), e_out.as<uint64_t>(),
+                i_out.as<uint64_t>(), s);
+  HIP_TRY(hipGetLastError());
+  tm.mark(1, s);
+  HIP_TRY(hipStreamSynchronize(s));
+  g_view_ms = tm.ok ? tm.span(0, 1) : 0.0;
+  t->bu_frames = std::move(f_out);
+  t->bu_excl = std::move(e_out);
+  t->bu_incl = std::move(i_out);
+  t->bu_k = G;
+  return CCT_OK;
+}
+
+}  // namespace
+
+cct_status cct_bottom_up(cct_tree *tree, void *hip_stream, int64_t capacity, uint32_t *frames, uint64_t *excl,
+                         uint64_t *incl, int64_t *n_frames) {
+  g_error.clear();
+  g_view_ms = 0;
+  if (!tree || !n_frames) return fail(CCT_EINVAL, "NULL argument");
+  if (capacity < 0) return fail(CCT_EINVAL, "negative capacity");
+  int dev = 0;
+  (void)hipGetDevice(&dev);
+  if (dev != tree->device) return fail(CCT_EINVAL, "tree belongs to another device");
+  hipStream_t s = (hipStream_t)hip_stream;
+  AllocHook hook;
+  if (tree->bu_k < 0) {
+    cct_status st = compute_bottom_up(tree, s);
+    if (st) return st;
+  }
+  const int64_t K = tree->bu_k;
+  if (K > 0 && capacity >= K) {
+    const size_t m = (size_t)tree->m;
+    if (frames) HIP_TRY(hipMemcpyAsync(frames, tree->bu_frames.p, (size_t)K * 4, hipMemcpyDefault, s));
+    if (excl) HIP_TRY(hipMemcpyAsync(excl, tree->bu_excl.p, (size_t)K * m * 8, hipMemcpyDefault, s));
+    if (incl) HIP_TRY(hipMemcpyAsync(incl, tree->bu_incl.p, (size_t)K * m * 8, hipMemcpyDefault, s));
+    HIP_TRY(hipStreamSynchronize(s));
+  }
+  *n_frames = K;
+  return CCT_OK;
+}
+
 cct_status cct_query(const cct_tree *tree, const cct_paths *q, void *hip_stream, int64_t *node_ids, uint64_t *excl,
                      uint64_t *incl) {
   g_error.clear();
@@ -693,7 +794,7 @@ cct_status cct_query(const cct_tree *tree, const cct_paths *q, void *hip_stream,
   hipStream_t s = (hipStream_t)hip_stream;
   unsigned long long *hs = host_scratch();
   if (!hs) return fail(CCT_ENOMEM, "pinned host allocation failed");
-  g_alloc_countdown = 0;
+  g_alloc_countdown = 0;  // queries allocate one word; the hook is not armed
   Buf err;
   if (!err.alloc(8)) return fail(CCT_ENOMEM, "device allocation failed");
   HIP_TRY(hipMemsetAsync(err.p, 0, 8, s));
@@ -756,9 +857,10 @@ const char *cct_last_error(void) { return g_error.c_str(); }
 
 int cct_last_timings(double *ms, int n) {
   if (!ms || n <= 0) return 0;
-  const int k = n < 6 ? n : 6;
+  const int k = n < 7 ? n : 7;
   for (int i = 0; i < k && i < 5; ++i) ms[i] = g_timings[i];
   if (k > 5) ms[5] = g_join_ms;
+  if (k > 6) ms[6] = g_view_ms;
   return k;
 }
 

@@ -327,3 +327,73 @@ def test_join_edge_cases():
     assert (o.tolist(), f.size, w.shape, u) == ([0], 0, (0, 1), 2)
     o, f, w, u = oracle.join_activity([0, 2], [4, 4], [9], [], np.zeros((0, 3), np.uint64))
     assert (o.tolist(), f.size, w.shape, u) == ([0], 0, (0, 3), 0)
+
+
+# ---- bottom-up view -----------------------------------------------------------------
+# Events [1,2,1,2]:5, [2,3]:7, [9]:11, []:13.  By hand: excl(f) sums the events ending
+# with f: 2 <- 5, 3 <- 7, 9 <- 11 (the empty path ends with no frame); incl(f) sums the
+# events containing f once each: 1 <- 5, 2 <- 5 + 7, 3 <- 7, 9 <- 11 (frame 1 and 2 recur
+# on the first path and count once).
+def test_bottom_up_hand_worked():
+    fr, ex, inc = oracle.bottom_up([0, 4, 6, 7, 7], [1, 2, 1, 2, 2, 3, 9], [[5], [7], [11], [13]])
+    assert fr.tolist() == [1, 2, 3, 9]
+    assert ex.ravel().tolist() == [0, 5, 7, 11]
+    assert inc.ravel().tolist() == [5, 12, 7, 11]
+
+
+def py_bottom_up_from_tree(t):
+    """Second definition, from the tree: every node adds its exclusive sums to its frame;
+    a node whose proper ancestors carry no node of its frame adds its inclusive sums
+    (each event passes through exactly one such topmost node of each frame it contains)."""
+    parent, frame = t["parent"], t["frame"]
+    m = t["excl"].shape[1]
+    mask = (1 << 64) - 1
+    ex, inc = {}, {}
+    for v in range(1, parent.size):
+        f = int(frame[v])
+        ex.setdefault(f, [0] * m)
+        inc.setdefault(f, [0] * m)
+        u, top = int(parent[v]), True
+        while u != 0:
+            if int(frame[u]) == f:
+                top = False
+                break
+            u = int(parent[u])
+        for j in range(m):
+            ex[f][j] = (ex[f][j] + int(t["excl"][v, j])) & mask
+            if top:
+                inc[f][j] = (inc[f][j] + int(t["incl"][v, j])) & mask
+    keys = sorted(ex)
+    return keys, [ex[k] for k in keys], [inc[k] for k in keys]
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_bottom_up_events_match_the_tree_rule(seed):
+    # small frame alphabets make recursion (repeated frames on a path) frequent
+    o, f, w = tracegen.random_paths(300, 3 + seed, 12, 2, seed=seed)  # (events, frame ids, max length, M)
+    fr, ex, inc = oracle.bottom_up(o, f, w)
+    keys, tex, tinc = py_bottom_up_from_tree(oracle.build_tree(o, f, w))
+    assert fr.tolist() == keys
+    assert ex.tolist() == tex
+    assert inc.tolist() == tinc
+
+
+def test_bottom_up_closed_forms():
+    # one path of distinct frames: every frame's incl is the path's weight
+    fr, ex, inc = oracle.bottom_up([0, 5], [10, 20, 30, 40, 50], [[7]])
+    assert fr.tolist() == [10, 20, 30, 40, 50]
+    assert inc.ravel().tolist() == [7] * 5 and ex.ravel().tolist() == [0, 0, 0, 0, 7]
+    # pure recursion of one frame: counted once in incl and once in excl
+    fr, ex, inc = oracle.bottom_up([0, 4], [6, 6, 6, 6], [[9]])
+    assert (fr.tolist(), ex.ravel().tolist(), inc.ravel().tolist()) == ([6], [9], [9])
+    # the root's placeholder is no frame; an empty trace has an empty view
+    fr, ex, inc = oracle.bottom_up([0, 0], [], [[3]])
+    assert fr.size == 0 and ex.shape == (0, 1)
+
+
+def test_bottom_up_exclusive_total():
+    # every non-empty event ends with exactly one frame: the exclusive view sums to the total
+    o, f, w = tracegen.random_paths(2000, 20, 50, 3, seed=9)
+    fr, ex, inc = oracle.bottom_up(o, f, w)
+    nonempty = np.diff(o) > 0
+    assert np.array_equal(ex.sum(axis=0, dtype=np.uint64), w[nonempty].sum(axis=0, dtype=np.uint64))
