@@ -14,6 +14,10 @@ of a 2,097,152-path registry once, in shuffled order, 10% repeated records, 2% r
 with unregistered IDs) with the registry by correlation ID and merges the result; the
 rate is records per second.
 
+With --workload bottom_up, one step = one cct_bottom_up computation (the view is
+recomputed: every step starts from a tree built untimed from the 16M-event trace); the
+rate is tree nodes per second.
+
     python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload layered_16m]
 """
 import argparse
@@ -39,6 +43,8 @@ DESCRIPTIONS = {
     "tiny": "10,000 events on a random call-site tree, 1 uint64 metric",
     "merge": "8,388,608-event base (layered_16m program, 60% of its paths) + 32 merged chunks of 2,097,152 events "
              "(20% from paths new to the chunk), 4 uint64 metrics (one full-range)",
+    "bottom_up": "bottom-up view of the layered_16m tree (4,407,055 nodes, 2 uint64 metrics): per frame, exclusive "
+                 "sums and inclusive sums counted once per path",
     "activity": "8,388,608-event base (as merge) + 8 activity flushes, each a registry of 2,097,152 call paths "
                 "(a merge chunk) under distinct correlation IDs and 2,348,810 records (every ID once, shuffled, "
                 "+10% repeated IDs, +2% unregistered IDs), 4 uint64 metrics",
@@ -126,6 +132,8 @@ def main():
         return bench_merge(args, torch, tracegen, cct, dev)
     if args.workload == "activity":
         return bench_activity(args, torch, tracegen, cct, dev)
+    if args.workload == "bottom_up":
+        return bench_bottom_up(args, torch, tracegen, cct, dev)
     o, f, w = tracegen.generate(args.workload)
     N, F, M = o.size - 1, f.size, w.shape[1]
     log(f"generated {args.workload}: N={N:,} F={F:,} M={M} in {time.perf_counter() - t0:.1f}s")
@@ -328,6 +336,49 @@ def bench_activity(args, torch, tracegen, cct, dev):
         "phase_ms_per_flush": {"join": join_ms, "ingest": float(ph[:, 0].mean()), "publish": float(ph[:, 1].mean()),
                                "sort": float(ph[:, 2].mean()), "emit": float(ph[:, 3].mean()),
                                "merge_call": float(ph[:, 4].mean())},
+    }
+    print(json.dumps(line), flush=True)
+
+
+def bench_bottom_up(args, torch, tracegen, cct, dev):
+    o, f, w = tracegen.generate("layered_16m")
+    to = torch.from_numpy(o).to(dev)
+    tf = torch.from_numpy(f.view(np.int32)).to(dev)
+    tw = torch.from_numpy(w.view(np.int64)).to(dev)
+    M = w.shape[1]
+    view_ms, wall_ms = [], []
+    U = K = 0
+    for step in range(args.warmup + args.steps):
+        tree = cct.build(to, tf, tw)
+        U = tree.n_nodes
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        v = tree.bottom_up()
+        torch.cuda.synchronize()
+        wall = (time.perf_counter() - t0) * 1000.0
+        K = v["frames"].numel()
+        ms = cct.last_timings()[6]
+        tree.free()
+        del v
+        if step >= args.warmup:
+            view_ms.append(ms)
+            wall_ms.append(wall)
+        log(f"{'warmup' if step < args.warmup else 'step'} {step}: view {ms:.3f} ms (call {wall:.3f} ms), "
+            f"U={U:,} K={K:,}")
+    ms = float(np.mean(view_ms))
+    # algorithmic bytes: every node's frame, subtree end and sums read once, the view written once
+    b_alg = U * (4 + 4 + 16 * M) + K * (4 + 16 * M)
+    achieved = b_alg / (ms * 1e-3) / 1e9
+    line = {
+        "metric": METRIC, "value": U / (ms * 1e-3), "unit": "nodes/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "u64", "data": "synthetic",
+        "config": {"workload": f"bottom_up: {DESCRIPTIONS['bottom_up']}", "nodes": U, "frames_in_view": K,
+                   "metrics": M, "call_ms_with_copy_out": float(np.mean(wall_ms))},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                     "kernel": "bottom-up view (radix sort by frame, max-scan, prefix sums)",
+                     "bytes_per_launch": b_alg, "avg_launch_ms": ms},
     }
     print(json.dumps(line), flush=True)
 

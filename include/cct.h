@@ -171,9 +171,9 @@ const char *cct_last_error(void);
  * ingest (hash, dedup, exclusive aggregation), [1] publish of new paths, [2] canonical
  * ordering (sort, LCP, scans), [3] node emission (parents, exclusive, inclusive), [4]
  * whole merge, [5] the correlation-ID join before the merge (cct_merge_activity only;
- * 0 otherwise), [6] the computation of the bottom-up view by the last cct_bottom_up (0
- * when it was kept from an earlier call).  Returns the number of values written (<= n,
- * at most 7). */
+ * 0 otherwise), [6] the most recent computation of a bottom-up view by cct_bottom_up
+ * (calls that only copy a kept view leave it as it is).  Returns the number of values
+ * written (<= n, at most 7). */
 int cct_last_timings(double *ms, int n);
 
 #ifdef __cplusplus

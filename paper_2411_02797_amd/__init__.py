@@ -253,8 +253,8 @@ def build(offsets, frames, metrics):
 def last_timings():
     """Per-phase HIP-event times (ms) of this thread's last calls: ingest, publish, sort,
     canonical emission and total of the last build/merge, the correlation-ID join of a
-    merge_activity call (0 otherwise), and the bottom-up view computed by the last
-    bottom_up call (0 when it was kept from an earlier call)."""
+    merge_activity call (0 otherwise), and the most recent computation of a bottom-up
+    view (bottom_up)."""
     buf = (ctypes.c_double * 7)()
     n = load_library().cct_last_timings(buf, 7)
     return list(buf)[:n]

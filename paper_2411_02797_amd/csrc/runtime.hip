@@ -23,7 +23,7 @@ namespace {
 thread_local std::string g_error;
 thread_local double g_timings[5] = {0, 0, 0, 0, 0};
 thread_local double g_join_ms = 0;  // correlation-ID join of the last cct_merge_activity
-thread_local double g_view_ms = 0;  // bottom-up view computed by the last cct_bottom_up (0: cached)
+thread_local double g_view_ms = 0;  // the most recent computation of a bottom-up view
 thread_local int g_alloc_countdown = 0;  // test hook: >0 makes the n-th allocation of a call fail
 
 int64_t env_int(const char *name, int64_t dflt) {
@@ -758,7 +758,6 @@ cct_status compute_bottom_up(cct_tree *t, hipStream_t s) {
 cct_status cct_bottom_up(cct_tree *tree, void *hip_stream, int64_t capacity, uint32_t *frames, uint64_t *excl,
                          uint64_t *incl, int64_t *n_frames) {
   g_error.clear();
-  g_view_ms = 0;
   if (!tree || !n_frames) return fail(CCT_EINVAL, "NULL argument");
   if (capacity < 0) return fail(CCT_EINVAL, "negative capacity");
   int dev = 0;
