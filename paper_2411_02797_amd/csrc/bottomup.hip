@@ -17,8 +17,12 @@
 //   2. a node is topmost iff no earlier node of its group has a subtree that reaches past
 //      it: one exclusive max-scan over (group index << 32 | subend) decides every node
 //      (an earlier group has a smaller high word);
-//   3. prefix sums over the sorted order of (excl, incl if topmost) give each group's sums
-//      as a difference, with no atomics on hot frames.
+//   3. every node learns its group (scattered back to node order), and the aggregation
+//      kernels of the ingest (LDS maps per workgroup, staged buckets) sum the nodes'
+//      exclusive sums, and the topmost nodes' inclusive sums, per group: the sums are read
+//      in node order, and hot frames meet in LDS.
+#include <algorithm>
+
 #include "common.h"
 
 namespace cct {
@@ -200,34 +204,24 @@ __global__ void bu_tag_kernel(const uint32_t *V, const uint64_t *head, const uin
   if (i == n - 1) gstart[g + 1] = n;  // g + 1 = the number of groups
 }
 
-// rows of the sums scan: the node's exclusive sums, and its inclusive sums if it is the
-// topmost of its frame on its root path
-__global__ void bu_rows_kernel(const uint32_t *V, const uint64_t *head, const uint64_t *gscan, const uint64_t *mx,
-                               const uint64_t *excl, const uint64_t *incl, int32_t m, int64_t n, uint64_t *rows) {
+// group of every node in node order: slot_ex[v] = group of v, slot_in[v] = group of v if
+// v is the topmost node of its frame on its root path, else none; the root is in no group
+__global__ void bu_slots_kernel(const uint32_t *V, const uint64_t *head, const uint64_t *gscan, const uint64_t *mx,
+                                int64_t n, uint32_t *slot_ex, uint32_t *slot_in) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i == 0) slot_ex[0] = slot_in[0] = kNoSlot;
   if (i >= n) return;
   const uint64_t g = gscan[i] + head[i] - 1;
   const uint32_t v = V[i];
   const bool top = (mx[i] >> 32) != g || (uint64_t)v >= (mx[i] & 0xFFFFFFFFull);
-  uint64_t *row = rows + i * 2 * m;
-  for (int j = 0; j < m; ++j) {
-    row[j] = excl[(int64_t)v * m + j];
-    row[m + j] = top ? incl[(int64_t)v * m + j] : 0;
-  }
+  slot_ex[v] = (uint32_t)g;
+  slot_in[v] = top ? (uint32_t)g : kNoSlot;
 }
 
-// group g = sorted positions [gstart[g], gstart[g + 1]) (gstart[G] = n): its frame and the
-// differences of the prefix sums S (row n holds the totals)
-__global__ void bu_out_kernel(const uint32_t *K, const int64_t *gstart, int64_t G, const uint64_t *S, int32_t m,
-                              uint32_t *frames, uint64_t *excl, uint64_t *incl) {
+// frame of every group (its first sorted position)
+__global__ void bu_frames_kernel(const uint32_t *K, const int64_t *gstart, int64_t G, uint32_t *frames) {
   const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (g >= G) return;
-  const int64_t st = gstart[g], en = gstart[g + 1];
-  frames[g] = K[st];
-  for (int j = 0; j < m; ++j) {
-    excl[g * m + j] = S[en * 2 * m + j] - S[st * 2 * m + j];
-    incl[g * m + j] = S[en * 2 * m + m + j] - S[st * 2 * m + m + j];
-  }
+  if (g < G) frames[g] = K[gstart[g]];
 }
 
 inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
@@ -272,16 +266,13 @@ void launch_bu_tag(const uint32_t *V, const uint64_t *head, const uint64_t *gsca
   if (n > 0)
     hipLaunchKernelGGL(bu_tag_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, V, head, gscan, subend, n, tag, gstart);
 }
-void launch_bu_rows(const uint32_t *V, const uint64_t *head, const uint64_t *gscan, const uint64_t *mx,
-                    const uint64_t *excl, const uint64_t *incl, int32_t m, int64_t n, uint64_t *rows, hipStream_t s) {
-  if (n > 0)
-    hipLaunchKernelGGL(bu_rows_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, V, head, gscan, mx, excl, incl, m, n,
-                       rows);
+void launch_bu_slots(const uint32_t *V, const uint64_t *head, const uint64_t *gscan, const uint64_t *mx, int64_t n,
+                     uint32_t *slot_ex, uint32_t *slot_in, hipStream_t s) {
+  hipLaunchKernelGGL(bu_slots_kernel, dim3(blocks_for(std::max<int64_t>(n, 1), 256)), dim3(256), 0, s, V, head, gscan,
+                     mx, n, slot_ex, slot_in);
 }
-void launch_bu_out(const uint32_t *K, const int64_t *gstart, int64_t G, const uint64_t *S, int32_t m, uint32_t *frames,
-                   uint64_t *excl, uint64_t *incl, hipStream_t s) {
-  if (G > 0)
-    hipLaunchKernelGGL(bu_out_kernel, dim3(blocks_for(G, 256)), dim3(256), 0, s, K, gstart, G, S, m, frames, excl, incl);
+void launch_bu_frames(const uint32_t *K, const int64_t *gstart, int64_t G, uint32_t *frames, hipStream_t s) {
+  if (G > 0) hipLaunchKernelGGL(bu_frames_kernel, dim3(blocks_for(G, 256)), dim3(256), 0, s, K, gstart, G, frames);
 }
 
 }  // namespace cct

@@ -331,9 +331,9 @@ void launch_bu_keys(const uint32_t *frame, int64_t n, uint32_t *keys, uint32_t *
 void launch_bu_heads(const uint32_t *K, int64_t n, uint64_t *head, hipStream_t s);
 void launch_bu_tag(const uint32_t *V, const uint64_t *head, const uint64_t *gscan, const uint32_t *subend, int64_t n,
                    uint64_t *tag, int64_t *gstart, hipStream_t s);
-void launch_bu_rows(const uint32_t *V, const uint64_t *head, const uint64_t *gscan, const uint64_t *mx,
-                    const uint64_t *excl, const uint64_t *incl, int32_t m, int64_t n, uint64_t *rows, hipStream_t s);
-void launch_bu_out(const uint32_t *K, const int64_t *gstart, int64_t G, const uint64_t *S, int32_t m, uint32_t *frames,
-                   uint64_t *excl, uint64_t *incl, hipStream_t s);
+// slot_ex / slot_in: [n + 1] in node order (the root gets kNoSlot)
+void launch_bu_slots(const uint32_t *V, const uint64_t *head, const uint64_t *gscan, const uint64_t *mx, int64_t n,
+                     uint32_t *slot_ex, uint32_t *slot_in, hipStream_t s);
+void launch_bu_frames(const uint32_t *K, const int64_t *gstart, int64_t G, uint32_t *frames, hipStream_t s);
 
 }  // namespace cct

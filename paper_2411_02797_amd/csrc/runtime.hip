@@ -249,6 +249,27 @@ struct Timer {
   }
 };
 
+// Staging of the metric aggregation (launch_aggregate) for `n_rows` rows keyed by slots
+// below `cap`: bucket counts zeroed on `s`.  Leaves st.nbuckets = 0 (atomic flush) when
+// the slots need more buckets than a workgroup can count.
+cct_status setup_stage(int32_t m, uint64_t cap, int agg_grid, Buf &count, Buf &keys, Buf &sums, AggStage &st,
+                       hipStream_t s) {
+  st = AggStage{};
+  st.bshift = agg_bucket_shift(m);
+  const int64_t nbk = std::max<int64_t>(1, (int64_t)((cap + (1ull << st.bshift) - 1) >> st.bshift));
+  if (nbk > agg_max_buckets()) return CCT_OK;
+  const int64_t total = (int64_t)agg_grid * agg_map_entries(m);
+  st.nbuckets = nbk;
+  st.bucket_cap = 2 * ((total + nbk - 1) / nbk) + 256;  // twice the even share (slots are hashed)
+  if (!count.alloc(nbk * 4) || !keys.alloc(nbk * st.bucket_cap * 4) || !sums.alloc(nbk * st.bucket_cap * m * 8))
+    return fail(CCT_ENOMEM, "device allocation failed");
+  HIP_TRY(hipMemsetAsync(count.p, 0, nbk * 4, s));
+  st.count = count.as<uint32_t>();
+  st.keys = keys.as<uint32_t>();
+  st.sums = sums.as<uint64_t>();
+  return CCT_OK;
+}
+
 // Re-insert the tree's stored paths into a fresh table of capacity `cap`.
 cct_status rehash(cct_tree *t, uint64_t cap, uint64_t hash_mask, hipStream_t s) {
   Buf ns;
@@ -329,20 +350,8 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
       // must hold, so fewer events overflow into device atomics
       const int agg_grid = (int)std::max<int64_t>(1, std::min<int64_t>((N + 8191) / 8192, (int64_t)cu_count() * 2));
       AggStage stg{};
-      stg.bshift = agg_bucket_shift(m);
-      const int64_t nbk = std::max<int64_t>(1, (int64_t)(t->cap >> stg.bshift));
-      if (nbk <= agg_max_buckets()) {
-        const int64_t total = (int64_t)agg_grid * agg_map_entries(m);
-        stg.nbuckets = nbk;
-        stg.bucket_cap = 2 * ((total + nbk - 1) / nbk) + 256;  // twice the even share (slots are hashed)
-        if (!agg_count.alloc(nbk * 4) || !agg_keys.alloc(nbk * stg.bucket_cap * 4) ||
-            !agg_sums.alloc(nbk * stg.bucket_cap * m * 8))
-          return fail(CCT_ENOMEM, "device allocation failed");
-        HIP_TRY(hipMemsetAsync(agg_count.p, 0, nbk * 4, s));
-        stg.count = agg_count.as<uint32_t>();
-        stg.keys = agg_keys.as<uint32_t>();
-        stg.sums = agg_sums.as<uint64_t>();
-      }
+      cct_status sst = setup_stage(m, t->cap, agg_grid, agg_count, agg_keys, agg_sums, stg, s);
+      if (sst) return sst;
       launch_aggregate(a.slot_of, p->metrics, N, m, delta.as<uint64_t>(), t->cap, agg_grid, stg, s);
       launch_collect_new(t->slot.as<Slot>(), t->cap, p->offsets, new_slots.as<uint32_t>(), dctr,
                          cpart.as<unsigned long long>(), s);
@@ -703,6 +712,7 @@ namespace {
 // on failure.
 cct_status compute_bottom_up(cct_tree *t, hipStream_t s) {
   const int64_t n = t->u - 1;  // nodes other than the root
+  const int64_t U = t->u;
   const int32_t m = t->m;
   unsigned long long *hs = host_scratch();
   if (!hs) return fail(CCT_ENOMEM, "pinned host allocation failed");
@@ -712,12 +722,12 @@ cct_status compute_bottom_up(cct_tree *t, hipStream_t s) {
   }
   const int64_t rb = radix_blocks(n), hist_rows = 256 * rb;
   const int64_t scan_rows = std::max<int64_t>(hist_rows, n);
-  Buf keys, vals, keys_t, vals_t, hist, offs, scan_blk, head, gscan, tag, mx, ms_blk, gstart, rows, S;
+  Buf keys, vals, keys_t, vals_t, hist, offs, scan_blk, head, gscan, tag, mx, ms_blk, gstart, slot_ex, slot_in;
   if (!keys.alloc(n * 4) || !vals.alloc(n * 4) || !keys_t.alloc(n * 4) || !vals_t.alloc(n * 4) ||
-      !hist.alloc(hist_rows * 8) || !offs.alloc((hist_rows + 1) * 8) ||
-      !scan_blk.alloc((scan_rows / 1024 + 2) * 2 * m * 8) || !head.alloc(n * 8) || !gscan.alloc((n + 1) * 8) ||
-      !tag.alloc(n * 8) || !mx.alloc(n * 8) || !ms_blk.alloc((maxscan_blocks(n) + 1) * 8) ||
-      !gstart.alloc((n + 1) * 8) || !rows.alloc(n * 2 * m * 8) || !S.alloc((n + 1) * 2 * m * 8))
+      !hist.alloc(hist_rows * 8) || !offs.alloc((hist_rows + 1) * 8) || !scan_blk.alloc((scan_rows / 1024 + 2) * 8) ||
+      !head.alloc(n * 8) || !gscan.alloc((n + 1) * 8) || !tag.alloc(n * 8) || !mx.alloc(n * 8) ||
+      !ms_blk.alloc((maxscan_blocks(n) + 1) * 8) || !gstart.alloc((n + 1) * 8) || !slot_ex.alloc(U * 4) ||
+      !slot_in.alloc(U * 4))
     return fail(CCT_ENOMEM, "device allocation failed");
   Timer tm;
   tm.mark(0, s);
@@ -730,18 +740,28 @@ cct_status compute_bottom_up(cct_tree *t, hipStream_t s) {
   launch_bu_tag(V, head.as<uint64_t>(), gscan.as<uint64_t>(), t->subend.as<uint32_t>(), n, tag.as<uint64_t>(),
                 gstart.as<int64_t>(), s);
   launch_maxscan(tag.as<uint64_t>(), n, ms_blk.as<uint64_t>(), mx.as<uint64_t>(), s);
-  launch_bu_rows(V, head.as<uint64_t>(), gscan.as<uint64_t>(), mx.as<uint64_t>(), t->excl.as<uint64_t>(),
-                 t->incl.as<uint64_t>(), m, n, rows.as<uint64_t>(), s);
-  launch_scan(rows.as<uint64_t>(), n, 2 * m, scan_blk.as<uint64_t>(), S.as<uint64_t>(), s);
+  launch_bu_slots(V, head.as<uint64_t>(), gscan.as<uint64_t>(), mx.as<uint64_t>(), n, slot_ex.as<uint32_t>(),
+                  slot_in.as<uint32_t>(), s);
   HIP_TRY(hipGetLastError());
   HIP_TRY(hipMemcpyAsync(hs, gscan.as<uint64_t>() + n, 8, hipMemcpyDeviceToHost, s));
   HIP_TRY(hipStreamSynchronize(s));
   const int64_t G = (int64_t)hs[0];
-  Buf f_out, e_out, i_out;
+  // per-group sums: exclusive sums of every node, inclusive sums of the topmost ones
+  Buf f_out, e_out, i_out, cnt_e, keys_e, sums_e, cnt_i, keys_i, sums_i;
+  const int agg_grid = (int)std::max<int64_t>(1, std::min<int64_t>((U + 8191) / 8192, (int64_t)cu_count() * 2));
+  AggStage st_e{}, st_i{};
   if (!f_out.alloc(G * 4) || !e_out.alloc(G * m * 8) || !i_out.alloc(G * m * 8))
     return fail(CCT_ENOMEM, "device allocation failed");
-  launch_bu_out(K, gstart.as<int64_t>(), G, S.as<uint64_t>(), m, f_out.as<uint32_t>(), e_out.as<uint64_t>(),
-                i_out.as<uint64_t>(), s);
+  cct_status st = setup_stage(m, (uint64_t)G, agg_grid, cnt_e, keys_e, sums_e, st_e, s);
+  if (!st) st = setup_stage(m, (uint64_t)G, agg_grid, cnt_i, keys_i, sums_i, st_i, s);
+  if (st) return st;
+  HIP_TRY(hipMemsetAsync(e_out.p, 0, G * m * 8, s));
+  HIP_TRY(hipMemsetAsync(i_out.p, 0, G * m * 8, s));
+  launch_bu_frames(K, gstart.as<int64_t>(), G, f_out.as<uint32_t>(), s);
+  launch_aggregate(slot_ex.as<uint32_t>(), t->excl.as<uint64_t>(), U, m, e_out.as<uint64_t>(), (uint64_t)G, agg_grid,
+                   st_e, s);
+  launch_aggregate(slot_in.as<uint32_t>(), t->incl.as<uint64_t>(), U, m, i_out.as<uint64_t>(), (uint64_t)G, agg_grid,
+                   st_i, s);
   HIP_TRY(hipGetLastError());
   tm.mark(1, s);
   HIP_TRY(hipStreamSynchronize(s));
