@@ -45,6 +45,9 @@ DESCRIPTIONS = {
              "(20% from paths new to the chunk), 4 uint64 metrics (one full-range)",
     "bottom_up": "bottom-up view of the layered_16m tree (4,407,055 nodes, 2 uint64 metrics): per frame, exclusive "
                  "sums and inclusive sums counted once per path",
+    "filter": "ratio filter over the layered_16m tree (4,407,055 nodes, 2 uint64 metrics): nodes whose incl "
+              "metric 0 per unit of incl metric 1 is below the root's ratio (the shape of the kernel-fusion and "
+              "CPU-latency analyses), exact 128-bit products, ids listed in preorder",
     "activity": "8,388,608-event base (as merge) + 8 activity flushes, each a registry of 2,097,152 call paths "
                 "(a merge chunk) under distinct correlation IDs and 2,348,810 records (every ID once, shuffled, "
                 "+10% repeated IDs, +2% unregistered IDs), 4 uint64 metrics",
@@ -134,6 +137,8 @@ def main():
         return bench_activity(args, torch, tracegen, cct, dev)
     if args.workload == "bottom_up":
         return bench_bottom_up(args, torch, tracegen, cct, dev)
+    if args.workload == "filter":
+        return bench_filter(args, torch, tracegen, cct, dev)
     o, f, w = tracegen.generate(args.workload)
     N, F, M = o.size - 1, f.size, w.shape[1]
     log(f"generated {args.workload}: N={N:,} F={F:,} M={M} in {time.perf_counter() - t0:.1f}s")
@@ -381,6 +386,51 @@ def bench_bottom_up(args, torch, tracegen, cct, dev):
                      "bytes_per_launch": b_alg, "avg_launch_ms": ms},
     }
     print(json.dumps(line), flush=True)
+
+def bench_filter(args, torch, tracegen, cct, dev):
+    o, f, w = tracegen.generate("layered_16m")
+    tree = cct.build(torch.from_numpy(o).to(dev), torch.from_numpy(f.view(np.int32)).to(dev),
+                     torch.from_numpy(w.view(np.int64)).to(dev))
+    U, M = tree.n_nodes, w.shape[1]
+    root = tree.to_tensors(device="cpu")["incl"][0].numpy().view(np.uint64)
+    p, q = int(root[0]), max(int(root[1]), 1)  # the root's ratio of metric 0 to metric 1
+    del o, f, w
+    filt_ms, hot_ms, wall_ms = [], [], []
+    K = H = 0
+    for step in range(args.warmup + args.steps):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ids = tree.filter(0, -1, p, q, den="metric", den_metric=1)
+        wall = (time.perf_counter() - t0) * 1000.0
+        K, ms = ids.numel(), cct.last_timings()[7]
+        H = tree.hotspots(0, 1, 1000).numel()  # leaves above 0.1% of the root's metric 0
+        hot = cct.last_timings()[7]
+        del ids
+        if step >= args.warmup:
+            filt_ms.append(ms)
+            hot_ms.append(hot)
+            wall_ms.append(wall)
+        log(f"{'warmup' if step < args.warmup else 'step'} {step}: filter {ms * 1000:.1f} us (call {wall * 1000:.1f} us), "
+            f"K={K:,}; hotspots {hot * 1000:.1f} us, {H:,} leaves")
+    tree.free()
+    ms = float(np.mean(filt_ms))
+    # algorithmic bytes: both sums of every node read once, each match's id written once
+    b_alg = U * 16 + K * 8
+    achieved = b_alg / (ms * 1e-3) / 1e9
+    line = {
+        "metric": METRIC, "value": U / (ms * 1e-3), "unit": "nodes/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "u64", "data": "synthetic",
+        "config": {"workload": f"filter: {DESCRIPTIONS['filter']}", "nodes": U, "metrics": M, "matches": K,
+                   "threshold": [p, q], "call_ms_with_count_readback": float(np.mean(wall_ms)),
+                   "hotspot_ms": float(np.mean(hot_ms)), "hotspot_leaves": H},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                     "kernel": "ratio filter (predicate mask, scan of tile counts, id write)",
+                     "bytes_per_launch": b_alg, "avg_launch_ms": ms},
+    }
+    print(json.dumps(line), flush=True)
+
 
 if __name__ == "__main__":
     main()

@@ -141,6 +141,39 @@ cct_status cct_merge_activity(cct_tree *tree, const cct_paths *registry, const u
 cct_status cct_bottom_up(cct_tree *tree, void *hip_stream, int64_t capacity, uint32_t *frames, uint64_t *excl,
                          uint64_t *incl, int64_t *n_frames);
 
+/* A ratio test on a node's metrics (the paper's example analyses flag nodes whose metric
+ * ratio crosses a threshold: Implementation, "Performance Analyzer", "Example Analyses").
+ * Node v matches when a(v) / b(v) is above (op = +1) or below (op = -1) thr_num / thr_den,
+ * tested without division as a(v) * thr_den > thr_num * b(v) (or <) on exact 128-bit
+ * products; so b(v) = 0 makes an above-test match iff a(v) * thr_den > 0, and a below-test
+ * never match.
+ *   a(v) = (num_excl ? excl : incl)[v][num_metric]
+ *   b(v) = 1 (den_kind 0), (den_excl ? excl : incl)[v][den_metric] (den_kind 1), or the
+ *          root's incl[0][den_metric] (den_kind 2)
+ *   leaves_only  1: only nodes without children can match
+ * Examples: hotspot = incl time above tau of the root's, leaves only; small kernels = incl
+ * GPU time / incl launch count below tau; CPU latency = incl CPU time / incl GPU time above
+ * tau. */
+typedef struct {
+  int32_t num_metric;
+  int32_t num_excl;
+  int32_t den_kind;
+  int32_t den_metric;
+  int32_t den_excl;
+  int32_t op;
+  uint64_t thr_num;
+  uint64_t thr_den;  /* > 0 */
+  int32_t leaves_only;
+} cct_filter_spec;
+
+/* Node ids of `tree` matching `spec`, ascending (preorder).  Writes the first
+ * min(K, capacity) matches to node_ids (DEVICE int64[capacity], written by a kernel; may
+ * be NULL when capacity is 0) and K to *n_matches (HOST); returns after the stream has
+ * finished the call's work.  Metric indices out of range, an unknown
+ * den_kind or op, or thr_den = 0 give CCT_EINVAL. */
+cct_status cct_filter(const cct_tree *tree, const cct_filter_spec *spec, void *hip_stream, int64_t capacity,
+                      int64_t *node_ids, int64_t *n_matches);
+
 /* Look up Q call paths (queries->offsets/frames, metrics ignored) in `tree`.
  * Writes DEVICE arrays: node_ids int64[Q] (the canonical id, or -1 if the path is
  * not a node), and, when non-NULL, excl/incl uint64[Q][M] (zeros for absent paths). */
@@ -172,8 +205,8 @@ const char *cct_last_error(void);
  * ordering (sort, LCP, scans), [3] node emission (parents, exclusive, inclusive), [4]
  * whole merge, [5] the correlation-ID join before the merge (cct_merge_activity only;
  * 0 otherwise), [6] the most recent computation of a bottom-up view by cct_bottom_up
- * (calls that only copy a kept view leave it as it is).  Returns the number of values
- * written (<= n, at most 7). */
+ * (calls that only copy a kept view leave it as it is), [7] the last cct_filter.  Returns
+ * the number of values written (<= n, at most 8). */
 int cct_last_timings(double *ms, int n);
 
 #ifdef __cplusplus

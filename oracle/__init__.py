@@ -267,3 +267,30 @@ def bottom_up(offsets, frames, metrics):
         lib.or_bottom_up_free(h)
     return fr[:K], ex[:K], inc[:K]
 
+
+def filter_nodes(tree, num_metric, op, thr_num, thr_den, num_excl=False, den="one", den_metric=0, den_excl=False,
+                 leaves_only=False):
+    """Node ids whose metric ratio crosses a threshold, ascending (the example analyses
+    flag nodes whose ratio of metrics is above or below a threshold: Implementation,
+    "Performance Analyzer", "Example Analyses").  Reading fixed here: a / b above p / q
+    means a * q > p * b (below: <), in exact integers, so no division; a is the node's
+    incl (or excl) sum of num_metric; b is 1, the node's sum of den_metric, or the root's
+    incl sum of den_metric; leaves_only keeps nodes that are nobody's parent."""
+    parent = tree["parent"]
+    U = parent.size
+    a = [int(x) for x in tree["excl" if num_excl else "incl"][:, num_metric]]
+    if den == "one":
+        b = [1] * U
+    elif den == "metric":
+        b = [int(x) for x in tree["excl" if den_excl else "incl"][:, den_metric]]
+    else:
+        b = [int(tree["incl"][0, den_metric])] * U
+    parents = set(int(p) for p in parent[1:])
+    p, q = int(thr_num), int(thr_den)
+    out = []
+    for v in range(U):
+        lhs, rhs = a[v] * q, p * b[v]
+        if (lhs > rhs if op > 0 else lhs < rhs) and not (leaves_only and v in parents):
+            out.append(v)
+    return np.asarray(out, np.int64)
+

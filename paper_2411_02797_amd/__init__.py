@@ -11,6 +11,7 @@ to load, every call raises; there is no CPU fallback.
     ids, excl, incl = tree.query(q_offsets, q_frames)
     arrays = tree.to_tensors()               # parent, frame, depth, excl, incl on the GPU
     view = tree.bottom_up()                  # frames, excl, incl per distinct frame
+    ids = tree.filter(0, +1, 1, 100, den="root", leaves_only=True)  # hotspots above 1% of the root
 """
 from __future__ import annotations
 
@@ -26,8 +27,9 @@ _lib = None
 
 NO_PARENT = 0xFFFFFFFF
 MAX_METRICS = 8
-EXPORTED_SYMBOLS = ("cct_build", "cct_merge", "cct_merge_activity", "cct_bottom_up", "cct_query", "cct_info",
-                    "cct_export", "cct_free", "cct_release_cached_memory", "cct_last_error", "cct_last_timings")
+EXPORTED_SYMBOLS = ("cct_build", "cct_merge", "cct_merge_activity", "cct_bottom_up", "cct_filter", "cct_query",
+                    "cct_info", "cct_export", "cct_free", "cct_release_cached_memory", "cct_last_error",
+                    "cct_last_timings")
 _STATUS = {0: "CCT_OK", -1: "CCT_EINVAL", -2: "CCT_ENOMEM", -3: "CCT_EDEVICE", -4: "CCT_EMISMATCH",
            -5: "CCT_EOVERFLOW"}
 
@@ -49,6 +51,15 @@ class _Activity(ctypes.Structure):
                 ("metrics", ctypes.c_void_p)]
 
 
+class _FilterSpec(ctypes.Structure):
+    _fields_ = [("num_metric", ctypes.c_int32), ("num_excl", ctypes.c_int32), ("den_kind", ctypes.c_int32),
+                ("den_metric", ctypes.c_int32), ("den_excl", ctypes.c_int32), ("op", ctypes.c_int32),
+                ("thr_num", ctypes.c_uint64), ("thr_den", ctypes.c_uint64), ("leaves_only", ctypes.c_int32)]
+
+
+_DEN_KINDS = {"one": 0, "metric": 1, "root": 2}
+
+
 def library_path():
     return _LIB_PATH
 
@@ -67,6 +78,7 @@ def load_library():
     lib.cct_merge.argtypes = [vp, P(_Paths), vp]
     lib.cct_merge_activity.argtypes = [vp, P(_Paths), vp, P(_Activity), vp, P(i64)]
     lib.cct_bottom_up.argtypes = [vp, vp, i64, vp, vp, vp, P(i64)]
+    lib.cct_filter.argtypes = [vp, P(_FilterSpec), vp, i64, vp, P(i64)]
     lib.cct_query.argtypes = [vp, P(_Paths), vp, vp, vp, vp]
     lib.cct_info.argtypes = [vp, P(i64), P(i32), P(i64)]
     lib.cct_export.argtypes = [vp, vp, vp, vp, vp, vp, vp]
@@ -76,8 +88,8 @@ def load_library():
     lib.cct_release_cached_memory.restype = None
     lib.cct_last_error.restype = ctypes.c_char_p
     lib.cct_last_timings.argtypes = [P(ctypes.c_double), ctypes.c_int]
-    for name in ("cct_build", "cct_merge", "cct_merge_activity", "cct_bottom_up", "cct_query", "cct_info",
-                 "cct_export"):
+    for name in ("cct_build", "cct_merge", "cct_merge_activity", "cct_bottom_up", "cct_filter", "cct_query",
+                 "cct_info", "cct_export"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -210,6 +222,36 @@ class Tree:
                                      out["incl"].data_ptr(), ctypes.byref(k)))
         return out
 
+    def filter(self, num_metric, op, thr_num, thr_den, num_excl=False, den="one", den_metric=0, den_excl=False,
+               leaves_only=False):
+        """Node ids matching a ratio test (cct_filter), ascending, as an int64 device
+        tensor: a / b above (op=+1) or below (op=-1) thr_num / thr_den, with a the node's
+        incl (or excl) sum of num_metric and b = 1 (den="one"), the node's sum of den_metric
+        (den="metric") or the root's incl sum of den_metric (den="root")."""
+        import torch
+        spec = _FilterSpec(num_metric, int(bool(num_excl)), _DEN_KINDS[den], den_metric, int(bool(den_excl)), op,
+                           thr_num, thr_den, int(bool(leaves_only)))
+        u = self.n_nodes
+        out = torch.empty(max(u, 1), dtype=torch.int64, device=torch.device("cuda", torch.cuda.current_device()))
+        k = ctypes.c_int64(0)
+        _check(load_library().cct_filter(self._h, ctypes.byref(spec), _stream(), u, out.data_ptr(), ctypes.byref(k)))
+        return out[:k.value]
+
+    def hotspots(self, time_metric, thr_num, thr_den):
+        """Leaves whose inclusive time is above thr_num / thr_den of the root's (the paper's
+        hotspot identification)."""
+        return self.filter(time_metric, +1, thr_num, thr_den, den="root", den_metric=time_metric, leaves_only=True)
+
+    def small_kernels(self, time_metric, count_metric, thr_num, thr_den):
+        """Nodes whose inclusive time per launch is below thr_num / thr_den (the paper's
+        kernel fusion analysis)."""
+        return self.filter(time_metric, -1, thr_num, thr_den, den="metric", den_metric=count_metric)
+
+    def cpu_latency(self, cpu_metric, gpu_metric, thr_num, thr_den):
+        """Nodes whose inclusive CPU time is above thr_num / thr_den of their GPU time (the
+        paper's CPU latency analysis)."""
+        return self.filter(cpu_metric, +1, thr_num, thr_den, den="metric", den_metric=gpu_metric)
+
     def to_tensors(self, device=None):
         """Canonical arrays as tensors: parent/frame/depth int32[U] (bit patterns of
         uint32), excl/incl int64[U, M] (bit patterns of uint64)."""
@@ -253,10 +295,10 @@ def build(offsets, frames, metrics):
 def last_timings():
     """Per-phase HIP-event times (ms) of this thread's last calls: ingest, publish, sort,
     canonical emission and total of the last build/merge, the correlation-ID join of a
-    merge_activity call (0 otherwise), and the most recent computation of a bottom-up
-    view (bottom_up)."""
-    buf = (ctypes.c_double * 7)()
-    n = load_library().cct_last_timings(buf, 7)
+    merge_activity call (0 otherwise), the most recent computation of a bottom-up view
+    (bottom_up), and the last filter."""
+    buf = (ctypes.c_double * 8)()
+    n = load_library().cct_last_timings(buf, 8)
     return list(buf)[:n]
 
 

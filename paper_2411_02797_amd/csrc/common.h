@@ -336,4 +336,27 @@ void launch_bu_slots(const uint32_t *V, const uint64_t *head, const uint64_t *gs
                      uint32_t *slot_ex, uint32_t *slot_in, hipStream_t s);
 void launch_bu_frames(const uint32_t *K, const int64_t *gstart, int64_t G, uint32_t *frames, hipStream_t s);
 
+// Ratio filters over the tree's nodes (filter.hip)
+enum : int32_t { kDenOne = 0, kDenMetric = 1, kDenRoot = 2 };
+struct FilterArgs {
+  int64_t u;
+  int32_t m;
+  const uint64_t *excl, *incl;  // [U][m]
+  const uint32_t *subend;       // [U]
+  int32_t num_metric, num_excl;
+  int32_t den_kind, den_metric, den_excl;
+  int32_t op;                   // +1: ratio above the threshold, -1: below
+  uint64_t thr_num, thr_den;
+  int32_t leaves_only;
+};
+constexpr int kFilterTile = 2048;  // nodes per tile of the two passes
+int64_t filter_tiles(int64_t u);
+// mask [filter_tiles(U) * kFilterTile / 64] (bit per node), count [filter_tiles(U)]
+void launch_filter_mask(const FilterArgs &a, uint64_t *mask, uint32_t *count, hipStream_t s);
+// pos [tiles + 1]: exclusive scan of count, pos[tiles] = all matches
+void launch_filter_scan(const uint32_t *count, int64_t tiles, uint64_t *pos, hipStream_t s);
+// writes the first `capacity` matches to out
+void launch_filter_write(int64_t u, const uint64_t *mask, const uint64_t *pos, int64_t capacity, int64_t *out,
+                         hipStream_t s);
+
 }  // namespace cct

@@ -24,6 +24,7 @@ thread_local std::string g_error;
 thread_local double g_timings[5] = {0, 0, 0, 0, 0};
 thread_local double g_join_ms = 0;  // correlation-ID join of the last cct_merge_activity
 thread_local double g_view_ms = 0;  // the most recent computation of a bottom-up view
+thread_local double g_filter_ms = 0;  // the last cct_filter
 thread_local int g_alloc_countdown = 0;  // test hook: >0 makes the n-th allocation of a call fail
 
 int64_t env_int(const char *name, int64_t dflt) {
@@ -801,6 +802,50 @@ cct_status cct_bottom_up(cct_tree *tree, void *hip_stream, int64_t capacity, uin
   return CCT_OK;
 }
 
+cct_status cct_filter(const cct_tree *tree, const cct_filter_spec *spec, void *hip_stream, int64_t capacity,
+                      int64_t *node_ids, int64_t *n_matches) {
+  AllocHook hook;
+  g_error.clear();
+  if (!tree || !spec || !n_matches) return fail(CCT_EINVAL, "NULL argument");
+  if (capacity < 0 || (capacity > 0 && !node_ids)) return fail(CCT_EINVAL, "bad output capacity");
+  const int32_t m = tree->m;
+  if (spec->num_metric < 0 || spec->num_metric >= m) return fail(CCT_EINVAL, "num_metric out of range");
+  if (spec->den_kind < kDenOne || spec->den_kind > kDenRoot) return fail(CCT_EINVAL, "unknown den_kind");
+  if (spec->den_kind != kDenOne && (spec->den_metric < 0 || spec->den_metric >= m))
+    return fail(CCT_EINVAL, "den_metric out of range");
+  if (spec->op != 1 && spec->op != -1) return fail(CCT_EINVAL, "op must be +1 or -1");
+  if (spec->thr_den == 0) return fail(CCT_EINVAL, "thr_den is 0");
+  int dev = 0;
+  (void)hipGetDevice(&dev);
+  if (dev != tree->device) return fail(CCT_EINVAL, "tree belongs to another device");
+  hipStream_t s = (hipStream_t)hip_stream;
+  unsigned long long *hs = host_scratch();
+  if (!hs) return fail(CCT_ENOMEM, "pinned host allocation failed");
+  const int64_t U = tree->u;
+  const int64_t T = filter_tiles(U);
+  Buf mask, count, pos;
+  if (!mask.alloc(T * (kFilterTile / 64) * 8) || !count.alloc(T * 4) || !pos.alloc((T + 1) * 8))
+    return fail(CCT_ENOMEM, "device allocation failed");
+  FilterArgs a{};
+  a.u = U; a.m = m; a.excl = tree->excl.as<uint64_t>(); a.incl = tree->incl.as<uint64_t>();
+  a.subend = tree->subend.as<uint32_t>();
+  a.num_metric = spec->num_metric; a.num_excl = spec->num_excl != 0;
+  a.den_kind = spec->den_kind; a.den_metric = spec->den_metric; a.den_excl = spec->den_excl != 0;
+  a.op = spec->op; a.thr_num = spec->thr_num; a.thr_den = spec->thr_den; a.leaves_only = spec->leaves_only != 0;
+  Timer tm;
+  tm.mark(0, s);
+  launch_filter_mask(a, mask.as<uint64_t>(), count.as<uint32_t>(), s);
+  launch_filter_scan(count.as<uint32_t>(), T, pos.as<uint64_t>(), s);
+  launch_filter_write(U, mask.as<uint64_t>(), pos.as<uint64_t>(), capacity, node_ids, s);
+  tm.mark(1, s);
+  HIP_TRY(hipGetLastError());
+  HIP_TRY(hipMemcpyAsync(hs, pos.as<uint64_t>() + T, 8, hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  g_filter_ms = tm.ok ? tm.span(0, 1) : 0.0;
+  *n_matches = (int64_t)hs[0];
+  return CCT_OK;
+}
+
 cct_status cct_query(const cct_tree *tree, const cct_paths *q, void *hip_stream, int64_t *node_ids, uint64_t *excl,
                      uint64_t *incl) {
   g_error.clear();
@@ -876,10 +921,11 @@ const char *cct_last_error(void) { return g_error.c_str(); }
 
 int cct_last_timings(double *ms, int n) {
   if (!ms || n <= 0) return 0;
-  const int k = n < 7 ? n : 7;
+  const int k = n < 8 ? n : 8;
   for (int i = 0; i < k && i < 5; ++i) ms[i] = g_timings[i];
   if (k > 5) ms[5] = g_join_ms;
   if (k > 6) ms[6] = g_view_ms;
+  if (k > 7) ms[7] = g_filter_ms;
   return k;
 }
 

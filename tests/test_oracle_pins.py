@@ -397,3 +397,42 @@ def test_bottom_up_exclusive_total():
     fr, ex, inc = oracle.bottom_up(o, f, w)
     nonempty = np.diff(o) > 0
     assert np.array_equal(ex.sum(axis=0, dtype=np.uint64), w[nonempty].sum(axis=0, dtype=np.uint64))
+
+
+# ---- ratio filters --------------------------------------------------------------------
+# The hand-worked tree of the join pin: ids () (5) (5,7) (5,9) (5,9,2), inclusive
+# 22 20 4 16 16; leaves are (5,7) and (5,9,2).  Above half of the root: 22/22, 20/22,
+# 16/22, 16/22 -> nodes 0 1 3 4; among leaves only node 4 (4/22 is below).  A ratio equal
+# to the threshold matches neither way: 11/22 against 1/2.
+def test_filter_hand_worked():
+    t = oracle.build_tree([0, 3, 5, 8, 8], [5, 9, 2, 5, 7, 5, 9, 2], [[10], [4], [6], [2]])
+    assert oracle.filter_nodes(t, 0, +1, 1, 2, den="root").tolist() == [0, 1, 3, 4]
+    assert oracle.filter_nodes(t, 0, +1, 1, 2, den="root", leaves_only=True).tolist() == [4]
+    assert oracle.filter_nodes(t, 0, -1, 1, 2, den="root").tolist() == [2]
+    assert oracle.filter_nodes(t, 0, +1, 16, 1).tolist() == [0, 1]        # incl > 16
+    assert oracle.filter_nodes(t, 0, +1, 2, 1, num_excl=True).tolist() == [2, 4]  # excl > 2 (root's is 2)
+
+
+def test_filter_matches_fractions():
+    # an independent evaluation with fractions.Fraction for non-zero denominators, and
+    # the cross-multiplied reading for zero ones (above: a > 0; below: never)
+    from fractions import Fraction
+    o, f, w = tracegen.random_paths(400, 15, 10, 3, seed=4)
+    w[::7, 2] = 0  # zero denominators
+    t = oracle.build_tree(o, f, w)
+    parents = set(t["parent"][1:].tolist())
+    for op in (+1, -1):
+        for p, q in ((1, 3), (7, 2), (0, 1)):
+            got = oracle.filter_nodes(t, 0, op, p, q, den="metric", den_metric=2).tolist()
+            want = []
+            for v in range(t["parent"].size):
+                a, b = int(t["incl"][v, 0]), int(t["incl"][v, 2])
+                if b == 0:
+                    hit = op > 0 and a * q > 0
+                else:
+                    hit = Fraction(a, b) > Fraction(p, q) if op > 0 else Fraction(a, b) < Fraction(p, q)
+                if hit:
+                    want.append(v)
+            assert got == want
+    leaves = oracle.filter_nodes(t, 0, +1, 0, 1, leaves_only=True).tolist()
+    assert leaves == [v for v in range(t["parent"].size) if v not in parents and int(t["incl"][v, 0]) > 0]
