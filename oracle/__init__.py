@@ -52,6 +52,9 @@ def _load():
         vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
         lib.or_create.restype = vp
         lib.or_create.argtypes = [i32]
+        lib.or_create_stats.restype = vp
+        lib.or_create_stats.argtypes = [i32]
+        lib.or_stats_export.argtypes = [vp, vp, vp, vp, vp, vp, vp]
         lib.or_destroy.argtypes = [vp]
         lib.or_destroy.restype = None
         lib.or_ingest.argtypes = [vp, i64, vp, vp, vp]
@@ -98,9 +101,10 @@ class Tree(dict):
 class Oracle:
     """Incremental std::map trie: ``ingest`` any number of CSR batches, then ``tree``."""
 
-    def __init__(self, n_metrics):
+    def __init__(self, n_metrics, stats=False):
         self.m = int(n_metrics)
-        self._h = _load().or_create(self.m)
+        self.stats = bool(stats)
+        self._h = (_load().or_create_stats if self.stats else _load().or_create)(self.m)
         if not self._h:
             raise ValueError("bad metric count")
 
@@ -117,6 +121,15 @@ class Oracle:
         t = Tree(parent=np.empty(U, np.uint32), frame=np.empty(U, np.uint32), depth=np.empty(U, np.uint32),
                  excl=np.empty((U, self.m), np.uint64), incl=np.empty((U, self.m), np.uint64))
         lib.or_export(self._h, _p(t["parent"]), _p(t["frame"]), _p(t["depth"]), _p(t["excl"]), _p(t["incl"]))
+        if self.stats:
+            for k in ("count_excl", "count_incl"):
+                t[k] = np.empty(U, np.uint64)
+            for k in ("min_excl", "min_incl"):
+                t[k] = np.empty((U, self.m), np.uint64)
+            for k in ("sumsq_excl", "sumsq_incl"):
+                t[k] = np.empty((U, self.m, 2), np.uint64)
+            lib.or_stats_export(self._h, *(_p(t[k]) for k in ("count_excl", "count_incl", "min_excl", "min_incl",
+                                                               "sumsq_excl", "sumsq_incl")))
         return t
 
     def close(self):
@@ -131,10 +144,10 @@ class Oracle:
             pass
 
 
-def build_tree(offsets, frames, metrics) -> Tree:
-    """One-shot oracle tree of a CSR trace."""
+def build_tree(offsets, frames, metrics, stats=False) -> Tree:
+    """One-shot oracle tree of a CSR trace (with per-node statistics if ``stats``)."""
     o, f, w = _csr(offsets, frames, metrics)
-    orc = Oracle(w.shape[1])
+    orc = Oracle(w.shape[1], stats=stats)
     try:
         orc.ingest(o, f, w)
         return orc.tree()
@@ -294,3 +307,40 @@ def filter_nodes(tree, num_metric, op, thr_num, thr_den, num_excl=False, den="on
             out.append(v)
     return np.asarray(out, np.int64)
 
+
+def derived_stats(tree, nodes=None):
+    """Mean and standard deviation of every metric at the given nodes (all by default),
+    exclusive and inclusive, from a statistics tree (``build_tree(..., stats=True)``).
+
+    The paper keeps sum, minimum, average and standard deviation per node metric
+    (Design, "Profiler", "Calling Context Tree").  Readings fixed here: the average is
+    sum / count over the node's samples (the events ending at the node, or passing
+    through it); the standard deviation is the population one, sqrt(n * S2 - S1^2) / n
+    with S1 the node's sum (modulo 2^64, as the tree keeps it) and S2 its sum of squares
+    (modulo 2^128); both are NaN where the count is 0, and the deviation is NaN where
+    n * S2 - S1^2 is negative (possible only when a sum wrapped).  Each value is the
+    exact quantity rounded once to float64 (Fraction for the mean, 60-digit Decimal
+    square root for the deviation)."""
+    from decimal import Context
+    from fractions import Fraction
+    ctx = Context(prec=60)
+    U, m = tree["parent"].size, tree["excl"].shape[1]
+    idx = np.arange(U) if nodes is None else np.asarray(nodes, np.int64)
+    out = {}
+    for side in ("excl", "incl"):
+        mean = np.full((idx.size, m), np.nan)
+        std = np.full((idx.size, m), np.nan)
+        for r, v in enumerate(idx):
+            n = int(tree["count_" + side][v])
+            if n == 0:
+                continue
+            for j in range(m):
+                s1 = int(tree[side][v, j])
+                lo, hi = (int(x) for x in tree["sumsq_" + side][v, j])
+                s2 = lo | (hi << 64)
+                mean[r, j] = float(Fraction(s1, n))
+                d = n * s2 - s1 * s1
+                if d >= 0:
+                    std[r, j] = float(ctx.divide(ctx.sqrt(ctx.create_decimal(d)), ctx.create_decimal(n)))
+        out["mean_" + side], out["std_" + side] = mean, std
+    return out

@@ -12,6 +12,13 @@
 // and node ids are the rank of a node's root path in unsigned lexicographic order
 // (a proper prefix first), i.e. preorder with children visited by ascending frame.
 //
+// Optionally (or_create_stats) each node also keeps the other aggregates the paper
+// names for a node's metrics (same paragraph: sum, minimum, average and standard
+// deviation), updated by every event on every node of its path, the root included
+// (inclusive), and at the path's end node (exclusive): the sample count, the minimum
+// and the sum of squares (exact modulo 2^128).  The mean and the standard deviation are
+// derived from these integers by the Python side.
+//
 // Parity of every function here is pinned by tests against hand-worked trees,
 // brute-force prefix enumeration, closed forms and invariants; the paper itself prints
 // no tree values, so nothing here is pinned to a printed number.
@@ -40,12 +47,39 @@ struct Trie {
   // canonical arrays after finalize()
   std::vector<uint32_t> parent, frame, depth;
   std::vector<uint64_t> c_excl, c_incl;
+  // statistics (when `stats`), indexed like excl: [node] counts, [node][m] minima and
+  // sums of squares; c_* in canonical order after finalize()
+  bool stats = false;
+  std::vector<uint64_t> ex_cnt, in_cnt, ex_min, in_min;
+  std::vector<unsigned __int128> ex_sq, in_sq;
+  std::vector<uint64_t> c_ex_cnt, c_in_cnt, c_ex_min, c_in_min;
+  std::vector<unsigned __int128> c_ex_sq, c_in_sq;
 
-  explicit Trie(int32_t m_) : m(m_), nodes(1), excl(m_, 0) {}
+  explicit Trie(int32_t m_, bool with_stats = false) : m(m_), nodes(1), excl(m_, 0), stats(with_stats) {
+    if (stats) add_stat_rows();
+  }
+
+  void add_stat_rows() {
+    ex_cnt.push_back(0); in_cnt.push_back(0);
+    ex_min.insert(ex_min.end(), m, UINT64_MAX); in_min.insert(in_min.end(), m, UINT64_MAX);
+    ex_sq.insert(ex_sq.end(), m, 0); in_sq.insert(in_sq.end(), m, 0);
+  }
+
+  // one sample per metric at node v: count, minimum, sum of squares
+  static void sample(uint64_t &cnt, uint64_t *mn, unsigned __int128 *sq, const uint64_t *w, int32_t m) {
+    ++cnt;
+    for (int32_t j = 0; j < m; ++j) {
+      const uint64_t x = w ? w[j] : 0;
+      mn[j] = std::min(mn[j], x);
+      sq[j] += (unsigned __int128)x * x;  // wraps mod 2^128
+    }
+  }
 
   // Insert one call path and add its metrics at the node it ends on.
+  // With statistics, the event is a sample of every node on its path, the root included.
   void insert(const uint32_t *path, int64_t len, const uint64_t *w) {
     uint32_t v = 0;
+    if (stats) sample(in_cnt[0], &in_min[0], &in_sq[0], w, m);
     for (int64_t k = 0; k < len; ++k) {
       auto it = nodes[v].kids.find(path[k]);
       if (it == nodes[v].kids.end()) {
@@ -53,12 +87,15 @@ struct Trie {
         nodes[v].kids.emplace(path[k], c);
         nodes.emplace_back();
         excl.insert(excl.end(), m, 0);
+        if (stats) add_stat_rows();
         v = c;
       } else {
         v = it->second;
       }
+      if (stats) sample(in_cnt[v], &in_min[(size_t)v * m], &in_sq[(size_t)v * m], w, m);
     }
     for (int32_t j = 0; j < m; ++j) excl[(size_t)v * m + j] += w ? w[j] : 0;  // wraps mod 2^64
+    if (stats) sample(ex_cnt[v], &ex_min[(size_t)v * m], &ex_sq[(size_t)v * m], w, m);
   }
 
   // Number the nodes in preorder with children in ascending frame order (std::map
@@ -69,6 +106,10 @@ struct Trie {
     parent.assign(U, 0); frame.assign(U, 0); depth.assign(U, 0);
     c_excl.assign(U * m, 0); c_incl.assign(U * m, 0);
     std::vector<uint32_t> id_of(U);
+    if (stats) {
+      c_ex_cnt.assign(U, 0); c_in_cnt.assign(U, 0);
+      c_ex_min.assign(U * m, 0); c_in_min.assign(U * m, 0); c_ex_sq.assign(U * m, 0); c_in_sq.assign(U * m, 0);
+    }
     struct Item { uint32_t node, parent_id, frame, depth; };
     std::vector<Item> stack{{0, kNoParent, 0, 0}};
     uint32_t next = 0;
@@ -79,6 +120,13 @@ struct Trie {
       id_of[it.node] = id;
       parent[id] = it.parent_id; frame[id] = it.frame; depth[id] = it.depth;
       for (int32_t j = 0; j < m; ++j) c_excl[(size_t)id * m + j] = excl[(size_t)it.node * m + j];
+      if (stats) {
+        c_ex_cnt[id] = ex_cnt[it.node]; c_in_cnt[id] = in_cnt[it.node];
+        for (int32_t j = 0; j < m; ++j) {
+          const size_t a = (size_t)id * m + j, b = (size_t)it.node * m + j;
+          c_ex_min[a] = ex_min[b]; c_in_min[a] = in_min[b]; c_ex_sq[a] = ex_sq[b]; c_in_sq[a] = in_sq[b];
+        }
+      }
       // push children in descending frame order so the smallest is visited first
       const auto &kids = nodes[it.node].kids;
       for (auto r = kids.rbegin(); r != kids.rend(); ++r) stack.push_back({r->second, id, r->first, it.depth + 1});
@@ -106,6 +154,11 @@ void *or_create(int32_t n_metrics) {
   if (n_metrics < 1 || n_metrics > 64) return nullptr;
   return new Trie(n_metrics);
 }
+// The same, keeping per-node statistics (count, minimum, sum of squares).
+void *or_create_stats(int32_t n_metrics) {
+  if (n_metrics < 1 || n_metrics > 64) return nullptr;
+  return new Trie(n_metrics, true);
+}
 void or_destroy(void *h) { delete static_cast<Trie *>(h); }
 
 // Insert events [0, n) of one CSR batch.  Returns 0, or -1 on malformed offsets.
@@ -129,6 +182,25 @@ int or_export(void *h, uint32_t *parent, uint32_t *frame, uint32_t *depth, uint6
   if (depth) std::memcpy(depth, t->depth.data(), U * 4);
   if (excl) std::memcpy(excl, t->c_excl.data(), U * t->m * 8);
   if (incl) std::memcpy(incl, t->c_incl.data(), U * t->m * 8);
+  return 0;
+}
+
+// Statistics in canonical order after or_finalize (any pointer may be NULL): counts
+// [U], minima [U][M] (UINT64_MAX where the count is 0), sums of squares [U][M][2]
+// (low word first).  Returns -1 if the oracle keeps no statistics.
+int or_stats_export(void *h, uint64_t *ex_cnt, uint64_t *in_cnt, uint64_t *ex_min, uint64_t *in_min,
+                    uint64_t *ex_sq, uint64_t *in_sq) {
+  Trie *t = static_cast<Trie *>(h);
+  if (!t->stats) return -1;
+  const size_t U = t->parent.size(), um = U * t->m;
+  if (ex_cnt) std::memcpy(ex_cnt, t->c_ex_cnt.data(), U * 8);
+  if (in_cnt) std::memcpy(in_cnt, t->c_in_cnt.data(), U * 8);
+  if (ex_min) std::memcpy(ex_min, t->c_ex_min.data(), um * 8);
+  if (in_min) std::memcpy(in_min, t->c_in_min.data(), um * 8);
+  for (size_t i = 0; i < um; ++i) {
+    if (ex_sq) { ex_sq[2 * i] = (uint64_t)t->c_ex_sq[i]; ex_sq[2 * i + 1] = (uint64_t)(t->c_ex_sq[i] >> 64); }
+    if (in_sq) { in_sq[2 * i] = (uint64_t)t->c_in_sq[i]; in_sq[2 * i + 1] = (uint64_t)(t->c_in_sq[i] >> 64); }
+  }
   return 0;
 }
 

@@ -6,6 +6,8 @@ enumeration in two independent implementations (C++ std::set and pure Python tup
 sorting), closed forms for special shapes, algebraic laws, and an invariant checker
 that is itself shown to catch planted mistakes.
 """
+import math
+
 import numpy as np
 import pytest
 
@@ -436,3 +438,120 @@ def test_filter_matches_fractions():
             assert got == want
     leaves = oracle.filter_nodes(t, 0, +1, 0, 1, leaves_only=True).tolist()
     assert leaves == [v for v in range(t["parent"].size) if v not in parents and int(t["incl"][v, 0]) > 0]
+
+
+# ---- per-node statistics (count, minimum, sum of squares; mean and deviation) -------------
+STAT_KEYS = ("count_excl", "count_incl", "min_excl", "min_incl", "sumsq_excl", "sumsq_incl")
+U64_MAX = 2**64 - 1
+
+
+def py_stats_brute(o, f, w):
+    """Every prefix of every event as a node (ids: sorted prefixes, which is the
+    canonical order), with the list of samples each node receives: excl from the events
+    that end there, incl from the events that pass through it."""
+    n, m = len(o) - 1, w.shape[1]
+    paths = [tuple(int(x) for x in f[o[i]:o[i + 1]]) for i in range(n)]
+    prefixes = sorted({p[:k] for p in paths for k in range(len(p) + 1)} | {()})
+    ex = {p: [] for p in prefixes}
+    inc = {p: [] for p in prefixes}
+    for i, p in enumerate(paths):
+        row = [int(x) for x in w[i]]
+        ex[p].append(row)
+        for k in range(len(p) + 1):
+            inc[p[:k]].append(row)
+    return prefixes, ex, inc, m
+
+
+def assert_stats_match_brute(t, o, f, w):
+    prefixes, ex, inc, m = py_stats_brute(o, f, w)
+    assert t["parent"].size == len(prefixes)
+    for v, p in enumerate(prefixes):
+        for side, samples in (("excl", ex[p]), ("incl", inc[p])):
+            assert int(t["count_" + side][v]) == len(samples)
+            for j in range(m):
+                xs = [r[j] for r in samples]
+                assert int(t["min_" + side][v, j]) == (min(xs) if xs else U64_MAX)
+                lo, hi = (int(x) for x in t["sumsq_" + side][v, j])
+                assert lo | (hi << 64) == sum(x * x for x in xs) % 2**128
+
+
+# Events (5,7) w=(3,1), (5) w=(5,2), () w=(4,0): nodes () (5) (5,7).  Metric 0 through the
+# root: samples 3, 5, 4 -> count 3, min 3, sum of squares 50, mean 4, population deviation
+# sqrt(2/3); through (5): 3, 5 -> mean 4, deviation 1; metric 1 through (5): 1, 2 -> mean
+# 1.5, deviation 0.5.  Exclusive: one sample at each node, deviation 0.
+def test_stats_hand_worked():
+    t = oracle.build_tree([0, 2, 3, 3], [5, 7, 5], [[3, 1], [5, 2], [4, 0]], stats=True)
+    assert t["count_excl"].tolist() == [1, 1, 1] and t["count_incl"].tolist() == [3, 2, 1]
+    assert t["min_incl"].tolist() == [[3, 0], [3, 1], [3, 1]]
+    assert t["min_excl"].tolist() == [[4, 0], [5, 2], [3, 1]]
+    assert t["sumsq_incl"][:, :, 0].tolist() == [[50, 5], [34, 5], [9, 1]]
+    assert not t["sumsq_incl"][:, :, 1].any()
+    d = oracle.derived_stats(t)
+    assert d["mean_incl"].tolist() == [[4.0, 1.0], [4.0, 1.5], [3.0, 1.0]]
+    assert d["std_incl"][0, 0] == math.sqrt(2 / 3) and d["std_incl"][1].tolist() == [1.0, 0.5]
+    assert not d["std_excl"].any()
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_stats_match_brute_force_and_statistics(seed):
+    # small alphabets make paths share prefixes; values below 2^20 never wrap
+    import statistics
+    from fractions import Fraction
+    o, f, w = tracegen.random_paths(120, 4 + seed, 6, 2, seed=300 + seed)
+    w %= np.uint64(1 << 20)
+    t = oracle.build_tree(o, f, w, stats=True)
+    assert_stats_match_brute(t, o, f, w)
+    prefixes, ex, inc, m = py_stats_brute(o, f, w)
+    d = oracle.derived_stats(t)
+    for v, p in enumerate(prefixes):
+        for side, samples in (("excl", ex[p]), ("incl", inc[p])):
+            for j in range(m):
+                xs = [r[j] for r in samples]
+                got_mean, got_std = d["mean_" + side][v, j], d["std_" + side][v, j]
+                if not xs:
+                    assert math.isnan(got_mean) and math.isnan(got_std)
+                    continue
+                assert got_mean == float(Fraction(sum(xs), len(xs)))
+                want = statistics.pstdev(xs)
+                assert abs(got_std - want) <= 2 * math.ulp(want)
+
+
+def test_stats_wrap_and_extremes():
+    # values near 2^64: squares wrap modulo 2^128, minima stay exact
+    o, f, w = tracegen.random_paths(200, 5, 5, 2, seed=17)
+    rng = np.random.default_rng(5)
+    w = rng.integers(2**63, 2**64, size=w.shape, dtype=np.uint64)
+    w[::11] = 0
+    t = oracle.build_tree(o, f, w, stats=True)
+    assert_stats_match_brute(t, o, f, w)
+
+
+def test_stats_incremental_equals_one_shot():
+    o, f, w = tracegen.random_paths(700, 20, 12, 3, seed=41)
+    one = oracle.build_tree(o, f, w, stats=True)
+    orc = oracle.Oracle(3, stats=True)
+    for a, b in ((0, 250), (250, 251), (251, 700)):
+        orc.ingest(*_subset(o, f, w, np.arange(a, b)))
+    inc = orc.tree()
+    orc.close()
+    for k in STAT_KEYS + ("excl", "incl"):
+        assert np.array_equal(one[k], inc[k]), k
+
+
+@pytest.mark.parametrize("k", [1, 2, 7, 40])
+def test_stats_closed_form_repeated_path(k):
+    # one path of 4 frames taken k times with values 1..k: every node on it sees all k
+    # samples (count k, min 1, mean (k+1)/2, deviation sqrt((k^2-1)/12)); only the end node
+    # holds them exclusively
+    o = np.arange(k + 1, dtype=np.int64) * 4
+    f = np.tile(np.array([9, 3, 3, 1], np.uint32), k)
+    w = np.arange(1, k + 1, dtype=np.uint64)[:, None]
+    t = oracle.build_tree(o, f, w, stats=True)
+    d = oracle.derived_stats(t)
+    assert t["count_incl"].tolist() == [k] * 5 and t["count_excl"].tolist() == [0] * 4 + [k]
+    assert t["min_incl"][:, 0].tolist() == [1] * 5 and t["min_excl"][:4, 0].tolist() == [U64_MAX] * 4
+    assert int(t["sumsq_incl"][0, 0, 0]) == k * (k + 1) * (2 * k + 1) // 6
+    assert d["mean_incl"][:, 0].tolist() == [(k + 1) / 2] * 5
+    want = math.sqrt((k * k - 1) / 12)
+    assert all(abs(x - want) <= 2 * math.ulp(max(want, 1e-300)) for x in d["std_incl"][:, 0])
+    assert np.isnan(d["mean_excl"][:4]).all() and d["std_excl"][4, 0] == d["std_incl"][4, 0]
