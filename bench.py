@@ -48,6 +48,9 @@ DESCRIPTIONS = {
     "filter": "ratio filter over the layered_16m tree (4,407,055 nodes, 2 uint64 metrics): nodes whose incl "
               "metric 0 per unit of incl metric 1 is below the root's ratio (the shape of the kernel-fusion and "
               "CPU-latency analyses), exact 128-bit products, ids listed in preorder",
+    "stats": "layered_16m built with per-node statistics (16,777,216 events, 2 uint64 metrics): sample counts, "
+             "minima and sums of squares kept per path, then every node's exclusive and inclusive count, min, sum of "
+             "squares, mean and population deviation",
     "activity": "8,388,608-event base (as merge) + 8 activity flushes, each a registry of 2,097,152 call paths "
                 "(a merge chunk) under distinct correlation IDs and 2,348,810 records (every ID once, shuffled, "
                 "+10% repeated IDs, +2% unregistered IDs), 4 uint64 metrics",
@@ -139,6 +142,8 @@ def main():
         return bench_bottom_up(args, torch, tracegen, cct, dev)
     if args.workload == "filter":
         return bench_filter(args, torch, tracegen, cct, dev)
+    if args.workload == "stats":
+        return bench_stats(args, torch, tracegen, cct, dev)
     o, f, w = tracegen.generate(args.workload)
     N, F, M = o.size - 1, f.size, w.shape[1]
     log(f"generated {args.workload}: N={N:,} F={F:,} M={M} in {time.perf_counter() - t0:.1f}s")
@@ -428,6 +433,53 @@ def bench_filter(args, torch, tracegen, cct, dev):
                      "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
                      "kernel": "ratio filter (predicate mask, scan of tile counts, id write)",
                      "bytes_per_launch": b_alg, "avg_launch_ms": ms},
+    }
+    print(json.dumps(line), flush=True)
+
+
+def bench_stats(args, torch, tracegen, cct, dev):
+    o, f, w = tracegen.generate("layered_16m")
+    N, F, M = o.size - 1, f.size, w.shape[1]
+    to = torch.from_numpy(o).to(dev)
+    tf = torch.from_numpy(f.view(np.int32)).to(dev)
+    tw = torch.from_numpy(w.view(np.int64)).to(dev)
+    del o, f, w
+    build_ms, kept_ms, node_ms, plain_ms = [], [], [], []
+    U = 0
+    for step in range(args.warmup + args.steps):
+        tree = cct.build(to, tf, tw)  # the same build without statistics, for the overhead
+        plain = cct.last_timings()[4]
+        tree.free()
+        tree = cct.build(to, tf, tw, stats=True)
+        t = cct.last_timings()
+        U = tree.n_nodes
+        st = tree.stats()
+        node = cct.last_timings()[9]
+        del st
+        tree.free()
+        if step >= args.warmup:
+            build_ms.append(t[4])
+            kept_ms.append(t[8])
+            node_ms.append(node)
+            plain_ms.append(plain)
+        log(f"{'warmup' if step < args.warmup else 'step'} {step}: build with statistics {t[4]:.3f} ms "
+            f"(statistics {t[8]:.3f} ms; plain build {plain:.3f} ms), node statistics {node:.3f} ms, U={U:,}")
+    ms = float(np.mean(build_ms))
+    kept = float(np.mean(kept_ms))
+    # algorithmic bytes of the kept statistics: every event's slot id and metric row read once
+    b_alg = N * (4 + 8 * M)
+    achieved = b_alg / (kept * 1e-3) / 1e9
+    line = {
+        "metric": METRIC, "value": N / (ms * 1e-3), "unit": "events/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "u64", "data": "synthetic",
+        "config": {"workload": f"stats: {DESCRIPTIONS['stats']}", "events": N, "frames": F, "metrics": M,
+                   "nodes": U, "statistics_ms": kept, "plain_build_ms": float(np.mean(plain_ms)),
+                   "node_statistics_ms": float(np.mean(node_ms))},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                     "kernel": "statistics kept by the build (per-slot samples, fold into the paths)",
+                     "bytes_per_launch": b_alg, "avg_launch_ms": kept},
     }
     print(json.dumps(line), flush=True)
 

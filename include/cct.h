@@ -84,6 +84,16 @@ typedef struct {
  * *out receives a tree owned by the caller (release with cct_free). */
 cct_status cct_build(const cct_paths *events, void *hip_stream, cct_tree **out);
 
+/* The same, and the tree also keeps the other aggregates the paper names for a node's
+ * metrics besides the sum: minimum, average and standard deviation (Design, "Profiler",
+ * "Calling Context Tree").  Every event is one sample of each metric, at the node its
+ * path ends on (exclusive) and at every node of the path up to the root (inclusive).
+ * Per distinct path the tree keeps the sample count, each metric's minimum and its sum
+ * of squares modulo 2^128; cct_merge and cct_merge_activity fold their batches in (a
+ * joined activity flush gives one sample per registered call path: the sum of its
+ * records).  Read them per node with cct_stats. */
+cct_status cct_build_stats(const cct_paths *events, void *hip_stream, cct_tree **out);
+
 /* Aggregate one more batch into `tree` (the flush of a full metric buffer into the
  * existing tree).  The result equals cct_build over the concatenation of every batch
  * the tree has seen; node ids are renumbered.  chunk->n_metrics must equal the
@@ -174,6 +184,29 @@ typedef struct {
 cct_status cct_filter(const cct_tree *tree, const cct_filter_spec *spec, void *hip_stream, int64_t capacity,
                       int64_t *node_ids, int64_t *n_matches);
 
+/* Per-node statistics of a tree built with cct_build_stats: DEVICE arrays, each written
+ * by a kernel, any of them may be NULL.  U nodes, M metrics, row-major.
+ *   count_excl/incl  uint64[U]: samples ending at the node / passing through it
+ *   min_excl/incl    uint64[U][M]: smallest sample; UINT64_MAX where the count is 0
+ *   sumsq_excl/incl  uint64[U][M][2]: sum of squared samples modulo 2^128, low word first
+ *   mean_excl/incl   double[U][M]: sum / count (the tree's 64-bit sum); NaN where count is 0
+ *   std_excl/incl    double[U][M]: population deviation sqrt(n*S2 - S1^2) / n from the
+ *                    count n, the 64-bit sum S1 and the 128-bit S2, the integer under the
+ *                    root exact and rounded once; NaN where the count is 0, or where that
+ *                    integer is negative (only when a sum wrapped)
+ * Mean and deviation are within 4 units in the last place of the exact quantity. */
+typedef struct {
+  uint64_t *count_excl, *count_incl;
+  uint64_t *min_excl, *min_incl;
+  uint64_t *sumsq_excl, *sumsq_incl;
+  double *mean_excl, *mean_incl;
+  double *std_excl, *std_incl;
+} cct_node_stats;
+
+/* Compute the statistics of every node of `tree` into `out` (returns after the stream
+ * has finished).  A tree built without statistics gives CCT_EINVAL. */
+cct_status cct_stats(const cct_tree *tree, void *hip_stream, const cct_node_stats *out);
+
 /* Look up Q call paths (queries->offsets/frames, metrics ignored) in `tree`.
  * Writes DEVICE arrays: node_ids int64[Q] (the canonical id, or -1 if the path is
  * not a node), and, when non-NULL, excl/incl uint64[Q][M] (zeros for absent paths). */
@@ -205,8 +238,10 @@ const char *cct_last_error(void);
  * ordering (sort, LCP, scans), [3] node emission (parents, exclusive, inclusive), [4]
  * whole merge, [5] the correlation-ID join before the merge (cct_merge_activity only;
  * 0 otherwise), [6] the most recent computation of a bottom-up view by cct_bottom_up
- * (calls that only copy a kept view leave it as it is), [7] the last cct_filter.  Returns
- * the number of values written (<= n, at most 8). */
+ * (calls that only copy a kept view leave it as it is), [7] the last cct_filter, [8] the
+ * statistics kept by the last build or merge (per-slot samples and their fold into the
+ * paths; 0 for a tree without statistics), [9] the last cct_stats.  Returns the number
+ * of values written (<= n, at most 10). */
 int cct_last_timings(double *ms, int n);
 
 #ifdef __cplusplus

@@ -258,6 +258,35 @@ def join_activity(reg_offsets, reg_frames, reg_corr_ids, corr_ids, metrics):
     return offsets, frames, w[np.asarray(rec, np.int64)].reshape(len(rec), w.shape[1]), unmatched
 
 
+def join_activity_calls(reg_offsets, reg_frames, reg_corr_ids, corr_ids, metrics):
+    """The same join with one event per API call rather than per record: every
+    registered path that at least one record names, in registry order, carrying the sum
+    (modulo 2^64) of its records' metrics.  Several records of one correlation ID report
+    one call, so a tree keeping per-node statistics takes one sample per call.  For sums
+    the two batches give the same tree.  Returns (offsets, frames, metrics, n_unmatched)."""
+    o, f, w, unmatched = join_activity(reg_offsets, reg_frames, reg_corr_ids, corr_ids, metrics)
+    ro = np.asarray(reg_offsets, np.int64)
+    rf = np.asarray(reg_frames, np.uint32)
+    index = {c: i for i, c in enumerate(np.asarray(reg_corr_ids, np.uint64).tolist())}
+    m = w.shape[1]
+    total = {}
+    for c, row in zip(np.asarray(corr_ids, np.uint64).tolist(), np.asarray(metrics, np.uint64).reshape(-1, m).tolist()):
+        i = index.get(c)
+        if i is None:
+            continue
+        acc = total.setdefault(i, [0] * m)
+        for j in range(m):
+            acc[j] = (acc[j] + row[j]) % 2**64
+    calls = sorted(total)
+    offsets = np.zeros(len(calls) + 1, np.int64)
+    frames, rows = [], []
+    for k, i in enumerate(calls):
+        frames.extend(rf[ro[i]:ro[i + 1]].tolist())
+        offsets[k + 1] = len(frames)
+        rows.append(total[i])
+    return offsets, np.asarray(frames, np.uint32), np.asarray(rows, np.uint64).reshape(len(calls), m), unmatched
+
+
 def bottom_up(offsets, frames, metrics):
     """Bottom-up view from the events (``or_bottom_up`` in oracle.cpp): for every frame on
     some path, ascending, (frames[K], excl[K, M], incl[K, M]) where excl sums the events

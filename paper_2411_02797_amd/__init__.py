@@ -27,7 +27,7 @@ _lib = None
 
 NO_PARENT = 0xFFFFFFFF
 MAX_METRICS = 8
-EXPORTED_SYMBOLS = ("cct_build", "cct_merge", "cct_merge_activity", "cct_bottom_up", "cct_filter", "cct_query",
+EXPORTED_SYMBOLS = ("cct_build", "cct_build_stats", "cct_stats", "cct_merge", "cct_merge_activity", "cct_bottom_up", "cct_filter", "cct_query",
                     "cct_info", "cct_export", "cct_free", "cct_release_cached_memory", "cct_last_error",
                     "cct_last_timings")
 _STATUS = {0: "CCT_OK", -1: "CCT_EINVAL", -2: "CCT_ENOMEM", -3: "CCT_EDEVICE", -4: "CCT_EMISMATCH",
@@ -59,6 +59,13 @@ class _FilterSpec(ctypes.Structure):
 
 _DEN_KINDS = {"one": 0, "metric": 1, "root": 2}
 
+_STAT_FIELDS = ("count_excl", "count_incl", "min_excl", "min_incl", "sumsq_excl", "sumsq_incl", "mean_excl",
+                "mean_incl", "std_excl", "std_incl")
+
+
+class _NodeStats(ctypes.Structure):
+    _fields_ = [(k, ctypes.c_void_p) for k in _STAT_FIELDS]
+
 
 def library_path():
     return _LIB_PATH
@@ -75,6 +82,8 @@ def load_library():
     vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
     P = ctypes.POINTER
     lib.cct_build.argtypes = [P(_Paths), vp, P(vp)]
+    lib.cct_build_stats.argtypes = [P(_Paths), vp, P(vp)]
+    lib.cct_stats.argtypes = [vp, vp, P(_NodeStats)]
     lib.cct_merge.argtypes = [vp, P(_Paths), vp]
     lib.cct_merge_activity.argtypes = [vp, P(_Paths), vp, P(_Activity), vp, P(i64)]
     lib.cct_bottom_up.argtypes = [vp, vp, i64, vp, vp, vp, P(i64)]
@@ -88,7 +97,7 @@ def load_library():
     lib.cct_release_cached_memory.restype = None
     lib.cct_last_error.restype = ctypes.c_char_p
     lib.cct_last_timings.argtypes = [P(ctypes.c_double), ctypes.c_int]
-    for name in ("cct_build", "cct_merge", "cct_merge_activity", "cct_bottom_up", "cct_filter", "cct_query",
+    for name in ("cct_build", "cct_build_stats", "cct_stats", "cct_merge", "cct_merge_activity", "cct_bottom_up", "cct_filter", "cct_query",
                  "cct_info", "cct_export"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
@@ -252,6 +261,25 @@ class Tree:
         paper's CPU latency analysis)."""
         return self.filter(cpu_metric, +1, thr_num, thr_den, den="metric", den_metric=gpu_metric)
 
+    def stats(self, device=None, fields=_STAT_FIELDS):
+        """Per-node statistics (cct_stats) as tensors: count_* int64[U], min_* int64[U, M],
+        sumsq_* int64[U, M, 2] (bit patterns of uint64; low word first), mean_* and std_*
+        float64[U, M].  Only the named fields are computed into tensors."""
+        import torch
+        u, m, _ = self._info()
+        dev = torch.device("cuda", torch.cuda.current_device())
+        shapes = {"count": (u,), "min": (u, m), "sumsq": (u, m, 2), "mean": (u, m), "std": (u, m)}
+        out = {}
+        for k in fields:
+            kind = k.split("_")[0]
+            out[k] = torch.empty(shapes[kind], dtype=torch.float64 if kind in ("mean", "std") else torch.int64,
+                                 device=dev)
+        spec = _NodeStats(**{k: (out[k].data_ptr() if k in out else None) for k in _STAT_FIELDS})
+        _check(load_library().cct_stats(self._h, _stream(), ctypes.byref(spec)))
+        if device is not None:
+            out = {k: v.to(device) for k, v in out.items()}
+        return out
+
     def to_tensors(self, device=None):
         """Canonical arrays as tensors: parent/frame/depth int32[U] (bit patterns of
         uint32), excl/incl int64[U, M] (bit patterns of uint64)."""
@@ -284,11 +312,14 @@ class Tree:
             pass
 
 
-def build(offsets, frames, metrics):
-    """Build a calling context tree from one CSR batch of device tensors."""
+def build(offsets, frames, metrics, stats=False):
+    """Build a calling context tree from one CSR batch of device tensors; with
+    ``stats=True`` the tree also keeps per-node counts, minima and sums of squares
+    (cct_build_stats), read with ``Tree.stats``."""
     p, _ = _paths(offsets, frames, metrics)
     h = ctypes.c_void_p()
-    _check(load_library().cct_build(ctypes.byref(p), _stream(), ctypes.byref(h)))
+    lib = load_library()
+    _check((lib.cct_build_stats if stats else lib.cct_build)(ctypes.byref(p), _stream(), ctypes.byref(h)))
     return Tree(h.value)
 
 
@@ -296,9 +327,10 @@ def last_timings():
     """Per-phase HIP-event times (ms) of this thread's last calls: ingest, publish, sort,
     canonical emission and total of the last build/merge, the correlation-ID join of a
     merge_activity call (0 otherwise), the most recent computation of a bottom-up view
-    (bottom_up), and the last filter."""
-    buf = (ctypes.c_double * 8)()
-    n = load_library().cct_last_timings(buf, 8)
+    (bottom_up), the last filter, the statistics kept by the last build/merge (0 without),
+    and the last ``Tree.stats``."""
+    buf = (ctypes.c_double * 10)()
+    n = load_library().cct_last_timings(buf, 10)
     return list(buf)[:n]
 
 

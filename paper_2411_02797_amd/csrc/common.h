@@ -359,4 +359,41 @@ void launch_filter_scan(const uint32_t *count, int64_t tiles, uint64_t *pos, hip
 void launch_filter_write(int64_t u, const uint64_t *mask, const uint64_t *pos, int64_t capacity, int64_t *out,
                          hipStream_t s);
 
+// Per-path and per-node statistics (stats.hip)
+struct StatDelta {  // one batch, by table slot: cnt [cap], min [cap][m], sq [cap][m][2]
+  uint64_t *cnt, *min, *sq;
+};
+struct PathStats {  // kept per path: cnt [D], min [D][m], sq [D][m][2]
+  uint64_t *cnt, *min, *sq;
+};
+struct NodeStatOut {  // any pointer may be null
+  uint64_t *count_excl, *count_incl;  // [U]
+  uint64_t *min_excl, *min_incl;      // [U][m]
+  uint64_t *sumsq_excl, *sumsq_incl;  // [U][m][2]
+  double *mean_excl, *mean_incl;      // [U][m]
+  double *std_excl, *std_incl;        // [U][m]
+};
+struct NodeStatArgs {
+  int64_t u, d;
+  int32_t m;
+  const uint64_t *scan_out;  // [d + 1][1 + m] of the canonical emission
+  const uint32_t *order;     // [d] canonical position -> path
+  const uint64_t *pcnt, *pmin, *psq;
+  const uint32_t *subend;         // [u]
+  const uint64_t *excl, *incl;    // [u][m]
+  uint64_t *rows, *prefix;        // [u][1 + 4m], [u + 1][1 + 4m]
+  uint64_t *exmin, *pre, *suf;    // [u][m]
+  uint64_t *tab;                  // [levels][nblk][m]
+  int64_t nblk;
+  int levels;
+  NodeStatOut out;
+};
+int64_t stats_map_entries(int32_t m);
+void launch_stats_agg(const uint32_t *slot_of, const uint64_t *w, int64_t n, int32_t m, int grid, const StatDelta &d,
+                      hipStream_t s);
+void launch_stats_fold(int64_t D, int64_t d_old, int32_t m, const uint32_t *pslot, const StatDelta &d,
+                       const PathStats &p, hipStream_t s);
+int64_t rmq_blocks(int64_t u);
+void launch_node_stats(const NodeStatArgs &a, uint64_t *scan_blk, hipStream_t s);
+
 }  // namespace cct

@@ -25,6 +25,8 @@ thread_local double g_timings[5] = {0, 0, 0, 0, 0};
 thread_local double g_join_ms = 0;  // correlation-ID join of the last cct_merge_activity
 thread_local double g_view_ms = 0;  // the most recent computation of a bottom-up view
 thread_local double g_filter_ms = 0;  // the last cct_filter
+thread_local double g_stats_ms = 0;   // statistics kept by the last build/merge (0 without)
+thread_local double g_node_stats_ms = 0;  // the last cct_stats
 thread_local int g_alloc_countdown = 0;  // test hook: >0 makes the n-th allocation of a call fail
 
 int64_t env_int(const char *name, int64_t dflt) {
@@ -173,6 +175,9 @@ struct cct_tree {
   int64_t d = 0, dcap = 0;
   int64_t store_used = 0, store_cap = 0, sum_len = 0;
   Buf pframes, pcp, pstart, plen, pslot, psums;
+  // per-path statistics (count, minima, sums of squares), kept when built with them
+  bool stats = false;
+  Buf pcnt, pmin, psq;
   // canonical arrays
   int64_t u = 0;
   Buf parent, frame, depth, subend, excl, incl;
@@ -386,6 +391,14 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     return st;
   };
   if (sum_len + 1 > (int64_t)0xFFFFFFFE) return rollback(fail(CCT_EOVERFLOW, "tree would exceed 2^32-2 nodes"));
+  // this batch's statistics by table slot (before anything of the tree changes)
+  Buf d_cnt, d_min, d_sq;
+  StatDelta sd{};
+  if (t->stats && N > 0) {
+    if (!d_cnt.alloc(t->cap * 8) || !d_min.alloc(t->cap * m * 8) || !d_sq.alloc(t->cap * m * 16))
+      return rollback(fail(CCT_ENOMEM, "device allocation failed"));
+    sd.cnt = d_cnt.as<uint64_t>(); sd.min = d_min.as<uint64_t>(); sd.sq = d_sq.as<uint64_t>();
+  }
   const int64_t store_need = t->store_used + (int64_t)new_store;
   const int64_t dneed = std::max<int64_t>(D, 1);
   cct_tree old_arrays_holder;  // receives replaced buffers, released on return
@@ -408,8 +421,10 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     }
     if (dneed > t->dcap || !t->pstart.p) {
       const int64_t ncap = std::max<int64_t>(dneed + dneed / 2, 256);
-      Buf a1, a2, a3, a4;
+      Buf a1, a2, a3, a4, s1, s2, s3;
       if (!a1.alloc(ncap * 8) || !a2.alloc(ncap * 4) || !a3.alloc(ncap * 4) || !a4.alloc(ncap * m * 8))
+        return rollback(fail(CCT_ENOMEM, "device allocation failed"));
+      if (t->stats && (!s1.alloc(ncap * 8) || !s2.alloc(ncap * m * 8) || !s3.alloc(ncap * m * 16)))
         return rollback(fail(CCT_ENOMEM, "device allocation failed"));
       if (t->d) {
         if (hipMemcpyAsync(a1.p, t->pstart.p, t->d * 8, hipMemcpyDeviceToDevice, s) != hipSuccess ||
@@ -417,6 +432,17 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
             hipMemcpyAsync(a3.p, t->pslot.p, t->d * 4, hipMemcpyDeviceToDevice, s) != hipSuccess ||
             hipMemcpyAsync(a4.p, t->psums.p, t->d * m * 8, hipMemcpyDeviceToDevice, s) != hipSuccess)
           return rollback(fail(CCT_EDEVICE, "copy failed"));
+        if (t->stats &&
+            (hipMemcpyAsync(s1.p, t->pcnt.p, t->d * 8, hipMemcpyDeviceToDevice, s) != hipSuccess ||
+             hipMemcpyAsync(s2.p, t->pmin.p, t->d * m * 8, hipMemcpyDeviceToDevice, s) != hipSuccess ||
+             hipMemcpyAsync(s3.p, t->psq.p, t->d * m * 16, hipMemcpyDeviceToDevice, s) != hipSuccess))
+          return rollback(fail(CCT_EDEVICE, "copy failed"));
+      }
+      if (t->stats) {
+        old_arrays_holder.pcnt = std::move(t->pcnt);
+        old_arrays_holder.pmin = std::move(t->pmin);
+        old_arrays_holder.psq = std::move(t->psq);
+        t->pcnt = std::move(s1); t->pmin = std::move(s2); t->psq = std::move(s3);
       }
       old_arrays_holder.pstart = std::move(t->pstart);
       old_arrays_holder.plen = std::move(t->plen);
@@ -486,6 +512,19 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     ta.ctr = tr_ctr.as<unsigned long long>(); ta.order = order.as<uint32_t>();
   }
 
+  // ---- this batch's statistics by slot -----------------------------------------------------
+  Timer ts;
+  g_stats_ms = 0;
+  if (sd.cnt) {
+    ts.mark(0, s);
+    HIP_TRY(hipMemsetAsync(sd.cnt, 0, t->cap * 8, s));
+    HIP_TRY(hipMemsetAsync(sd.min, 0xFF, t->cap * m * 8, s));
+    HIP_TRY(hipMemsetAsync(sd.sq, 0, t->cap * m * 16, s));
+    const int st_grid = (int)std::max<int64_t>(1, std::min<int64_t>((N + 8191) / 8192, (int64_t)cu_count() * 2));
+    launch_stats_agg(slot_of.as<uint32_t>(), p->metrics, N, m, st_grid, sd, s);
+    ts.mark(1, s);
+  }
+
   // ---- publish new paths, fold this call's sums into the old ones -----------------------
   HIP_TRY(hipMemsetAsync(cursor.p, 0, 64, s));
   if (n_new) {
@@ -504,6 +543,12 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     launch_publish(pa, s);
   }
   if (N > 0) launch_fold_old(t->d, m, t->pslot.as<uint32_t>(), delta.as<uint64_t>(), t->psums.as<uint64_t>(), s);
+  if (sd.cnt) {
+    ts.mark(2, s);
+    PathStats ps{t->pcnt.as<uint64_t>(), t->pmin.as<uint64_t>(), t->psq.as<uint64_t>()};
+    launch_stats_fold(D, t->d, m, t->pslot.as<uint32_t>(), sd, ps, s);
+    ts.mark(3, s);
+  }
   HIP_TRY(hipGetLastError());
   tm.mark(3, s);
 
@@ -547,6 +592,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     HIP_TRY(hipMemsetAsync(cursor.as<unsigned long long>() + 2, 0, 16, s));
   }
   tm.collect(N > 0);
+  if (sd.cnt && ts.ok) g_stats_ms = ts.span(0, 1) + ts.span(2, 3);
 
   // ---- commit -------------------------------------------------------------------------------
   t->store_used += (int64_t)hs[0];
@@ -565,7 +611,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
 
 extern "C" {
 
-cct_status cct_build(const cct_paths *events, void *hip_stream, cct_tree **out) {
+cct_status build_tree(const cct_paths *events, void *hip_stream, bool stats, cct_tree **out) {
   AllocHook hook;
   g_join_ms = 0;
   g_error.clear();
@@ -577,6 +623,7 @@ cct_status cct_build(const cct_paths *events, void *hip_stream, cct_tree **out) 
   if (!t) return fail(CCT_ENOMEM, "host allocation failed");
   (void)hipGetDevice(&t->device);
   t->m = events->n_metrics;
+  t->stats = stats;
   const int64_t N = events->n_events;
   int64_t cap = env_int("CCT_TEST_TABLE_CAP", 0);
   if (cap <= 0) cap = (int64_t)std::min<uint64_t>(pow2_at_least((uint64_t)std::max<int64_t>(2 * N, 1024)), 1ull << 21);
@@ -592,6 +639,14 @@ cct_status cct_build(const cct_paths *events, void *hip_stream, cct_tree **out) 
   if (st) { delete t; return st; }
   *out = t;
   return CCT_OK;
+}
+
+cct_status cct_build(const cct_paths *events, void *hip_stream, cct_tree **out) {
+  return build_tree(events, hip_stream, false, out);
+}
+
+cct_status cct_build_stats(const cct_paths *events, void *hip_stream, cct_tree **out) {
+  return build_tree(events, hip_stream, true, out);
 }
 
 cct_status cct_merge(cct_tree *tree, const cct_paths *chunk, void *hip_stream) {
@@ -846,6 +901,43 @@ cct_status cct_filter(const cct_tree *tree, const cct_filter_spec *spec, void *h
   return CCT_OK;
 }
 
+cct_status cct_stats(const cct_tree *tree, void *hip_stream, const cct_node_stats *out) {
+  AllocHook hook;
+  g_error.clear();
+  if (!tree || !out) return fail(CCT_EINVAL, "NULL argument");
+  if (!tree->stats) return fail(CCT_EINVAL, "the tree keeps no statistics (build it with cct_build_stats)");
+  int dev = 0;
+  (void)hipGetDevice(&dev);
+  if (dev != tree->device) return fail(CCT_EINVAL, "tree belongs to another device");
+  hipStream_t s = (hipStream_t)hip_stream;
+  const int32_t m = tree->m;
+  const int64_t U = tree->u, C = 1 + 4 * (int64_t)m;
+  const int64_t nblk = rmq_blocks(U);
+  const int levels = floor_log2((uint64_t)nblk) + 1;
+  Buf rows, prefix, blk, exmin, pre, suf, tab;
+  if (!rows.alloc(U * C * 8) || !prefix.alloc((U + 1) * C * 8) || !blk.alloc((U / 1024 + 2) * C * 8) ||
+      !exmin.alloc(U * m * 8) || !pre.alloc(U * m * 8) || !suf.alloc(U * m * 8) || !tab.alloc(levels * nblk * m * 8))
+    return fail(CCT_ENOMEM, "device allocation failed");
+  NodeStatArgs a{};
+  a.u = U; a.d = tree->d; a.m = m;
+  a.scan_out = tree->scan_out.as<uint64_t>(); a.order = tree->order.as<uint32_t>();
+  a.pcnt = tree->pcnt.as<uint64_t>(); a.pmin = tree->pmin.as<uint64_t>(); a.psq = tree->psq.as<uint64_t>();
+  a.subend = tree->subend.as<uint32_t>(); a.excl = tree->excl.as<uint64_t>(); a.incl = tree->incl.as<uint64_t>();
+  a.rows = rows.as<uint64_t>(); a.prefix = prefix.as<uint64_t>(); a.exmin = exmin.as<uint64_t>();
+  a.pre = pre.as<uint64_t>(); a.suf = suf.as<uint64_t>(); a.tab = tab.as<uint64_t>();
+  a.nblk = nblk; a.levels = levels;
+  a.out = NodeStatOut{out->count_excl, out->count_incl, out->min_excl, out->min_incl, out->sumsq_excl,
+                      out->sumsq_incl, out->mean_excl, out->mean_incl, out->std_excl, out->std_incl};
+  Timer tm;
+  tm.mark(0, s);
+  launch_node_stats(a, blk.as<uint64_t>(), s);
+  tm.mark(1, s);
+  HIP_TRY(hipGetLastError());
+  HIP_TRY(hipStreamSynchronize(s));
+  g_node_stats_ms = tm.ok ? tm.span(0, 1) : 0.0;
+  return CCT_OK;
+}
+
 cct_status cct_query(const cct_tree *tree, const cct_paths *q, void *hip_stream, int64_t *node_ids, uint64_t *excl,
                      uint64_t *incl) {
   g_error.clear();
@@ -921,11 +1013,13 @@ const char *cct_last_error(void) { return g_error.c_str(); }
 
 int cct_last_timings(double *ms, int n) {
   if (!ms || n <= 0) return 0;
-  const int k = n < 8 ? n : 8;
+  const int k = n < 10 ? n : 10;
   for (int i = 0; i < k && i < 5; ++i) ms[i] = g_timings[i];
   if (k > 5) ms[5] = g_join_ms;
   if (k > 6) ms[6] = g_view_ms;
   if (k > 7) ms[7] = g_filter_ms;
+  if (k > 8) ms[8] = g_stats_ms;
+  if (k > 9) ms[9] = g_node_stats_ms;
   return k;
 }
 

@@ -1,0 +1,352 @@
+// Per-node statistics beyond the sum.  The paper's tree keeps, for a node's metrics,
+// the sum, the minimum, the average and the standard deviation, and a metric recorded at
+// the bottom of a call path updates every node along it up to the root (Design,
+// "Profiler", "Calling Context Tree").
+//
+// Kept per distinct path (the tree's path store), folded by every build and merge:
+//   count           events on the path
+//   min[j]          smallest value of metric j
+//   sumsq[j]        sum of squares of metric j, exact modulo 2^128 (two words, low first)
+// Per node, on request (cct_stats): the exclusive values are those of the path ending at
+// the node; the inclusive ones combine the paths of the node's subtree, which is the id
+// range [u, subend[u]) in preorder: counts and sums of squares by differences of prefix
+// sums over node order, minima by a range-minimum structure (in-block prefix and suffix
+// minima over 64-node blocks plus a sparse table over the blocks).  The mean is sum /
+// count and the deviation the population one, sqrt(n * S2 - S1^2) / n, with the 192-bit
+// integer n * S2 - S1^2 computed exactly and rounded once to float64.
+#include "common.h"
+
+namespace cct {
+
+namespace {
+
+constexpr uint32_t kStatEmpty = 0xFFFFFFFFu;
+constexpr int kStatThreads = 1024;
+constexpr int kStatLdsBytes = 163840 - 256;
+constexpr int kRmqBlock = 64;  // nodes per range-minimum block (one wave)
+
+constexpr int stat_entries(int m) {
+  int e = kStatLdsBytes / (4 + 8 + 24 * m);  // key, count, min and two square words per metric
+  if (e > 4096) e = 4096;
+  return e & ~63;
+}
+
+// a += (lo, hi) on two 64-bit words modulo 2^128.  The add that wraps the low word sees
+// an old value whose sum with lo overflows, and only that add carries into the high word.
+__device__ inline void lds_add_u128(uint64_t *p, uint64_t lo, uint64_t hi) {
+  const uint64_t old = atomicAdd((unsigned long long *)p, (unsigned long long)lo);
+  const uint64_t h = hi + (old + lo < old ? 1 : 0);
+  if (h) atomicAdd((unsigned long long *)(p + 1), (unsigned long long)h);
+}
+__device__ inline void hbm_add_u128(uint64_t *p, uint64_t lo, uint64_t hi) {
+  const uint64_t old = atomicAdd((unsigned long long *)p, (unsigned long long)lo);
+  const uint64_t h = hi + (old + lo < old ? 1 : 0);
+  if (h) atomicAdd((unsigned long long *)(p + 1), (unsigned long long)h);
+}
+
+// One batch's samples per table slot.  Each workgroup walks a contiguous range of events
+// and combines them in an LDS map keyed by slot (hot paths meet there), falling back to
+// device atomics when a key's probe window is full; the map is flushed with device
+// atomics.  d.cnt starts at 0, d.min at all ones, d.sq at 0.
+template <int M>
+__global__ __launch_bounds__(kStatThreads) void stats_agg_kernel(const uint32_t *slot_of, const uint64_t *w,
+                                                                 int64_t n, StatDelta d) {
+  constexpr int kE = stat_entries(M);
+  __shared__ uint32_t key[kE];
+  __shared__ uint64_t cnt[kE];
+  __shared__ uint64_t mn[kE * M];
+  __shared__ uint64_t sq[kE * M * 2];
+  const int tid = threadIdx.x;
+  for (int i = tid; i < kE; i += kStatThreads) { key[i] = kStatEmpty; cnt[i] = 0; }
+  for (int i = tid; i < kE * M; i += kStatThreads) { mn[i] = ~0ull; sq[2 * i] = 0; sq[2 * i + 1] = 0; }
+  __syncthreads();
+  const int64_t b = blockIdx.x, nb = gridDim.x;
+  const int64_t lo = b * n / nb, hi = (b + 1) * n / nb;
+  for (int64_t e = lo + tid; e < hi; e += kStatThreads) {
+    const uint32_t s = slot_of[e];
+    uint64_t v[M];
+#pragma unroll
+    for (int j = 0; j < M; ++j) v[j] = w[e * M + j];
+    if (s == kNoSlot) continue;
+    uint32_t k = __umulhi(hash32(s), (uint32_t)kE);
+    int mi = -1;
+    for (int t = 0; t < 8; ++t) {
+      uint32_t cur = key[k];
+      if (cur == kStatEmpty) cur = atomicCAS(&key[k], kStatEmpty, s);
+      if (cur == kStatEmpty || cur == s) { mi = (int)k; break; }
+      k = k + 1 == (uint32_t)kE ? 0 : k + 1;
+    }
+    if (mi >= 0) {
+      atomicAdd((unsigned long long *)&cnt[mi], 1ull);
+#pragma unroll
+      for (int j = 0; j < M; ++j) {
+        atomicMin((unsigned long long *)&mn[mi * M + j], (unsigned long long)v[j]);
+        lds_add_u128(&sq[(mi * M + j) * 2], v[j] * v[j], __umul64hi(v[j], v[j]));
+      }
+    } else {
+      atomicAdd((unsigned long long *)&d.cnt[s], 1ull);
+#pragma unroll
+      for (int j = 0; j < M; ++j) {
+        atomicMin((unsigned long long *)&d.min[(uint64_t)s * M + j], (unsigned long long)v[j]);
+        hbm_add_u128(&d.sq[((uint64_t)s * M + j) * 2], v[j] * v[j], __umul64hi(v[j], v[j]));
+      }
+    }
+  }
+  __syncthreads();
+  for (int k = tid; k < kE; k += kStatThreads) {
+    const uint32_t s = key[k];
+    if (s == kStatEmpty) continue;
+    atomicAdd((unsigned long long *)&d.cnt[s], (unsigned long long)cnt[k]);
+#pragma unroll
+    for (int j = 0; j < M; ++j) {
+      atomicMin((unsigned long long *)&d.min[(uint64_t)s * M + j], (unsigned long long)mn[k * M + j]);
+      hbm_add_u128(&d.sq[((uint64_t)s * M + j) * 2], sq[(k * M + j) * 2], sq[(k * M + j) * 2 + 1]);
+    }
+  }
+}
+
+// Path i takes its slot's batch values; paths from earlier calls (i < d_old) combine them
+// with what they hold.
+__global__ void stats_fold_kernel(int64_t D, int64_t d_old, int32_t m, const uint32_t *pslot, StatDelta d,
+                                  PathStats p) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= D) return;
+  const uint64_t s = pslot[i];
+  const bool fresh = i >= d_old;
+  p.cnt[i] = (fresh ? 0 : p.cnt[i]) + d.cnt[s];
+  for (int j = 0; j < m; ++j) {
+    const uint64_t x = d.min[s * m + j];
+    const uint64_t old = fresh ? ~0ull : p.min[i * m + j];
+    p.min[i * m + j] = x < old ? x : old;
+    const uint64_t lo = d.sq[(s * m + j) * 2], hi = d.sq[(s * m + j) * 2 + 1];
+    const uint64_t olo = fresh ? 0 : p.sq[(i * m + j) * 2], ohi = fresh ? 0 : p.sq[(i * m + j) * 2 + 1];
+    const uint64_t nlo = olo + lo;
+    p.sq[(i * m + j) * 2] = nlo;
+    p.sq[(i * m + j) * 2 + 1] = ohi + hi + (nlo < olo ? 1 : 0);
+  }
+}
+
+// ---- node statistics on request ---------------------------------------------------------
+// Row of node u for the prefix sums: [count, then per metric the four 32-bit limbs of
+// its sum of squares], each in a 64-bit column; a limb column's prefix over at most 2^32
+// nodes stays below 2^64, so every difference of prefixes is exact.
+__global__ void node_fill_kernel(NodeStatArgs a) {
+  const int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (u >= a.u) return;
+  const int C = 1 + 4 * a.m;
+  for (int c = 0; c < C; ++c) a.rows[u * C + c] = 0;
+  for (int j = 0; j < a.m; ++j) a.exmin[u * a.m + j] = ~0ull;
+}
+
+// path at canonical position i ends at node scan_out[(i + 1) * (1 + m)] (its first new node
+// plus its new-node count, minus one; the empty path ends at the root)
+__global__ void node_scatter_kernel(NodeStatArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= a.d) return;
+  const int64_t u = (int64_t)a.scan_out[(i + 1) * (1 + a.m)];
+  const uint64_t pid = a.order[i];
+  const int C = 1 + 4 * a.m;
+  a.rows[u * C] = a.pcnt[pid];
+  for (int j = 0; j < a.m; ++j) {
+    const uint64_t lo = a.psq[(pid * a.m + j) * 2], hi = a.psq[(pid * a.m + j) * 2 + 1];
+    uint64_t *r = a.rows + u * C + 1 + 4 * j;
+    r[0] = lo & 0xFFFFFFFFull; r[1] = lo >> 32; r[2] = hi & 0xFFFFFFFFull; r[3] = hi >> 32;
+    a.exmin[u * a.m + j] = a.pmin[pid * a.m + j];
+  }
+}
+
+__device__ inline uint64_t min_u64(uint64_t x, uint64_t y) { return x < y ? x : y; }
+__device__ inline uint64_t shfl_u64(uint64_t v, int src) {
+  const uint32_t lo = __shfl((uint32_t)v, src), hi = __shfl((uint32_t)(v >> 32), src);
+  return ((uint64_t)hi << 32) | lo;
+}
+__device__ inline uint64_t shfl_up_u64(uint64_t v, int o) {
+  const uint32_t lo = __shfl_up((uint32_t)v, o), hi = __shfl_up((uint32_t)(v >> 32), o);
+  return ((uint64_t)hi << 32) | lo;
+}
+__device__ inline uint64_t shfl_down_u64(uint64_t v, int o) {
+  const uint32_t lo = __shfl_down((uint32_t)v, o), hi = __shfl_down((uint32_t)(v >> 32), o);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// one wave per block of kRmqBlock nodes: pre[v] = min of the block's nodes up to v,
+// suf[v] = min from v to the block's end, tab level 0 = the block's minimum
+__global__ __launch_bounds__(64) void rmq_block_kernel(NodeStatArgs a) {
+  const int64_t blk = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int64_t v = blk * kRmqBlock + lane;
+  for (int j = 0; j < a.m; ++j) {
+    const uint64_t x = v < a.u ? a.exmin[v * a.m + j] : ~0ull;
+    uint64_t p = x, q = x;
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint64_t y = shfl_up_u64(p, o), z = shfl_down_u64(q, o);
+      if (lane >= o) p = min_u64(p, y);
+      if (lane + o < 64) q = min_u64(q, z);
+    }
+    if (v < a.u) {
+      a.pre[v * a.m + j] = p;
+      a.suf[v * a.m + j] = q;
+    }
+    const uint64_t all = shfl_u64(p, 63);
+    if (lane == 0) a.tab[blk * a.m + j] = all;
+  }
+}
+
+// level k of the sparse table: entry b covers blocks [b, b + 2^k)
+__global__ void rmq_level_kernel(NodeStatArgs a, int k) {
+  const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= a.nblk) return;
+  const int64_t half = (int64_t)1 << (k - 1);
+  const int64_t b2 = b + half < a.nblk ? b + half : a.nblk - 1;
+  const uint64_t *prev = a.tab + (int64_t)(k - 1) * a.nblk * a.m;
+  uint64_t *cur = a.tab + (int64_t)k * a.nblk * a.m;
+  for (int j = 0; j < a.m; ++j) cur[b * a.m + j] = min_u64(prev[b * a.m + j], prev[b2 * a.m + j]);
+}
+
+__device__ inline int floor_log2_u64(uint64_t x) { return 63 - __clzll((long long)x); }
+
+// minimum of metric j over nodes [l, r] (inclusive, r >= l)
+__device__ uint64_t range_min(const NodeStatArgs &a, int64_t l, int64_t r, int j) {
+  const int64_t bl = l / kRmqBlock, br = r / kRmqBlock;
+  if (bl == br) {
+    uint64_t x = ~0ull;
+    for (int64_t v = l; v <= r; ++v) x = min_u64(x, a.exmin[v * a.m + j]);
+    return x;
+  }
+  uint64_t x = min_u64(a.suf[l * a.m + j], a.pre[r * a.m + j]);
+  if (bl + 1 <= br - 1) {
+    const int k = floor_log2_u64((uint64_t)(br - 1 - bl));
+    const uint64_t *lev = a.tab + (int64_t)k * a.nblk * a.m;
+    x = min_u64(x, min_u64(lev[(bl + 1) * a.m + j], lev[(br - ((int64_t)1 << k)) * a.m + j]));
+  }
+  return x;
+}
+
+// 128-bit value of four limb sums (each below 2^64), modulo 2^128
+__device__ inline void limbs_to_u128(uint64_t d0, uint64_t d1, uint64_t d2, uint64_t d3, uint64_t &lo,
+                                     uint64_t &hi) {
+  lo = d0 + (d1 << 32);
+  const uint64_t c = lo < d0 ? 1 : 0;
+  hi = (d1 >> 32) + d2 + (d3 << 32) + c;
+}
+
+// float64 nearest to the 192-bit integer (w2, w1, w0): the top 64 significant bits with
+// every lower bit folded into the lowest one (a sticky bit), converted once, scaled exactly
+__device__ inline double u192_to_f64(uint64_t w0, uint64_t w1, uint64_t w2) {
+  uint64_t top, rest;
+  int e;
+  if (w2) {
+    const int sh = __clzll((long long)w2);
+    top = sh ? (w2 << sh) | (w1 >> (64 - sh)) : w2;
+    rest = (sh ? w1 << sh : w1) | w0;
+    e = 128 - sh;
+  } else if (w1) {
+    const int sh = __clzll((long long)w1);
+    top = sh ? (w1 << sh) | (w0 >> (64 - sh)) : w1;
+    rest = sh ? w0 << sh : w0;
+    e = 64 - sh;
+  } else {
+    return (double)w0;
+  }
+  return ldexp((double)(top | (rest ? 1ull : 0ull)), e);
+}
+
+// population deviation from n, S1 (64-bit) and S2 (128-bit): sqrt(n S2 - S1^2) / n
+__device__ inline double deviation(uint64_t n, uint64_t s1, uint64_t s2lo, uint64_t s2hi) {
+  if (n == 0) return __longlong_as_double(0x7FF8000000000000ll);
+  // n * S2 as three words
+  const uint64_t a0 = n * s2lo, a1 = __umul64hi(n, s2lo);
+  const uint64_t b0 = n * s2hi, b1 = __umul64hi(n, s2hi);
+  const uint64_t w0 = a0, w1 = a1 + b0;
+  const uint64_t w2 = b1 + (w1 < a1 ? 1 : 0);
+  // minus S1^2
+  const uint64_t q0 = s1 * s1, q1 = __umul64hi(s1, s1);
+  const uint64_t r0 = w0 - q0, br0 = w0 < q0 ? 1 : 0;
+  const uint64_t t1 = w1 - q1, bt = w1 < q1 ? 1 : 0;
+  const uint64_t r1 = t1 - br0, br1 = bt | (t1 < br0 ? 1 : 0);
+  if (w2 < br1) return __longlong_as_double(0x7FF8000000000000ll);  // negative: a sum wrapped
+  const uint64_t r2 = w2 - br1;
+  return sqrt(u192_to_f64(r0, r1, r2)) / (double)n;
+}
+
+__device__ inline double mean_of(uint64_t s1, uint64_t n) {
+  return n ? (double)s1 / (double)n : __longlong_as_double(0x7FF8000000000000ll);
+}
+
+__global__ void node_final_kernel(NodeStatArgs a) {
+  const int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (u >= a.u) return;
+  const int C = 1 + 4 * a.m, m = a.m;
+  const int64_t r = a.subend[u];
+  const uint64_t *row = a.rows + u * C, *pu = a.prefix + u * C, *pr = a.prefix + r * C;
+  const uint64_t n_ex = row[0], n_in = pr[0] - pu[0];
+  if (a.out.count_excl) a.out.count_excl[u] = n_ex;
+  if (a.out.count_incl) a.out.count_incl[u] = n_in;
+  for (int j = 0; j < m; ++j) {
+    const int64_t o = u * m + j;
+    uint64_t ex_lo, ex_hi, in_lo, in_hi;
+    limbs_to_u128(row[1 + 4 * j], row[2 + 4 * j], row[3 + 4 * j], row[4 + 4 * j], ex_lo, ex_hi);
+    limbs_to_u128(pr[1 + 4 * j] - pu[1 + 4 * j], pr[2 + 4 * j] - pu[2 + 4 * j], pr[3 + 4 * j] - pu[3 + 4 * j],
+                  pr[4 + 4 * j] - pu[4 + 4 * j], in_lo, in_hi);
+    if (a.out.min_excl) a.out.min_excl[o] = a.exmin[o];
+    if (a.out.min_incl) a.out.min_incl[o] = range_min(a, u, r - 1, j);
+    if (a.out.sumsq_excl) { a.out.sumsq_excl[2 * o] = ex_lo; a.out.sumsq_excl[2 * o + 1] = ex_hi; }
+    if (a.out.sumsq_incl) { a.out.sumsq_incl[2 * o] = in_lo; a.out.sumsq_incl[2 * o + 1] = in_hi; }
+    const uint64_t s_ex = a.excl[o], s_in = a.incl[o];
+    if (a.out.mean_excl) a.out.mean_excl[o] = mean_of(s_ex, n_ex);
+    if (a.out.mean_incl) a.out.mean_incl[o] = mean_of(s_in, n_in);
+    if (a.out.std_excl) a.out.std_excl[o] = deviation(n_ex, s_ex, ex_lo, ex_hi);
+    if (a.out.std_incl) a.out.std_incl[o] = deviation(n_in, s_in, in_lo, in_hi);
+  }
+}
+
+inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
+
+}  // namespace
+
+int64_t stats_map_entries(int32_t m) {
+  switch (m) {
+    case 1: return stat_entries(1);
+    case 2: return stat_entries(2);
+    case 3: return stat_entries(3);
+    case 4: return stat_entries(4);
+    case 5: return stat_entries(5);
+    case 6: return stat_entries(6);
+    case 7: return stat_entries(7);
+    default: return stat_entries(8);
+  }
+}
+
+void launch_stats_agg(const uint32_t *slot_of, const uint64_t *w, int64_t n, int32_t m, int grid, const StatDelta &d,
+                      hipStream_t s) {
+  if (n <= 0) return;
+  switch (m) {
+#define CCT_STAT_CASE(M)                                                                                   \
+  case M:                                                                                                  \
+    hipLaunchKernelGGL(stats_agg_kernel<M>, dim3(grid), dim3(kStatThreads), 0, s, slot_of, w, n, d);      \
+    break;
+    CCT_STAT_CASE(1) CCT_STAT_CASE(2) CCT_STAT_CASE(3) CCT_STAT_CASE(4)
+    CCT_STAT_CASE(5) CCT_STAT_CASE(6) CCT_STAT_CASE(7) CCT_STAT_CASE(8)
+#undef CCT_STAT_CASE
+    default: break;
+  }
+}
+
+void launch_stats_fold(int64_t D, int64_t d_old, int32_t m, const uint32_t *pslot, const StatDelta &d,
+                       const PathStats &p, hipStream_t s) {
+  if (D > 0) hipLaunchKernelGGL(stats_fold_kernel, dim3(blocks_for(D, 256)), dim3(256), 0, s, D, d_old, m, pslot, d, p);
+}
+
+int64_t rmq_blocks(int64_t u) { return (u + kRmqBlock - 1) / kRmqBlock; }
+
+void launch_node_stats(const NodeStatArgs &a, uint64_t *scan_blk, hipStream_t s) {
+  hipLaunchKernelGGL(node_fill_kernel, dim3(blocks_for(a.u, 256)), dim3(256), 0, s, a);
+  if (a.d > 0) hipLaunchKernelGGL(node_scatter_kernel, dim3(blocks_for(a.d, 256)), dim3(256), 0, s, a);
+  launch_scan(a.rows, a.u, 1 + 4 * a.m, scan_blk, a.prefix, s);
+  hipLaunchKernelGGL(rmq_block_kernel, dim3((unsigned)a.nblk), dim3(64), 0, s, a);
+  for (int k = 1; k < a.levels; ++k)
+    hipLaunchKernelGGL(rmq_level_kernel, dim3(blocks_for(a.nblk, 256)), dim3(256), 0, s, a, k);
+  hipLaunchKernelGGL(node_final_kernel, dim3(blocks_for(a.u, 256)), dim3(256), 0, s, a);
+}
+
+}  // namespace cct

@@ -8,7 +8,7 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libcct.so")
-SOURCES = ["ingest.hip", "canon.hip", "trie.hip", "query.hip", "activity.hip", "bottomup.hip", "filter.hip", "runtime.hip"]
+SOURCES = ["ingest.hip", "canon.hip", "trie.hip", "query.hip", "activity.hip", "bottomup.hip", "filter.hip", "stats.hip", "runtime.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
          "-I", os.path.join(os.path.dirname(HERE), "include"),

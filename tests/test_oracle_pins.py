@@ -555,3 +555,29 @@ def test_stats_closed_form_repeated_path(k):
     want = math.sqrt((k * k - 1) / 12)
     assert all(abs(x - want) <= 2 * math.ulp(max(want, 1e-300)) for x in d["std_incl"][:, 0])
     assert np.isnan(d["mean_excl"][:4]).all() and d["std_excl"][4, 0] == d["std_incl"][4, 0]
+
+
+# The join of test_join_hand_worked with one event per call: ID 100 -> (5,7) once (4),
+# ID 7 -> (5,9,2) twice (10 + 6), ID 3 -> () once (2), in registry order; 999 unmatched.
+def test_join_per_call_hand_worked():
+    o, f, w, unmatched = oracle.join_activity_calls([0, 2, 5, 5], [5, 7, 5, 9, 2], [100, 7, 3],
+                                                    [7, 999, 100, 7, 3], [[10], [1], [4], [6], [2]])
+    assert unmatched == 1 and o.tolist() == [0, 2, 5, 5] and f.tolist() == [5, 7, 5, 9, 2]
+    assert w.ravel().tolist() == [4, 16, 2]
+    t = oracle.build_tree(o, f, w, stats=True)
+    assert t["incl"].ravel().tolist() == [22, 20, 4, 16, 16]  # the per-record tree's sums
+    assert t["count_incl"].tolist() == [3, 2, 1, 1, 1] and t["min_incl"].ravel().tolist() == [2, 4, 4, 16, 16]
+
+
+def test_join_per_call_and_per_record_give_one_sum_tree():
+    o, f, w = tracegen.random_paths(300, 25, 10, 2, seed=23)
+    rng = np.random.default_rng(23)
+    ids = rng.permutation(10**6)[:300].astype(np.uint64)
+    rec = np.concatenate([ids, ids[rng.integers(0, 300, 90)], np.arange(10**6, 10**6 + 20, dtype=np.uint64)])
+    met = rng.integers(0, 2**64, size=(rec.size, 2), dtype=np.uint64)
+    a = oracle.join_activity(o, f, ids, rec, met)
+    b = oracle.join_activity_calls(o, f, ids, rec, met)
+    assert a[3] == b[3] == 20 and b[0].size - 1 == 300
+    ta, tb = oracle.build_tree(*a[:3]), oracle.build_tree(*b[:3])
+    for k in ("parent", "frame", "depth", "excl", "incl"):
+        assert np.array_equal(ta[k], tb[k]), k
