@@ -381,9 +381,10 @@ struct NodeStatArgs {
   const uint64_t *pcnt, *pmin, *psq;
   const uint32_t *subend;         // [u]
   const uint64_t *excl, *incl;    // [u][m]
-  uint64_t *rows, *prefix;        // [u][1 + 4m], [u + 1][1 + 4m]
-  uint64_t *exmin, *pre, *suf;    // [u][m]
-  uint64_t *tab;                  // [levels][nblk][m]
+  uint64_t *rows, *prefix;        // [d][1 + 4m], [d + 1][1 + 4m], canonical path order
+  uint32_t *node_path;            // [u]: canonical position of the path that created the node
+  uint64_t *cmin, *pre, *suf;     // [d][m]
+  uint64_t *tab;                  // [levels][nblk][m], nblk = rmq_blocks(d)
   int64_t nblk;
   int levels;
   NodeStatOut out;

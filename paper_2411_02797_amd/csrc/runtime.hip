@@ -911,19 +911,21 @@ cct_status cct_stats(const cct_tree *tree, void *hip_stream, const cct_node_stat
   if (dev != tree->device) return fail(CCT_EINVAL, "tree belongs to another device");
   hipStream_t s = (hipStream_t)hip_stream;
   const int32_t m = tree->m;
-  const int64_t U = tree->u, C = 1 + 4 * (int64_t)m;
-  const int64_t nblk = rmq_blocks(U);
+  const int64_t U = tree->u, D = tree->d, C = 1 + 4 * (int64_t)m;
+  const int64_t nblk = std::max<int64_t>(rmq_blocks(D), 1);
   const int levels = floor_log2((uint64_t)nblk) + 1;
-  Buf rows, prefix, blk, exmin, pre, suf, tab;
-  if (!rows.alloc(U * C * 8) || !prefix.alloc((U + 1) * C * 8) || !blk.alloc((U / 1024 + 2) * C * 8) ||
-      !exmin.alloc(U * m * 8) || !pre.alloc(U * m * 8) || !suf.alloc(U * m * 8) || !tab.alloc(levels * nblk * m * 8))
+  Buf rows, prefix, blk, node_path, cmin, pre, suf, tab;
+  if (!rows.alloc(D * C * 8) || !prefix.alloc((D + 1) * C * 8) || !blk.alloc((D / 1024 + 2) * C * 8) ||
+      !node_path.alloc(U * 4) || !cmin.alloc(D * m * 8) || !pre.alloc(D * m * 8) || !suf.alloc(D * m * 8) ||
+      !tab.alloc(levels * nblk * m * 8))
     return fail(CCT_ENOMEM, "device allocation failed");
   NodeStatArgs a{};
   a.u = U; a.d = tree->d; a.m = m;
   a.scan_out = tree->scan_out.as<uint64_t>(); a.order = tree->order.as<uint32_t>();
   a.pcnt = tree->pcnt.as<uint64_t>(); a.pmin = tree->pmin.as<uint64_t>(); a.psq = tree->psq.as<uint64_t>();
   a.subend = tree->subend.as<uint32_t>(); a.excl = tree->excl.as<uint64_t>(); a.incl = tree->incl.as<uint64_t>();
-  a.rows = rows.as<uint64_t>(); a.prefix = prefix.as<uint64_t>(); a.exmin = exmin.as<uint64_t>();
+  a.rows = rows.as<uint64_t>(); a.prefix = prefix.as<uint64_t>(); a.node_path = node_path.as<uint32_t>();
+  a.cmin = cmin.as<uint64_t>();
   a.pre = pre.as<uint64_t>(); a.suf = suf.as<uint64_t>(); a.tab = tab.as<uint64_t>();
   a.nblk = nblk; a.levels = levels;
   a.out = NodeStatOut{out->count_excl, out->count_incl, out->min_excl, out->min_incl, out->sumsq_excl,

@@ -8,12 +8,14 @@
 //   min[j]          smallest value of metric j
 //   sumsq[j]        sum of squares of metric j, exact modulo 2^128 (two words, low first)
 // Per node, on request (cct_stats): the exclusive values are those of the path ending at
-// the node; the inclusive ones combine the paths of the node's subtree, which is the id
-// range [u, subend[u]) in preorder: counts and sums of squares by differences of prefix
-// sums over node order, minima by a range-minimum structure (in-block prefix and suffix
-// minima over 64-node blocks plus a sparse table over the blocks).  The mean is sum /
-// count and the deviation the population one, sqrt(n * S2 - S1^2) / n, with the 192-bit
-// integer n * S2 - S1^2 computed exactly and rounded once to float64.
+// the node; the inclusive ones combine the paths of the node's subtree, which are the
+// canonical positions [i, e): i is the path that created the node, e the path that created
+// node subend[u] (the first node after the subtree), or D.  Counts and sums of squares come
+// from differences of prefix sums over the D paths in canonical order, minima from a
+// range-minimum structure over them (in-block prefix and suffix minima over 64-path blocks
+// plus a sparse table over the blocks).  The mean is sum / count and the deviation the
+// population one, sqrt(n * S2 - S1^2) / n, with the 192-bit integer n * S2 - S1^2 computed
+// exactly and rounded once to float64.
 #include "common.h"
 
 namespace cct {
@@ -127,32 +129,35 @@ __global__ void stats_fold_kernel(int64_t D, int64_t d_old, int32_t m, const uin
 }
 
 // ---- node statistics on request ---------------------------------------------------------
-// Row of node u for the prefix sums: [count, then per metric the four 32-bit limbs of
-// its sum of squares], each in a 64-bit column; a limb column's prefix over at most 2^32
-// nodes stays below 2^64, so every difference of prefixes is exact.
-__global__ void node_fill_kernel(NodeStatArgs a) {
-  const int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (u >= a.u) return;
+// Row of the path at canonical position r for the prefix sums: [count, then per metric the
+// four 32-bit limbs of its sum of squares], each in a 64-bit column; a limb column's prefix
+// over fewer than 2^32 paths stays below 2^64, so every difference of prefixes is exact.
+// cmin[r] holds the path's minima in canonical order.
+__global__ void path_rows_kernel(NodeStatArgs a) {
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= a.d) return;
+  const uint64_t pid = a.order[r];
   const int C = 1 + 4 * a.m;
-  for (int c = 0; c < C; ++c) a.rows[u * C + c] = 0;
-  for (int j = 0; j < a.m; ++j) a.exmin[u * a.m + j] = ~0ull;
-}
-
-// path at canonical position i ends at node scan_out[(i + 1) * (1 + m)] (its first new node
-// plus its new-node count, minus one; the empty path ends at the root)
-__global__ void node_scatter_kernel(NodeStatArgs a) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= a.d) return;
-  const int64_t u = (int64_t)a.scan_out[(i + 1) * (1 + a.m)];
-  const uint64_t pid = a.order[i];
-  const int C = 1 + 4 * a.m;
-  a.rows[u * C] = a.pcnt[pid];
+  uint64_t *row = a.rows + r * C;
+  row[0] = a.pcnt[pid];
   for (int j = 0; j < a.m; ++j) {
     const uint64_t lo = a.psq[(pid * a.m + j) * 2], hi = a.psq[(pid * a.m + j) * 2 + 1];
-    uint64_t *r = a.rows + u * C + 1 + 4 * j;
-    r[0] = lo & 0xFFFFFFFFull; r[1] = lo >> 32; r[2] = hi & 0xFFFFFFFFull; r[3] = hi >> 32;
-    a.exmin[u * a.m + j] = a.pmin[pid * a.m + j];
+    row[1 + 4 * j] = lo & 0xFFFFFFFFull;
+    row[2 + 4 * j] = lo >> 32;
+    row[3 + 4 * j] = hi & 0xFFFFFFFFull;
+    row[4 + 4 * j] = hi >> 32;
+    a.cmin[r * a.m + j] = a.pmin[pid * a.m + j];
   }
+}
+
+// the path at canonical position r created nodes [1 + scan_out[r], 1 + scan_out[r + 1])
+// (column 0 of the emission's scan counts new nodes); its last one is where it ends
+__global__ void node_path_kernel(NodeStatArgs a) {
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= a.d) return;
+  const int C0 = 1 + a.m;
+  const uint64_t b = 1 + a.scan_out[r * C0], e = 1 + a.scan_out[(r + 1) * C0];
+  for (uint64_t u = b; u < e; ++u) a.node_path[u] = (uint32_t)r;
 }
 
 __device__ inline uint64_t min_u64(uint64_t x, uint64_t y) { return x < y ? x : y; }
@@ -169,21 +174,21 @@ __device__ inline uint64_t shfl_down_u64(uint64_t v, int o) {
   return ((uint64_t)hi << 32) | lo;
 }
 
-// one wave per block of kRmqBlock nodes: pre[v] = min of the block's nodes up to v,
+// one wave per block of kRmqBlock paths: pre[v] = min of the block's paths up to v,
 // suf[v] = min from v to the block's end, tab level 0 = the block's minimum
 __global__ __launch_bounds__(64) void rmq_block_kernel(NodeStatArgs a) {
   const int64_t blk = blockIdx.x;
   const int lane = threadIdx.x;
   const int64_t v = blk * kRmqBlock + lane;
   for (int j = 0; j < a.m; ++j) {
-    const uint64_t x = v < a.u ? a.exmin[v * a.m + j] : ~0ull;
+    const uint64_t x = v < a.d ? a.cmin[v * a.m + j] : ~0ull;
     uint64_t p = x, q = x;
     for (int o = 1; o < 64; o <<= 1) {
       const uint64_t y = shfl_up_u64(p, o), z = shfl_down_u64(q, o);
       if (lane >= o) p = min_u64(p, y);
       if (lane + o < 64) q = min_u64(q, z);
     }
-    if (v < a.u) {
+    if (v < a.d) {
       a.pre[v * a.m + j] = p;
       a.suf[v * a.m + j] = q;
     }
@@ -205,12 +210,12 @@ __global__ void rmq_level_kernel(NodeStatArgs a, int k) {
 
 __device__ inline int floor_log2_u64(uint64_t x) { return 63 - __clzll((long long)x); }
 
-// minimum of metric j over nodes [l, r] (inclusive, r >= l)
+// minimum of metric j over the paths at canonical positions [l, r] (inclusive, r >= l)
 __device__ uint64_t range_min(const NodeStatArgs &a, int64_t l, int64_t r, int j) {
   const int64_t bl = l / kRmqBlock, br = r / kRmqBlock;
   if (bl == br) {
     uint64_t x = ~0ull;
-    for (int64_t v = l; v <= r; ++v) x = min_u64(x, a.exmin[v * a.m + j]);
+    for (int64_t v = l; v <= r; ++v) x = min_u64(x, a.cmin[v * a.m + j]);
     return x;
   }
   uint64_t x = min_u64(a.suf[l * a.m + j], a.pre[r * a.m + j]);
@@ -276,20 +281,30 @@ __device__ inline double mean_of(uint64_t s1, uint64_t n) {
 __global__ void node_final_kernel(NodeStatArgs a) {
   const int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (u >= a.u) return;
-  const int C = 1 + 4 * a.m, m = a.m;
-  const int64_t r = a.subend[u];
-  const uint64_t *row = a.rows + u * C, *pu = a.prefix + u * C, *pr = a.prefix + r * C;
-  const uint64_t n_ex = row[0], n_in = pr[0] - pu[0];
+  const int C = 1 + 4 * a.m, C0 = 1 + a.m, m = a.m;
+  // the subtree's paths [i, e) and the path ending at u, if any (the root: all paths, and
+  // the empty path if there is one, which sorts first and creates no node)
+  int64_t i = 0, e = a.d, own = -1;
+  if (u == 0) {
+    if (a.d > 0 && a.scan_out[C0] == 0) own = 0;
+  } else {
+    i = a.node_path[u];
+    const uint32_t se = a.subend[u];
+    e = se < a.u ? (int64_t)a.node_path[se] : a.d;
+    if ((uint64_t)u == a.scan_out[(i + 1) * C0]) own = i;
+  }
+  const uint64_t *pi = a.prefix + i * C, *pe = a.prefix + e * C, *row = own >= 0 ? a.rows + own * C : nullptr;
+  const uint64_t n_ex = row ? row[0] : 0, n_in = pe[0] - pi[0];
   if (a.out.count_excl) a.out.count_excl[u] = n_ex;
   if (a.out.count_incl) a.out.count_incl[u] = n_in;
   for (int j = 0; j < m; ++j) {
     const int64_t o = u * m + j;
-    uint64_t ex_lo, ex_hi, in_lo, in_hi;
-    limbs_to_u128(row[1 + 4 * j], row[2 + 4 * j], row[3 + 4 * j], row[4 + 4 * j], ex_lo, ex_hi);
-    limbs_to_u128(pr[1 + 4 * j] - pu[1 + 4 * j], pr[2 + 4 * j] - pu[2 + 4 * j], pr[3 + 4 * j] - pu[3 + 4 * j],
-                  pr[4 + 4 * j] - pu[4 + 4 * j], in_lo, in_hi);
-    if (a.out.min_excl) a.out.min_excl[o] = a.exmin[o];
-    if (a.out.min_incl) a.out.min_incl[o] = range_min(a, u, r - 1, j);
+    uint64_t ex_lo = 0, ex_hi = 0, in_lo, in_hi;
+    if (row) limbs_to_u128(row[1 + 4 * j], row[2 + 4 * j], row[3 + 4 * j], row[4 + 4 * j], ex_lo, ex_hi);
+    limbs_to_u128(pe[1 + 4 * j] - pi[1 + 4 * j], pe[2 + 4 * j] - pi[2 + 4 * j], pe[3 + 4 * j] - pi[3 + 4 * j],
+                  pe[4 + 4 * j] - pi[4 + 4 * j], in_lo, in_hi);
+    if (a.out.min_excl) a.out.min_excl[o] = own >= 0 ? a.cmin[own * m + j] : ~0ull;
+    if (a.out.min_incl) a.out.min_incl[o] = e > i ? range_min(a, i, e - 1, j) : ~0ull;
     if (a.out.sumsq_excl) { a.out.sumsq_excl[2 * o] = ex_lo; a.out.sumsq_excl[2 * o + 1] = ex_hi; }
     if (a.out.sumsq_incl) { a.out.sumsq_incl[2 * o] = in_lo; a.out.sumsq_incl[2 * o + 1] = in_hi; }
     const uint64_t s_ex = a.excl[o], s_in = a.incl[o];
@@ -340,12 +355,14 @@ void launch_stats_fold(int64_t D, int64_t d_old, int32_t m, const uint32_t *pslo
 int64_t rmq_blocks(int64_t u) { return (u + kRmqBlock - 1) / kRmqBlock; }
 
 void launch_node_stats(const NodeStatArgs &a, uint64_t *scan_blk, hipStream_t s) {
-  hipLaunchKernelGGL(node_fill_kernel, dim3(blocks_for(a.u, 256)), dim3(256), 0, s, a);
-  if (a.d > 0) hipLaunchKernelGGL(node_scatter_kernel, dim3(blocks_for(a.d, 256)), dim3(256), 0, s, a);
-  launch_scan(a.rows, a.u, 1 + 4 * a.m, scan_blk, a.prefix, s);
-  hipLaunchKernelGGL(rmq_block_kernel, dim3((unsigned)a.nblk), dim3(64), 0, s, a);
-  for (int k = 1; k < a.levels; ++k)
-    hipLaunchKernelGGL(rmq_level_kernel, dim3(blocks_for(a.nblk, 256)), dim3(256), 0, s, a, k);
+  if (a.d > 0) {
+    hipLaunchKernelGGL(path_rows_kernel, dim3(blocks_for(a.d, 256)), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(node_path_kernel, dim3(blocks_for(a.d, 256)), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(rmq_block_kernel, dim3((unsigned)a.nblk), dim3(64), 0, s, a);
+    for (int k = 1; k < a.levels; ++k)
+      hipLaunchKernelGGL(rmq_level_kernel, dim3(blocks_for(a.nblk, 256)), dim3(256), 0, s, a, k);
+  }
+  launch_scan(a.rows, a.d, 1 + 4 * a.m, scan_blk, a.prefix, s);
   hipLaunchKernelGGL(node_final_kernel, dim3(blocks_for(a.u, 256)), dim3(256), 0, s, a);
 }
 
