@@ -363,6 +363,23 @@ void launch_filter_write(int64_t u, const uint64_t *mask, const uint64_t *pos, i
 struct StatDelta {  // one batch, by table slot: cnt [cap], min [cap][m], sq [cap][m][2]
   uint64_t *cnt, *min, *sq;
 };
+struct StatStage {  // staged per-slot statistics (nbuckets = 0: device atomics instead)
+  int32_t bshift;       // bucket of slot s: s >> bshift
+  int64_t nbuckets;
+  int grid;             // workgroups of the per-slot kernel
+  int64_t map_entries;  // LDS map entries per workgroup
+  uint32_t *ev_slot;    // [N] misses: workgroup g's from its first event index on
+  uint64_t *ev_w;       // [N][m]
+  uint32_t *map_key;    // [grid][map_entries]
+  uint64_t *map_rec;    // [grid][map_entries][1 + 3m]: count, min[m], sq[m][2]
+  uint64_t *hist_ev, *hist_map;  // [nbuckets][grid] entries per bucket and workgroup
+  uint64_t *off_ev, *off_map;    // their exclusive scans, [nbuckets * grid + 1]
+  uint32_t *wg_count;   // [grid][2]: misses, map entries
+  uint32_t *st_ev_slot;  // bucketed misses [N], values [N][m]
+  uint64_t *st_ev_w;
+  uint32_t *st_map_key;  // bucketed map entries [grid * map_entries], records
+  uint64_t *st_map_rec;
+};
 struct PathStats {  // kept per path: cnt [D], min [D][m], sq [D][m][2]
   uint64_t *cnt, *min, *sq;
 };
@@ -389,9 +406,11 @@ struct NodeStatArgs {
   int levels;
   NodeStatOut out;
 };
-int64_t stats_map_entries(int32_t m);
-void launch_stats_agg(const uint32_t *slot_of, const uint64_t *w, int64_t n, int32_t m, int grid, const StatDelta &d,
-                      hipStream_t s);
+int64_t stats_staged_entries(int32_t m);
+int stats_bucket_shift(int32_t m);
+int64_t stats_max_buckets();
+void launch_stats_agg(const uint32_t *slot_of, const uint64_t *w, int64_t n, int32_t m, uint64_t cap, int grid,
+                      const StatDelta &d, const StatStage &st, uint64_t *scan_blk, hipStream_t s);
 void launch_stats_fold(int64_t D, int64_t d_old, int32_t m, const uint32_t *pslot, const StatDelta &d,
                        const PathStats &p, hipStream_t s);
 int64_t rmq_blocks(int64_t u);

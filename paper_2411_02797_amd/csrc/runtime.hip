@@ -391,13 +391,37 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     return st;
   };
   if (sum_len + 1 > (int64_t)0xFFFFFFFE) return rollback(fail(CCT_EOVERFLOW, "tree would exceed 2^32-2 nodes"));
-  // this batch's statistics by table slot (before anything of the tree changes)
-  Buf d_cnt, d_min, d_sq;
+  // this batch's statistics by table slot (before anything of the tree changes): staged in
+  // slot-range buckets when the table has few enough of them (a test setting forces device
+  // atomics instead)
+  Buf d_cnt, d_min, d_sq, sg_ev_slot, sg_ev_w, sg_map_key, sg_map_rec, sg_hist, sg_off, sg_blk, sg_wg, sg_st_slot,
+      sg_st_w, sg_st_key, sg_st_rec;
   StatDelta sd{};
+  StatStage sst{};
+  const int st_grid = (int)std::max<int64_t>(1, std::min<int64_t>((N + 8191) / 8192, (int64_t)cu_count() * 2));
   if (t->stats && N > 0) {
     if (!d_cnt.alloc(t->cap * 8) || !d_min.alloc(t->cap * m * 8) || !d_sq.alloc(t->cap * m * 16))
       return rollback(fail(CCT_ENOMEM, "device allocation failed"));
     sd.cnt = d_cnt.as<uint64_t>(); sd.min = d_min.as<uint64_t>(); sd.sq = d_sq.as<uint64_t>();
+    const int bshift = stats_bucket_shift(m);
+    const int64_t nbk = (int64_t)((t->cap + (1ull << bshift) - 1) >> bshift);
+    if (nbk <= stats_max_buckets() && !env_int("CCT_TEST_STATS_ATOMIC", 0)) {
+      const int64_t me = stats_staged_entries(m), R = 1 + 3 * (int64_t)m, rows = nbk * st_grid;
+      const int64_t nmap = st_grid * me;
+      if (!sg_ev_slot.alloc(N * 4) || !sg_ev_w.alloc(N * m * 8) || !sg_map_key.alloc(nmap * 4) ||
+          !sg_map_rec.alloc(nmap * R * 8) || !sg_hist.alloc(2 * rows * 8) || !sg_off.alloc(2 * (rows + 1) * 8) ||
+          !sg_blk.alloc((rows / 1024 + 2) * 8) || !sg_wg.alloc(st_grid * 8) || !sg_st_slot.alloc(N * 4) ||
+          !sg_st_w.alloc(N * m * 8) || !sg_st_key.alloc(nmap * 4) || !sg_st_rec.alloc(nmap * R * 8))
+        return rollback(fail(CCT_ENOMEM, "device allocation failed"));
+      sst.bshift = bshift; sst.nbuckets = nbk; sst.grid = st_grid; sst.map_entries = me;
+      sst.ev_slot = sg_ev_slot.as<uint32_t>(); sst.ev_w = sg_ev_w.as<uint64_t>();
+      sst.map_key = sg_map_key.as<uint32_t>(); sst.map_rec = sg_map_rec.as<uint64_t>();
+      sst.hist_ev = sg_hist.as<uint64_t>(); sst.hist_map = sst.hist_ev + rows;
+      sst.off_ev = sg_off.as<uint64_t>(); sst.off_map = sst.off_ev + rows + 1;
+      sst.wg_count = sg_wg.as<uint32_t>();
+      sst.st_ev_slot = sg_st_slot.as<uint32_t>(); sst.st_ev_w = sg_st_w.as<uint64_t>();
+      sst.st_map_key = sg_st_key.as<uint32_t>(); sst.st_map_rec = sg_st_rec.as<uint64_t>();
+    }
   }
   const int64_t store_need = t->store_used + (int64_t)new_store;
   const int64_t dneed = std::max<int64_t>(D, 1);
@@ -517,11 +541,12 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   g_stats_ms = 0;
   if (sd.cnt) {
     ts.mark(0, s);
-    HIP_TRY(hipMemsetAsync(sd.cnt, 0, t->cap * 8, s));
-    HIP_TRY(hipMemsetAsync(sd.min, 0xFF, t->cap * m * 8, s));
-    HIP_TRY(hipMemsetAsync(sd.sq, 0, t->cap * m * 16, s));
-    const int st_grid = (int)std::max<int64_t>(1, std::min<int64_t>((N + 8191) / 8192, (int64_t)cu_count() * 2));
-    launch_stats_agg(slot_of.as<uint32_t>(), p->metrics, N, m, st_grid, sd, s);
+    if (!sst.nbuckets) {  // the staged reduction writes every slot; device atomics need a cleared start
+      HIP_TRY(hipMemsetAsync(sd.cnt, 0, t->cap * 8, s));
+      HIP_TRY(hipMemsetAsync(sd.min, 0xFF, t->cap * m * 8, s));
+      HIP_TRY(hipMemsetAsync(sd.sq, 0, t->cap * m * 16, s));
+    }
+    launch_stats_agg(slot_of.as<uint32_t>(), p->metrics, N, m, t->cap, st_grid, sd, sst, sg_blk.as<uint64_t>(), s);
     ts.mark(1, s);
   }
 

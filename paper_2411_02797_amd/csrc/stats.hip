@@ -25,12 +25,27 @@ namespace {
 constexpr uint32_t kStatEmpty = 0xFFFFFFFFu;
 constexpr int kStatThreads = 1024;
 constexpr int kStatLdsBytes = 163840 - 256;
-constexpr int kRmqBlock = 64;  // nodes per range-minimum block (one wave)
+constexpr int kRmqBlock = 64;  // paths per range-minimum block (one wave)
+constexpr int kStageHist = 4096;  // most slot-range buckets of the staged per-slot statistics
+constexpr int ilog2(int x) { return x <= 1 ? 0 : 1 + ilog2(x / 2); }
 
 constexpr int stat_entries(int m) {
   int e = kStatLdsBytes / (4 + 8 + 24 * m);  // key, count, min and two square words per metric
   if (e > 4096) e = 4096;
   return e & ~63;
+}
+// the staged map leaves room for the per-bucket counts
+constexpr int stat_entries_staged(int m) {
+  int e = (kStatLdsBytes - kStageHist * 4 - 64) / (4 + 8 + 24 * m);
+  if (e > 4096) e = 4096;
+  return e & ~63;
+}
+// slots per bucket: the largest power of two whose records fit the reduction's LDS
+constexpr int kReduceLdsBytes = 120 * 1024;
+constexpr int stage_slots(int m) {
+  int b = 1;
+  while (b * 2 * (1 + 3 * m) * 8 <= kReduceLdsBytes) b *= 2;
+  return b;
 }
 
 // a += (lo, hi) on two 64-bit words modulo 2^128.  The add that wraps the low word sees
@@ -47,20 +62,32 @@ __device__ inline void hbm_add_u128(uint64_t *p, uint64_t lo, uint64_t hi) {
 }
 
 // One batch's samples per table slot.  Each workgroup walks a contiguous range of events
-// and combines them in an LDS map keyed by slot (hot paths meet there), falling back to
-// device atomics when a key's probe window is full; the map is flushed with device
-// atomics.  d.cnt starts at 0, d.min at all ones, d.sq at 0.
-template <int M>
+// [lo, hi) and combines them in an LDS map keyed by slot (hot paths meet there).  An event
+// whose key finds no room in its probe window is a miss:
+//   staged (kStaged): the miss goes with plain stores to the workgroup's own list (entries
+//     lo.. of an N-entry array, so it cannot overflow), and at the end the map's entries go
+//     to a second per-workgroup list; both count their entries per slot-range bucket, and
+//     stats_bucket_kernel and stats_reduce_kernel finish the job without device atomics;
+//   otherwise: misses and the map's entries are added with device atomics (d.cnt starting
+//     at 0, d.min at all ones, d.sq at 0).
+template <int M, bool kStaged>
 __global__ __launch_bounds__(kStatThreads) void stats_agg_kernel(const uint32_t *slot_of, const uint64_t *w,
-                                                                 int64_t n, StatDelta d) {
-  constexpr int kE = stat_entries(M);
+                                                                 int64_t n, StatDelta d, StatStage st) {
+  constexpr int kE = kStaged ? stat_entries_staged(M) : stat_entries(M);
+  constexpr int R = 1 + 3 * M;  // record: count, min[M], sq[M][2]
   __shared__ uint32_t key[kE];
   __shared__ uint64_t cnt[kE];
   __shared__ uint64_t mn[kE * M];
   __shared__ uint64_t sq[kE * M * 2];
+  __shared__ uint32_t hist[kStaged ? kStageHist : 1];
+  __shared__ uint32_t n_miss, n_map;
   const int tid = threadIdx.x;
   for (int i = tid; i < kE; i += kStatThreads) { key[i] = kStatEmpty; cnt[i] = 0; }
   for (int i = tid; i < kE * M; i += kStatThreads) { mn[i] = ~0ull; sq[2 * i] = 0; sq[2 * i + 1] = 0; }
+  if (kStaged) {
+    for (int i = tid; i < st.nbuckets; i += kStatThreads) hist[i] = 0;
+    if (tid == 0) { n_miss = 0; n_map = 0; }
+  }
   __syncthreads();
   const int64_t b = blockIdx.x, nb = gridDim.x;
   const int64_t lo = b * n / nb, hi = (b + 1) * n / nb;
@@ -85,6 +112,12 @@ __global__ __launch_bounds__(kStatThreads) void stats_agg_kernel(const uint32_t 
         atomicMin((unsigned long long *)&mn[mi * M + j], (unsigned long long)v[j]);
         lds_add_u128(&sq[(mi * M + j) * 2], v[j] * v[j], __umul64hi(v[j], v[j]));
       }
+    } else if (kStaged) {
+      const int64_t at = lo + atomicAdd(&n_miss, 1u);
+      st.ev_slot[at] = s;
+#pragma unroll
+      for (int j = 0; j < M; ++j) st.ev_w[at * M + j] = v[j];
+      atomicAdd(&hist[s >> st.bshift], 1u);
     } else {
       atomicAdd((unsigned long long *)&d.cnt[s], 1ull);
 #pragma unroll
@@ -95,6 +128,36 @@ __global__ __launch_bounds__(kStatThreads) void stats_agg_kernel(const uint32_t 
     }
   }
   __syncthreads();
+  if (kStaged) {
+    const int64_t nbk = st.nbuckets;
+    for (int64_t i = tid; i < nbk; i += kStatThreads) {
+      st.hist_ev[i * nb + b] = hist[i];
+      hist[i] = 0;
+    }
+    __syncthreads();
+    for (int k = tid; k < kE; k += kStatThreads) {
+      const uint32_t s = key[k];
+      if (s == kStatEmpty) continue;
+      const int64_t at = b * kE + atomicAdd(&n_map, 1u);
+      st.map_key[at] = s;
+      uint64_t *rec = st.map_rec + at * R;
+      rec[0] = cnt[k];
+#pragma unroll
+      for (int j = 0; j < M; ++j) {
+        rec[1 + j] = mn[k * M + j];
+        rec[1 + M + 2 * j] = sq[(k * M + j) * 2];
+        rec[2 + M + 2 * j] = sq[(k * M + j) * 2 + 1];
+      }
+      atomicAdd(&hist[s >> st.bshift], 1u);
+    }
+    __syncthreads();
+    for (int64_t i = tid; i < nbk; i += kStatThreads) st.hist_map[i * nb + b] = hist[i];
+    if (tid == 0) {
+      st.wg_count[2 * b] = n_miss;
+      st.wg_count[2 * b + 1] = n_map;
+    }
+    return;
+  }
   for (int k = tid; k < kE; k += kStatThreads) {
     const uint32_t s = key[k];
     if (s == kStatEmpty) continue;
@@ -103,6 +166,89 @@ __global__ __launch_bounds__(kStatThreads) void stats_agg_kernel(const uint32_t 
     for (int j = 0; j < M; ++j) {
       atomicMin((unsigned long long *)&d.min[(uint64_t)s * M + j], (unsigned long long)mn[k * M + j]);
       hbm_add_u128(&d.sq[((uint64_t)s * M + j) * 2], sq[(k * M + j) * 2], sq[(k * M + j) * 2 + 1]);
+    }
+  }
+}
+
+// Workgroup g moves its two lists into their buckets: bucket k's entries from workgroup g
+// start at off[k * grid + g] (the exclusive scan of the counts, bucket-major), and a rank
+// within them comes from an LDS cursor per bucket.
+template <int M>
+__global__ __launch_bounds__(kStatThreads) void stats_bucket_kernel(int64_t n, StatStage st) {
+  constexpr int R = 1 + 3 * M;
+  __shared__ uint64_t cur[kStageHist];
+  const int tid = threadIdx.x;
+  const int64_t b = blockIdx.x, nb = gridDim.x, nbk = st.nbuckets;
+  const int64_t lo = b * n / nb;
+  for (int64_t i = tid; i < nbk; i += kStatThreads) cur[i] = st.off_ev[i * nb + b];
+  __syncthreads();
+  const uint32_t n_miss = st.wg_count[2 * b], n_map = st.wg_count[2 * b + 1];
+  for (uint32_t i = tid; i < n_miss; i += kStatThreads) {
+    const uint32_t s = st.ev_slot[lo + i];
+    const uint64_t at = atomicAdd((unsigned long long *)&cur[s >> st.bshift], 1ull);
+    st.st_ev_slot[at] = s;
+#pragma unroll
+    for (int j = 0; j < M; ++j) st.st_ev_w[at * M + j] = st.ev_w[(lo + i) * M + j];
+  }
+  __syncthreads();
+  for (int64_t i = tid; i < nbk; i += kStatThreads) cur[i] = st.off_map[i * nb + b];
+  __syncthreads();
+  const int64_t m0 = b * st.map_entries;
+  for (uint32_t i = tid; i < n_map; i += kStatThreads) {
+    const uint32_t s = st.map_key[m0 + i];
+    const uint64_t at = atomicAdd((unsigned long long *)&cur[s >> st.bshift], 1ull);
+    st.st_map_key[at] = s;
+#pragma unroll
+    for (int r = 0; r < R; ++r) st.st_map_rec[at * R + r] = st.map_rec[(m0 + i) * R + r];
+  }
+}
+
+// One workgroup per bucket of kB = 2^bshift slots: sums its misses and map entries into
+// LDS records and writes every slot of its range (so d needs no clearing).
+template <int M>
+__global__ __launch_bounds__(kStatThreads) void stats_reduce_kernel(StatStage st, uint64_t cap, StatDelta d) {
+  constexpr int kB = stage_slots(M), R = 1 + 3 * M;
+  __shared__ uint64_t cnt[kB];
+  __shared__ uint64_t mn[kB * M];
+  __shared__ uint64_t sq[kB * M * 2];
+  const int tid = threadIdx.x;
+  for (int i = tid; i < kB; i += kStatThreads) cnt[i] = 0;
+  for (int i = tid; i < kB * M; i += kStatThreads) { mn[i] = ~0ull; sq[2 * i] = 0; sq[2 * i + 1] = 0; }
+  __syncthreads();
+  const int64_t bk = blockIdx.x, g = st.grid;
+  const uint64_t s0 = (uint64_t)bk << st.bshift;
+  const uint64_t e0 = st.off_ev[bk * g], e1 = st.off_ev[(bk + 1) * g];
+  for (uint64_t i = e0 + tid; i < e1; i += kStatThreads) {
+    const uint32_t l = (uint32_t)(st.st_ev_slot[i] - s0);
+    atomicAdd((unsigned long long *)&cnt[l], 1ull);
+#pragma unroll
+    for (int j = 0; j < M; ++j) {
+      const uint64_t v = st.st_ev_w[i * M + j];
+      atomicMin((unsigned long long *)&mn[l * M + j], (unsigned long long)v);
+      lds_add_u128(&sq[(l * M + j) * 2], v * v, __umul64hi(v, v));
+    }
+  }
+  const uint64_t m0 = st.off_map[bk * g], m1 = st.off_map[(bk + 1) * g];
+  for (uint64_t i = m0 + tid; i < m1; i += kStatThreads) {
+    const uint32_t l = (uint32_t)(st.st_map_key[i] - s0);
+    const uint64_t *rec = st.st_map_rec + i * R;
+    atomicAdd((unsigned long long *)&cnt[l], (unsigned long long)rec[0]);
+#pragma unroll
+    for (int j = 0; j < M; ++j) {
+      atomicMin((unsigned long long *)&mn[l * M + j], (unsigned long long)rec[1 + j]);
+      lds_add_u128(&sq[(l * M + j) * 2], rec[1 + M + 2 * j], rec[2 + M + 2 * j]);
+    }
+  }
+  __syncthreads();
+  for (int i = tid; i < kB; i += kStatThreads) {
+    const uint64_t slot = s0 + (uint64_t)i;
+    if (slot >= cap) break;
+    d.cnt[slot] = cnt[i];
+#pragma unroll
+    for (int j = 0; j < M; ++j) {
+      d.min[slot * M + j] = mn[i * M + j];
+      d.sq[(slot * M + j) * 2] = sq[(i * M + j) * 2];
+      d.sq[(slot * M + j) * 2 + 1] = sq[(i * M + j) * 2 + 1];
     }
   }
 }
@@ -319,26 +465,54 @@ inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1)
 
 }  // namespace
 
-int64_t stats_map_entries(int32_t m) {
+int64_t stats_staged_entries(int32_t m) {
   switch (m) {
-    case 1: return stat_entries(1);
-    case 2: return stat_entries(2);
-    case 3: return stat_entries(3);
-    case 4: return stat_entries(4);
-    case 5: return stat_entries(5);
-    case 6: return stat_entries(6);
-    case 7: return stat_entries(7);
-    default: return stat_entries(8);
+    case 1: return stat_entries_staged(1);
+    case 2: return stat_entries_staged(2);
+    case 3: return stat_entries_staged(3);
+    case 4: return stat_entries_staged(4);
+    case 5: return stat_entries_staged(5);
+    case 6: return stat_entries_staged(6);
+    case 7: return stat_entries_staged(7);
+    default: return stat_entries_staged(8);
   }
 }
-
-void launch_stats_agg(const uint32_t *slot_of, const uint64_t *w, int64_t n, int32_t m, int grid, const StatDelta &d,
-                      hipStream_t s) {
-  if (n <= 0) return;
+int stats_bucket_shift(int32_t m) {
   switch (m) {
-#define CCT_STAT_CASE(M)                                                                                   \
-  case M:                                                                                                  \
-    hipLaunchKernelGGL(stats_agg_kernel<M>, dim3(grid), dim3(kStatThreads), 0, s, slot_of, w, n, d);      \
+    case 1: return ilog2(stage_slots(1));
+    case 2: return ilog2(stage_slots(2));
+    case 3: return ilog2(stage_slots(3));
+    case 4: return ilog2(stage_slots(4));
+    case 5: return ilog2(stage_slots(5));
+    case 6: return ilog2(stage_slots(6));
+    case 7: return ilog2(stage_slots(7));
+    default: return ilog2(stage_slots(8));
+  }
+}
+int64_t stats_max_buckets() { return kStageHist; }
+
+// staged (st.nbuckets > 0): the per-slot kernel, the scans of its counts, the bucketing and
+// the per-bucket reduction; otherwise the per-slot kernel with device atomics (d cleared
+// by the caller)
+void launch_stats_agg(const uint32_t *slot_of, const uint64_t *w, int64_t n, int32_t m, uint64_t cap, int grid,
+                      const StatDelta &d, const StatStage &st, uint64_t *scan_blk, hipStream_t s) {
+  if (n <= 0) return;
+  const bool staged = st.nbuckets > 0;
+  const int64_t rows = st.nbuckets * grid;
+  switch (m) {
+#define CCT_STAT_CASE(M)                                                                                           \
+  case M:                                                                                                          \
+    if (staged) {                                                                                                  \
+      hipLaunchKernelGGL((stats_agg_kernel<M, true>), dim3(grid), dim3(kStatThreads), 0, s, slot_of, w, n, d, st); \
+      launch_scan(st.hist_ev, rows, 1, scan_blk, st.off_ev, s);                                                   \
+      launch_scan(st.hist_map, rows, 1, scan_blk, st.off_map, s);                                                 \
+      hipLaunchKernelGGL(stats_bucket_kernel<M>, dim3(grid), dim3(kStatThreads), 0, s, n, st);                    \
+      hipLaunchKernelGGL(stats_reduce_kernel<M>, dim3((unsigned)st.nbuckets), dim3(kStatThreads), 0, s, st, cap, \
+                         d);                                                                                       \
+    } else {                                                                                                       \
+      hipLaunchKernelGGL((stats_agg_kernel<M, false>), dim3(grid), dim3(kStatThreads), 0, s, slot_of, w, n, d,    \
+                         st);                                                                                      \
+    }                                                                                                              \
     break;
     CCT_STAT_CASE(1) CCT_STAT_CASE(2) CCT_STAT_CASE(3) CCT_STAT_CASE(4)
     CCT_STAT_CASE(5) CCT_STAT_CASE(6) CCT_STAT_CASE(7) CCT_STAT_CASE(8)

@@ -81,10 +81,16 @@ def test_stats_full_range_values():
     tree.free()
 
 
-def test_stats_hot_and_cold_paths():
+MODES = pytest.mark.parametrize("atomic", [False, True], ids=["staged", "atomic"])
+
+
+@MODES
+def test_stats_hot_and_cold_paths(atomic, monkeypatch):
     # one path takes most events (LDS maps, same-address atomics); 150,000 distinct paths
-    # overflow every workgroup's map (device atomics)
+    # overflow every workgroup's map (staged lists, or device atomics when forced)
     import paper_2411_02797_amd as cct
+    if atomic:
+        monkeypatch.setenv("CCT_TEST_STATS_ATOMIC", "1")
     n = 200_000
     rng = np.random.default_rng(12)
     hot = rng.random(n) < 0.6
@@ -100,10 +106,13 @@ def test_stats_hot_and_cold_paths():
     tree.free()
 
 
-def test_stats_follow_merges():
+@MODES
+def test_stats_follow_merges(atomic, monkeypatch):
     # a base, a merge of mostly known paths, and one with more new paths than the tree
-    # holds (the path arrays grow); a forced small table makes the ingest regrow it
+    # holds (the path arrays grow)
     import paper_2411_02797_amd as cct
+    if atomic:
+        monkeypatch.setenv("CCT_TEST_STATS_ATOMIC", "1")
     m = 3
     batches = [tracegen.random_paths(3000, 20, 10, m, seed=30),
                tracegen.random_paths(2000, 20, 10, m, seed=31),
@@ -134,9 +143,12 @@ def test_stats_with_table_regrow(monkeypatch):
     tree.free()
 
 
-def test_stats_of_activity_flushes():
+@MODES
+def test_stats_of_activity_flushes(atomic, monkeypatch):
     # one sample per registered call with records (the sum of its records)
     import paper_2411_02797_amd as cct
+    if atomic:
+        monkeypatch.setenv("CCT_TEST_STATS_ATOMIC", "1")
     torch = torch_or_skip()
     m = 2
     o, f, w = tracegen.random_paths(2000, 25, 10, m, seed=40)
