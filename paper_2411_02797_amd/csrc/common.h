@@ -360,15 +360,12 @@ void launch_filter_write(int64_t u, const uint64_t *mask, const uint64_t *pos, i
                          hipStream_t s);
 
 // Per-path and per-node statistics (stats.hip)
-struct StatDelta {  // one batch, by table slot: cnt [cap], min [cap][m], sq [cap][m][2]
-  uint64_t *cnt, *min, *sq;
-};
-struct StatStage {  // staged per-slot statistics (nbuckets = 0: device atomics instead)
-  int32_t bshift;       // bucket of slot s: s >> bshift
+struct StatStage {  // staged per-path statistics of a batch (nbuckets = 0: device atomics instead)
+  int32_t bshift;       // bucket of path i: i >> bshift
   int64_t nbuckets;
   int grid;             // workgroups of the per-slot kernel
   int64_t map_entries;  // LDS map entries per workgroup
-  uint32_t *ev_slot;    // [N] misses: workgroup g's from its first event index on
+  uint32_t *ev_slot;    // [N] misses (path indices): workgroup g's from its first event index on
   uint64_t *ev_w;       // [N][m]
   uint32_t *map_key;    // [grid][map_entries]
   uint64_t *map_rec;    // [grid][map_entries][1 + 3m]: count, min[m], sq[m][2]
@@ -407,12 +404,13 @@ struct NodeStatArgs {
   NodeStatOut out;
 };
 int64_t stats_staged_entries(int32_t m);
-int stats_bucket_shift(int32_t m);
+int stats_bucket_shift(int32_t m);  // largest bucket: 2^shift paths
 int64_t stats_max_buckets();
-void launch_stats_agg(const uint32_t *slot_of, const uint64_t *w, int64_t n, int32_t m, uint64_t cap, int grid,
-                      const StatDelta &d, const StatStage &st, uint64_t *scan_blk, hipStream_t s);
-void launch_stats_fold(int64_t D, int64_t d_old, int32_t m, const uint32_t *pslot, const StatDelta &d,
-                       const PathStats &p, hipStream_t s);
+// slot -> path map for paths [0, D); paths [d_old, D) set to no sample
+void launch_stats_prepare(int64_t D, int64_t d_old, int32_t m, const uint32_t *pslot, uint32_t *path_of_slot,
+                          const PathStats &p, hipStream_t s);
+void launch_stats_agg(const uint32_t *slot_of, const uint32_t *path_of_slot, const uint64_t *w, int64_t n, int32_t m,
+                      int64_t D, int grid, const PathStats &p, const StatStage &st, uint64_t *scan_blk, hipStream_t s);
 int64_t rmq_blocks(int64_t u);
 void launch_node_stats(const NodeStatArgs &a, uint64_t *scan_blk, hipStream_t s);
 

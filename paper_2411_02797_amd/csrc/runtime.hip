@@ -391,20 +391,21 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     return st;
   };
   if (sum_len + 1 > (int64_t)0xFFFFFFFE) return rollback(fail(CCT_EOVERFLOW, "tree would exceed 2^32-2 nodes"));
-  // this batch's statistics by table slot (before anything of the tree changes): staged in
-  // slot-range buckets when the table has few enough of them (a test setting forces device
-  // atomics instead)
-  Buf d_cnt, d_min, d_sq, sg_ev_slot, sg_ev_w, sg_map_key, sg_map_rec, sg_hist, sg_off, sg_blk, sg_wg, sg_st_slot,
-      sg_st_w, sg_st_key, sg_st_rec;
-  StatDelta sd{};
+  // this batch's statistics, staged in path-range buckets when there are few enough of them
+  // (a test setting forces device atomics instead); allocated before anything of the tree
+  // changes
+  Buf sg_pos, sg_ev_slot, sg_ev_w, sg_map_key, sg_map_rec, sg_hist, sg_off, sg_blk, sg_wg, sg_st_slot, sg_st_w,
+      sg_st_key, sg_st_rec;
   StatStage sst{};
+  const bool keep_stats = t->stats && N > 0;
   const int st_grid = (int)std::max<int64_t>(1, std::min<int64_t>((N + 8191) / 8192, (int64_t)cu_count() * 2));
-  if (t->stats && N > 0) {
-    if (!d_cnt.alloc(t->cap * 8) || !d_min.alloc(t->cap * m * 8) || !d_sq.alloc(t->cap * m * 16))
-      return rollback(fail(CCT_ENOMEM, "device allocation failed"));
-    sd.cnt = d_cnt.as<uint64_t>(); sd.min = d_min.as<uint64_t>(); sd.sq = d_sq.as<uint64_t>();
-    const int bshift = stats_bucket_shift(m);
-    const int64_t nbk = (int64_t)((t->cap + (1ull << bshift) - 1) >> bshift);
+  if (keep_stats) {
+    if (!sg_pos.alloc(t->cap * 4)) return rollback(fail(CCT_ENOMEM, "device allocation failed"));
+    // buckets of 2^bshift paths: about 256 of them, each within the reduction's LDS
+    const int64_t D_all = t->d + (int64_t)n_new;
+    int bshift = 6;
+    while (bshift < stats_bucket_shift(m) && (D_all >> bshift) > 256) ++bshift;
+    const int64_t nbk = (D_all + (1ll << bshift) - 1) >> bshift;
     if (nbk <= stats_max_buckets() && !env_int("CCT_TEST_STATS_ATOMIC", 0)) {
       const int64_t me = stats_staged_entries(m), R = 1 + 3 * (int64_t)m, rows = nbk * st_grid;
       const int64_t nmap = st_grid * me;
@@ -536,19 +537,8 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     ta.ctr = tr_ctr.as<unsigned long long>(); ta.order = order.as<uint32_t>();
   }
 
-  // ---- this batch's statistics by slot -----------------------------------------------------
   Timer ts;
   g_stats_ms = 0;
-  if (sd.cnt) {
-    ts.mark(0, s);
-    if (!sst.nbuckets) {  // the staged reduction writes every slot; device atomics need a cleared start
-      HIP_TRY(hipMemsetAsync(sd.cnt, 0, t->cap * 8, s));
-      HIP_TRY(hipMemsetAsync(sd.min, 0xFF, t->cap * m * 8, s));
-      HIP_TRY(hipMemsetAsync(sd.sq, 0, t->cap * m * 16, s));
-    }
-    launch_stats_agg(slot_of.as<uint32_t>(), p->metrics, N, m, t->cap, st_grid, sd, sst, sg_blk.as<uint64_t>(), s);
-    ts.mark(1, s);
-  }
 
   // ---- publish new paths, fold this call's sums into the old ones -----------------------
   HIP_TRY(hipMemsetAsync(cursor.p, 0, 64, s));
@@ -568,11 +558,13 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     launch_publish(pa, s);
   }
   if (N > 0) launch_fold_old(t->d, m, t->pslot.as<uint32_t>(), delta.as<uint64_t>(), t->psums.as<uint64_t>(), s);
-  if (sd.cnt) {
-    ts.mark(2, s);
+  if (keep_stats) {  // the batch's samples into the path arrays (new paths start empty)
+    ts.mark(0, s);
     PathStats ps{t->pcnt.as<uint64_t>(), t->pmin.as<uint64_t>(), t->psq.as<uint64_t>()};
-    launch_stats_fold(D, t->d, m, t->pslot.as<uint32_t>(), sd, ps, s);
-    ts.mark(3, s);
+    launch_stats_prepare(D, t->d, m, t->pslot.as<uint32_t>(), sg_pos.as<uint32_t>(), ps, s);
+    launch_stats_agg(slot_of.as<uint32_t>(), sg_pos.as<uint32_t>(), p->metrics, N, m, D, st_grid, ps, sst,
+                     sg_blk.as<uint64_t>(), s);
+    ts.mark(1, s);
   }
   HIP_TRY(hipGetLastError());
   tm.mark(3, s);
@@ -617,7 +609,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     HIP_TRY(hipMemsetAsync(cursor.as<unsigned long long>() + 2, 0, 16, s));
   }
   tm.collect(N > 0);
-  if (sd.cnt && ts.ok) g_stats_ms = ts.span(0, 1) + ts.span(2, 3);
+  if (keep_stats && ts.ok) g_stats_ms = ts.span(0, 1);
 
   // ---- commit -------------------------------------------------------------------------------
   t->store_used += (int64_t)hs[0];

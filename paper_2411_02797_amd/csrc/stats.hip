@@ -61,18 +61,36 @@ __device__ inline void hbm_add_u128(uint64_t *p, uint64_t lo, uint64_t hi) {
   if (h) atomicAdd((unsigned long long *)(p + 1), (unsigned long long)h);
 }
 
-// One batch's samples per table slot.  Each workgroup walks a contiguous range of events
-// [lo, hi) and combines them in an LDS map keyed by slot (hot paths meet there).  An event
-// whose key finds no room in its probe window is a miss:
+// The paths new in this batch start from the identity (no sample); the slot -> path map
+// inverts pslot for the batch's slots (every event's slot belongs to a path once the new
+// paths are published).
+__global__ void stats_prepare_kernel(int64_t D, int64_t d_old, int32_t m, const uint32_t *pslot, uint32_t *path_of_slot,
+                                     PathStats p) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= D) return;
+  path_of_slot[pslot[i]] = (uint32_t)i;
+  if (i < d_old) return;
+  p.cnt[i] = 0;
+  for (int j = 0; j < m; ++j) {
+    p.min[i * m + j] = ~0ull;
+    p.sq[(i * m + j) * 2] = 0;
+    p.sq[(i * m + j) * 2 + 1] = 0;
+  }
+}
+
+// One batch's samples, combined per path.  Each workgroup walks a contiguous range of
+// events [lo, hi) and combines them in an LDS map keyed by path (hot paths meet there).  An
+// event whose key finds no room in its probe window is a miss:
 //   staged (kStaged): the miss goes with plain stores to the workgroup's own list (entries
 //     lo.. of an N-entry array, so it cannot overflow), and at the end the map's entries go
-//     to a second per-workgroup list; both count their entries per slot-range bucket, and
+//     to a second per-workgroup list; both count their entries per path-range bucket, and
 //     stats_bucket_kernel and stats_reduce_kernel finish the job without device atomics;
-//   otherwise: misses and the map's entries are added with device atomics (d.cnt starting
-//     at 0, d.min at all ones, d.sq at 0).
+//   otherwise: misses and the map's entries are added into the path arrays with device
+//     atomics.
 template <int M, bool kStaged>
-__global__ __launch_bounds__(kStatThreads) void stats_agg_kernel(const uint32_t *slot_of, const uint64_t *w,
-                                                                 int64_t n, StatDelta d, StatStage st) {
+__global__ __launch_bounds__(kStatThreads) void stats_agg_kernel(const uint32_t *slot_of, const uint32_t *path_of_slot,
+                                                                 const uint64_t *w, int64_t n, PathStats ps,
+                                                                 StatStage st) {
   constexpr int kE = kStaged ? stat_entries_staged(M) : stat_entries(M);
   constexpr int R = 1 + 3 * M;  // record: count, min[M], sq[M][2]
   __shared__ uint32_t key[kE];
@@ -92,11 +110,12 @@ __global__ __launch_bounds__(kStatThreads) void stats_agg_kernel(const uint32_t 
   const int64_t b = blockIdx.x, nb = gridDim.x;
   const int64_t lo = b * n / nb, hi = (b + 1) * n / nb;
   for (int64_t e = lo + tid; e < hi; e += kStatThreads) {
-    const uint32_t s = slot_of[e];
+    const uint32_t slot = slot_of[e];
     uint64_t v[M];
 #pragma unroll
     for (int j = 0; j < M; ++j) v[j] = w[e * M + j];
-    if (s == kNoSlot) continue;
+    if (slot == kNoSlot) continue;
+    const uint32_t s = path_of_slot[slot];
     uint32_t k = __umulhi(hash32(s), (uint32_t)kE);
     int mi = -1;
     for (int t = 0; t < 8; ++t) {
@@ -119,11 +138,11 @@ __global__ __launch_bounds__(kStatThreads) void stats_agg_kernel(const uint32_t 
       for (int j = 0; j < M; ++j) st.ev_w[at * M + j] = v[j];
       atomicAdd(&hist[s >> st.bshift], 1u);
     } else {
-      atomicAdd((unsigned long long *)&d.cnt[s], 1ull);
+      atomicAdd((unsigned long long *)&ps.cnt[s], 1ull);
 #pragma unroll
       for (int j = 0; j < M; ++j) {
-        atomicMin((unsigned long long *)&d.min[(uint64_t)s * M + j], (unsigned long long)v[j]);
-        hbm_add_u128(&d.sq[((uint64_t)s * M + j) * 2], v[j] * v[j], __umul64hi(v[j], v[j]));
+        atomicMin((unsigned long long *)&ps.min[(uint64_t)s * M + j], (unsigned long long)v[j]);
+        hbm_add_u128(&ps.sq[((uint64_t)s * M + j) * 2], v[j] * v[j], __umul64hi(v[j], v[j]));
       }
     }
   }
@@ -161,11 +180,11 @@ __global__ __launch_bounds__(kStatThreads) void stats_agg_kernel(const uint32_t 
   for (int k = tid; k < kE; k += kStatThreads) {
     const uint32_t s = key[k];
     if (s == kStatEmpty) continue;
-    atomicAdd((unsigned long long *)&d.cnt[s], (unsigned long long)cnt[k]);
+    atomicAdd((unsigned long long *)&ps.cnt[s], (unsigned long long)cnt[k]);
 #pragma unroll
     for (int j = 0; j < M; ++j) {
-      atomicMin((unsigned long long *)&d.min[(uint64_t)s * M + j], (unsigned long long)mn[k * M + j]);
-      hbm_add_u128(&d.sq[((uint64_t)s * M + j) * 2], sq[(k * M + j) * 2], sq[(k * M + j) * 2 + 1]);
+      atomicMin((unsigned long long *)&ps.min[(uint64_t)s * M + j], (unsigned long long)mn[k * M + j]);
+      hbm_add_u128(&ps.sq[((uint64_t)s * M + j) * 2], sq[(k * M + j) * 2], sq[(k * M + j) * 2 + 1]);
     }
   }
 }
@@ -203,17 +222,18 @@ __global__ __launch_bounds__(kStatThreads) void stats_bucket_kernel(int64_t n, S
   }
 }
 
-// One workgroup per bucket of kB = 2^bshift slots: sums its misses and map entries into
-// LDS records and writes every slot of its range (so d needs no clearing).
+// One workgroup per bucket of 2^bshift paths: sums its misses and map entries into LDS
+// records, then combines them into the paths it owns (no other writer).
 template <int M>
-__global__ __launch_bounds__(kStatThreads) void stats_reduce_kernel(StatStage st, uint64_t cap, StatDelta d) {
+__global__ __launch_bounds__(kStatThreads) void stats_reduce_kernel(StatStage st, int64_t D, PathStats ps) {
   constexpr int kB = stage_slots(M), R = 1 + 3 * M;
   __shared__ uint64_t cnt[kB];
   __shared__ uint64_t mn[kB * M];
   __shared__ uint64_t sq[kB * M * 2];
   const int tid = threadIdx.x;
-  for (int i = tid; i < kB; i += kStatThreads) cnt[i] = 0;
-  for (int i = tid; i < kB * M; i += kStatThreads) { mn[i] = ~0ull; sq[2 * i] = 0; sq[2 * i + 1] = 0; }
+  const int nloc = 1 << st.bshift;
+  for (int i = tid; i < nloc; i += kStatThreads) cnt[i] = 0;
+  for (int i = tid; i < nloc * M; i += kStatThreads) { mn[i] = ~0ull; sq[2 * i] = 0; sq[2 * i + 1] = 0; }
   __syncthreads();
   const int64_t bk = blockIdx.x, g = st.grid;
   const uint64_t s0 = (uint64_t)bk << st.bshift;
@@ -240,37 +260,20 @@ __global__ __launch_bounds__(kStatThreads) void stats_reduce_kernel(StatStage st
     }
   }
   __syncthreads();
-  for (int i = tid; i < kB; i += kStatThreads) {
-    const uint64_t slot = s0 + (uint64_t)i;
-    if (slot >= cap) break;
-    d.cnt[slot] = cnt[i];
+  for (int i = tid; i < nloc; i += kStatThreads) {
+    const uint64_t path = s0 + (uint64_t)i;
+    if ((int64_t)path >= D) break;
+    if (!cnt[i]) continue;  // no sample of this path in the batch
+    ps.cnt[path] += cnt[i];
 #pragma unroll
     for (int j = 0; j < M; ++j) {
-      d.min[slot * M + j] = mn[i * M + j];
-      d.sq[(slot * M + j) * 2] = sq[(i * M + j) * 2];
-      d.sq[(slot * M + j) * 2 + 1] = sq[(i * M + j) * 2 + 1];
+      const uint64_t x = mn[i * M + j], old = ps.min[path * M + j];
+      ps.min[path * M + j] = x < old ? x : old;
+      const uint64_t lo = sq[(i * M + j) * 2], olo = ps.sq[(path * M + j) * 2];
+      const uint64_t nlo = olo + lo;
+      ps.sq[(path * M + j) * 2] = nlo;
+      ps.sq[(path * M + j) * 2 + 1] += sq[(i * M + j) * 2 + 1] + (nlo < olo ? 1 : 0);
     }
-  }
-}
-
-// Path i takes its slot's batch values; paths from earlier calls (i < d_old) combine them
-// with what they hold.
-__global__ void stats_fold_kernel(int64_t D, int64_t d_old, int32_t m, const uint32_t *pslot, StatDelta d,
-                                  PathStats p) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= D) return;
-  const uint64_t s = pslot[i];
-  const bool fresh = i >= d_old;
-  p.cnt[i] = (fresh ? 0 : p.cnt[i]) + d.cnt[s];
-  for (int j = 0; j < m; ++j) {
-    const uint64_t x = d.min[s * m + j];
-    const uint64_t old = fresh ? ~0ull : p.min[i * m + j];
-    p.min[i * m + j] = x < old ? x : old;
-    const uint64_t lo = d.sq[(s * m + j) * 2], hi = d.sq[(s * m + j) * 2 + 1];
-    const uint64_t olo = fresh ? 0 : p.sq[(i * m + j) * 2], ohi = fresh ? 0 : p.sq[(i * m + j) * 2 + 1];
-    const uint64_t nlo = olo + lo;
-    p.sq[(i * m + j) * 2] = nlo;
-    p.sq[(i * m + j) * 2 + 1] = ohi + hi + (nlo < olo ? 1 : 0);
   }
 }
 
@@ -491,39 +494,41 @@ int stats_bucket_shift(int32_t m) {
 }
 int64_t stats_max_buckets() { return kStageHist; }
 
-// staged (st.nbuckets > 0): the per-slot kernel, the scans of its counts, the bucketing and
-// the per-bucket reduction; otherwise the per-slot kernel with device atomics (d cleared
-// by the caller)
-void launch_stats_agg(const uint32_t *slot_of, const uint64_t *w, int64_t n, int32_t m, uint64_t cap, int grid,
-                      const StatDelta &d, const StatStage &st, uint64_t *scan_blk, hipStream_t s) {
+void launch_stats_prepare(int64_t D, int64_t d_old, int32_t m, const uint32_t *pslot, uint32_t *path_of_slot,
+                          const PathStats &p, hipStream_t s) {
+  if (D > 0)
+    hipLaunchKernelGGL(stats_prepare_kernel, dim3(blocks_for(D, 256)), dim3(256), 0, s, D, d_old, m, pslot,
+                       path_of_slot, p);
+}
+
+// staged (st.nbuckets > 0): the per-path kernel, the scans of its counts, the bucketing and
+// the per-bucket reduction; otherwise the per-path kernel with device atomics
+void launch_stats_agg(const uint32_t *slot_of, const uint32_t *path_of_slot, const uint64_t *w, int64_t n, int32_t m,
+                      int64_t D, int grid, const PathStats &p, const StatStage &st, uint64_t *scan_blk, hipStream_t s) {
   if (n <= 0) return;
   const bool staged = st.nbuckets > 0;
   const int64_t rows = st.nbuckets * grid;
   switch (m) {
-#define CCT_STAT_CASE(M)                                                                                           \
-  case M:                                                                                                          \
-    if (staged) {                                                                                                  \
-      hipLaunchKernelGGL((stats_agg_kernel<M, true>), dim3(grid), dim3(kStatThreads), 0, s, slot_of, w, n, d, st); \
-      launch_scan(st.hist_ev, rows, 1, scan_blk, st.off_ev, s);                                                   \
-      launch_scan(st.hist_map, rows, 1, scan_blk, st.off_map, s);                                                 \
-      hipLaunchKernelGGL(stats_bucket_kernel<M>, dim3(grid), dim3(kStatThreads), 0, s, n, st);                    \
-      hipLaunchKernelGGL(stats_reduce_kernel<M>, dim3((unsigned)st.nbuckets), dim3(kStatThreads), 0, s, st, cap, \
-                         d);                                                                                       \
-    } else {                                                                                                       \
-      hipLaunchKernelGGL((stats_agg_kernel<M, false>), dim3(grid), dim3(kStatThreads), 0, s, slot_of, w, n, d,    \
-                         st);                                                                                      \
-    }                                                                                                              \
+#define CCT_STAT_CASE(M)                                                                                        \
+  case M:                                                                                                       \
+    if (staged) {                                                                                               \
+      hipLaunchKernelGGL((stats_agg_kernel<M, true>), dim3(grid), dim3(kStatThreads), 0, s, slot_of,            \
+                         path_of_slot, w, n, p, st);                                                            \
+      launch_scan(st.hist_ev, rows, 1, scan_blk, st.off_ev, s);                                                \
+      launch_scan(st.hist_map, rows, 1, scan_blk, st.off_map, s);                                              \
+      hipLaunchKernelGGL(stats_bucket_kernel<M>, dim3(grid), dim3(kStatThreads), 0, s, n, st);                 \
+      hipLaunchKernelGGL(stats_reduce_kernel<M>, dim3((unsigned)st.nbuckets), dim3(kStatThreads), 0, s, st, D, \
+                         p);                                                                                    \
+    } else {                                                                                                    \
+      hipLaunchKernelGGL((stats_agg_kernel<M, false>), dim3(grid), dim3(kStatThreads), 0, s, slot_of,           \
+                         path_of_slot, w, n, p, st);                                                            \
+    }                                                                                                           \
     break;
     CCT_STAT_CASE(1) CCT_STAT_CASE(2) CCT_STAT_CASE(3) CCT_STAT_CASE(4)
     CCT_STAT_CASE(5) CCT_STAT_CASE(6) CCT_STAT_CASE(7) CCT_STAT_CASE(8)
 #undef CCT_STAT_CASE
     default: break;
   }
-}
-
-void launch_stats_fold(int64_t D, int64_t d_old, int32_t m, const uint32_t *pslot, const StatDelta &d,
-                       const PathStats &p, hipStream_t s) {
-  if (D > 0) hipLaunchKernelGGL(stats_fold_kernel, dim3(blocks_for(D, 256)), dim3(256), 0, s, D, d_old, m, pslot, d, p);
 }
 
 int64_t rmq_blocks(int64_t u) { return (u + kRmqBlock - 1) / kRmqBlock; }
