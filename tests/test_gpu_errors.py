@@ -150,3 +150,41 @@ def test_early_exit_after_pool_reuse(monkeypatch, kind):
     t = cct.build(to, tf, tw)  # the library is still usable
     assert_same(t.to_numpy(), oracle.build_tree(o, f, w), "after EINVAL")
     t.free()
+
+
+@pytest.mark.parametrize("k", [1, 4, 7, 9, 10, 12, 15, 18, 21, 24, 27, 30, 34, 38, 42, 46, 50])
+def test_allocation_failure_with_statistics(monkeypatch, k):
+    # a tree keeping statistics allocates more per merge (slot -> path map, staging lists,
+    # larger path arrays): a failure at any of them leaves the tree and its statistics as
+    # they were, and the same merge then succeeds
+    import paper_2411_02797_amd as cct
+    o, f, w = tracegen.random_paths(3000, 40, 10, 2, seed=k)
+    tree = cct.build(*to_dev(o, f, w), stats=True)
+    before = tree.to_numpy()
+    stats_before = {n: v.cpu() for n, v in tree.stats().items()}
+    o2, f2, w2 = tracegen.random_paths(2000, 80, 10, 2, seed=200 + k)
+    d2 = to_dev(o2, f2, w2)
+    monkeypatch.setenv("CCT_TEST_FAIL_ALLOC", str(k))
+    try:
+        tree.merge(*d2)
+        merged = True
+    except cct.CctError as e:
+        assert e.name == "CCT_ENOMEM"
+        merged = False
+    monkeypatch.delenv("CCT_TEST_FAIL_ALLOC")
+    orc = oracle.Oracle(2, stats=True)
+    orc.ingest(o, f, w)
+    orc.ingest(o2, f2, w2)
+    want = orc.tree()
+    orc.close()
+    if not merged:
+        assert_same(tree.to_numpy(), before, "unchanged after ENOMEM")
+        after = tree.stats()
+        for n, v in stats_before.items():
+            assert np.array_equal(v.numpy(), after[n].cpu().numpy(), equal_nan=True), n
+        tree.merge(*d2)
+    assert_same(tree.to_numpy(), want, "merged")
+    got = tree.stats(device="cpu")
+    for n in ("count_excl", "count_incl", "min_excl", "min_incl", "sumsq_excl", "sumsq_incl"):
+        assert np.array_equal(got[n].numpy().view(np.uint64), want[n]), n
+    tree.free()
