@@ -149,14 +149,11 @@ struct PublishArgs {
   const uint32_t *new_slots;
   int64_t n_new;
   int64_t d_old;
-  int32_t m;
-  const uint64_t *delta;     // [cap][m]
   uint32_t *pframes;
   uint64_t *pcp;             // checkpoint hashes
   int64_t *pstart;
   uint32_t *plen;
   uint32_t *pslot;
-  uint64_t *psums;           // [D][m]
   int64_t store_used;        // frames already used in the store
   const uint64_t *starts;    // [n_new] exclusive prefix sums of the padded lengths
   const int64_t *src_len;    // [n_new][2] first frame in the batch and length of each new path
@@ -167,8 +164,9 @@ void launch_publish(const PublishArgs &a, hipStream_t s);
 // Exclusive prefix sums of `rows` rows of C uint64 columns (mod 2^64) into out[0..rows),
 // totals into out row `rows`; blk holds (rows / 1024 + 1) * C scratch words.
 void launch_scan(const uint64_t *in, int64_t rows, int C, uint64_t *blk, uint64_t *out, hipStream_t s);
-void launch_fold_old(int64_t d_old, int32_t m, const uint32_t *pslot, const uint64_t *delta, uint64_t *psums,
-                     hipStream_t s);
+// psums[d] for d < D after a batch: old paths (d < d_old) add their slot's delta, new ones take it
+void launch_fold_sums(int64_t D, int64_t d_old, int32_t m, const uint32_t *pslot, const uint64_t *delta,
+                      uint64_t *psums, hipStream_t s);
 void launch_unclaim(Slot *slot, uint64_t cap, hipStream_t s);
 void launch_rehash(const uint32_t *pframes, const int64_t *pstart, const uint32_t *plen, int64_t d,
                    Slot *slot, uint64_t cap_mask, uint64_t hash_mask, uint32_t *pslot, hipStream_t s);

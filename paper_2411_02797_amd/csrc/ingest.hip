@@ -852,7 +852,6 @@ __global__ __launch_bounds__(256) void publish_kernel(PublishArgs a) {
     a.slot[s].word = (w & 0xFFFFFFFF00000000ull) | (uint64_t)id;
     a.slot[s].info = make_info((uint64_t)start, true, (uint64_t)len);
   }
-  if (lane < a.m) a.psums[id * a.m + lane] = a.delta[(uint64_t)s * a.m + lane];
 }
 
 // Padded store length of every new path (input of the scan that places them), and the
@@ -869,12 +868,15 @@ __global__ void new_lengths_kernel(const int64_t *off, const Slot *slot, const u
   out[i] = (uint64_t)round_store(len);
 }
 
-__global__ void fold_old_kernel(int64_t d_old, int32_t m, const uint32_t *pslot, const uint64_t *delta,
-                                uint64_t *psums) {
+// Every path's sums after the batch: paths from earlier calls add their slot's batch sums,
+// new paths (d >= d_old) take them.
+__global__ void fold_sums_kernel(int64_t D, int64_t d_old, int32_t m, const uint32_t *pslot, const uint64_t *delta,
+                                 uint64_t *psums) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= d_old * m) return;
+  if (t >= D * m) return;
   const int64_t d = t / m, j = t - d * m;
-  psums[t] += delta[(uint64_t)pslot[d] * m + j];
+  const uint64_t x = delta[(uint64_t)pslot[d] * m + j];
+  psums[t] = d < d_old ? psums[t] + x : x;
 }
 
 // Roll back every slot claimed in the current call (after an error or overflow).
@@ -974,10 +976,10 @@ void launch_publish(const PublishArgs &a, hipStream_t s) {
   if (a.n_new <= 0) return;
   hipLaunchKernelGGL(publish_kernel, dim3(blocks_for(a.n_new * 64, 256)), dim3(256), 0, s, a);
 }
-void launch_fold_old(int64_t d_old, int32_t m, const uint32_t *pslot, const uint64_t *delta, uint64_t *psums,
-                     hipStream_t s) {
-  if (d_old <= 0) return;
-  hipLaunchKernelGGL(fold_old_kernel, dim3(blocks_for(d_old * m, 256)), dim3(256), 0, s, d_old, m, pslot, delta,
+void launch_fold_sums(int64_t D, int64_t d_old, int32_t m, const uint32_t *pslot, const uint64_t *delta,
+                      uint64_t *psums, hipStream_t s) {
+  if (D <= 0) return;
+  hipLaunchKernelGGL(fold_sums_kernel, dim3(blocks_for(D * m, 256)), dim3(256), 0, s, D, d_old, m, pslot, delta,
                      psums);
 }
 void launch_unclaim(Slot *slot, uint64_t cap, hipStream_t s) {

@@ -150,6 +150,41 @@ unsigned long long *host_scratch() {
   return h;
 }
 
+// A second stream per device for work that overlaps the caller's stream within one call
+// (default priority, non-blocking: ordered only by the events the call records).
+hipStream_t side_stream() {
+  static std::mutex mu;
+  static hipStream_t streams[64] = {nullptr};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!streams[dev] && hipStreamCreateWithFlags(&streams[dev], hipStreamNonBlocking) != hipSuccess) {
+    (void)hipGetLastError();
+    streams[dev] = nullptr;
+  }
+  return streams[dev];
+}
+
+// Waits for the side stream when a call returns, before the buffers its work uses are
+// released (declared after them).
+struct SideGuard {
+  hipStream_t st = nullptr;
+  ~SideGuard() {
+    if (st) (void)hipStreamSynchronize(st);
+  }
+};
+
+// An event for ordering two streams (no timing).
+struct Event {
+  hipEvent_t ev = nullptr;
+  Event() {
+    if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess) { (void)hipGetLastError(); ev = nullptr; }
+  }
+  ~Event() {
+    if (ev) (void)hipEventDestroy(ev);
+  }
+};
+
 uint64_t pow2_at_least(uint64_t x) {
   uint64_t p = 1;
   while (p < x) p <<= 1;
@@ -351,14 +386,6 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
       tm.mark(1, s);
       launch_ingest(a, grid, s);
       tm.mark(2, s);
-      // metric sums: per-workgroup LDS maps, flushed through staging buckets of slots; two
-      // workgroups per CU (run one after the other) halve the distinct slots each map
-      // must hold, so fewer events overflow into device atomics
-      const int agg_grid = (int)std::max<int64_t>(1, std::min<int64_t>((N + 8191) / 8192, (int64_t)cu_count() * 2));
-      AggStage stg{};
-      cct_status sst = setup_stage(m, t->cap, agg_grid, agg_count, agg_keys, agg_sums, stg, s);
-      if (sst) return sst;
-      launch_aggregate(a.slot_of, p->metrics, N, m, delta.as<uint64_t>(), t->cap, agg_grid, stg, s);
       launch_collect_new(t->slot.as<Slot>(), t->cap, p->offsets, new_slots.as<uint32_t>(), dctr,
                          cpart.as<unsigned long long>(), s);
       HIP_TRY(hipGetLastError());
@@ -380,6 +407,29 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
       new_store = hs[kCtrNewFrames];
       break;
     }
+  }
+
+  // ---- metric sums on the side stream, overlapping the publish and the ordering: the
+  // host has synchronised the caller's stream, so the ingest's slot ids are complete.
+  // Per-workgroup LDS maps, flushed through staging buckets of slots; two workgroups per
+  // CU (run one after the other) halve the distinct slots each map must hold, so fewer
+  // events overflow into device atomics.
+  SideGuard side_guard;
+  hipStream_t side = s;
+  if (N > 0) {
+    hipStream_t ss = side_stream();
+    if (ss) side = ss;
+    side_guard.st = side == s ? nullptr : side;
+    const int agg_grid = (int)std::max<int64_t>(1, std::min<int64_t>((N + 8191) / 8192, (int64_t)cu_count() * 2));
+    AggStage stg{};
+    cct_status sst = setup_stage(m, t->cap, agg_grid, agg_count, agg_keys, agg_sums, stg, side);
+    if (sst) {
+      if (n_new) launch_unclaim(t->slot.as<Slot>(), t->cap, s);
+      (void)hipStreamSynchronize(s);
+      return sst;
+    }
+    launch_aggregate(slot_of.as<uint32_t>(), p->metrics, N, m, delta.as<uint64_t>(), t->cap, agg_grid, stg, side);
+    HIP_TRY(hipGetLastError());
   }
 
   // ---- allocate everything the rest of the call needs (rollback possible until here)
@@ -550,14 +600,25 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     HIP_TRY(hipMemcpyAsync(cursor.p, nstart.as<uint64_t>() + n_new, 8, hipMemcpyDeviceToDevice, s));
     PublishArgs pa{};
     pa.off = p->offsets; pa.fr = p->frames; pa.slot = t->slot.as<Slot>();
-    pa.new_slots = new_slots.as<uint32_t>(); pa.n_new = (int64_t)n_new; pa.d_old = t->d; pa.m = m;
-    pa.delta = delta.as<uint64_t>(); pa.pframes = t->pframes.as<uint32_t>(); pa.pcp = t->pcp.as<uint64_t>();
+    pa.new_slots = new_slots.as<uint32_t>(); pa.n_new = (int64_t)n_new; pa.d_old = t->d;
+    pa.pframes = t->pframes.as<uint32_t>(); pa.pcp = t->pcp.as<uint64_t>();
     pa.pstart = t->pstart.as<int64_t>(); pa.plen = t->plen.as<uint32_t>(); pa.pslot = t->pslot.as<uint32_t>();
-    pa.psums = t->psums.as<uint64_t>(); pa.store_used = t->store_used; pa.starts = nstart.as<uint64_t>();
+    pa.store_used = t->store_used; pa.starts = nstart.as<uint64_t>();
     pa.src_len = nsrc.as<int64_t>();
     launch_publish(pa, s);
   }
-  if (N > 0) launch_fold_old(t->d, m, t->pslot.as<uint32_t>(), delta.as<uint64_t>(), t->psums.as<uint64_t>(), s);
+  // every path's sums, once both the side stream's aggregation and the publish (which
+  // records the new paths' slots) are done; the emission waits for them
+  Event published, folded;
+  if (N > 0) {
+    if (side != s) {
+      if (!published.ev || !folded.ev) return fail(CCT_EDEVICE, "event creation failed");
+      HIP_TRY(hipEventRecord(published.ev, s));
+      HIP_TRY(hipStreamWaitEvent(side, published.ev, 0));
+    }
+    launch_fold_sums(D, t->d, m, t->pslot.as<uint32_t>(), delta.as<uint64_t>(), t->psums.as<uint64_t>(), side);
+    if (side != s) HIP_TRY(hipEventRecord(folded.ev, side));
+  }
   if (keep_stats) {  // the batch's samples into the path arrays (new paths start empty)
     ts.mark(0, s);
     PathStats ps{t->pcnt.as<uint64_t>(), t->pmin.as<uint64_t>(), t->psq.as<uint64_t>()};
@@ -592,6 +653,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     else if (mode == 3) launch_merge_order(run, t->order.as<uint32_t>(), t->d, merge_scratch.as<uint32_t>(), s);
     else launch_sort(run, s);
     tm.mark(4, s);
+    if (N > 0 && side != s) HIP_TRY(hipStreamWaitEvent(s, folded.ev, 0));  // the emission reads psums
     launch_canon(run, s);
     HIP_TRY(hipGetLastError());
     tm.mark(5, s);
