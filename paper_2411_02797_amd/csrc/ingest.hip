@@ -782,17 +782,15 @@ __global__ __launch_bounds__(256) void collect_sum_kernel(const unsigned long lo
   if (threadIdx.x == 0) { ctr[kCtrNewFrames] = sf[0]; ctr[kCtrNewLen] = sl[0]; }
 }
 
-// Publish the paths first seen in this call: give each a path id, copy its frames
-// into the tree's path store (16-frame aligned, zero tail), write its checkpoint
-// hashes and exclusive sums, and point its table slot at the path id and the stored
-// frames.  One wave per path.
-// Publish: copy every new path into the path store (zero tail up to its padded length),
-// record its checkpoint hashes, its start, length and table slot, and its sums.  One
-// wave per new path.  Its first frame and length come from new_lengths_kernel (one
-// load), and the frames of up to four 64-frame chunks are requested before any is used
-// (paths of up to 256 frames take one round trip; deeper prefetch measured slower).  Within a chunk each group of 16
-// lanes holds one block, sums its frame terms with shuffles, and the blocks' prefix sums
-// are carried across chunks.
+// Publish the paths first seen in this call: give each a path id, copy its frames into
+// the tree's path store (16-frame aligned, zero tail up to its padded length), write its
+// checkpoint hashes, its start, length and table slot, and point the slot at the path id
+// and the stored frames (the sums are folded in later, by fold_sums_kernel).  One wave
+// per new path.  Its first frame and length come from new_lengths_kernel (one load), and
+// the frames of up to four 64-frame chunks are requested before any is used (paths of up
+// to 256 frames take one round trip; deeper prefetch measured slower).  Within a chunk
+// each group of 16 lanes holds one block, sums its frame terms with shuffles, and the
+// blocks' prefix sums are carried across chunks.
 constexpr int kPublishChunks = 4;  // 64-frame chunks requested ahead
 __global__ __launch_bounds__(256) void publish_kernel(PublishArgs a) {
   const int lane = threadIdx.x & 63;

@@ -150,27 +150,48 @@ unsigned long long *host_scratch() {
   return h;
 }
 
-// A second stream per device for work that overlaps the caller's stream within one call
-// (default priority, non-blocking: ordered only by the events the call records).
-hipStream_t side_stream() {
-  static std::mutex mu;
-  static hipStream_t streams[64] = {nullptr};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
-  std::lock_guard<std::mutex> lock(mu);
-  if (!streams[dev] && hipStreamCreateWithFlags(&streams[dev], hipStreamNonBlocking) != hipSuccess) {
-    (void)hipGetLastError();
-    streams[dev] = nullptr;
-  }
-  return streams[dev];
+// Second streams for work that overlaps the caller's stream within one call (default
+// priority, non-blocking: ordered only by the events the call records).  A call takes one
+// from its device's pool and gives it back when it returns, so concurrent calls on other
+// trees never share one.
+struct StreamPool {
+  std::mutex mu;
+  std::vector<std::pair<int, hipStream_t>> free;  // (device, stream)
+};
+StreamPool &stream_pool() {
+  static StreamPool *p = new StreamPool;  // never destroyed: streams live until the process ends
+  return *p;
 }
 
-// Waits for the side stream when a call returns, before the buffers its work uses are
-// released (declared after them).
+// Holds a side stream for one call; on return it waits for the stream (before the
+// buffers its work uses are released: declare it after them) and gives it back.
 struct SideGuard {
   hipStream_t st = nullptr;
+  int dev = 0;
+  hipStream_t acquire() {
+    if (hipGetDevice(&dev) != hipSuccess) { (void)hipGetLastError(); return nullptr; }
+    StreamPool &P = stream_pool();
+    {
+      std::lock_guard<std::mutex> lock(P.mu);
+      for (size_t i = 0; i < P.free.size(); ++i)
+        if (P.free[i].first == dev) {
+          st = P.free[i].second;
+          P.free.erase(P.free.begin() + (long)i);
+          return st;
+        }
+    }
+    if (hipStreamCreateWithFlags(&st, hipStreamNonBlocking) != hipSuccess) {
+      (void)hipGetLastError();
+      st = nullptr;
+    }
+    return st;
+  }
   ~SideGuard() {
-    if (st) (void)hipStreamSynchronize(st);
+    if (!st) return;
+    (void)hipStreamSynchronize(st);
+    StreamPool &P = stream_pool();
+    std::lock_guard<std::mutex> lock(P.mu);
+    P.free.emplace_back(dev, st);
   }
 };
 
@@ -417,9 +438,8 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   SideGuard side_guard;
   hipStream_t side = s;
   if (N > 0) {
-    hipStream_t ss = side_stream();
+    hipStream_t ss = side_guard.acquire();
     if (ss) side = ss;
-    side_guard.st = side == s ? nullptr : side;
     const int agg_grid = (int)std::max<int64_t>(1, std::min<int64_t>((N + 8191) / 8192, (int64_t)cu_count() * 2));
     AggStage stg{};
     cct_status sst = setup_stage(m, t->cap, agg_grid, agg_count, agg_keys, agg_sums, stg, side);

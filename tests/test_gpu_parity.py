@@ -282,3 +282,39 @@ def test_query_every_node_and_absent_paths():
     assert np.array_equal(inc.cpu().numpy()[:U].view(np.uint64), want["incl"])
     assert np.all(inc.cpu().numpy()[U:] == 0)
     tree.free()
+
+
+def test_concurrent_builds_on_two_threads():
+    # distinct trees built and merged at the same time from two host threads, each on its
+    # own stream: every call takes its own side stream, so neither waits for or corrupts
+    # the other
+    import threading
+
+    import paper_2411_02797_amd as cct
+    torch = torch_or_skip()
+    results, errors = {}, []
+
+    def work(k):
+        try:
+            st = torch.cuda.Stream()
+            with torch.cuda.stream(st):
+                o, f, w = tracegen.random_paths(20000, 300 + 50 * k, 30, 2, seed=70 + k)
+                o2, f2, w2 = tracegen.random_paths(8000, 300 + 50 * k, 30, 2, seed=80 + k)
+                for _ in range(3):
+                    tree = cct.build(*to_dev(o, f, w), stats=True)
+                    tree.merge(*to_dev(o2, f2, w2))
+                    got = tree.to_numpy()
+                    tree.free()
+            oc = np.concatenate([o, o[-1] + o2[1:]])
+            results[k] = (got, oracle.build_tree(oc, np.concatenate([f, f2]), np.concatenate([w, w2])))
+        except Exception as e:  # reported by the main thread
+            errors.append(repr(e))
+
+    threads = [threading.Thread(target=work, args=(k,)) for k in range(2)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    for k, (got, want) in results.items():
+        assert_same(got, want, f"thread {k}")
