@@ -325,21 +325,35 @@ __global__ __launch_bounds__(1024) void sparse_tile_kernel(uint32_t *sp, const u
   }
 }
 
-// first j >= s with lcp[j] < t (exists: lcp[D] = 0 < t for t >= 1)
+// first j >= s with lcp[j] < t (exists: lcp[D] = 0 < t for t >= 1).  Exponential search:
+// skip blocks of 1, 2, 4, ... entries while a whole block is >= t, then descend within the
+// block that holds the answer; about 2 log2(j - s) dependent loads instead of one per
+// level, and most subtrees end a few paths on.
 __device__ inline int64_t next_smaller(const CanonArgs &a, int64_t n, int64_t s, uint32_t t) {
   int64_t j = s;
-  for (int k = a.levels - 1; k >= 0; --k) {
-    const int64_t w = (int64_t)1 << k;
-    if (j + w <= n && a.sparse[(int64_t)k * n + j] >= t) j += w;
+  int k = 0;
+  while (k < a.levels && j + ((int64_t)1 << k) <= n && a.sparse[(int64_t)k * n + j] >= t) {
+    j += (int64_t)1 << k;
+    ++k;
+  }
+  for (int q = k - 1; q >= 0; --q) {
+    const int64_t w = (int64_t)1 << q;
+    if (j + w <= n && a.sparse[(int64_t)q * n + j] >= t) j += w;
   }
   return j;
 }
-// largest j <= s with lcp[j] < t (exists: lcp[0] = 0 < t for t >= 1)
+// largest j <= s with lcp[j] < t (exists: lcp[0] = 0 < t for t >= 1), the same search
+// towards smaller indices
 __device__ inline int64_t prev_smaller(const CanonArgs &a, int64_t n, int64_t s, uint32_t t) {
   int64_t j = s;
-  for (int k = a.levels - 1; k >= 0; --k) {
-    const int64_t w = (int64_t)1 << k;
-    if (j - w + 1 >= 0 && a.sparse[(int64_t)k * n + (j - w + 1)] >= t) j -= w;
+  int k = 0;
+  while (k < a.levels && j - ((int64_t)1 << k) + 1 >= 0 && a.sparse[(int64_t)k * n + (j - ((int64_t)1 << k) + 1)] >= t) {
+    j -= (int64_t)1 << k;
+    ++k;
+  }
+  for (int q = k - 1; q >= 0; --q) {
+    const int64_t w = (int64_t)1 << q;
+    if (j - w + 1 >= 0 && a.sparse[(int64_t)q * n + (j - w + 1)] >= t) j -= w;
   }
   return j;
 }
