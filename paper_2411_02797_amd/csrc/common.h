@@ -363,14 +363,14 @@ struct StatStage {  // staged per-path statistics of a batch (nbuckets = 0: devi
   int64_t nbuckets;
   int grid;             // workgroups of the per-slot kernel
   int64_t map_entries;  // LDS map entries per workgroup
-  uint32_t *ev_slot;    // [N] misses (path indices): workgroup g's from its first event index on
+  uint32_t *ev_path;    // [N] misses (path indices): workgroup g's from its first event index on
   uint64_t *ev_w;       // [N][m]
   uint32_t *map_key;    // [grid][map_entries]
   uint64_t *map_rec;    // [grid][map_entries][1 + 3m]: count, min[m], sq[m][2]
   uint64_t *hist_ev, *hist_map;  // [nbuckets][grid] entries per bucket and workgroup
   uint64_t *off_ev, *off_map;    // their exclusive scans, [nbuckets * grid + 1]
   uint32_t *wg_count;   // [grid][2]: misses, map entries
-  uint32_t *st_ev_slot;  // bucketed misses [N], values [N][m]
+  uint32_t *st_ev_path;  // bucketed misses [N], values [N][m]
   uint64_t *st_ev_w;
   uint32_t *st_map_key;  // bucketed map entries [grid * map_entries], records
   uint64_t *st_map_rec;

@@ -464,7 +464,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   // this batch's statistics, staged in path-range buckets when there are few enough of them
   // (a test setting forces device atomics instead); allocated before anything of the tree
   // changes
-  Buf sg_pos, sg_ev_slot, sg_ev_w, sg_map_key, sg_map_rec, sg_hist, sg_off, sg_blk, sg_wg, sg_st_slot, sg_st_w,
+  Buf sg_pos, sg_ev_path, sg_ev_w, sg_map_key, sg_map_rec, sg_hist, sg_off, sg_blk, sg_wg, sg_st_path, sg_st_w,
       sg_st_key, sg_st_rec;
   StatStage sst{};
   const bool keep_stats = t->stats && N > 0;
@@ -479,18 +479,18 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     if (nbk <= stats_max_buckets() && !env_int("CCT_TEST_STATS_ATOMIC", 0)) {
       const int64_t me = stats_staged_entries(m), R = 1 + 3 * (int64_t)m, rows = nbk * st_grid;
       const int64_t nmap = st_grid * me;
-      if (!sg_ev_slot.alloc(N * 4) || !sg_ev_w.alloc(N * m * 8) || !sg_map_key.alloc(nmap * 4) ||
+      if (!sg_ev_path.alloc(N * 4) || !sg_ev_w.alloc(N * m * 8) || !sg_map_key.alloc(nmap * 4) ||
           !sg_map_rec.alloc(nmap * R * 8) || !sg_hist.alloc(2 * rows * 8) || !sg_off.alloc(2 * (rows + 1) * 8) ||
-          !sg_blk.alloc((rows / 1024 + 2) * 8) || !sg_wg.alloc(st_grid * 8) || !sg_st_slot.alloc(N * 4) ||
+          !sg_blk.alloc((rows / 1024 + 2) * 8) || !sg_wg.alloc(st_grid * 8) || !sg_st_path.alloc(N * 4) ||
           !sg_st_w.alloc(N * m * 8) || !sg_st_key.alloc(nmap * 4) || !sg_st_rec.alloc(nmap * R * 8))
         return rollback(fail(CCT_ENOMEM, "device allocation failed"));
       sst.bshift = bshift; sst.nbuckets = nbk; sst.grid = st_grid; sst.map_entries = me;
-      sst.ev_slot = sg_ev_slot.as<uint32_t>(); sst.ev_w = sg_ev_w.as<uint64_t>();
+      sst.ev_path = sg_ev_path.as<uint32_t>(); sst.ev_w = sg_ev_w.as<uint64_t>();
       sst.map_key = sg_map_key.as<uint32_t>(); sst.map_rec = sg_map_rec.as<uint64_t>();
       sst.hist_ev = sg_hist.as<uint64_t>(); sst.hist_map = sst.hist_ev + rows;
       sst.off_ev = sg_off.as<uint64_t>(); sst.off_map = sst.off_ev + rows + 1;
       sst.wg_count = sg_wg.as<uint32_t>();
-      sst.st_ev_slot = sg_st_slot.as<uint32_t>(); sst.st_ev_w = sg_st_w.as<uint64_t>();
+      sst.st_ev_path = sg_st_path.as<uint32_t>(); sst.st_ev_w = sg_st_w.as<uint64_t>();
       sst.st_map_key = sg_st_key.as<uint32_t>(); sst.st_map_rec = sg_st_rec.as<uint64_t>();
     }
   }

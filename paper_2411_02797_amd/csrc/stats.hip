@@ -133,7 +133,7 @@ __global__ __launch_bounds__(kStatThreads) void stats_agg_kernel(const uint32_t 
       }
     } else if (kStaged) {
       const int64_t at = lo + atomicAdd(&n_miss, 1u);
-      st.ev_slot[at] = s;
+      st.ev_path[at] = s;
 #pragma unroll
       for (int j = 0; j < M; ++j) st.ev_w[at * M + j] = v[j];
       atomicAdd(&hist[s >> st.bshift], 1u);
@@ -203,9 +203,9 @@ __global__ __launch_bounds__(kStatThreads) void stats_bucket_kernel(int64_t n, S
   __syncthreads();
   const uint32_t n_miss = st.wg_count[2 * b], n_map = st.wg_count[2 * b + 1];
   for (uint32_t i = tid; i < n_miss; i += kStatThreads) {
-    const uint32_t s = st.ev_slot[lo + i];
+    const uint32_t s = st.ev_path[lo + i];
     const uint64_t at = atomicAdd((unsigned long long *)&cur[s >> st.bshift], 1ull);
-    st.st_ev_slot[at] = s;
+    st.st_ev_path[at] = s;
 #pragma unroll
     for (int j = 0; j < M; ++j) st.st_ev_w[at * M + j] = st.ev_w[(lo + i) * M + j];
   }
@@ -239,7 +239,7 @@ __global__ __launch_bounds__(kStatThreads) void stats_reduce_kernel(StatStage st
   const uint64_t s0 = (uint64_t)bk << st.bshift;
   const uint64_t e0 = st.off_ev[bk * g], e1 = st.off_ev[(bk + 1) * g];
   for (uint64_t i = e0 + tid; i < e1; i += kStatThreads) {
-    const uint32_t l = (uint32_t)(st.st_ev_slot[i] - s0);
+    const uint32_t l = (uint32_t)(st.st_ev_path[i] - s0);
     atomicAdd((unsigned long long *)&cnt[l], 1ull);
 #pragma unroll
     for (int j = 0; j < M; ++j) {
