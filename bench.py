@@ -51,6 +51,9 @@ DESCRIPTIONS = {
     "stats": "layered_16m built with per-node statistics (16,777,216 events, 2 uint64 metrics): sample counts, "
              "minima and sums of squares kept per path, then every node's exclusive and inclusive count, min, sum of "
              "squares, mean and population deviation",
+    "query": "1,048,576 query paths (the first events' paths of the layered_16m trace, so every one is a node, "
+             "plus 1,024 absent ones) looked up in the layered_16m tree (4,407,055 nodes, 2 uint64 metrics): node "
+             "ids and both sums",
     "activity": "8,388,608-event base (as merge) + 8 activity flushes, each a registry of 2,097,152 call paths "
                 "(a merge chunk) under distinct correlation IDs and 2,348,810 records (every ID once, shuffled, "
                 "+10% repeated IDs, +2% unregistered IDs), 4 uint64 metrics",
@@ -144,6 +147,8 @@ def main():
         return bench_filter(args, torch, tracegen, cct, dev)
     if args.workload == "stats":
         return bench_stats(args, torch, tracegen, cct, dev)
+    if args.workload == "query":
+        return bench_query(args, torch, tracegen, cct, dev)
     o, f, w = tracegen.generate(args.workload)
     N, F, M = o.size - 1, f.size, w.shape[1]
     log(f"generated {args.workload}: N={N:,} F={F:,} M={M} in {time.perf_counter() - t0:.1f}s")
@@ -480,6 +485,51 @@ def bench_stats(args, torch, tracegen, cct, dev):
                      "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
                      "kernel": "statistics kept by the build (per-slot samples, fold into the paths)",
                      "bytes_per_launch": b_alg, "avg_launch_ms": kept},
+    }
+    print(json.dumps(line), flush=True)
+
+
+def bench_query(args, torch, tracegen, cct, dev):
+    o, f, w = tracegen.generate("layered_16m")
+    tree = cct.build(torch.from_numpy(o).to(dev), torch.from_numpy(f.view(np.int32)).to(dev),
+                     torch.from_numpy(w.view(np.int64)).to(dev))
+    U, M = tree.n_nodes, w.shape[1]
+    Q = 1 << 20
+    absent = 1024
+    qo = np.concatenate([o[:Q + 1], o[Q] + 3 * np.arange(1, absent + 1, dtype=np.int64)])
+    qf = np.concatenate([f[:o[Q]], np.full(3 * absent, 0xFFFFFFF0, np.uint32)])
+    del o, f, w
+    tqo, tqf = torch.from_numpy(qo).to(dev), torch.from_numpy(qf.view(np.int32)).to(dev)
+    nq, nf = qo.size - 1, int(qo[-1])
+    q_ms, wall_ms = [], []
+    for step in range(args.warmup + args.steps):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ids, ex, inc = tree.query(tqo, tqf)
+        wall = (time.perf_counter() - t0) * 1000.0
+        ms = cct.last_timings()[10]
+        found = int((ids >= 0).sum().item())
+        del ids, ex, inc
+        if step >= args.warmup:
+            q_ms.append(ms)
+            wall_ms.append(wall)
+        log(f"{'warmup' if step < args.warmup else 'step'} {step}: lookup {ms:.3f} ms (call {wall:.3f} ms), "
+            f"{found:,} of {nq:,} found")
+    tree.free()
+    ms = float(np.mean(q_ms))
+    # algorithmic bytes: every query's offsets and frames read once, its id and sums written once
+    b_alg = 8 * (nq + 1) + 4 * nf + nq * (8 + 16 * M)
+    achieved = b_alg / (ms * 1e-3) / 1e9
+    line = {
+        "metric": METRIC, "value": nq / (ms * 1e-3), "unit": "queries/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "u32", "data": "synthetic",
+        "config": {"workload": f"query: {DESCRIPTIONS['query']}", "queries": nq, "query_frames": nf, "nodes": U,
+                   "metrics": M, "call_ms_with_readback": float(np.mean(wall_ms))},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                     "kernel": "query_kernel (binary search over the sorted paths, exact frame comparison)",
+                     "bytes_per_launch": b_alg, "avg_launch_ms": ms},
     }
     print(json.dumps(line), flush=True)
 

@@ -239,9 +239,9 @@ const char *cct_last_error(void);
  * whole merge, [5] the correlation-ID join before the merge (cct_merge_activity only;
  * 0 otherwise), [6] the most recent computation of a bottom-up view by cct_bottom_up
  * (calls that only copy a kept view leave it as it is), [7] the last cct_filter, [8] the
- * statistics kept by the last build or merge (per-slot samples and their fold into the
- * paths; 0 for a tree without statistics), [9] the last cct_stats.  Returns the number
- * of values written (<= n, at most 10). */
+ * statistics kept by the last build or merge (the batch's samples folded into the paths;
+ * 0 for a tree without statistics), [9] the last cct_stats, [10] the last cct_query's
+ * lookup kernel.  Returns the number of values written (<= n, at most 11). */
 int cct_last_timings(double *ms, int n);
 
 #ifdef __cplusplus

@@ -328,9 +328,9 @@ def last_timings():
     canonical emission and total of the last build/merge, the correlation-ID join of a
     merge_activity call (0 otherwise), the most recent computation of a bottom-up view
     (bottom_up), the last filter, the statistics kept by the last build/merge (0 without),
-    and the last ``Tree.stats``."""
-    buf = (ctypes.c_double * 10)()
-    n = load_library().cct_last_timings(buf, 10)
+    the last ``Tree.stats``, and the last query's lookup."""
+    buf = (ctypes.c_double * 11)()
+    n = load_library().cct_last_timings(buf, 11)
     return list(buf)[:n]
 
 

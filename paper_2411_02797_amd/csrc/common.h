@@ -272,6 +272,7 @@ struct QueryArgs {
   int64_t *node_ids;
   uint64_t *qexcl, *qincl;
   unsigned long long *err;
+  int64_t *sorted;           // scratch [D][2]: first frame and length of the path at each canonical position
 };
 void launch_query(const QueryArgs &a, hipStream_t s);
 

@@ -12,17 +12,41 @@ namespace cct {
 
 namespace {
 
-// compare stored path p with query frames qf[0..ql): sign and common prefix length
-__device__ int cmp_path_query(const QueryArgs &a, uint32_t p, const uint32_t *qf, int64_t ql, int64_t *lcp) {
-  const int64_t lp = a.plen[p];
-  const uint32_t *pf = a.pframes + a.pstart[p];
+// four frames at a 4-byte-aligned address (one 16-byte load)
+struct __attribute__((aligned(4))) Frames4 {
+  uint32_t f[4];
+};
+
+// compare the path at canonical position i with query frames qf[0..ql), both known to
+// agree on their first k0 frames: sign and common prefix length.  The path's first frame
+// and length come from one 16-byte record; four frames per step, then one at a time.
+__device__ int cmp_path_query(const QueryArgs &a, int64_t i, const uint32_t *qf, int64_t ql, int64_t k0,
+                              int64_t *lcp) {
+  const int64_t *rec = a.sorted + 2 * i;
+  const int64_t fs = rec[0], lp = rec[1];
+  const uint32_t *pf = a.pframes + fs;
   const int64_t n = min(lp, ql);
-  for (int64_t k = 0; k < n; ++k) {
+  int64_t k = k0;
+  for (; k + 4 <= n; k += 4) {
+    const Frames4 x = *reinterpret_cast<const Frames4 *>(pf + k);
+    const Frames4 y = *reinterpret_cast<const Frames4 *>(qf + k);
+    if (x.f[0] != y.f[0] || x.f[1] != y.f[1] || x.f[2] != y.f[2] || x.f[3] != y.f[3]) break;
+  }
+  for (; k < n; ++k) {
     const uint32_t x = pf[k], y = qf[k];
     if (x != y) { *lcp = k; return x < y ? -1 : 1; }
   }
   *lcp = n;
   return lp < ql ? -1 : (lp > ql ? 1 : 0);
+}
+
+// record of canonical position i: the path's first frame in the store and its length
+__global__ void sorted_paths_kernel(QueryArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= a.d) return;
+  const uint32_t p = a.order[i];
+  a.sorted[2 * i] = a.pstart[p];
+  a.sorted[2 * i + 1] = a.plen[p];
 }
 
 __global__ void query_kernel(QueryArgs a) {
@@ -38,14 +62,25 @@ __global__ void query_kernel(QueryArgs a) {
   } else {
     const uint32_t *qf = a.qfr + qs;
     const int64_t ql = qe - qs;
-    int64_t lo = 0, hi = a.d;  // first i with path_i >= q
+    // first i with path_i >= q.  llo and lhi: common prefix of q with the path below the
+    // range (path_{lo-1}) and with the path above it (path_hi), 0 for the open ends.  Every
+    // path between two paths that share a prefix with q shares it too (paths with a given
+    // prefix are consecutive in lexicographic order), so a comparison can skip
+    // min(llo, lhi) frames.
+    int64_t lo = 0, hi = a.d, llo = 0, lhi = 0;
     int64_t l;
     while (lo < hi) {
       const int64_t mid = (lo + hi) >> 1;
-      if (cmp_path_query(a, a.order[mid], qf, ql, &l) < 0) lo = mid + 1; else hi = mid;
+      if (cmp_path_query(a, mid, qf, ql, min(llo, lhi), &l) < 0) {
+        lo = mid + 1;
+        llo = l;
+      } else {
+        hi = mid;
+        lhi = l;
+      }
     }
     if (lo < a.d) {
-      cmp_path_query(a, a.order[lo], qf, ql, &l);
+      l = lhi;  // lo = hi < D: set by the comparison with path_hi, which measured its prefix
       if (l == ql) id = (int64_t)(1 + a.scan_out[lo * C]) + ql - (int64_t)a.lcp[lo] - 1;
       if (id >= a.u || (l == ql && ql <= (int64_t)a.lcp[lo])) {  // cannot happen on a canonical tree
         atomicOr(a.err, 2ull);
@@ -64,6 +99,7 @@ __global__ void query_kernel(QueryArgs a) {
 
 void launch_query(const QueryArgs &a, hipStream_t s) {
   if (a.q <= 0) return;
+  if (a.d > 0) hipLaunchKernelGGL(sorted_paths_kernel, dim3((unsigned)((a.d + 255) / 256)), dim3(256), 0, s, a);
   hipLaunchKernelGGL(query_kernel, dim3((unsigned)((a.q + 255) / 256)), dim3(256), 0, s, a);
 }
 

@@ -27,6 +27,7 @@ thread_local double g_view_ms = 0;  // the most recent computation of a bottom-u
 thread_local double g_filter_ms = 0;  // the last cct_filter
 thread_local double g_stats_ms = 0;   // statistics kept by the last build/merge (0 without)
 thread_local double g_node_stats_ms = 0;  // the last cct_stats
+thread_local double g_query_ms = 0;       // the last cct_query
 thread_local int g_alloc_countdown = 0;  // test hook: >0 makes the n-th allocation of a call fail
 
 int64_t env_int(const char *name, int64_t dflt) {
@@ -1051,9 +1052,9 @@ cct_status cct_query(const cct_tree *tree, const cct_paths *q, void *hip_stream,
   hipStream_t s = (hipStream_t)hip_stream;
   unsigned long long *hs = host_scratch();
   if (!hs) return fail(CCT_ENOMEM, "pinned host allocation failed");
-  g_alloc_countdown = 0;  // queries allocate one word; the hook is not armed
-  Buf err;
-  if (!err.alloc(8)) return fail(CCT_ENOMEM, "device allocation failed");
+  g_alloc_countdown = 0;  // queries allocate two small buffers; the hook is not armed
+  Buf err, sorted;
+  if (!err.alloc(8) || !sorted.alloc(std::max<int64_t>(tree->d, 1) * 16)) return fail(CCT_ENOMEM, "device allocation failed");
   HIP_TRY(hipMemsetAsync(err.p, 0, 8, s));
   QueryArgs a{};
   a.q = q->n_events; a.qn_frames = q->n_frames; a.qoff = q->offsets; a.qfr = q->frames;
@@ -1062,10 +1063,15 @@ cct_status cct_query(const cct_tree *tree, const cct_paths *q, void *hip_stream,
   a.order = tree->order.as<uint32_t>(); a.lcp = tree->lcp.as<uint32_t>(); a.scan_out = tree->scan_out.as<uint64_t>();
   a.excl = tree->excl.as<uint64_t>(); a.incl = tree->incl.as<uint64_t>();
   a.node_ids = node_ids; a.qexcl = excl; a.qincl = incl; a.err = err.as<unsigned long long>();
+  a.sorted = sorted.as<int64_t>();
+  Timer tm;
+  tm.mark(0, s);
   launch_query(a, s);
+  tm.mark(1, s);
   HIP_TRY(hipGetLastError());
   HIP_TRY(hipMemcpyAsync(hs, err.p, 8, hipMemcpyDeviceToHost, s));
   HIP_TRY(hipStreamSynchronize(s));
+  g_query_ms = tm.ok ? tm.span(0, 1) : 0.0;
   if (hs[0] & 2) return fail(CCT_EDEVICE, "query found an inconsistent tree");
   if (hs[0]) return fail(CCT_EINVAL, "malformed query offsets");
   return CCT_OK;
@@ -1114,13 +1120,14 @@ const char *cct_last_error(void) { return g_error.c_str(); }
 
 int cct_last_timings(double *ms, int n) {
   if (!ms || n <= 0) return 0;
-  const int k = n < 10 ? n : 10;
+  const int k = n < 11 ? n : 11;
   for (int i = 0; i < k && i < 5; ++i) ms[i] = g_timings[i];
   if (k > 5) ms[5] = g_join_ms;
   if (k > 6) ms[6] = g_view_ms;
   if (k > 7) ms[7] = g_filter_ms;
   if (k > 8) ms[8] = g_stats_ms;
   if (k > 9) ms[9] = g_node_stats_ms;
+  if (k > 10) ms[10] = g_query_ms;
   return k;
 }
 
