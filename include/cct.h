@@ -207,7 +207,9 @@ typedef struct {
  * has finished).  A tree built without statistics gives CCT_EINVAL. */
 cct_status cct_stats(const cct_tree *tree, void *hip_stream, const cct_node_stats *out);
 
-/* Look up Q call paths (queries->offsets/frames, metrics ignored) in `tree`.
+/* Look up Q call paths (queries->offsets/frames, metrics ignored) in `tree`.  The first
+ * query on a tree builds a hash index of its node prefixes (about 32 bytes per node, kept
+ * with the tree until it changes; without room for it, queries use binary search).
  * Writes DEVICE arrays: node_ids int64[Q] (the canonical id, or -1 if the path is
  * not a node), and, when non-NULL, excl/incl uint64[Q][M] (zeros for absent paths). */
 cct_status cct_query(const cct_tree *tree, const cct_paths *queries, void *hip_stream,
@@ -241,7 +243,8 @@ const char *cct_last_error(void);
  * (calls that only copy a kept view leave it as it is), [7] the last cct_filter, [8] the
  * statistics kept by the last build or merge (the batch's samples folded into the paths;
  * 0 for a tree without statistics), [9] the last cct_stats, [10] the last cct_query's
- * lookup kernel.  Returns the number of values written (<= n, at most 11). */
+ * lookups, [11] the prefix index that call built (0 when the tree's index was kept).
+ * Returns the number of values written (<= n, at most 12). */
 int cct_last_timings(double *ms, int n);
 
 #ifdef __cplusplus

@@ -328,9 +328,10 @@ def last_timings():
     canonical emission and total of the last build/merge, the correlation-ID join of a
     merge_activity call (0 otherwise), the most recent computation of a bottom-up view
     (bottom_up), the last filter, the statistics kept by the last build/merge (0 without),
-    the last ``Tree.stats``, and the last query's lookup."""
-    buf = (ctypes.c_double * 11)()
-    n = load_library().cct_last_timings(buf, 11)
+    the last ``Tree.stats``, the last query's lookups, and the prefix index it built (0 if
+    the tree's index was kept)."""
+    buf = (ctypes.c_double * 12)()
+    n = load_library().cct_last_timings(buf, 12)
     return list(buf)[:n]
 
 

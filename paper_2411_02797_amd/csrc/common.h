@@ -272,8 +272,16 @@ struct QueryArgs {
   int64_t *node_ids;
   uint64_t *qexcl, *qincl;
   unsigned long long *err;
-  int64_t *sorted;           // scratch [D][2]: first frame and length of the path at each canonical position
+  int64_t *sorted;           // [D][2]: first frame and length of the path at each canonical position
+  uint64_t *qtab;            // prefix index [qcap][2] {key, (length << 32) | position}, or null
+  uint64_t qcap_mask;
+  uint64_t qhash_mask;       // test setting: keys keep only these bits (forced collisions)
 };
+// the records of `sorted`
+void launch_sorted_paths(const QueryArgs &a, hipStream_t s);
+// the prefix index of every node (qtab cleared to zero first)
+void launch_query_index(const QueryArgs &a, hipStream_t s);
+// lookups: through the index when a.qtab is set, else by binary search
 void launch_query(const QueryArgs &a, hipStream_t s);
 
 // Correlation-ID join of an activity flush with the registered call paths (activity.hip)

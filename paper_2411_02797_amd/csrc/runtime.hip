@@ -27,7 +27,8 @@ thread_local double g_view_ms = 0;  // the most recent computation of a bottom-u
 thread_local double g_filter_ms = 0;  // the last cct_filter
 thread_local double g_stats_ms = 0;   // statistics kept by the last build/merge (0 without)
 thread_local double g_node_stats_ms = 0;  // the last cct_stats
-thread_local double g_query_ms = 0;       // the last cct_query
+thread_local double g_query_ms = 0;       // the last cct_query's lookups
+thread_local double g_qindex_ms = 0;      // the prefix index built by the last cct_query (0 if kept)
 thread_local int g_alloc_countdown = 0;  // test hook: >0 makes the n-th allocation of a call fail
 
 int64_t env_int(const char *name, int64_t dflt) {
@@ -241,6 +242,11 @@ struct cct_tree {
   // bottom-up view (cct_bottom_up), kept until the tree changes; bu_k < 0: not computed
   int64_t bu_k = -1;
   Buf bu_frames, bu_excl, bu_incl;
+  // query index, built by the first cct_query and kept until the tree changes (mutable: a
+  // query leaves the tree itself as it is)
+  mutable bool q_ready = false;
+  mutable uint64_t q_cap = 0, q_hash_mask = 0;  // q_cap = 0: no index (binary search)
+  mutable Buf q_sorted, q_tab;
   // canonical metadata kept for queries
   Buf order, lcp, scan_out;
 };
@@ -701,7 +707,8 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   t->u = (int64_t)hs[2];
   t->parent = std::move(n_parent); t->frame = std::move(n_frame); t->depth = std::move(n_depth);
   t->subend = std::move(n_subend);
-  t->bu_k = -1;  // the bottom-up view of the old tree is stale
+  t->bu_k = -1;        // the bottom-up view of the old tree is stale
+  t->q_ready = false;  // and so is the query index
   t->excl = std::move(n_excl); t->incl = std::move(n_incl);
   t->order = std::move(order); t->lcp = std::move(lcp); t->scan_out = std::move(scan_out);
   return CCT_OK;
@@ -1052,9 +1059,9 @@ cct_status cct_query(const cct_tree *tree, const cct_paths *q, void *hip_stream,
   hipStream_t s = (hipStream_t)hip_stream;
   unsigned long long *hs = host_scratch();
   if (!hs) return fail(CCT_ENOMEM, "pinned host allocation failed");
-  g_alloc_countdown = 0;  // queries allocate two small buffers; the hook is not armed
-  Buf err, sorted;
-  if (!err.alloc(8) || !sorted.alloc(std::max<int64_t>(tree->d, 1) * 16)) return fail(CCT_ENOMEM, "device allocation failed");
+  g_alloc_countdown = 0;  // queries allocate only what the index needs; the hook is not armed
+  Buf err;
+  if (!err.alloc(8)) return fail(CCT_ENOMEM, "device allocation failed");
   HIP_TRY(hipMemsetAsync(err.p, 0, 8, s));
   QueryArgs a{};
   a.q = q->n_events; a.qn_frames = q->n_frames; a.qoff = q->offsets; a.qfr = q->frames;
@@ -1063,7 +1070,40 @@ cct_status cct_query(const cct_tree *tree, const cct_paths *q, void *hip_stream,
   a.order = tree->order.as<uint32_t>(); a.lcp = tree->lcp.as<uint32_t>(); a.scan_out = tree->scan_out.as<uint64_t>();
   a.excl = tree->excl.as<uint64_t>(); a.incl = tree->incl.as<uint64_t>();
   a.node_ids = node_ids; a.qexcl = excl; a.qincl = incl; a.err = err.as<unsigned long long>();
-  a.sorted = sorted.as<int64_t>();
+  // the index: every node under the hash of its prefix (a test setting keeps fewer key bits,
+  // forcing collisions; another one uses the binary search); a table at most half full
+  const int qbits = (int)env_int("CCT_TEST_QUERY_HASH_BITS", 64);
+  const uint64_t hash_mask = qbits >= 64 ? ~0ull : ((1ull << (qbits < 1 ? 1 : qbits)) - 1);
+  const bool use_index = !env_int("CCT_TEST_QUERY_SEARCH", 0);
+  g_qindex_ms = 0;
+  if (!tree->q_ready || tree->q_hash_mask != hash_mask || (tree->q_cap != 0) != use_index) {
+    tree->q_ready = false;
+    Timer ti;
+    ti.mark(0, s);
+    if (!tree->q_sorted.alloc((size_t)std::max<int64_t>(tree->d, 1) * 16))
+      return fail(CCT_ENOMEM, "device allocation failed");
+    a.sorted = tree->q_sorted.as<int64_t>();
+    launch_sorted_paths(a, s);
+    tree->q_cap = 0;
+    tree->q_tab.release();
+    const uint64_t cap = pow2_at_least((uint64_t)std::max<int64_t>(2 * tree->u, 64));
+    if (use_index && tree->q_tab.alloc(cap * 16)) {  // without room for it, the binary search
+      tree->q_cap = cap;
+      HIP_TRY(hipMemsetAsync(tree->q_tab.p, 0, cap * 16, s));
+      a.qtab = tree->q_tab.as<uint64_t>(); a.qcap_mask = cap - 1; a.qhash_mask = hash_mask;
+      launch_query_index(a, s);
+    }
+    ti.mark(1, s);
+    HIP_TRY(hipGetLastError());
+    HIP_TRY(hipStreamSynchronize(s));
+    g_qindex_ms = ti.ok ? ti.span(0, 1) : 0.0;
+    tree->q_hash_mask = hash_mask;
+    tree->q_ready = true;
+  }
+  a.sorted = tree->q_sorted.as<int64_t>();
+  if (tree->q_cap) {
+    a.qtab = tree->q_tab.as<uint64_t>(); a.qcap_mask = tree->q_cap - 1; a.qhash_mask = hash_mask;
+  }
   Timer tm;
   tm.mark(0, s);
   launch_query(a, s);
@@ -1120,7 +1160,7 @@ const char *cct_last_error(void) { return g_error.c_str(); }
 
 int cct_last_timings(double *ms, int n) {
   if (!ms || n <= 0) return 0;
-  const int k = n < 11 ? n : 11;
+  const int k = n < 12 ? n : 12;
   for (int i = 0; i < k && i < 5; ++i) ms[i] = g_timings[i];
   if (k > 5) ms[5] = g_join_ms;
   if (k > 6) ms[6] = g_view_ms;
@@ -1128,6 +1168,7 @@ int cct_last_timings(double *ms, int n) {
   if (k > 8) ms[8] = g_stats_ms;
   if (k > 9) ms[9] = g_node_stats_ms;
   if (k > 10) ms[10] = g_query_ms;
+  if (k > 11) ms[11] = g_qindex_ms;
   return k;
 }
 

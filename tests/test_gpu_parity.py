@@ -264,9 +264,16 @@ def test_merge_into_empty_and_empty_merge():
 
 
 # ---- queries ---------------------------------------------------------------------------------
-def test_query_every_node_and_absent_paths():
+@pytest.mark.parametrize("mode", ["index", "search", "collisions"])
+def test_query_every_node_and_absent_paths(mode, monkeypatch):
+    # the prefix index, the binary search, and the index with 3-bit keys (every lookup
+    # meets many entries of other nodes with its key and must verify them)
     import paper_2411_02797_amd as cct
     torch = torch_or_skip()
+    if mode == "search":
+        monkeypatch.setenv("CCT_TEST_QUERY_SEARCH", "1")
+    elif mode == "collisions":
+        monkeypatch.setenv("CCT_TEST_QUERY_HASH_BITS", "3")
     o, f, w = tracegen.random_paths(3000, 40, 12, 2, seed=4)
     want = oracle.build_tree(o, f, w)
     tree = cct.build(*to_dev(o, f, w))
@@ -281,6 +288,18 @@ def test_query_every_node_and_absent_paths():
     assert np.array_equal(ex.cpu().numpy()[:U].view(np.uint64), want["excl"])
     assert np.array_equal(inc.cpu().numpy()[:U].view(np.uint64), want["incl"])
     assert np.all(inc.cpu().numpy()[U:] == 0)
+    # the kept index follows a merge: the same queries against the merged tree
+    o2, f2, w2 = tracegen.random_paths(2000, 60, 12, 2, seed=5)
+    tree.merge(*to_dev(o2, f2, w2))
+    oc = np.concatenate([o, o[-1] + o2[1:]])
+    want2 = oracle.build_tree(oc, np.concatenate([f, f2]), np.concatenate([w, w2]))
+    ids2, _, inc2 = tree.query(torch.from_numpy(qo).to(dev), torch.from_numpy(qf.view(np.int32)).to(dev))
+    paths2 = node_paths(want2, range(want2.n_nodes))
+    index_of = {tuple(p_): v for v, p_ in enumerate(paths2)}
+    exp = np.array([index_of.get(tuple(p_), -1) for p_ in paths + absent])
+    assert np.array_equal(ids2.cpu().numpy(), exp)
+    hit = exp >= 0
+    assert np.array_equal(inc2.cpu().numpy()[hit].view(np.uint64), want2["incl"][exp[hit]])
     tree.free()
 
 
