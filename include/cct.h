@@ -23,14 +23,18 @@
  *   - Node ids are canonical: the rank of the node's root path in unsigned
  *     lexicographic order, a proper prefix before its extensions (preorder, children
  *     by ascending frame id).  Subtrees are therefore contiguous id ranges.
- *   - The only aggregate is the sum, over uint64 modulo 2^64.
+ *   - Every tree keeps the sum, over uint64 modulo 2^64; a tree built with
+ *     cct_build_stats also keeps counts, minima and sums of squares (cct_stats).
  *   - excl[v][j] = sum of metric j over events whose path ends at v;
  *     incl[v][j] = sum of metric j over events whose path passes through v.
  *
  * Threads and streams: calls order all their device work on the given HIP stream
  * (NULL = the default stream) of the current device and return only after that
- * work has completed; input buffers may be freed on return.  Distinct trees may be
- * used from different threads at once; one tree must not be used concurrently.
+ * work has completed; input buffers may be freed on return.  A build or merge also runs
+ * part of its work on a second stream of its own, ordered by events and finished before
+ * it returns.  Distinct trees may be used from different threads at once; one tree must
+ * not be used concurrently, queries and views included (they build indexes and views
+ * that the tree keeps).
  *
  * Errors: every call returns a cct_status; nothing aborts, throws or prints.  On an
  * error, out-parameters are untouched and a tree passed to cct_merge is unchanged.
