@@ -1071,8 +1071,9 @@ cct_status cct_query(const cct_tree *tree, const cct_paths *q, void *hip_stream,
   a.excl = tree->excl.as<uint64_t>(); a.incl = tree->incl.as<uint64_t>();
   a.node_ids = node_ids; a.qexcl = excl; a.qincl = incl; a.err = err.as<unsigned long long>();
   // the index: every node under the hash of its prefix (a test setting keeps fewer key bits,
-  // forcing collisions; another one uses the binary search); a table at most half full
-  const int qbits = (int)env_int("CCT_TEST_QUERY_HASH_BITS", 64);
+  // forcing collisions, on trees of at most 2^15 nodes: on larger ones a few keys would
+  // make probing quadratic; another one uses the binary search); a table at most half full
+  const int qbits = tree->u <= (1 << 15) ? (int)env_int("CCT_TEST_QUERY_HASH_BITS", 64) : 64;
   const uint64_t hash_mask = qbits >= 64 ? ~0ull : ((1ull << (qbits < 1 ? 1 : qbits)) - 1);
   const bool use_index = !env_int("CCT_TEST_QUERY_SEARCH", 0);
   g_qindex_ms = 0;
