@@ -1056,6 +1056,9 @@ cct_status cct_query(const cct_tree *tree, const cct_paths *q, void *hip_stream,
   if (q->n_events > CCT_MAX_EVENTS) return fail(CCT_EOVERFLOW, "too many queries in one call");
   if (q->n_events > 0 && !node_ids) return fail(CCT_EINVAL, "node_ids is NULL");
   if (q->n_events == 0) return CCT_OK;
+  int dev = 0;
+  (void)hipGetDevice(&dev);
+  if (dev != tree->device) return fail(CCT_EINVAL, "tree belongs to another device");
   hipStream_t s = (hipStream_t)hip_stream;
   unsigned long long *hs = host_scratch();
   if (!hs) return fail(CCT_ENOMEM, "pinned host allocation failed");
