@@ -3,6 +3,8 @@ declares (no compute calls: there is no GPU here)."""
 import ctypes
 import os
 import re
+import shutil
+import subprocess
 
 import pytest
 
@@ -21,6 +23,19 @@ def test_header_declares_the_boundary():
     names = declared_symbols()
     for required in ("cct_build", "cct_merge", "cct_query", "cct_export", "cct_free", "cct_info"):
         assert required in names
+
+
+def test_header_is_plain_c_and_links(tmp_path):
+    # the plain C client of the GPU tests compiles as C11 with every warning an error and
+    # links against libcct.so and the HIP runtime (it is not run: there is no GPU here)
+    if shutil.which("gcc") is None or not os.path.isdir("/opt/rocm/include"):
+        pytest.skip("gcc or the HIP headers are not available")
+    pkg = os.path.dirname(cct.library_path())
+    subprocess.run(["gcc", "-std=c11", "-Wall", "-Wextra", "-Werror", "-D__HIP_PLATFORM_AMD__", "-I",
+                    "/opt/rocm/include", "-I", os.path.join(ROOT, "include"),
+                    os.path.join(ROOT, "tests", "c_abi", "cct_c_example.c"), "-L", pkg, "-lcct", "-L",
+                    "/opt/rocm/lib", "-lamdhip64", "-o", str(tmp_path / "cct_c_example")], check=True)
+    assert os.path.exists(tmp_path / "cct_c_example")
 
 
 def test_library_exports_every_declared_symbol():
