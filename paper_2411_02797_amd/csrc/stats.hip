@@ -428,9 +428,13 @@ __device__ inline double mean_of(uint64_t s1, uint64_t n) {
 }
 
 __global__ void node_final_kernel(NodeStatArgs a) {
-  const int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (u >= a.u) return;
-  const int C = 1 + 4 * a.m, C0 = 1 + a.m, m = a.m;
+  // one thread per (node, metric): consecutive threads write consecutive output entries
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int m = a.m;
+  if (t >= a.u * m) return;
+  const int64_t u = t / m;
+  const int j = (int)(t - u * m);
+  const int C = 1 + 4 * m, C0 = 1 + m;
   // the subtree's paths [i, e) and the path ending at u, if any (the root: all paths, and
   // the empty path if there is one, which sorts first and creates no node)
   int64_t i = 0, e = a.d, own = -1;
@@ -444,24 +448,24 @@ __global__ void node_final_kernel(NodeStatArgs a) {
   }
   const uint64_t *pi = a.prefix + i * C, *pe = a.prefix + e * C, *row = own >= 0 ? a.rows + own * C : nullptr;
   const uint64_t n_ex = row ? row[0] : 0, n_in = pe[0] - pi[0];
-  if (a.out.count_excl) a.out.count_excl[u] = n_ex;
-  if (a.out.count_incl) a.out.count_incl[u] = n_in;
-  for (int j = 0; j < m; ++j) {
-    const int64_t o = u * m + j;
-    uint64_t ex_lo = 0, ex_hi = 0, in_lo, in_hi;
-    if (row) limbs_to_u128(row[1 + 4 * j], row[2 + 4 * j], row[3 + 4 * j], row[4 + 4 * j], ex_lo, ex_hi);
-    limbs_to_u128(pe[1 + 4 * j] - pi[1 + 4 * j], pe[2 + 4 * j] - pi[2 + 4 * j], pe[3 + 4 * j] - pi[3 + 4 * j],
-                  pe[4 + 4 * j] - pi[4 + 4 * j], in_lo, in_hi);
-    if (a.out.min_excl) a.out.min_excl[o] = own >= 0 ? a.cmin[own * m + j] : ~0ull;
-    if (a.out.min_incl) a.out.min_incl[o] = e > i ? range_min(a, i, e - 1, j) : ~0ull;
-    if (a.out.sumsq_excl) { a.out.sumsq_excl[2 * o] = ex_lo; a.out.sumsq_excl[2 * o + 1] = ex_hi; }
-    if (a.out.sumsq_incl) { a.out.sumsq_incl[2 * o] = in_lo; a.out.sumsq_incl[2 * o + 1] = in_hi; }
-    const uint64_t s_ex = a.excl[o], s_in = a.incl[o];
-    if (a.out.mean_excl) a.out.mean_excl[o] = mean_of(s_ex, n_ex);
-    if (a.out.mean_incl) a.out.mean_incl[o] = mean_of(s_in, n_in);
-    if (a.out.std_excl) a.out.std_excl[o] = deviation(n_ex, s_ex, ex_lo, ex_hi);
-    if (a.out.std_incl) a.out.std_incl[o] = deviation(n_in, s_in, in_lo, in_hi);
+  if (j == 0) {
+    if (a.out.count_excl) a.out.count_excl[u] = n_ex;
+    if (a.out.count_incl) a.out.count_incl[u] = n_in;
   }
+  const int64_t o = t;  // u * m + j
+  uint64_t ex_lo = 0, ex_hi = 0, in_lo, in_hi;
+  if (row) limbs_to_u128(row[1 + 4 * j], row[2 + 4 * j], row[3 + 4 * j], row[4 + 4 * j], ex_lo, ex_hi);
+  limbs_to_u128(pe[1 + 4 * j] - pi[1 + 4 * j], pe[2 + 4 * j] - pi[2 + 4 * j], pe[3 + 4 * j] - pi[3 + 4 * j],
+                pe[4 + 4 * j] - pi[4 + 4 * j], in_lo, in_hi);
+  if (a.out.min_excl) a.out.min_excl[o] = own >= 0 ? a.cmin[own * m + j] : ~0ull;
+  if (a.out.min_incl) a.out.min_incl[o] = e > i ? range_min(a, i, e - 1, j) : ~0ull;
+  if (a.out.sumsq_excl) { a.out.sumsq_excl[2 * o] = ex_lo; a.out.sumsq_excl[2 * o + 1] = ex_hi; }
+  if (a.out.sumsq_incl) { a.out.sumsq_incl[2 * o] = in_lo; a.out.sumsq_incl[2 * o + 1] = in_hi; }
+  const uint64_t s_ex = a.excl[o], s_in = a.incl[o];
+  if (a.out.mean_excl) a.out.mean_excl[o] = mean_of(s_ex, n_ex);
+  if (a.out.mean_incl) a.out.mean_incl[o] = mean_of(s_in, n_in);
+  if (a.out.std_excl) a.out.std_excl[o] = deviation(n_ex, s_ex, ex_lo, ex_hi);
+  if (a.out.std_incl) a.out.std_incl[o] = deviation(n_in, s_in, in_lo, in_hi);
 }
 
 inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
@@ -542,7 +546,7 @@ void launch_node_stats(const NodeStatArgs &a, uint64_t *scan_blk, hipStream_t s)
       hipLaunchKernelGGL(rmq_level_kernel, dim3(blocks_for(a.nblk, 256)), dim3(256), 0, s, a, k);
   }
   launch_scan(a.rows, a.d, 1 + 4 * a.m, scan_blk, a.prefix, s);
-  hipLaunchKernelGGL(node_final_kernel, dim3(blocks_for(a.u, 256)), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(node_final_kernel, dim3(blocks_for(a.u * a.m, 256)), dim3(256), 0, s, a);
 }
 
 }  // namespace cct
