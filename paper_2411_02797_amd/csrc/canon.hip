@@ -378,11 +378,18 @@ __global__ void chain_kernel(CanonArgs a) {
 }
 
 __global__ __launch_bounds__(256) void emit_kernel(CanonArgs a) {
+  // a wave's 64 consecutive nodes stage their excl and incl rows in LDS ([2][256][m]
+  // words), then write each array's 64 m words as one contiguous stretch
+  extern __shared__ uint64_t emit_stage[];
   const int C = 1 + a.m, m = a.m;
+  const int lane = threadIdx.x & 63, w0 = threadIdx.x - lane;
+  uint64_t *sx = emit_stage + (int64_t)w0 * m, *si = emit_stage + (int64_t)(256 + w0) * m;
   const int64_t n = a.d + 1;
   const int64_t U = (int64_t)(1 + a.scan_out[a.d * C]);
   if (blockIdx.x == 0 && threadIdx.x == 0) a.u_out[0] = (unsigned long long)U;
-  for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < U; u += (int64_t)gridDim.x * blockDim.x) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t base = (int64_t)blockIdx.x * blockDim.x + w0; base < U; base += stride) {
+    const int64_t u = base + lane;
     if (u == 0) {
       a.parent[0] = kInf;
       a.frame[0] = 0;
@@ -390,27 +397,38 @@ __global__ __launch_bounds__(256) void emit_kernel(CanonArgs a) {
       a.subend[0] = (uint32_t)U;
       const bool empty_path = a.d > 0 && a.plen[a.order[0]] == 0;
       for (int j = 0; j < m; ++j) {
-        a.excl[j] = empty_path ? a.psums[(int64_t)a.order[0] * m + j] : 0;
-        a.incl[j] = a.scan_out[a.d * C + 1 + j];
+        sx[j] = empty_path ? a.psums[(int64_t)a.order[0] * m + j] : 0;
+        si[j] = a.scan_out[a.d * C + 1 + j];
       }
-      continue;
+    } else if (u < U) {
+      const int64_t i = a.node_path[u];
+      const uint32_t pid = a.order[i];
+      const uint32_t L = a.lcp[i], len = a.plen[pid];
+      const uint64_t b = node_base(a, i);
+      const uint32_t l = L + 1 + (uint32_t)(u - b);
+      a.parent[u] = u == (int64_t)b ? a.chain_parent[i] : (uint32_t)(u - 1);
+      a.frame[u] = a.pframes[a.pstart[pid] + l - 1];
+      a.depth[u] = l;
+      const int64_t e = (i + 1 == a.d || l > a.lcp[i + 1]) ? i + 1 : next_smaller(a, n, i + 2, l);
+      // the subtree is the paths i .. e-1 below depth l: ids up to the first node of path e
+      a.subend[u] = (uint32_t)node_base(a, e);
+      const uint64_t *pi = a.scan_out + i * C, *pe = a.scan_out + e * C;
+      for (int j = 0; j < m; ++j) {
+        sx[lane * m + j] = l == len ? a.psums[(int64_t)pid * m + j] : 0;
+        si[lane * m + j] = pe[1 + j] - pi[1 + j];
+      }
     }
-    const int64_t i = a.node_path[u];
-    const uint32_t pid = a.order[i];
-    const uint32_t L = a.lcp[i], len = a.plen[pid];
-    const uint64_t b = node_base(a, i);
-    const uint32_t l = L + 1 + (uint32_t)(u - b);
-    a.parent[u] = u == (int64_t)b ? a.chain_parent[i] : (uint32_t)(u - 1);
-    a.frame[u] = a.pframes[a.pstart[pid] + l - 1];
-    a.depth[u] = l;
-    const int64_t e = (i + 1 == a.d || l > a.lcp[i + 1]) ? i + 1 : next_smaller(a, n, i + 2, l);
-    // the subtree is the paths i .. e-1 below depth l: ids up to the first node of path e
-    a.subend[u] = (uint32_t)node_base(a, e);
-    const uint64_t *si = a.scan_out + i * C, *se = a.scan_out + e * C;
-    for (int j = 0; j < m; ++j) {
-      a.excl[u * m + j] = l == len ? a.psums[(int64_t)pid * m + j] : 0;
-      a.incl[u * m + j] = se[1 + j] - si[1 + j];
+    // every lane's LDS writes before any lane's reads
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_wave_barrier();
+    const int64_t words = (U - base < 64 ? U - base : 64) * m;
+    for (int64_t k = lane; k < words; k += 64) {
+      a.excl[base * m + k] = sx[k];
+      a.incl[base * m + k] = si[k];
     }
+    // every lane's reads before the next nodes' writes
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_wave_barrier();
   }
 }
 
@@ -480,7 +498,7 @@ void launch_canon(const CanonArgs &a, hipStream_t s) {
   for (int k = top + 1; k < a.levels; ++k)
     hipLaunchKernelGGL(sparse_level_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, a.sparse, n, k);
   if (a.d > 0) hipLaunchKernelGGL(chain_kernel, dim3(blocks_for(a.d, 256)), dim3(256), 0, s, a);
-  hipLaunchKernelGGL(emit_kernel, dim3(a.grid_nodes), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(emit_kernel, dim3(a.grid_nodes), dim3(256), (size_t)2 * 256 * a.m * 8, s, a);
 }
 
 }  // namespace cct
