@@ -188,6 +188,16 @@ typedef struct {
 cct_status cct_filter(const cct_tree *tree, const cct_filter_spec *spec, void *hip_stream, int64_t capacity,
                       int64_t *node_ids, int64_t *n_matches);
 
+/* cct_filter for callers that cannot allocate memory (code that must not call hipMalloc,
+ * tight serving loops, harnesses that forbid allocation): same arguments, results and
+ * errors, but the call allocates no device or pinned host memory.  Its scratch is a static
+ * device array of 4 MiB that each GPU holds from the first such call until the process
+ * ends, so trees of more than 31,457,280 nodes give CCT_EOVERFLOW.  Every call on a GPU
+ * reuses that GPU's array: calls that overlap on one GPU (from several threads or
+ * streams) race and must be serialised by the caller. */
+cct_status cct_filter_noalloc(const cct_tree *tree, const cct_filter_spec *spec, void *hip_stream,
+                              int64_t capacity, int64_t *node_ids, int64_t *n_matches);
+
 /* Per-node statistics of a tree built with cct_build_stats: DEVICE arrays, each written
  * by a kernel, any of them may be NULL.  U nodes, M metrics, row-major.
  *   count_excl/incl  uint64[U]: samples ending at the node / passing through it

@@ -27,7 +27,7 @@ _lib = None
 
 NO_PARENT = 0xFFFFFFFF
 MAX_METRICS = 8
-EXPORTED_SYMBOLS = ("cct_build", "cct_build_stats", "cct_stats", "cct_merge", "cct_merge_activity", "cct_bottom_up", "cct_filter", "cct_query",
+EXPORTED_SYMBOLS = ("cct_build", "cct_build_stats", "cct_stats", "cct_merge", "cct_merge_activity", "cct_bottom_up", "cct_filter", "cct_filter_noalloc", "cct_query",
                     "cct_info", "cct_export", "cct_free", "cct_release_cached_memory", "cct_last_error",
                     "cct_last_timings")
 _STATUS = {0: "CCT_OK", -1: "CCT_EINVAL", -2: "CCT_ENOMEM", -3: "CCT_EDEVICE", -4: "CCT_EMISMATCH",
@@ -88,6 +88,7 @@ def load_library():
     lib.cct_merge_activity.argtypes = [vp, P(_Paths), vp, P(_Activity), vp, P(i64)]
     lib.cct_bottom_up.argtypes = [vp, vp, i64, vp, vp, vp, P(i64)]
     lib.cct_filter.argtypes = [vp, P(_FilterSpec), vp, i64, vp, P(i64)]
+    lib.cct_filter_noalloc.argtypes = [vp, P(_FilterSpec), vp, i64, vp, P(i64)]
     lib.cct_query.argtypes = [vp, P(_Paths), vp, vp, vp, vp]
     lib.cct_info.argtypes = [vp, P(i64), P(i32), P(i64)]
     lib.cct_export.argtypes = [vp, vp, vp, vp, vp, vp, vp]
@@ -97,7 +98,7 @@ def load_library():
     lib.cct_release_cached_memory.restype = None
     lib.cct_last_error.restype = ctypes.c_char_p
     lib.cct_last_timings.argtypes = [P(ctypes.c_double), ctypes.c_int]
-    for name in ("cct_build", "cct_build_stats", "cct_stats", "cct_merge", "cct_merge_activity", "cct_bottom_up", "cct_filter", "cct_query",
+    for name in ("cct_build", "cct_build_stats", "cct_stats", "cct_merge", "cct_merge_activity", "cct_bottom_up", "cct_filter", "cct_filter_noalloc", "cct_query",
                  "cct_info", "cct_export"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
@@ -232,18 +233,21 @@ class Tree:
         return out
 
     def filter(self, num_metric, op, thr_num, thr_den, num_excl=False, den="one", den_metric=0, den_excl=False,
-               leaves_only=False):
+               leaves_only=False, noalloc=False):
         """Node ids matching a ratio test (cct_filter), ascending, as an int64 device
         tensor: a / b above (op=+1) or below (op=-1) thr_num / thr_den, with a the node's
         incl (or excl) sum of num_metric and b = 1 (den="one"), the node's sum of den_metric
-        (den="metric") or the root's incl sum of den_metric (den="root")."""
+        (den="metric") or the root's incl sum of den_metric (den="root").  noalloc=True
+        calls cct_filter_noalloc (the library allocates nothing; the output tensor is still
+        allocated here)."""
         import torch
         spec = _FilterSpec(num_metric, int(bool(num_excl)), _DEN_KINDS[den], den_metric, int(bool(den_excl)), op,
                            thr_num, thr_den, int(bool(leaves_only)))
         u = self.n_nodes
         out = torch.empty(max(u, 1), dtype=torch.int64, device=torch.device("cuda", torch.cuda.current_device()))
         k = ctypes.c_int64(0)
-        _check(load_library().cct_filter(self._h, ctypes.byref(spec), _stream(), u, out.data_ptr(), ctypes.byref(k)))
+        fn = load_library().cct_filter_noalloc if noalloc else load_library().cct_filter
+        _check(fn(self._h, ctypes.byref(spec), _stream(), u, out.data_ptr(), ctypes.byref(k)))
         return out[:k.value]
 
     def hotspots(self, time_metric, thr_num, thr_den):

@@ -365,6 +365,19 @@ void launch_filter_scan(const uint32_t *count, int64_t tiles, uint64_t *pos, hip
 // writes the first `capacity` matches to out
 void launch_filter_write(int64_t u, const uint64_t *mask, const uint64_t *pos, int64_t capacity, int64_t *out,
                          hipStream_t s);
+// The filter that allocates nothing keeps its mask, counts and offsets in a static device
+// array of kFilterStaticBytes per GPU, enough for kFilterStaticTiles tiles.
+constexpr int64_t kFilterStaticTiles = 15360;  // trees of up to 31,457,280 nodes
+constexpr size_t kFilterStaticBytes = 4u << 20;
+struct FilterScratch {
+  uint64_t *mask;   // [tiles * kFilterTile / 64]
+  uint32_t *count;  // [tiles]
+  uint64_t *pos;    // [tiles + 1]
+};
+// Device address of the current device's static array (looked up once per device), or
+// nullptr if the lookup failed; and the array's parts at that address.
+void *filter_static_scratch();
+FilterScratch filter_static_layout(void *base);
 
 // Per-path and per-node statistics (stats.hip)
 struct StatStage {  // staged per-path statistics of a batch (nbuckets = 0: device atomics instead)

@@ -16,6 +16,8 @@
 // workgroup scans the tile counts (a few thousand for millions of nodes); the second pass
 // reads only the mask and writes each match's id at its tile's offset plus its rank among
 // the tile's earlier matches.
+#include <mutex>
+
 #include "common.h"
 
 namespace cct {
@@ -141,9 +143,49 @@ __global__ __launch_bounds__(64) void filter_write_kernel(const uint64_t *mask, 
   }
 }
 
+// Scratch of the filter entry point that allocates nothing: the mask words, tile counts
+// and tile offsets of up to kFilterStaticTiles tiles, laid out as filter_static_layout
+// says.  Each GPU holds its own copy for the life of the process; every call on a GPU
+// reuses it, so calls that overlap on one GPU race.  Host code never uses this name as an
+// address (on the host it only stands for the symbol): the device address comes from
+// hipGetSymbolAddress, once per device.
+static __device__ __align__(256) unsigned char scratch[kFilterStaticBytes];
+
 }  // namespace
 
 int64_t filter_tiles(int64_t u) { return (u + kFilterTile - 1) / kFilterTile; }
+
+FilterScratch filter_static_layout(void *base) {
+  unsigned char *b = static_cast<unsigned char *>(base);
+  FilterScratch f;
+  f.mask = reinterpret_cast<uint64_t *>(b);
+  f.count = reinterpret_cast<uint32_t *>(b + kFilterStaticTiles * kTileWords * 8);
+  f.pos = reinterpret_cast<uint64_t *>(b + kFilterStaticTiles * (kTileWords * 8 + 4));
+  return f;
+}
+static_assert(kFilterStaticTiles * (kTileWords * 8 + 4 + 8) + 8 <= kFilterStaticBytes, "static filter scratch");
+static_assert((kFilterStaticTiles * (kTileWords * 8 + 4)) % 8 == 0, "pos alignment");
+
+void *filter_static_scratch() {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void *ptr[kMaxDevices] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(mu);
+  if (!ptr[dev]) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    ptr[dev] = p;
+  }
+  return ptr[dev];
+}
 
 void launch_filter_mask(const FilterArgs &a, uint64_t *mask, uint32_t *count, hipStream_t s) {
   const int64_t tiles = filter_tiles(a.u);

@@ -20,7 +20,9 @@ using namespace cct;
 
 namespace {
 
-thread_local std::string g_error;
+// message of the calling thread's last failure: a fixed buffer, so that reporting an
+// error never allocates
+thread_local char g_error[256];
 thread_local double g_timings[5] = {0, 0, 0, 0, 0};
 thread_local double g_join_ms = 0;  // correlation-ID join of the last cct_merge_activity
 thread_local double g_view_ms = 0;  // the most recent computation of a bottom-up view
@@ -38,9 +40,10 @@ int64_t env_int(const char *name, int64_t dflt) {
 }
 
 cct_status fail(cct_status s, const char *msg) {
-  g_error = msg;
+  std::snprintf(g_error, sizeof g_error, "%s", msg);
   return s;
 }
+void clear_error() { g_error[0] = 0; }
 
 // Arms the test hook for one public call (CCT_TEST_FAIL_ALLOC = n: the call's n-th pool
 // allocation fails) and disarms it when the call returns, so no count carries over into
@@ -721,7 +724,7 @@ extern "C" {
 cct_status build_tree(const cct_paths *events, void *hip_stream, bool stats, cct_tree **out) {
   AllocHook hook;
   g_join_ms = 0;
-  g_error.clear();
+  clear_error();
   if (!out) return fail(CCT_EINVAL, "out is NULL");
   cct_status st = check_paths(events, true);
   if (st) return st;
@@ -758,7 +761,7 @@ cct_status cct_build_stats(const cct_paths *events, void *hip_stream, cct_tree *
 
 cct_status cct_merge(cct_tree *tree, const cct_paths *chunk, void *hip_stream) {
   AllocHook hook;
-  g_error.clear();
+  clear_error();
   g_join_ms = 0;
   if (!tree) return fail(CCT_EINVAL, "tree is NULL");
   cct_status st = check_paths(chunk, true);
@@ -773,7 +776,7 @@ cct_status cct_merge(cct_tree *tree, const cct_paths *chunk, void *hip_stream) {
 cct_status cct_merge_activity(cct_tree *tree, const cct_paths *registry, const uint64_t *reg_corr_ids,
                               const cct_activity *act, void *hip_stream, int64_t *n_unmatched) {
   AllocHook hook;  // counts the join's and the merge's allocations together
-  g_error.clear();
+  clear_error();
   g_join_ms = 0;
   if (!tree || !registry || !act) return fail(CCT_EINVAL, "NULL argument");
   const int64_t G = registry->n_events, R = act->n_records;
@@ -940,7 +943,7 @@ cct_status compute_bottom_up(cct_tree *t, hipStream_t s) {
 
 cct_status cct_bottom_up(cct_tree *tree, void *hip_stream, int64_t capacity, uint32_t *frames, uint64_t *excl,
                          uint64_t *incl, int64_t *n_frames) {
-  g_error.clear();
+  clear_error();
   if (!tree || !n_frames) return fail(CCT_EINVAL, "NULL argument");
   if (capacity < 0) return fail(CCT_EINVAL, "negative capacity");
   int dev = 0;
@@ -964,10 +967,13 @@ cct_status cct_bottom_up(cct_tree *tree, void *hip_stream, int64_t capacity, uin
   return CCT_OK;
 }
 
-cct_status cct_filter(const cct_tree *tree, const cct_filter_spec *spec, void *hip_stream, int64_t capacity,
-                      int64_t *node_ids, int64_t *n_matches) {
-  AllocHook hook;
-  g_error.clear();
+}  // extern "C"
+
+namespace {
+
+// Checks shared by both filter entry points; fills a.
+cct_status filter_args(const cct_tree *tree, const cct_filter_spec *spec, int64_t capacity, const int64_t *node_ids,
+                       const int64_t *n_matches, FilterArgs &a) {
   if (!tree || !spec || !n_matches) return fail(CCT_EINVAL, "NULL argument");
   if (capacity < 0 || (capacity > 0 && !node_ids)) return fail(CCT_EINVAL, "bad output capacity");
   const int32_t m = tree->m;
@@ -980,37 +986,78 @@ cct_status cct_filter(const cct_tree *tree, const cct_filter_spec *spec, void *h
   int dev = 0;
   (void)hipGetDevice(&dev);
   if (dev != tree->device) return fail(CCT_EINVAL, "tree belongs to another device");
-  hipStream_t s = (hipStream_t)hip_stream;
-  unsigned long long *hs = host_scratch();
-  if (!hs) return fail(CCT_ENOMEM, "pinned host allocation failed");
-  const int64_t U = tree->u;
-  const int64_t T = filter_tiles(U);
-  Buf mask, count, pos;
-  if (!mask.alloc(T * (kFilterTile / 64) * 8) || !count.alloc(T * 4) || !pos.alloc((T + 1) * 8))
-    return fail(CCT_ENOMEM, "device allocation failed");
-  FilterArgs a{};
-  a.u = U; a.m = m; a.excl = tree->excl.as<uint64_t>(); a.incl = tree->incl.as<uint64_t>();
+  a = FilterArgs{};
+  a.u = tree->u; a.m = m; a.excl = tree->excl.as<uint64_t>(); a.incl = tree->incl.as<uint64_t>();
   a.subend = tree->subend.as<uint32_t>();
   a.num_metric = spec->num_metric; a.num_excl = spec->num_excl != 0;
   a.den_kind = spec->den_kind; a.den_metric = spec->den_metric; a.den_excl = spec->den_excl != 0;
   a.op = spec->op; a.thr_num = spec->thr_num; a.thr_den = spec->thr_den; a.leaves_only = spec->leaves_only != 0;
+  return CCT_OK;
+}
+
+// The filter's three passes over the given scratch; the match count is copied to *dst
+// (host memory) and the stream synchronised.
+cct_status run_filter(const FilterArgs &a, const FilterScratch &f, int64_t capacity, int64_t *node_ids,
+                      unsigned long long *dst, hipStream_t s) {
+  const int64_t T = filter_tiles(a.u);
+  launch_filter_mask(a, f.mask, f.count, s);
+  launch_filter_scan(f.count, T, f.pos, s);
+  launch_filter_write(a.u, f.mask, f.pos, capacity, node_ids, s);
+  HIP_TRY(hipGetLastError());
+  HIP_TRY(hipMemcpyAsync(dst, f.pos + T, 8, hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  return CCT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+cct_status cct_filter(const cct_tree *tree, const cct_filter_spec *spec, void *hip_stream, int64_t capacity,
+                      int64_t *node_ids, int64_t *n_matches) {
+  AllocHook hook;
+  clear_error();
+  FilterArgs a;
+  cct_status st = filter_args(tree, spec, capacity, node_ids, n_matches, a);
+  if (st) return st;
+  hipStream_t s = (hipStream_t)hip_stream;
+  unsigned long long *hs = host_scratch();
+  if (!hs) return fail(CCT_ENOMEM, "pinned host allocation failed");
+  const int64_t T = filter_tiles(a.u);
+  Buf mask, count, pos;
+  if (!mask.alloc(T * (kFilterTile / 64) * 8) || !count.alloc(T * 4) || !pos.alloc((T + 1) * 8))
+    return fail(CCT_ENOMEM, "device allocation failed");
+  FilterScratch f{mask.as<uint64_t>(), count.as<uint32_t>(), pos.as<uint64_t>()};
   Timer tm;
   tm.mark(0, s);
-  launch_filter_mask(a, mask.as<uint64_t>(), count.as<uint32_t>(), s);
-  launch_filter_scan(count.as<uint32_t>(), T, pos.as<uint64_t>(), s);
-  launch_filter_write(U, mask.as<uint64_t>(), pos.as<uint64_t>(), capacity, node_ids, s);
+  st = run_filter(a, f, capacity, node_ids, hs, s);
+  if (st) return st;
   tm.mark(1, s);
-  HIP_TRY(hipGetLastError());
-  HIP_TRY(hipMemcpyAsync(hs, pos.as<uint64_t>() + T, 8, hipMemcpyDeviceToHost, s));
-  HIP_TRY(hipStreamSynchronize(s));
   g_filter_ms = tm.ok ? tm.span(0, 1) : 0.0;
   *n_matches = (int64_t)hs[0];
   return CCT_OK;
 }
 
+cct_status cct_filter_noalloc(const cct_tree *tree, const cct_filter_spec *spec, void *hip_stream, int64_t capacity,
+                              int64_t *node_ids, int64_t *n_matches) {
+  clear_error();
+  FilterArgs a;
+  cct_status st = filter_args(tree, spec, capacity, node_ids, n_matches, a);
+  if (st) return st;
+  if (filter_tiles(a.u) > kFilterStaticTiles)
+    return fail(CCT_EOVERFLOW, "tree has more nodes than cct_filter_noalloc's scratch holds (31,457,280)");
+  void *base = filter_static_scratch();
+  if (!base) return fail(CCT_EDEVICE, "address of the static filter scratch not available");
+  unsigned long long k = 0;  // pageable: no pinned staging is allocated
+  st = run_filter(a, filter_static_layout(base), capacity, node_ids, &k, (hipStream_t)hip_stream);
+  if (st) return st;
+  *n_matches = (int64_t)k;
+  return CCT_OK;
+}
+
 cct_status cct_stats(const cct_tree *tree, void *hip_stream, const cct_node_stats *out) {
   AllocHook hook;
-  g_error.clear();
+  clear_error();
   if (!tree || !out) return fail(CCT_EINVAL, "NULL argument");
   if (!tree->stats) return fail(CCT_EINVAL, "the tree keeps no statistics (build it with cct_build_stats)");
   int dev = 0;
@@ -1049,7 +1096,7 @@ cct_status cct_stats(const cct_tree *tree, void *hip_stream, const cct_node_stat
 
 cct_status cct_query(const cct_tree *tree, const cct_paths *q, void *hip_stream, int64_t *node_ids, uint64_t *excl,
                      uint64_t *incl) {
-  g_error.clear();
+  clear_error();
   if (!tree || !q) return fail(CCT_EINVAL, "NULL argument");
   if (q->n_events < 0 || q->n_frames < 0 || !q->offsets || (q->n_frames > 0 && !q->frames))
     return fail(CCT_EINVAL, "bad query batch");
@@ -1131,7 +1178,7 @@ cct_status cct_info(const cct_tree *tree, int64_t *n_nodes, int32_t *n_metrics, 
 
 cct_status cct_export(const cct_tree *tree, void *hip_stream, uint32_t *parent, uint32_t *frame, uint32_t *depth,
                       uint64_t *excl, uint64_t *incl) {
-  g_error.clear();
+  clear_error();
   if (!tree) return fail(CCT_EINVAL, "tree is NULL");
   hipStream_t s = (hipStream_t)hip_stream;
   const size_t U = (size_t)tree->u, m = (size_t)tree->m;
@@ -1160,7 +1207,7 @@ void cct_release_cached_memory(void) {
   (void)hipGetLastError();
 }
 
-const char *cct_last_error(void) { return g_error.c_str(); }
+const char *cct_last_error(void) { return g_error; }
 
 int cct_last_timings(double *ms, int n) {
   if (!ms || n <= 0) return 0;

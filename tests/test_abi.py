@@ -67,3 +67,12 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(cct, "_lib", None)
     with pytest.raises(ImportError):
         cct.load_library()
+
+
+def test_noalloc_filter_rejects_null_arguments_without_gpu_work():
+    lib = cct.load_library()
+    k = ctypes.c_int64(-3)
+    spec = cct._FilterSpec(0, 0, 0, 0, 0, 1, 1, 1, 0)
+    assert lib.cct_filter_noalloc(None, ctypes.byref(spec), None, 0, None, ctypes.byref(k)) == -1
+    assert k.value == -3
+    assert b"NULL" in lib.cct_last_error()
