@@ -87,6 +87,43 @@ def measured_traffic(workload):
     return r.get("bytes_per_launch")
 
 
+def host_cpu():
+    """Host CPU model and the logical CPUs this process may run on."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return model, len(os.sched_getaffinity(0)), os.cpu_count()
+
+
+def achievable_read(torch, buf):
+    """Same-run achievable read bandwidth: the best of five plain coalesced reads of the
+    frames buffer (libcct_readbw.so), as context for the 8 TB/s denominator."""
+    import ctypes
+    path = os.path.join(ROOT, "paper_2411_02797_amd", "libcct_readbw.so")
+    if not os.path.exists(path):
+        return None
+    lib = ctypes.CDLL(path)
+    lib.cctbw_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
+                               ctypes.POINTER(ctypes.c_float)]
+    lib.cctbw_read.restype = ctypes.c_int
+    sink = torch.zeros(4096, dtype=torch.int32, device=buf.device)
+    nbytes = buf.numel() * buf.element_size()
+    best = ctypes.c_float(0)
+    rc = lib.cctbw_read(ctypes.c_void_p(buf.data_ptr()), nbytes, ctypes.c_void_p(sink.data_ptr()),
+                        ctypes.c_void_p(torch.cuda.current_stream().cuda_stream), 5, ctypes.byref(best))
+    if rc != 0 or best.value <= 0:
+        return None
+    gbps = nbytes / (best.value * 1e-3) / 1e9
+    return {"gbps": gbps, "frac_of_peak": gbps / HBM_PEAK_GBPS, "bytes": nbytes, "best_ms": best.value,
+            "kernel": "plain coalesced read of the frames buffer, best of 5, same run"}
+
+
 def cpu_baseline(offsets, frames, metrics, sample_events):
     import oracle
     n = min(sample_events, offsets.size - 1)
@@ -99,9 +136,11 @@ def cpu_baseline(offsets, frames, metrics, sample_events):
     orc.tree()
     dt = time.perf_counter() - t0
     orc.close()
+    model, nproc, ncpu = host_cpu()
     return {"value": n / dt, "unit": "events/s", "cores": 1, "kind": "oracle",
             "sample": f"first {n:,} events ({int(o[-1]):,} frames) of the same trace, std::map trie "
-                      f"(single thread, g++ -O2), {dt:.1f} s"}
+                      f"(single thread, g++ -O2), {dt:.1f} s",
+            "nproc": nproc, "host_cpus": ncpu, "cpu_model": model}
 
 
 def main():
@@ -163,12 +202,14 @@ def main():
         tree.free()
         log(f"warmup {i}: U={U:,} D={D:,} phases(ms)={['%.3f' % x for x in cct.last_timings()]}")
     torch.cuda.synchronize()
-    phases = []
+    phases, step_wall = [], []
     t_start = time.perf_counter()
     for _ in range(args.steps):
-        tree = cct.build(to, tf, tw)
+        t_step = time.perf_counter()
+        tree = cct.build(to, tf, tw)  # returns once the stream has finished the build
         phases.append(cct.last_timings())
         tree.free()
+        step_wall.append((time.perf_counter() - t_step) * 1000.0)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
     ms = wall * 1000.0 / args.steps
@@ -207,6 +248,10 @@ def main():
         "effective_frac_of_peak": b_alg / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
         "phase_ms": {"ingest": ingest_ms, "publish": float(ph[:, 1].mean()), "sort": float(ph[:, 2].mean()),
                      "emit": float(ph[:, 3].mean()), "call": float(ph[:, 4].mean())},
+        "step_ms": {"mean": ms, "median": float(np.median(step_wall)), "min": float(np.min(step_wall))},
+        "call_ms": {"mean": float(ph[:, 4].mean()), "median": float(np.median(ph[:, 4])),
+                    "min": float(np.min(ph[:, 4]))},
+        "achievable_read": achievable_read(torch, tf),
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(o, f, w, args.cpu_sample)
@@ -232,19 +277,25 @@ def bench_merge(args, torch, tracegen, cct, dev):
         f"F={n_chunk_frames:,} in {time.perf_counter() - t0:.1f}s")
     merge_ms, phases, base_ms = [], [], []
     U = D = 0
+    sizes = []  # (U before, U after) of every merge of the last step
     for step in range(args.warmup + args.steps):
         tree = cct.build(*base)
         base_ms.append(cct.last_timings()[4])
         torch.cuda.synchronize()
         t_seq = time.perf_counter()
-        ph = []
+        ph, sz = [], []
+        u_prev = tree.n_nodes
         for ch in chunks:
             tree.merge(*ch)
             ph.append(cct.last_timings())
+            u_now = tree.n_nodes  # host-side (cct_info reads no device memory)
+            sz.append((u_prev, u_now))
+            u_prev = u_now
         torch.cuda.synchronize()
         wall = (time.perf_counter() - t_seq) * 1000.0
         U, _, D = tree._info()
         tree.free()
+        sizes = sz
         if step >= args.warmup:
             merge_ms.append(wall)
             phases.extend(ph)
@@ -254,6 +305,12 @@ def bench_merge(args, torch, tracegen, cct, dev):
     ingest_ms = float(ph[:, 0].mean())
     b_ingest = 8 * (n_chunk_events // 32 + 1) + 4 * (n_chunk_frames // 32)
     achieved = b_ingest / (ingest_ms * 1e-3) / 1e9
+    # whole-merge algorithmic bytes of the 32 merges of a step: each reads its chunk's
+    # offsets, frames and metrics and the old nodes' exclusive sums, and writes every
+    # node's parent, frame, depth, exclusive and inclusive sums
+    b_merge = (8 * (n_chunk_events + 32) + 4 * n_chunk_frames + 8 * M * n_chunk_events
+               + sum(u1 * (12 + 16 * M) + u0 * 8 * M for u0, u1 in sizes))
+    eff = b_merge / (ms * 1e-3) / 1e9
     line = {
         "metric": METRIC, "value": n_chunk_events / (ms * 1e-3), "unit": "events/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
@@ -268,6 +325,11 @@ def bench_merge(args, torch, tracegen, cct, dev):
         "phase_ms_per_merge": {"ingest": ingest_ms, "publish": float(ph[:, 1].mean()),
                                "sort": float(ph[:, 2].mean()), "emit": float(ph[:, 3].mean()),
                                "call": float(ph[:, 4].mean())},
+        "effective_hbm_gbps": eff,
+        "effective_frac_of_peak": eff / HBM_PEAK_GBPS,
+        "step_ms": {"mean": ms, "median": float(np.median(merge_ms)), "min": float(np.min(merge_ms))},
+        "merge_call_ms": {"median": float(np.median(ph[:, 4])), "min": float(np.min(ph[:, 4]))},
+        "achievable_read": achievable_read(torch, chunks[0][1]),
     }
     print(json.dumps(line), flush=True)
 

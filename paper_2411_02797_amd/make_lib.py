@@ -8,6 +8,10 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libcct.so")
+# the read-bandwidth probe the bench reports beside the tree-building kernels (not part
+# of the library's API)
+READBW_SRC = "readbw.hip"
+READBW_OUT = os.path.join(HERE, "libcct_readbw.so")
 SOURCES = ["ingest.hip", "canon.hip", "trie.hip", "query.hip", "activity.hip", "bottomup.hip", "filter.hip", "stats.hip", "runtime.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
@@ -42,6 +46,14 @@ def build(verbose: bool = False, jobs: int = 4) -> str:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True, capture_output=not verbose)
     os.replace(tmp, OUT)
+    tmp = READBW_OUT + ".tmp"
+    cmd = [HIPCC, *FLAGS, "-shared", os.path.join(CSRC, READBW_SRC), "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed for {READBW_SRC}:\n{r.stderr}")
+    os.replace(tmp, READBW_OUT)
     return OUT
 
 
