@@ -8,9 +8,9 @@
  * call path and propagated to the root along the whole path.  cct_merge
  * aggregates a further batch into an existing tree, as the profiler does when it
  * flushes a full metric buffer into its tree (Design, "Profiler", "GPU Metrics");
- * cct_query looks up the metrics of given call paths, the "query the metric data
- * associated with the tree nodes" step of the analysis API (Design, "Performance
- * Analyzer", "Analysis API").
+ * cct_query looks up the metrics of given call paths, as the analysis API reads the
+ * metrics of the nodes on matched call paths (Design, "Performance Analyzer",
+ * "Analysis API").
  *
  * Data conventions (the paper is silent on all of them; these are this library's
  * readings):

@@ -5,7 +5,7 @@
 //
 // What it computes: the calling context tree of the paper's profiler (Design,
 // "Profiler", paragraph "Calling Context Tree"): call paths are inserted into a tree
-// whose nodes collapse frames that refer to the same location, each node holds a list
+// whose nodes merge frames that name one location, each node holds a list
 // of metrics, a metric is added at the bottom node of its call path and propagated to
 // the root along the whole path.  Frames are uint32 ids (equal iff the ids are equal),
 // the sum is the only aggregate, sums wrap modulo 2^64, the root is the empty path,

@@ -13,9 +13,9 @@
 //     largest c < i with lcp_c < lcp_i (previous smaller value); every other chain
 //     node's parent is the node before it;
 //   - the paths through node (i, l) are exactly p_i .. p_{e-1}, e the first j > i
-//     with lcp_j < l (next smaller value), and since a metric lands at the end node
-//     of its path ("at the bottom of a call path") and is propagated "along the
-//     entire call path" to the root, inclusive(i, l) = S[e] - S[i] with S the
+//     with lcp_j < l (next smaller value), and since a metric is added at the last
+//     node of its path and then counted at every node up to the root (Design,
+//     "Profiler", "Calling Context Tree"), inclusive(i, l) = S[e] - S[i] with S the
 //     exclusive prefix sum of the per-path sums in sorted order (mod 2^64);
 //   - exclusive(i, len_i) = the sums of path i, every other node has none (the empty
 //     path, which sorts first, puts its sums on the root).
@@ -200,10 +200,19 @@ __global__ void lcp_kernel(CanonArgs a) {
   if (i > a.d) return;
   const int C = 1 + a.m;
   if (i == a.d) { a.lcp[i] = 0; a.sparse[i] = 0; return; }
-  const uint32_t p = a.order[i];
+  // an order from a misleading hash may hold entries that are not path ids: they raise
+  // the flag and read as path 0 here and in the kernels after this one
+  uint32_t p = a.order[i];
+  if (p >= (uint64_t)a.d) {
+    atomicOr(&a.u_out[1], 1ull);
+    p = 0;
+    a.order[i] = 0;
+  }
   uint32_t l = 0;
   if (i > 0) {
-    const int r = path_cmp_exact(a, a.order[i - 1], p, 0, &l);
+    uint32_t q = a.order[i - 1];
+    if (q >= (uint64_t)a.d) q = 0;
+    const int r = path_cmp_exact(a, q, p, 0, &l);
     if (r >= 0) atomicOr(&a.u_out[1], 1ull);  // not strictly increasing
   }
   a.lcp[i] = l;
@@ -360,7 +369,10 @@ __device__ inline int64_t prev_smaller(const CanonArgs &a, int64_t n, int64_t s,
 
 __device__ inline uint64_t node_base(const CanonArgs &a, int64_t i) { return 1 + a.scan_out[i * (1 + a.m)]; }
 
-// chain parent of each path and the node -> path map
+// chain parent of each path and the node -> path map.  The order is checked only after
+// these kernels: if it is not a permutation (a misleading hash can repeat a path), the
+// node count can exceed u_max, so nodes past it are not written and the order-violation
+// flag is raised (the host then sorts again by exact comparisons).
 __global__ void chain_kernel(CanonArgs a) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= a.d) return;
@@ -374,6 +386,10 @@ __global__ void chain_kernel(CanonArgs a) {
   a.chain_parent[i] = par;
   const uint64_t b = node_base(a, i);
   const uint32_t cnt = a.plen[a.order[i]] - L;
+  if (b + cnt > (uint64_t)a.u_max) {
+    atomicOr(&a.u_out[1], 1ull);
+    return;
+  }
   for (uint32_t k = 0; k < cnt; ++k) a.node_path[b + k] = (uint32_t)i;
 }
 
@@ -385,8 +401,13 @@ __global__ __launch_bounds__(256) void emit_kernel(CanonArgs a) {
   const int lane = threadIdx.x & 63, w0 = threadIdx.x - lane;
   uint64_t *sx = emit_stage + (int64_t)w0 * m, *si = emit_stage + (int64_t)(256 + w0) * m;
   const int64_t n = a.d + 1;
-  const int64_t U = (int64_t)(1 + a.scan_out[a.d * C]);
-  if (blockIdx.x == 0 && threadIdx.x == 0) a.u_out[0] = (unsigned long long)U;
+  // (bounded by u_max, as in chain_kernel: past it the order is not a permutation)
+  const int64_t U_all = (int64_t)(1 + a.scan_out[a.d * C]);
+  const int64_t U = U_all < a.u_max ? U_all : a.u_max;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    a.u_out[0] = (unsigned long long)U;
+    if (U_all > a.u_max) atomicOr(&a.u_out[1], 1ull);
+  }
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t base = (int64_t)blockIdx.x * blockDim.x + w0; base < U; base += stride) {
     const int64_t u = base + lane;
@@ -401,7 +422,11 @@ __global__ __launch_bounds__(256) void emit_kernel(CanonArgs a) {
         si[j] = a.scan_out[a.d * C + 1 + j];
       }
     } else if (u < U) {
-      const int64_t i = a.node_path[u];
+      int64_t i = a.node_path[u];
+      if (i >= a.d) {  // a node chain_kernel did not write (the order is not a permutation)
+        atomicOr(&a.u_out[1], 1ull);
+        i = 0;
+      }
       const uint32_t pid = a.order[i];
       const uint32_t L = a.lcp[i], len = a.plen[pid];
       const uint64_t b = node_base(a, i);

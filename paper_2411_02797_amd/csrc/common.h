@@ -157,6 +157,7 @@ struct PublishArgs {
   int64_t store_used;        // frames already used in the store
   const uint64_t *starts;    // [n_new] exclusive prefix sums of the padded lengths
   const int64_t *src_len;    // [n_new][2] first frame in the batch and length of each new path
+  uint64_t cp_mask;          // all ones, except under a test setting that forces collisions
 };
 void launch_new_lengths(const int64_t *off, const Slot *slot, const uint32_t *new_slots, int64_t n, int64_t *src_len,
                         uint64_t *out, hipStream_t s);
@@ -164,9 +165,12 @@ void launch_publish(const PublishArgs &a, hipStream_t s);
 // Exclusive prefix sums of `rows` rows of C uint64 columns (mod 2^64) into out[0..rows),
 // totals into out row `rows`; blk holds (rows / 1024 + 1) * C scratch words.
 void launch_scan(const uint64_t *in, int64_t rows, int C, uint64_t *blk, uint64_t *out, hipStream_t s);
-// psums[d] for d < D after a batch: old paths (d < d_old) add their slot's delta, new ones take it
+// sums[d] for d < D after a batch: old paths (d < d_old) add their slot's delta to
+// old_sums[d], new ones take it (sums and old_sums are distinct arrays)
 void launch_fold_sums(int64_t D, int64_t d_old, int32_t m, const uint32_t *pslot, const uint64_t *delta,
-                      uint64_t *psums, hipStream_t s);
+                      const uint64_t *old_sums, uint64_t *sums, hipStream_t s);
+// slot[list[i]] = empty for i < n (the slots published by a call that failed afterwards)
+void launch_reset_slots(Slot *slot, const uint32_t *list, int64_t n, hipStream_t s);
 void launch_unclaim(Slot *slot, uint64_t cap, hipStream_t s);
 void launch_rehash(const uint32_t *pframes, const int64_t *pstart, const uint32_t *plen, int64_t d,
                    Slot *slot, uint64_t cap_mask, uint64_t hash_mask, uint32_t *pslot, hipStream_t s);
@@ -281,6 +285,8 @@ struct QueryArgs {
 void launch_sorted_paths(const QueryArgs &a, hipStream_t s);
 // the prefix index of every node (qtab cleared to zero first)
 void launch_query_index(const QueryArgs &a, hipStream_t s);
+// offsets check of the query batch (err bit 0), run before any output is written
+void launch_query_check(const QueryArgs &a, hipStream_t s);
 // lookups: through the index when a.qtab is set, else by binary search
 void launch_query(const QueryArgs &a, hipStream_t s);
 

@@ -3,9 +3,9 @@
 // unique-path table (one table slot per distinct path), then a second, light pass
 // sums every event's metrics into its slot.
 //
-// This is the "insert call paths, collapse frames that refer to the same location"
-// and "aggregate metrics within the same context" step of the profiler (Design,
-// "Profiler", "Calling Context Tree"; Overview), done once per distinct full path
+// This is the profiler's step that puts call paths into the tree, merging frames that
+// name one location, and sums the metrics of equal contexts (Design, "Profiler",
+// "Calling Context Tree"; Overview), done once per distinct full path
 // instead of once per event and per frame: two events land on the same slot iff
 // their paths are equal frame by frame, which is exactly when the paper's tree
 // insertion would end them on the same node.
@@ -838,7 +838,7 @@ __global__ __launch_bounds__(256) void publish_kernel(PublishArgs a) {
         if (q <= g) pre += bs[q];
       const int64_t b = k0 / kStoreAlign + g;  // this lane group's block
       if ((lane & 15) == 15 && (b + 1) * kStoreAlign <= full)
-        a.pcp[start / kStoreAlign + b] = finish_hash(pre, (uint64_t)(b + 1) * kStoreAlign);
+        a.pcp[start / kStoreAlign + b] = finish_hash(pre, (uint64_t)(b + 1) * kStoreAlign) & a.cp_mask;
       carry += bs[0] + bs[1] + bs[2] + bs[3];
     }
   }
@@ -866,15 +866,25 @@ __global__ void new_lengths_kernel(const int64_t *off, const Slot *slot, const u
   out[i] = (uint64_t)round_store(len);
 }
 
-// Every path's sums after the batch: paths from earlier calls add their slot's batch sums,
-// new paths (d >= d_old) take them.
+// Every path's sums after the batch, into a fresh array (the tree's own sums stay as
+// they were until the call commits): paths from earlier calls add their slot's batch
+// sums to their old sums, new paths (d >= d_old) take them.
 __global__ void fold_sums_kernel(int64_t D, int64_t d_old, int32_t m, const uint32_t *pslot, const uint64_t *delta,
-                                 uint64_t *psums) {
+                                 const uint64_t *old_sums, uint64_t *sums) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= D * m) return;
   const int64_t d = t / m, j = t - d * m;
   const uint64_t x = delta[(uint64_t)pslot[d] * m + j];
-  psums[t] = d < d_old ? psums[t] + x : x;
+  sums[t] = d < d_old ? old_sums[t] + x : x;
+}
+
+// Empty the slots published in a call that then failed (they name path ids that the
+// tree does not commit).
+__global__ void reset_slots_kernel(Slot *slot, const uint32_t *list, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  slot[list[i]].word = kEmptySlot;
+  slot[list[i]].info = kEmptyInfo;
 }
 
 // Roll back every slot claimed in the current call (after an error or overflow).
@@ -975,10 +985,14 @@ void launch_publish(const PublishArgs &a, hipStream_t s) {
   hipLaunchKernelGGL(publish_kernel, dim3(blocks_for(a.n_new * 64, 256)), dim3(256), 0, s, a);
 }
 void launch_fold_sums(int64_t D, int64_t d_old, int32_t m, const uint32_t *pslot, const uint64_t *delta,
-                      uint64_t *psums, hipStream_t s) {
+                      const uint64_t *old_sums, uint64_t *sums, hipStream_t s) {
   if (D <= 0) return;
   hipLaunchKernelGGL(fold_sums_kernel, dim3(blocks_for(D * m, 256)), dim3(256), 0, s, D, d_old, m, pslot, delta,
-                     psums);
+                     old_sums, sums);
+}
+void launch_reset_slots(Slot *slot, const uint32_t *list, int64_t n, hipStream_t s) {
+  if (n <= 0) return;
+  hipLaunchKernelGGL(reset_slots_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, slot, list, n);
 }
 void launch_unclaim(Slot *slot, uint64_t cap, hipStream_t s) {
   hipLaunchKernelGGL(unclaim_kernel, dim3(blocks_for((int64_t)cap, 256)), dim3(256), 0, s, slot, cap);

@@ -1,6 +1,6 @@
-// Batched lookup of call paths in a canonical tree: the "query the metric data
-// associated with the tree nodes in the matched call paths" step of the analysis API
-// (Design, "Performance Analyzer", "Analysis API").
+// Batched lookup of call paths in a canonical tree: the analysis API's step that reads
+// the metrics of the tree nodes on the call paths a search matched (Design,
+// "Performance Analyzer", "Analysis API").
 //
 // A query path q is a node iff it is a prefix of some distinct full path.  With the
 // full paths sorted, the first path p_i >= q is the only candidate that can start
@@ -186,6 +186,16 @@ __device__ int64_t search_lookup(const QueryArgs &a, const uint32_t *qf, int64_t
   return id;
 }
 
+// The query batch's offsets, checked before any output is written: err bit 0 when they
+// do not start at 0, decrease, leave the frames or do not end at n_frames.
+__global__ void query_check_kernel(QueryArgs a) {
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= a.q) return;
+  const int64_t qs = a.qoff[q], qe = a.qoff[q + 1];
+  if (qs < 0 || qe < qs || qe > a.qn_frames || (q == 0 && qs != 0) || (q + 1 == a.q && qe != a.qn_frames))
+    atomicOr(a.err, 1ull);
+}
+
 __global__ void query_kernel(QueryArgs a) {
   const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (q >= a.q) return;
@@ -215,6 +225,10 @@ void launch_sorted_paths(const QueryArgs &a, hipStream_t s) {
 
 void launch_query_index(const QueryArgs &a, hipStream_t s) {
   if (a.d > 0) hipLaunchKernelGGL(query_index_kernel, dim3((unsigned)((a.d * 64 + 255) / 256)), dim3(256), 0, s, a);
+}
+
+void launch_query_check(const QueryArgs &a, hipStream_t s) {
+  if (a.q > 0) hipLaunchKernelGGL(query_check_kernel, dim3((unsigned)((a.q + 255) / 256)), dim3(256), 0, s, a);
 }
 
 void launch_query(const QueryArgs &a, hipStream_t s) {

@@ -342,26 +342,38 @@ cct_status setup_stage(int32_t m, uint64_t cap, int agg_grid, Buf &count, Buf &k
   return CCT_OK;
 }
 
-// Re-insert the tree's stored paths into a fresh table of capacity `cap`.
+// Re-insert the tree's stored paths into a fresh table of capacity `cap`.  Both new
+// arrays are allocated before any work is queued, and the stream is synchronised before
+// the old table and slot list go back to the pool (work queued earlier may still read
+// them; a pool block must be idle before it can be handed out again).
 cct_status rehash(cct_tree *t, uint64_t cap, uint64_t hash_mask, hipStream_t s) {
-  Buf ns;
-  if (!ns.alloc(cap * sizeof(Slot))) return fail(CCT_ENOMEM, "device allocation failed");
-  HIP_TRY(hipMemsetAsync(ns.p, 0xFF, cap * sizeof(Slot), s));
-  Buf np;
-  if (t->d > 0) {
-    if (!np.alloc(t->dcap * 4)) return fail(CCT_ENOMEM, "device allocation failed");
+  Buf ns, np;
+  if (!ns.alloc(cap * sizeof(Slot)) || (t->d > 0 && !np.alloc(t->dcap * 4)))
+    return fail(CCT_ENOMEM, "device allocation failed");
+  hipError_t e = hipMemsetAsync(ns.p, 0xFF, cap * sizeof(Slot), s);
+  if (e == hipSuccess && t->d > 0) {
     launch_rehash(t->pframes.as<uint32_t>(), t->pstart.as<int64_t>(), t->plen.as<uint32_t>(), t->d,
                   ns.as<Slot>(), cap - 1, hash_mask, np.as<uint32_t>(), s);
-    HIP_TRY(hipGetLastError());
-    t->pslot = std::move(np);
+    e = hipGetLastError();
   }
+  const hipError_t es = hipStreamSynchronize(s);
+  if (e == hipSuccess) e = es;
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(CCT_EDEVICE, hipGetErrorString(e));
+  }
+  if (t->d > 0) t->pslot = std::move(np);
   t->slot = std::move(ns);
   t->cap = cap;
   return CCT_OK;
 }
 
 // Aggregate one batch into `t` (fresh or existing).  Strong guarantee: on error the
-// tree's table, path store, sums and node arrays are as before.
+// tree's table, path store, sums and node arrays are as before.  Every array the call
+// changes is either new (sums and statistics are folded into fresh copies, swapped in
+// at the commit) or changed only past the part the tree uses (path store entries of new
+// paths); what the call puts into the table (claims, then the published slots) is
+// taken out again on the failure path.
 cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   const int32_t m = t->m;
   const int64_t N = p->n_events;
@@ -376,11 +388,35 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   if (!ctr.alloc(kCtrCount * 8 + 64)) return fail(CCT_ENOMEM, "device allocation failed");
   unsigned long long *dctr = ctr.as<unsigned long long>();
 
+  // Failure path: this call's claims (before they are published) or its published slots
+  // are emptied again, and both of the call's streams are synchronised before any of its
+  // buffers returns to the pool (a pool block must be idle before it is handed out).
+  Buf new_slots;
+  uint64_t n_new = 0;
+  bool claimed = false, published = false;
+  hipStream_t side = s;
+  auto undo = [&](cct_status st) -> cct_status {
+    if (published) launch_reset_slots(t->slot.as<Slot>(), new_slots.as<uint32_t>(), (int64_t)n_new, s);
+    else if (claimed) launch_unclaim(t->slot.as<Slot>(), t->cap, s);
+    (void)hipGetLastError();
+    (void)hipStreamSynchronize(s);
+    if (side != s) (void)hipStreamSynchronize(side);
+    return st;
+  };
+#define AGG_TRY(x)                                              \
+  do {                                                          \
+    hipError_t e_ = (x);                                        \
+    if (e_ != hipSuccess) {                                     \
+      (void)hipGetLastError();                                  \
+      return undo(fail(CCT_EDEVICE, hipGetErrorString(e_)));    \
+    }                                                           \
+  } while (0)
+
   if (N == 0) {
     // nothing to insert; offsets[0] must still be 0 and n_frames 0
     if (p->n_frames != 0) return fail(CCT_EINVAL, "n_frames != offsets[N]");
-    HIP_TRY(hipMemcpyAsync(hs, p->offsets, 8, hipMemcpyDeviceToHost, s));
-    HIP_TRY(hipStreamSynchronize(s));
+    AGG_TRY(hipMemcpyAsync(hs, p->offsets, 8, hipMemcpyDeviceToHost, s));
+    AGG_TRY(hipStreamSynchronize(s));
     if (hs[0] != 0) return fail(CCT_EINVAL, "offsets[0] != 0");
     if (t->parent.p) return CCT_OK;
     tm.mark(1, s);
@@ -393,8 +429,8 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     cct_status st = rehash(t, pow2_at_least((uint64_t)t->d * 4), hash_mask, s);
     if (st) return st;
   }
-  Buf delta, new_slots, slot_of, cpart, agg_count, agg_keys, agg_sums;
-  uint64_t n_new = 0, new_frames = 0, new_store = 0;
+  Buf delta, slot_of, cpart, agg_count, agg_keys, agg_sums;
+  uint64_t new_frames = 0, new_store = 0;
   if (N > 0) {
     if (!slot_of.alloc((size_t)N * 4)) return fail(CCT_ENOMEM, "device allocation failed");
     for (int attempt = 0;; ++attempt) {
@@ -402,8 +438,8 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
       if (!delta.alloc(t->cap * m * 8) || !new_slots.alloc(t->cap * 4) ||
           !cpart.alloc((size_t)collect_blocks(t->cap) * 16))
         return fail(CCT_ENOMEM, "device allocation failed");
-      HIP_TRY(hipMemsetAsync(delta.p, 0, t->cap * m * 8, s));
-      HIP_TRY(hipMemsetAsync(dctr, 0, kCtrCount * 8, s));
+      AGG_TRY(hipMemsetAsync(delta.p, 0, t->cap * m * 8, s));
+      AGG_TRY(hipMemsetAsync(dctr, 0, kCtrCount * 8, s));
       IngestArgs a{};
       a.off = p->offsets; a.fr = p->frames;
       a.n_events = N; a.n_frames = p->n_frames;
@@ -419,21 +455,21 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
       tm.mark(2, s);
       launch_collect_new(t->slot.as<Slot>(), t->cap, p->offsets, new_slots.as<uint32_t>(), dctr,
                          cpart.as<unsigned long long>(), s);
-      HIP_TRY(hipGetLastError());
-      HIP_TRY(hipMemcpyAsync(hs, dctr, kCtrCount * 8, hipMemcpyDeviceToHost, s));
-      HIP_TRY(hipStreamSynchronize(s));
-      if (hs[kCtrError] || hs[kCtrOverflow]) {
-        launch_unclaim(t->slot.as<Slot>(), t->cap, s);
-        HIP_TRY(hipGetLastError());
-        if (hs[kCtrError]) {
-          HIP_TRY(hipStreamSynchronize(s));
-          return fail(CCT_EINVAL, "malformed offsets");
-        }
+      claimed = true;  // (from the launch on: the table may hold this call's claims)
+      AGG_TRY(hipGetLastError());
+      AGG_TRY(hipMemcpyAsync(hs, dctr, kCtrCount * 8, hipMemcpyDeviceToHost, s));
+      AGG_TRY(hipStreamSynchronize(s));
+      if (hs[kCtrError]) return undo(fail(CCT_EINVAL, "malformed offsets"));
+      if (hs[kCtrOverflow]) {
+        // a larger table holding only the tree's paths; the old one, with this call's
+        // claims, is discarded once rehash has synchronised the stream
         cct_status st = rehash(t, t->cap * 4, hash_mask, s);
-        if (st) return st;
+        if (st) return undo(st);
+        claimed = false;
         continue;
       }
       n_new = hs[kCtrNew];
+      claimed = n_new > 0;
       new_frames = hs[kCtrNewLen];
       new_store = hs[kCtrNewFrames];
       break;
@@ -446,31 +482,21 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   // CU (run one after the other) halve the distinct slots each map must hold, so fewer
   // events overflow into device atomics.
   SideGuard side_guard;
-  hipStream_t side = s;
   if (N > 0) {
     hipStream_t ss = side_guard.acquire();
     if (ss) side = ss;
     const int agg_grid = (int)std::max<int64_t>(1, std::min<int64_t>((N + 8191) / 8192, (int64_t)cu_count() * 2));
     AggStage stg{};
     cct_status sst = setup_stage(m, t->cap, agg_grid, agg_count, agg_keys, agg_sums, stg, side);
-    if (sst) {
-      if (n_new) launch_unclaim(t->slot.as<Slot>(), t->cap, s);
-      (void)hipStreamSynchronize(s);
-      return sst;
-    }
+    if (sst) return undo(sst);
     launch_aggregate(slot_of.as<uint32_t>(), p->metrics, N, m, delta.as<uint64_t>(), t->cap, agg_grid, stg, side);
-    HIP_TRY(hipGetLastError());
+    AGG_TRY(hipGetLastError());
   }
 
   // ---- allocate everything the rest of the call needs (rollback possible until here)
   const int64_t D = t->d + (int64_t)n_new;
   const int64_t sum_len = t->sum_len + (int64_t)new_frames;
-  auto rollback = [&](cct_status st) {
-    if (n_new) launch_unclaim(t->slot.as<Slot>(), t->cap, s);
-    (void)hipStreamSynchronize(s);
-    return st;
-  };
-  if (sum_len + 1 > (int64_t)0xFFFFFFFE) return rollback(fail(CCT_EOVERFLOW, "tree would exceed 2^32-2 nodes"));
+  if (sum_len + 1 > (int64_t)0xFFFFFFFE) return undo(fail(CCT_EOVERFLOW, "tree would exceed 2^32-2 nodes"));
   // this batch's statistics, staged in path-range buckets when there are few enough of them
   // (a test setting forces device atomics instead); allocated before anything of the tree
   // changes
@@ -480,7 +506,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   const bool keep_stats = t->stats && N > 0;
   const int st_grid = (int)std::max<int64_t>(1, std::min<int64_t>((N + 8191) / 8192, (int64_t)cu_count() * 2));
   if (keep_stats) {
-    if (!sg_pos.alloc(t->cap * 4)) return rollback(fail(CCT_ENOMEM, "device allocation failed"));
+    if (!sg_pos.alloc(t->cap * 4)) return undo(fail(CCT_ENOMEM, "device allocation failed"));
     // buckets of 2^bshift paths: about 256 of them, each within the reduction's LDS
     const int64_t D_all = t->d + (int64_t)n_new;
     int bshift = 6;
@@ -493,7 +519,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
           !sg_map_rec.alloc(nmap * R * 8) || !sg_hist.alloc(2 * rows * 8) || !sg_off.alloc(2 * (rows + 1) * 8) ||
           !sg_blk.alloc((rows / 1024 + 2) * 8) || !sg_wg.alloc(st_grid * 8) || !sg_st_path.alloc(N * 4) ||
           !sg_st_w.alloc(N * m * 8) || !sg_st_key.alloc(nmap * 4) || !sg_st_rec.alloc(nmap * R * 8))
-        return rollback(fail(CCT_ENOMEM, "device allocation failed"));
+        return undo(fail(CCT_ENOMEM, "device allocation failed"));
       sst.bshift = bshift; sst.nbuckets = nbk; sst.grid = st_grid; sst.map_entries = me;
       sst.ev_path = sg_ev_path.as<uint32_t>(); sst.ev_w = sg_ev_w.as<uint64_t>();
       sst.map_key = sg_map_key.as<uint32_t>(); sst.map_rec = sg_map_rec.as<uint64_t>();
@@ -512,11 +538,11 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     if (store_need > t->store_cap || !t->pframes.p) {
       const int64_t ncap = std::max<int64_t>(store_need + store_need / 2, 1024);
       Buf f2, c2;
-      if (!f2.alloc(ncap * 4) || !c2.alloc((ncap / kStoreAlign + 1) * 8)) return rollback(fail(CCT_ENOMEM, "device allocation failed"));
+      if (!f2.alloc(ncap * 4) || !c2.alloc((ncap / kStoreAlign + 1) * 8)) return undo(fail(CCT_ENOMEM, "device allocation failed"));
       if (t->store_used) {
         if (hipMemcpyAsync(f2.p, t->pframes.p, t->store_used * 4, hipMemcpyDeviceToDevice, s) != hipSuccess ||
             hipMemcpyAsync(c2.p, t->pcp.p, (t->store_used / kStoreAlign) * 8, hipMemcpyDeviceToDevice, s) != hipSuccess)
-          return rollback(fail(CCT_EDEVICE, "copy failed"));
+          return undo(fail(CCT_EDEVICE, "copy failed"));
       }
       old_arrays_holder.pframes = std::move(t->pframes);
       old_arrays_holder.pcp = std::move(t->pcp);
@@ -526,37 +552,35 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     }
     if (dneed > t->dcap || !t->pstart.p) {
       const int64_t ncap = std::max<int64_t>(dneed + dneed / 2, 256);
-      Buf a1, a2, a3, a4, s1, s2, s3;
-      if (!a1.alloc(ncap * 8) || !a2.alloc(ncap * 4) || !a3.alloc(ncap * 4) || !a4.alloc(ncap * m * 8))
-        return rollback(fail(CCT_ENOMEM, "device allocation failed"));
-      if (t->stats && (!s1.alloc(ncap * 8) || !s2.alloc(ncap * m * 8) || !s3.alloc(ncap * m * 16)))
-        return rollback(fail(CCT_ENOMEM, "device allocation failed"));
+      Buf a1, a2, a3;
+      if (!a1.alloc(ncap * 8) || !a2.alloc(ncap * 4) || !a3.alloc(ncap * 4))
+        return undo(fail(CCT_ENOMEM, "device allocation failed"));
       if (t->d) {
         if (hipMemcpyAsync(a1.p, t->pstart.p, t->d * 8, hipMemcpyDeviceToDevice, s) != hipSuccess ||
             hipMemcpyAsync(a2.p, t->plen.p, t->d * 4, hipMemcpyDeviceToDevice, s) != hipSuccess ||
-            hipMemcpyAsync(a3.p, t->pslot.p, t->d * 4, hipMemcpyDeviceToDevice, s) != hipSuccess ||
-            hipMemcpyAsync(a4.p, t->psums.p, t->d * m * 8, hipMemcpyDeviceToDevice, s) != hipSuccess)
-          return rollback(fail(CCT_EDEVICE, "copy failed"));
-        if (t->stats &&
-            (hipMemcpyAsync(s1.p, t->pcnt.p, t->d * 8, hipMemcpyDeviceToDevice, s) != hipSuccess ||
-             hipMemcpyAsync(s2.p, t->pmin.p, t->d * m * 8, hipMemcpyDeviceToDevice, s) != hipSuccess ||
-             hipMemcpyAsync(s3.p, t->psq.p, t->d * m * 16, hipMemcpyDeviceToDevice, s) != hipSuccess))
-          return rollback(fail(CCT_EDEVICE, "copy failed"));
-      }
-      if (t->stats) {
-        old_arrays_holder.pcnt = std::move(t->pcnt);
-        old_arrays_holder.pmin = std::move(t->pmin);
-        old_arrays_holder.psq = std::move(t->psq);
-        t->pcnt = std::move(s1); t->pmin = std::move(s2); t->psq = std::move(s3);
+            hipMemcpyAsync(a3.p, t->pslot.p, t->d * 4, hipMemcpyDeviceToDevice, s) != hipSuccess)
+          return undo(fail(CCT_EDEVICE, "copy failed"));
       }
       old_arrays_holder.pstart = std::move(t->pstart);
       old_arrays_holder.plen = std::move(t->plen);
       old_arrays_holder.pslot = std::move(t->pslot);
-      old_arrays_holder.psums = std::move(t->psums);
-      t->pstart = std::move(a1); t->plen = std::move(a2); t->pslot = std::move(a3); t->psums = std::move(a4);
+      t->pstart = std::move(a1); t->plen = std::move(a2); t->pslot = std::move(a3);
       t->dcap = ncap;
     }
     (void)st;
+  }
+  // the paths' sums (and statistics) after this batch, in fresh arrays: the tree's own
+  // stay as they are until the commit
+  Buf nsums, ncnt, nmin, nsq;
+  if (!nsums.alloc(t->dcap * m * 8)) return undo(fail(CCT_ENOMEM, "device allocation failed"));
+  if (t->stats) {
+    if (!ncnt.alloc(t->dcap * 8) || !nmin.alloc(t->dcap * m * 8) || !nsq.alloc(t->dcap * m * 16))
+      return undo(fail(CCT_ENOMEM, "device allocation failed"));
+    if (t->d &&
+        (hipMemcpyAsync(ncnt.p, t->pcnt.p, t->d * 8, hipMemcpyDeviceToDevice, s) != hipSuccess ||
+         hipMemcpyAsync(nmin.p, t->pmin.p, t->d * m * 8, hipMemcpyDeviceToDevice, s) != hipSuccess ||
+         hipMemcpyAsync(nsq.p, t->psq.p, t->d * m * 16, hipMemcpyDeviceToDevice, s) != hipSuccess))
+      return undo(fail(CCT_EDEVICE, "copy failed"));
   }
   const int C = 1 + m;
   const int64_t n1 = D + 1;
@@ -571,7 +595,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
       !n_frame.alloc(u_max * 4) || !n_depth.alloc(u_max * 4) || !n_excl.alloc(u_max * m * 8) ||
       !n_incl.alloc(u_max * m * 8) || !nlen.alloc((n_new + 1) * 8) || !nstart.alloc((n_new + 1) * 8) ||
       !nblkbuf.alloc(((int64_t)n_new / 1024 + 2) * 8) || !nsrc.alloc(((int64_t)n_new + 1) * 16))
-    return rollback(fail(CCT_ENOMEM, "device allocation failed"));
+    return undo(fail(CCT_ENOMEM, "device allocation failed"));
 
   // sorting scratch, allocated before the tree is touched
   const bool exact_sort = env_int("CCT_TEST_EXACT_SORT", 0) != 0;
@@ -585,7 +609,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   const bool use_trie = !incremental && !exact_sort && !env_int("CCT_TEST_MERGE_SORT", 0) && D > 0;
   Buf merge_scratch;
   if (incremental && !merge_scratch.alloc(std::max<int64_t>(2 * (int64_t)n_new, 1) * 4))
-    return rollback(fail(CCT_ENOMEM, "device allocation failed"));
+    return undo(fail(CCT_ENOMEM, "device allocation failed"));
   Buf tr_key, tr_info, tr_pblk, tr_occ, tr_par, tr_cnt, tr_end, tr_hist, tr_gstart, tr_cidx, tr_rb, tr_lg, tr_spl, tr_bc, tr_grp, tr_grp2, tr_pos,
       tr_c, tr_cs, tr_blk, tr_lists, tr_ctr;
   TrieArgs ta{};
@@ -603,7 +627,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
         !tr_grp.alloc(nbk * 4) || !tr_grp2.alloc(nbk * 4) || !tr_pos.alloc(tcap * 4) || !tr_c.alloc(nbk * 8) ||
         !tr_cs.alloc((nbk + 1) * 8) || !tr_blk.alloc((scan_rows / 1024 + 2) * 8) || !tr_lists.alloc(3 * list_cap * 8) ||
         !tr_ctr.alloc(64))
-      return rollback(fail(CCT_ENOMEM, "device allocation failed"));
+      return undo(fail(CCT_ENOMEM, "device allocation failed"));
     ta.d = D; ta.nblocks = nblocks; ta.cap = tcap;
     ta.pframes = t->pframes.as<uint32_t>(); ta.pcp = t->pcp.as<uint64_t>(); ta.pstart = t->pstart.as<int64_t>();
     ta.plen = t->plen.as<uint32_t>();
@@ -621,13 +645,17 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   g_stats_ms = 0;
 
   // ---- publish new paths, fold this call's sums into the old ones -----------------------
-  HIP_TRY(hipMemsetAsync(cursor.p, 0, 64, s));
+  // events that order the side stream's fold after the publish, and the emission after
+  // the fold: created before anything is published
+  Event published_ev, folded;
+  if (N > 0 && side != s && (!published_ev.ev || !folded.ev)) return undo(fail(CCT_EDEVICE, "event creation failed"));
+  AGG_TRY(hipMemsetAsync(cursor.p, 0, 64, s));
   if (n_new) {
     // place the new paths in the store: exclusive scan of their padded lengths
     launch_new_lengths(p->offsets, t->slot.as<Slot>(), new_slots.as<uint32_t>(), (int64_t)n_new,
                        nsrc.as<int64_t>(), nlen.as<uint64_t>(), s);
     launch_scan(nlen.as<uint64_t>(), (int64_t)n_new, 1, nblkbuf.as<uint64_t>(), nstart.as<uint64_t>(), s);
-    HIP_TRY(hipMemcpyAsync(cursor.p, nstart.as<uint64_t>() + n_new, 8, hipMemcpyDeviceToDevice, s));
+    AGG_TRY(hipMemcpyAsync(cursor.p, nstart.as<uint64_t>() + n_new, 8, hipMemcpyDeviceToDevice, s));
     PublishArgs pa{};
     pa.off = p->offsets; pa.fr = p->frames; pa.slot = t->slot.as<Slot>();
     pa.new_slots = new_slots.as<uint32_t>(); pa.n_new = (int64_t)n_new; pa.d_old = t->d;
@@ -635,36 +663,43 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     pa.pstart = t->pstart.as<int64_t>(); pa.plen = t->plen.as<uint32_t>(); pa.pslot = t->pslot.as<uint32_t>();
     pa.store_used = t->store_used; pa.starts = nstart.as<uint64_t>();
     pa.src_len = nsrc.as<int64_t>();
+    // a test setting keeps fewer bits of the checkpoint hashes, so that the fast orders
+    // meet colliding prefixes and the exact comparison sort has to take over
+    const int cp_bits = (int)env_int("CCT_TEST_CP_HASH_BITS", 64);
+    pa.cp_mask = cp_bits >= 64 ? ~0ull : ((1ull << (cp_bits < 1 ? 1 : cp_bits)) - 1);
+    published = true;  // from here on, a failure empties the published slots
     launch_publish(pa, s);
   }
   // every path's sums, once both the side stream's aggregation and the publish (which
   // records the new paths' slots) are done; the emission waits for them
-  Event published, folded;
   if (N > 0) {
     if (side != s) {
-      if (!published.ev || !folded.ev) return fail(CCT_EDEVICE, "event creation failed");
-      HIP_TRY(hipEventRecord(published.ev, s));
-      HIP_TRY(hipStreamWaitEvent(side, published.ev, 0));
+      AGG_TRY(hipEventRecord(published_ev.ev, s));
+      AGG_TRY(hipStreamWaitEvent(side, published_ev.ev, 0));
     }
-    launch_fold_sums(D, t->d, m, t->pslot.as<uint32_t>(), delta.as<uint64_t>(), t->psums.as<uint64_t>(), side);
-    if (side != s) HIP_TRY(hipEventRecord(folded.ev, side));
+    launch_fold_sums(D, t->d, m, t->pslot.as<uint32_t>(), delta.as<uint64_t>(), t->psums.as<uint64_t>(),
+                     nsums.as<uint64_t>(), side);
+    if (side != s) AGG_TRY(hipEventRecord(folded.ev, side));
   }
-  if (keep_stats) {  // the batch's samples into the path arrays (new paths start empty)
+  if (keep_stats) {  // the batch's samples into the fresh path arrays (new paths start empty)
     ts.mark(0, s);
-    PathStats ps{t->pcnt.as<uint64_t>(), t->pmin.as<uint64_t>(), t->psq.as<uint64_t>()};
+    PathStats ps{ncnt.as<uint64_t>(), nmin.as<uint64_t>(), nsq.as<uint64_t>()};
     launch_stats_prepare(D, t->d, m, t->pslot.as<uint32_t>(), sg_pos.as<uint32_t>(), ps, s);
     launch_stats_agg(slot_of.as<uint32_t>(), sg_pos.as<uint32_t>(), p->metrics, N, m, D, st_grid, ps, sst,
                      sg_blk.as<uint64_t>(), s);
     ts.mark(1, s);
   }
-  HIP_TRY(hipGetLastError());
+  AGG_TRY(hipGetLastError());
   tm.mark(3, s);
+  // test setting: fail once everything is published and folded, to check that the
+  // tree is left as it was
+  if (env_int("CCT_TEST_FAIL_AFTER_PUBLISH", 0)) return undo(fail(CCT_EDEVICE, "test failure after publish"));
 
   // ---- A5-A9: canonical order and node arrays ------------------------------------------
   CanonArgs ca{};
   ca.d = D; ca.m = m; ca.exact = exact_sort ? 1 : 0;
   ca.pframes = t->pframes.as<uint32_t>(); ca.pcp = t->pcp.as<uint64_t>(); ca.pstart = t->pstart.as<int64_t>();
-  ca.plen = t->plen.as<uint32_t>(); ca.psums = t->psums.as<uint64_t>();
+  ca.plen = t->plen.as<uint32_t>(); ca.psums = nsums.as<uint64_t>();
   ca.order = order.as<uint32_t>(); ca.order_tmp = order_tmp.as<uint32_t>(); ca.lcp = lcp.as<uint32_t>();
   ca.scan_in = scan_in.as<uint64_t>(); ca.scan_out = scan_out.as<uint64_t>(); ca.scan_blk = scan_blk.as<uint64_t>();
   ca.scan_blocks = nblk; ca.sparse = sparse.as<uint32_t>(); ca.levels = levels;
@@ -683,22 +718,22 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     else if (mode == 3) launch_merge_order(run, t->order.as<uint32_t>(), t->d, merge_scratch.as<uint32_t>(), s);
     else launch_sort(run, s);
     tm.mark(4, s);
-    if (N > 0 && side != s) HIP_TRY(hipStreamWaitEvent(s, folded.ev, 0));  // the emission reads psums
+    if (N > 0 && side != s) AGG_TRY(hipStreamWaitEvent(s, folded.ev, 0));  // the emission reads the sums
     launch_canon(run, s);
-    HIP_TRY(hipGetLastError());
+    AGG_TRY(hipGetLastError());
     tm.mark(5, s);
-    HIP_TRY(hipMemcpyAsync(hs, cursor.p, 64, hipMemcpyDeviceToHost, s));
-    if (mode == 0) HIP_TRY(hipMemcpyAsync(hs + 8, ta.ctr, 64, hipMemcpyDeviceToHost, s));
-    HIP_TRY(hipStreamSynchronize(s));
+    AGG_TRY(hipMemcpyAsync(hs, cursor.p, 64, hipMemcpyDeviceToHost, s));
+    if (mode == 0) AGG_TRY(hipMemcpyAsync(hs + 8, ta.ctr, 64, hipMemcpyDeviceToHost, s));
+    AGG_TRY(hipStreamSynchronize(s));
     const bool trie_failed = mode == 0 && hs[8 + 3] != 0;
     if (!hs[3] && !trie_failed) {  // order verified strictly increasing
       if (run.order != ca.order) std::swap(order, order_tmp);
       break;
     }
-    if (mode == 2) return fail(CCT_EDEVICE, "canonical order failed exact verification");
-    if (mode == 0 && env_int("CCT_TEST_REQUIRE_TRIE", 0)) return fail(CCT_EDEVICE, "block-trie order not usable");
+    if (mode == 2) return undo(fail(CCT_EDEVICE, "canonical order failed exact verification"));
+    if (mode == 0 && env_int("CCT_TEST_REQUIRE_TRIE", 0)) return undo(fail(CCT_EDEVICE, "block-trie order not usable"));
     mode = 2;  // a hash collision misled the fast order: sort again with exact compares
-    HIP_TRY(hipMemsetAsync(cursor.as<unsigned long long>() + 2, 0, 16, s));
+    AGG_TRY(hipMemsetAsync(cursor.as<unsigned long long>() + 2, 0, 16, s));
   }
   tm.collect(N > 0);
   if (keep_stats && ts.ok) g_stats_ms = ts.span(0, 1);
@@ -714,7 +749,10 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   t->q_ready = false;  // and so is the query index
   t->excl = std::move(n_excl); t->incl = std::move(n_incl);
   t->order = std::move(order); t->lcp = std::move(lcp); t->scan_out = std::move(scan_out);
+  t->psums = std::move(nsums);
+  if (t->stats) { t->pcnt = std::move(ncnt); t->pmin = std::move(nmin); t->psq = std::move(nsq); }
   return CCT_OK;
+#undef AGG_TRY
 }
 
 }  // namespace
@@ -1102,6 +1140,9 @@ cct_status cct_query(const cct_tree *tree, const cct_paths *q, void *hip_stream,
     return fail(CCT_EINVAL, "bad query batch");
   if (q->n_events > CCT_MAX_EVENTS) return fail(CCT_EOVERFLOW, "too many queries in one call");
   if (q->n_events > 0 && !node_ids) return fail(CCT_EINVAL, "node_ids is NULL");
+  if (((uintptr_t)q->offsets & 7) || ((uintptr_t)q->frames & 3) || ((uintptr_t)node_ids & 7) ||
+      ((uintptr_t)excl & 7) || ((uintptr_t)incl & 7))
+    return fail(CCT_EINVAL, "misaligned pointer");
   if (q->n_events == 0) return CCT_OK;
   int dev = 0;
   (void)hipGetDevice(&dev);
@@ -1112,7 +1153,6 @@ cct_status cct_query(const cct_tree *tree, const cct_paths *q, void *hip_stream,
   g_alloc_countdown = 0;  // queries allocate only what the index needs; the hook is not armed
   Buf err;
   if (!err.alloc(8)) return fail(CCT_ENOMEM, "device allocation failed");
-  HIP_TRY(hipMemsetAsync(err.p, 0, 8, s));
   QueryArgs a{};
   a.q = q->n_events; a.qn_frames = q->n_frames; a.qoff = q->offsets; a.qfr = q->frames;
   a.d = tree->d; a.u = tree->u; a.m = tree->m;
@@ -1120,6 +1160,13 @@ cct_status cct_query(const cct_tree *tree, const cct_paths *q, void *hip_stream,
   a.order = tree->order.as<uint32_t>(); a.lcp = tree->lcp.as<uint32_t>(); a.scan_out = tree->scan_out.as<uint64_t>();
   a.excl = tree->excl.as<uint64_t>(); a.incl = tree->incl.as<uint64_t>();
   a.node_ids = node_ids; a.qexcl = excl; a.qincl = incl; a.err = err.as<unsigned long long>();
+  // the batch's offsets are checked before anything is written to the outputs
+  HIP_TRY(hipMemsetAsync(err.p, 0, 8, s));
+  launch_query_check(a, s);
+  HIP_TRY(hipGetLastError());
+  HIP_TRY(hipMemcpyAsync(hs, err.p, 8, hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  if (hs[0]) return fail(CCT_EINVAL, "malformed query offsets");
   // the index: every node under the hash of its prefix (a test setting keeps fewer key bits,
   // forcing collisions, on trees of at most 2^15 nodes: on larger ones a few keys would
   // make probing quadratic; another one uses the binary search); a table at most half full

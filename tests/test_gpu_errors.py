@@ -188,3 +188,69 @@ def test_allocation_failure_with_statistics(monkeypatch, k):
     for n in ("count_excl", "count_incl", "min_excl", "min_incl", "sumsq_excl", "sumsq_incl"):
         assert np.array_equal(got[n].numpy().view(np.uint64), want[n]), n
     tree.free()
+
+
+@pytest.mark.parametrize("stats", [False, True])
+def test_failure_after_publish_leaves_tree_unchanged(monkeypatch, stats):
+    # a merge that fails after its new paths are published and its sums folded (forced by
+    # a test setting) leaves the tree, its statistics and its table as they were: a merge
+    # of another batch, which reuses the failed call's path ids, and then the failed batch
+    # itself, equal the oracle
+    import paper_2411_02797_amd as cct
+    o, f, w = tracegen.random_paths(3000, 40, 10, 2, seed=71)
+    tree = cct.build(*to_dev(o, f, w), stats=stats)
+    before = tree.to_numpy()
+    stats_before = {n: v.cpu() for n, v in tree.stats().items()} if stats else None
+    oa, fa, wa = tracegen.random_paths(2000, 80, 10, 2, seed=72)   # the batch that fails
+    ob, fb, wb = tracegen.random_paths(2500, 90, 12, 2, seed=73)   # another batch
+    monkeypatch.setenv("CCT_TEST_FAIL_AFTER_PUBLISH", "1")
+    assert _status(lambda: tree.merge(*to_dev(oa, fa, wa))) == "CCT_EDEVICE"
+    monkeypatch.delenv("CCT_TEST_FAIL_AFTER_PUBLISH")
+    assert_same(tree.to_numpy(), before, "unchanged after a failure past publish")
+    if stats:
+        after = tree.stats()
+        for n, v in stats_before.items():
+            assert np.array_equal(v.numpy(), after[n].cpu().numpy(), equal_nan=True), n
+    tree.merge(*to_dev(ob, fb, wb))
+    tree.merge(*to_dev(oa, fa, wa))
+    orc = oracle.Oracle(2, stats=stats)
+    orc.ingest(o, f, w)
+    orc.ingest(ob, fb, wb)
+    orc.ingest(oa, fa, wa)
+    want = orc.tree()
+    orc.close()
+    assert_same(tree.to_numpy(), want, "merges after the failure")
+    if stats:
+        got = tree.stats(device="cpu")
+        for n in ("count_excl", "count_incl", "min_excl", "min_incl", "sumsq_excl", "sumsq_incl"):
+            assert np.array_equal(got[n].numpy().view(np.uint64), want[n]), n
+    # every node is still found by a query (the table and the path store agree)
+    ids, _, _ = tree.query(*to_dev(oa, fa, wa)[:2])
+    assert bool((ids >= 0).all())
+    tree.free()
+
+
+@pytest.mark.parametrize("kind", ["first_nonzero", "decreasing", "last_mismatch"])
+def test_malformed_query_offsets_leave_outputs_untouched(kind):
+    import ctypes
+    import paper_2411_02797_amd as cct
+    torch = torch_or_skip()
+    o, f, w = tracegen.random_paths(3000, 30, 10, 2, seed=5)
+    tree = cct.build(*to_dev(o, f, w))
+    qo, qf, _ = to_dev(o[:501], f[:o[500]], w[:500])
+    if kind == "first_nonzero":
+        qo[0] = 1
+    elif kind == "decreasing":
+        qo[250] = qo[249] - 1
+    else:
+        qo[-1] = qo[-1] - 1
+    ids = torch.full((500,), -7, dtype=torch.int64, device="cuda")
+    ex = torch.full((500, 2), -7, dtype=torch.int64, device="cuda")
+    inc = torch.full((500, 2), -7, dtype=torch.int64, device="cuda")
+    p, _ = cct._paths(qo, qf, None, need_metrics=False)
+    st = cct.load_library().cct_query(tree.handle, ctypes.byref(p), cct._stream(), ids.data_ptr(), ex.data_ptr(),
+                                      inc.data_ptr())
+    torch.cuda.synchronize()
+    assert st == -1
+    assert bool((ids == -7).all()) and bool((ex == -7).all()) and bool((inc == -7).all())
+    tree.free()

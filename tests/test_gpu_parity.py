@@ -169,6 +169,33 @@ def test_block_trie_order(monkeypatch, case):
     assert_same(gpu_tree(o, f, w), want, f"{case} comparison sort")
 
 
+@pytest.mark.parametrize("bits", [1, 4])
+@pytest.mark.parametrize("sort", ["trie", "comparison"])
+def test_forced_checkpoint_collisions(monkeypatch, bits, sort):
+    # checkpoint hashes cut to a few bits: the fast orders (block trie, comparison sort,
+    # the merge's gap search) meet colliding prefixes, their order is caught by the exact
+    # check, and the exact comparison sort takes over; a build and two merges equal the
+    # oracle
+    import paper_2411_02797_amd as cct
+    monkeypatch.setenv("CCT_TEST_CP_HASH_BITS", str(bits))
+    if sort == "comparison":
+        monkeypatch.setenv("CCT_TEST_MERGE_SORT", "1")
+    o, f, w = tracegen.random_paths(4000, 3, 70, 2, seed=90 + bits)
+    o2, f2, w2 = tracegen.random_paths(3000, 3, 90, 2, seed=95 + bits)
+    o3, f3, w3 = tracegen.generate("deep_recursion", n_events=3000)
+    w3 = np.repeat(w3, 2, axis=1)
+    tree = cct.build(*to_dev(o, f, w))
+    assert_same(tree.to_numpy(), oracle.build_tree(o, f, w), f"build bits={bits} {sort}")
+    tree.merge(*to_dev(o2, f2, w2))
+    tree.merge(*to_dev(o3, f3, w3))
+    orc = oracle.Oracle(2)
+    for t in ((o, f, w), (o2, f2, w2), (o3, f3, w3)):
+        orc.ingest(*t)
+    assert_same(tree.to_numpy(), orc.tree(), f"merges bits={bits} {sort}")
+    orc.close()
+    tree.free()
+
+
 def test_forced_table_overflow_regrows(monkeypatch):
     monkeypatch.setenv("CCT_TEST_TABLE_CAP", "16")
     o, f, w = tracegen.random_paths(5000, 500, 12, 1, seed=9)
