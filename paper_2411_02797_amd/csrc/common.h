@@ -145,6 +145,7 @@ __host__ __device__ inline int64_t round_store(int64_t len) {
 struct PublishArgs {
   const int64_t *off;        // batch offsets (frames of new paths come from the batch)
   const uint32_t *fr;
+  int64_t n_frames;          // frames in the batch
   Slot *slot;
   const uint32_t *new_slots;
   int64_t n_new;

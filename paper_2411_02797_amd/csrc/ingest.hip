@@ -785,64 +785,74 @@ __global__ __launch_bounds__(256) void collect_sum_kernel(const unsigned long lo
 // Publish the paths first seen in this call: give each a path id, copy its frames into
 // the tree's path store (16-frame aligned, zero tail up to its padded length), write its
 // checkpoint hashes, its start, length and table slot, and point the slot at the path id
-// and the stored frames (the sums are folded in later, by fold_sums_kernel).  One wave
-// per new path.  Its first frame and length come from new_lengths_kernel (one load), and
-// the frames of up to four 64-frame chunks are requested before any is used (paths of up
-// to 256 frames take one round trip; deeper prefetch measured slower).  Within a chunk
-// each group of 16 lanes holds one block, sums its frame terms with shuffles, and the
-// blocks' prefix sums are carried across chunks.
+// and the stored frames (the sums are folded in later, by fold_sums_kernel).  Sixteen
+// lanes per path, four paths per wave: a lane moves four frames of every 64-frame chunk
+// with one 16-byte load (the source, a 4-byte aligned stretch of the batch) and one
+// 16-byte store (the store is 64-byte aligned), so a wave has four paths' frames in
+// flight.  The chunks of a path up to 256 frames are requested before any is used.  Each
+// group of four lanes holds one 16-frame block: the block's frame terms meet by two
+// shuffles within the group, and the blocks' prefix sums are carried across chunks.
 constexpr int kPublishChunks = 4;  // 64-frame chunks requested ahead
 __global__ __launch_bounds__(256) void publish_kernel(PublishArgs a) {
-  const int lane = threadIdx.x & 63;
-  const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
-  if (i >= a.n_new) return;
-  const int64_t src = a.src_len[2 * i], len = a.src_len[2 * i + 1];
-  const uint32_t s = a.new_slots[i];
+  const int lane = threadIdx.x & 63, g = lane & 15;  // g: lane within the path's 16
+  const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 4;
+  const bool active = i < a.n_new;
+  const int64_t src = active ? a.src_len[2 * i] : 0, len = active ? a.src_len[2 * i + 1] : 0;
   const int64_t rl = round_store(len);
-  const int64_t start = a.store_used + (int64_t)a.starts[i];
-  const int64_t id = a.d_old + i;
+  const int64_t start = a.store_used + (active ? (int64_t)a.starts[i] : 0);
   const int64_t full = len / kStoreAlign * kStoreAlign;  // frames of the full blocks
-  const int g = lane >> 4;
+  const int64_t avail = a.n_frames - src;                // frames readable from src
   uint64_t carry = 0;
-  uint32_t fq[kPublishChunks];
-  for (int64_t k0 = 0; k0 < rl; k0 += 64) {
+  u32x4 fq[kPublishChunks];
+  for (int64_t k0 = 0; k0 < rl; k0 += 64) {  // uniform within the path's 16 lanes
     const int c = (int)((k0 >> 6) % kPublishChunks);
     if (c == 0) {
 #pragma unroll
       for (int u = 0; u < kPublishChunks; ++u) {
-        const int64_t k = k0 + 64 * u + lane;
-        fq[u] = k < len ? a.fr[src + k] : 0u;
+        const int64_t k = k0 + 64 * u + 4 * g;  // this lane's first frame of chunk u
+        u32x4 v = {0u, 0u, 0u, 0u};
+        if (k + 4 <= len && k + 4 <= avail) {
+          v = *(gptr4)((gptr)a.fr + src + k);
+        } else if (k < len) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = k + e < len ? a.fr[src + k + e] : 0u;
+        }
+        fq[u] = v;
       }
     }
-    {
-      const int64_t k = k0 + lane;
-      uint32_t f = fq[0];
+    u32x4 v = fq[0];
 #pragma unroll
-      for (int u = 1; u < kPublishChunks; ++u)
-        if (c == u) f = fq[u];
-      if (k < rl) a.pframes[start + k] = f;
-      uint64_t v = k < full ? frame_term(f, (uint32_t)k) : 0ull;
-      for (int o = 1; o < 16; o <<= 1) {  // sum over the 16 lanes of the block
-        const uint32_t lo = __shfl_xor((uint32_t)v, o, 64), hi = __shfl_xor((uint32_t)(v >> 32), o, 64);
-        v += ((uint64_t)hi << 32) | lo;
-      }
-      uint64_t bs[4];
+    for (int u = 1; u < kPublishChunks; ++u)
+      if (c == u) v = fq[u];
+    const int64_t k = k0 + 4 * g;
+    if (k < rl) *(u32x4 *)(a.pframes + start + k) = v;
+    uint64_t t = 0;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const uint32_t lo = __shfl((uint32_t)v, 16 * q, 64), hi = __shfl((uint32_t)(v >> 32), 16 * q, 64);
-        bs[q] = ((uint64_t)hi << 32) | lo;
-      }
-      uint64_t pre = carry;
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        if (q <= g) pre += bs[q];
-      const int64_t b = k0 / kStoreAlign + g;  // this lane group's block
-      if ((lane & 15) == 15 && (b + 1) * kStoreAlign <= full)
-        a.pcp[start / kStoreAlign + b] = finish_hash(pre, (uint64_t)(b + 1) * kStoreAlign) & a.cp_mask;
-      carry += bs[0] + bs[1] + bs[2] + bs[3];
+    for (int e = 0; e < 4; ++e) t += k + e < full ? frame_term(v[e], (uint32_t)(k + e)) : 0ull;
+    for (int o = 1; o < 4; o <<= 1) {  // the block's sum, on its four lanes
+      const uint32_t lo = __shfl_xor((uint32_t)t, o, 64), hi = __shfl_xor((uint32_t)(t >> 32), o, 64);
+      t += ((uint64_t)hi << 32) | lo;
     }
+    const int base = lane & ~15;  // the path's first lane
+    uint64_t bs[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t lo = __shfl((uint32_t)t, base + 4 * q, 64), hi = __shfl((uint32_t)(t >> 32), base + 4 * q, 64);
+      bs[q] = ((uint64_t)hi << 32) | lo;
+    }
+    const int blk = g >> 2;  // this lane's block within the chunk
+    uint64_t pre = carry;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (q <= blk) pre += bs[q];
+    const int64_t b = k0 / kStoreAlign + blk;  // the block within the path
+    if ((g & 3) == 3 && (b + 1) * kStoreAlign <= full)
+      a.pcp[start / kStoreAlign + b] = finish_hash(pre, (uint64_t)(b + 1) * kStoreAlign) & a.cp_mask;
+    carry += bs[0] + bs[1] + bs[2] + bs[3];
   }
-  if (lane == 0) {
+  if (active && g == 0) {
+    const uint32_t s = a.new_slots[i];
+    const int64_t id = a.d_old + i;
     const uint64_t w = a.slot[s].word;
     a.pstart[id] = start;
     a.plen[id] = (uint32_t)len;
@@ -982,7 +992,7 @@ void launch_new_lengths(const int64_t *off, const Slot *slot, const uint32_t *ne
 }
 void launch_publish(const PublishArgs &a, hipStream_t s) {
   if (a.n_new <= 0) return;
-  hipLaunchKernelGGL(publish_kernel, dim3(blocks_for(a.n_new * 64, 256)), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(publish_kernel, dim3(blocks_for(a.n_new * 16, 256)), dim3(256), 0, s, a);
 }
 void launch_fold_sums(int64_t D, int64_t d_old, int32_t m, const uint32_t *pslot, const uint64_t *delta,
                       const uint64_t *old_sums, uint64_t *sums, hipStream_t s) {

@@ -657,7 +657,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     launch_scan(nlen.as<uint64_t>(), (int64_t)n_new, 1, nblkbuf.as<uint64_t>(), nstart.as<uint64_t>(), s);
     AGG_TRY(hipMemcpyAsync(cursor.p, nstart.as<uint64_t>() + n_new, 8, hipMemcpyDeviceToDevice, s));
     PublishArgs pa{};
-    pa.off = p->offsets; pa.fr = p->frames; pa.slot = t->slot.as<Slot>();
+    pa.off = p->offsets; pa.fr = p->frames; pa.n_frames = p->n_frames; pa.slot = t->slot.as<Slot>();
     pa.new_slots = new_slots.as<uint32_t>(); pa.n_new = (int64_t)n_new; pa.d_old = t->d;
     pa.pframes = t->pframes.as<uint32_t>(); pa.pcp = t->pcp.as<uint64_t>();
     pa.pstart = t->pstart.as<int64_t>(); pa.plen = t->plen.as<uint32_t>(); pa.pslot = t->pslot.as<uint32_t>();
