@@ -102,8 +102,8 @@ def host_cpu():
 
 
 def achievable_read(torch, buf):
-    """Same-run achievable read bandwidth: the best of five plain coalesced reads of the
-    frames buffer (libcct_readbw.so), as context for the 8 TB/s denominator."""
+    """Same-run achievable read bandwidth: the best of five plain coalesced 16-byte buffer-load
+    reads of `buf` (libcct_readbw.so), as context for the 8 TB/s denominator."""
     import ctypes
     path = os.path.join(ROOT, "paper_2411_02797_amd", "libcct_readbw.so")
     if not os.path.exists(path):
@@ -154,6 +154,9 @@ def main():
     ap.add_argument("--copy-calibrate", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times (the reference kernel that "
                          "scales the HBM byte counters) and exit")
+    ap.add_argument("--read-calibrate", type=int, default=0, metavar="MIB",
+                    help="only run the plain 16-byte buffer-load read of MIB MiB five times (a second "
+                         "reference kernel for the fetched-byte counter) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "bench.py measures one GPU; sharding across GPUs is a design only, nothing here runs on several",
@@ -169,6 +172,14 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 5}))
+        return
+    if args.read_calibrate:
+        buf = torch.ones((args.read_calibrate << 20) // 4, dtype=torch.int32, device="cuda")
+        torch.cuda.synchronize()
+        r = achievable_read(torch, buf)
+        if r is None:
+            sys.exit("read calibration failed: libcct_readbw.so missing or the read kernel failed")
+        print(json.dumps({"read_bytes": r["bytes"], "launches": 5, "best_ms": r["best_ms"], "gbps": r["gbps"]}))
         return
     import tracegen
     import paper_2411_02797_amd as cct

@@ -12,25 +12,29 @@ constexpr int kThreads = 768;       // 12 waves per workgroup, one workgroup per
 constexpr int64_t kTile = 8192;     // bytes per wave and iteration: eight 1 KiB coalesced loads
 
 // Tiles of 8 KiB are dealt to the waves round-robin, so the whole grid sweeps memory in
-// order; every lane reads 16 bytes of each 1 KiB row.  The xor of the data is kept so
-// the loads stay live; one word per workgroup is written only if it matches a value
-// the data cannot produce by chance in this use.
-__global__ __launch_bounds__(kThreads) void read_kernel(const u32x4 *p, int64_t bytes, uint32_t *sink) {
+// order; every lane reads 16 bytes of each 1 KiB row with the same 16-byte raw buffer
+// load the ingest kernel streams its frames with (a wave-uniform descriptor per tile,
+// so the descriptor stays in scalar registers).  The xor of the data is kept so the
+// loads stay live; one word per workgroup is written only if it matches a value the
+// data cannot produce by chance in this use.
+__global__ __launch_bounds__(kThreads) void read_kernel(const unsigned char *p, int64_t bytes, uint32_t *sink) {
   const int lane = threadIdx.x & 63;
   const int64_t waves = (int64_t)gridDim.x * (kThreads / 64);
-  const int64_t w = (int64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+  const int64_t w = __builtin_amdgcn_readfirstlane((int)(blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6)));
   const int64_t tiles = bytes / kTile;
   uint32_t acc = 0;
   for (int64_t t = w; t < tiles; t += waves) {
-    const u32x4 *q = p + t * (kTile / 16) + lane;
+    const __amdgpu_buffer_rsrc_t r =
+        __builtin_amdgcn_make_buffer_rsrc((void *)(p + t * kTile), (short)0, (int)kTile, 0x00020000);
     u32x4 v[8];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) v[k] = q[64 * k];
+    for (int k = 0; k < 8; ++k) v[k] = __builtin_amdgcn_raw_buffer_load_b128(r, 16 * lane + 1024 * k, 0, 0);
 #pragma unroll
     for (int k = 0; k < 8; ++k) acc ^= v[k][0] ^ v[k][1] ^ v[k][2] ^ v[k][3];
   }
+  const u32x4 *q = (const u32x4 *)p;
   for (int64_t i = tiles * (kTile / 16) + w * 64 + lane; i < bytes / 16; i += waves * 64) {
-    const u32x4 v = p[i];
+    const u32x4 v = q[i];
     acc ^= v[0] ^ v[1] ^ v[2] ^ v[3];
   }
   if (acc == 0x9E3779B9u) sink[blockIdx.x] = acc;
@@ -58,7 +62,7 @@ int cctbw_read(const void *p, int64_t bytes, uint32_t *sink, void *stream, int r
   for (int r = 0; r < reps && rc == 0; ++r) {
     float ms = 0;
     if (hipEventRecord(e0, s) != hipSuccess) { rc = -1; break; }
-    hipLaunchKernelGGL(read_kernel, dim3(cus), dim3(kThreads), 0, s, (const u32x4 *)p, bytes, sink);
+    hipLaunchKernelGGL(read_kernel, dim3(cus), dim3(kThreads), 0, s, (const unsigned char *)p, bytes, sink);
     if (hipGetLastError() != hipSuccess || hipEventRecord(e1, s) != hipSuccess ||
         hipEventSynchronize(e1) != hipSuccess || hipEventElapsedTime(&ms, e0, e1) != hipSuccess) {
       rc = -1;
