@@ -125,13 +125,16 @@ int64_t agg_max_buckets();
 int64_t agg_map_entries(int32_t m);
 void launch_aggregate(const uint32_t *slot_of, const uint64_t *w, int64_t n, int32_t m, uint64_t *delta,
                       uint64_t cap, int grid, const AggStage &st, hipStream_t s);
-// List the slots claimed in this call (word ref with kEventRef): new_slots, and into
-// ctr: kCtrNew (count), kCtrNewFrames (sum of padded store lengths), kCtrNewLen (sum
-// of lengths).
+// List the slots claimed in this call (word ref with kEventRef): new_slots, each new
+// path's first frame in the batch and length (src_len, two words per path) and padded
+// store length (padded, the input of the scan that places the paths in the store), and
+// into ctr: kCtrNew (count), kCtrNewFrames (sum of padded store lengths), kCtrNewLen
+// (sum of lengths).  new_slots, src_len and padded hold room for every possible new
+// path: min(cap, events of the batch).
 // part: 2 * collect_blocks(cap) words of scratch.
 int64_t collect_blocks(uint64_t cap);
-void launch_collect_new(const Slot *slot, uint64_t cap, const int64_t *off, uint32_t *new_slots,
-                        unsigned long long *ctr, unsigned long long *part, hipStream_t s);
+void launch_collect_new(const Slot *slot, uint64_t cap, const int64_t *off, uint32_t *new_slots, int64_t *src_len,
+                        uint64_t *padded, unsigned long long *ctr, unsigned long long *part, hipStream_t s);
 
 // Path store: path d occupies frames [pstart[d], pstart[d] + round16(plen[d])) of
 // pframes (pstart is a multiple of kStoreAlign, the tail is zero-filled), and its
@@ -160,8 +163,6 @@ struct PublishArgs {
   const int64_t *src_len;    // [n_new][2] first frame in the batch and length of each new path
   uint64_t cp_mask;          // all ones, except under a test setting that forces collisions
 };
-void launch_new_lengths(const int64_t *off, const Slot *slot, const uint32_t *new_slots, int64_t n, int64_t *src_len,
-                        uint64_t *out, hipStream_t s);
 void launch_publish(const PublishArgs &a, hipStream_t s);
 // Exclusive prefix sums of `rows` rows of C uint64 columns (mod 2^64) into out[0..rows),
 // totals into out row `rows`; blk holds (rows / 1024 + 1) * C scratch words.
@@ -245,18 +246,22 @@ struct TrieArgs {
   uint64_t *cnt;               // [nblocks] path counts in grouped order
   uint64_t *cnt_scan;          // [nblocks + 1] their exclusive prefix sums
   uint64_t *scan_blk;          // scan scratch: (nblocks / 1024 + 2) words
-  uint64_t *lists;             // [3][list_cap] (start << 32 | size): buckets of up to 64, larger
-                               // buckets, groups of more than 1024 siblings
+  uint64_t *lists;             // [4][list_cap] (start << 32 | size): buckets of up to 64, groups of
+                               // 65 .. 512 siblings, groups of more than 512, buckets of 65 .. 2048
   int64_t list_cap;
   int64_t large_cap;           // groups of more than 1024 siblings that can be listed
   uint32_t *lgroup;            // [cap + 1] list index of a large group, by parent node
   uint32_t *spl;               // [large_cap][256] splitters (node ids)
   uint32_t *bcnt;              // [large_cap][256] bucket sizes
-  unsigned long long *ctr;     // [8]: [0..2] list counts, [3] failure
+  unsigned long long *ctr;     // [8]: [0..3] list counts, [kTrieCtrFail] failure
   uint32_t *order;             // [D] out: path ids in lexicographic order
 };
-// ctr[3] != 0 after the call: the trie could not be used (the caller sorts another way).
-void launch_trie_sort(const TrieArgs &a, hipStream_t s);
+constexpr int kTrieCtrFail = 4;
+// ctr[kTrieCtrFail] != 0 after the call: the trie could not be used (the caller sorts
+// another way).  s2 (may be s): a second stream for the part of the sibling ordering that
+// is independent of the large groups, forked from s with `fork` and joined back into s
+// with `join` (two events of the caller's, unused when s2 is s).
+void launch_trie_sort(const TrieArgs &a, hipStream_t s, hipStream_t s2, hipEvent_t fork, hipEvent_t join);
 void launch_canon(const CanonArgs &a, hipStream_t s);  // lcp, scans, sparse table, emission
 
 struct QueryArgs {

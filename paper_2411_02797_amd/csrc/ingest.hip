@@ -724,6 +724,7 @@ __global__ __launch_bounds__(kAggThreads) void agg_reduce_kernel(AggStage st, ui
 constexpr int kCollectThreads = 1024, kCollectPerThread = 4;
 __global__ __launch_bounds__(kCollectThreads) void collect_new_kernel(const Slot *slot, uint64_t cap,
                                                                       const int64_t *off, uint32_t *new_slots,
+                                                                      int64_t *src_len, uint64_t *padded,
                                                                       unsigned long long *ctr,
                                                                       unsigned long long *part) {
   __shared__ uint32_t cnt;
@@ -731,6 +732,7 @@ __global__ __launch_bounds__(kCollectThreads) void collect_new_kernel(const Slot
   if (threadIdx.x == 0) { cnt = 0; frames = 0; lens = 0; }
   __syncthreads();
   uint32_t found[kCollectPerThread], pos[kCollectPerThread];
+  int64_t fsrc[kCollectPerThread], flen[kCollectPerThread];
   uint64_t my_frames = 0, my_lens = 0;
   int nf = 0;
   for (int r = 0; r < kCollectPerThread; ++r) {
@@ -738,14 +740,20 @@ __global__ __launch_bounds__(kCollectThreads) void collect_new_kernel(const Slot
     if (s >= cap) break;
     const Slot sl = slot[s];
     if (sl.word != kEmptySlot && ((uint32_t)sl.word & kEventRef)) {
-      int64_t len;
+      // the claiming event's first frame and length: from info (written right after the
+      // claim, so complete once the ingest has finished), else from the offsets
+      int64_t src, len;
       if (sl.info != kEmptyInfo && (sl.info & kInfoLongLen) != kInfoLongLen) {
         len = (int64_t)(sl.info & kInfoLongLen);
+        src = (int64_t)(sl.info >> 24);
       } else {
         const int64_t e = (int64_t)((uint32_t)sl.word & kRefMask);
-        len = off[e + 1] - off[e];
+        src = off[e];
+        len = off[e + 1] - src;
       }
       found[nf] = (uint32_t)s;
+      fsrc[nf] = src;
+      flen[nf] = len;
       pos[nf] = atomicAdd(&cnt, 1u);
       ++nf;
       my_frames += (uint64_t)round_store(len);
@@ -763,7 +771,13 @@ __global__ __launch_bounds__(kCollectThreads) void collect_new_kernel(const Slot
     part[blockIdx.x * 2 + 1] = lens;
   }
   __syncthreads();
-  for (int i = 0; i < nf; ++i) new_slots[base + pos[i]] = found[i];
+  for (int i = 0; i < nf; ++i) {
+    const uint64_t j = base + pos[i];
+    new_slots[j] = found[i];
+    src_len[2 * j] = fsrc[i];
+    src_len[2 * j + 1] = flen[i];
+    padded[j] = (uint64_t)round_store(flen[i]);
+  }
 }
 
 // Totals of the per-block length sums into ctr (one block).
@@ -860,20 +874,6 @@ __global__ __launch_bounds__(256) void publish_kernel(PublishArgs a) {
     a.slot[s].word = (w & 0xFFFFFFFF00000000ull) | (uint64_t)id;
     a.slot[s].info = make_info((uint64_t)start, true, (uint64_t)len);
   }
-}
-
-// Padded store length of every new path (input of the scan that places them), and the
-// path's first frame and length in the batch (so that publish_kernel starts from one
-// load instead of the slot -> event -> offsets chain).
-__global__ void new_lengths_kernel(const int64_t *off, const Slot *slot, const uint32_t *new_slots, int64_t n,
-                                   int64_t *src_len, uint64_t *out) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  const int64_t e = (int64_t)((uint32_t)slot[new_slots[i]].word & kRefMask);
-  const int64_t src = off[e], len = off[e + 1] - src;
-  src_len[2 * i] = src;
-  src_len[2 * i + 1] = len;
-  out[i] = (uint64_t)round_store(len);
 }
 
 // Every path's sums after the batch, into a fresh array (the tree's own sums stay as
@@ -977,18 +977,12 @@ void launch_aggregate(const uint32_t *slot_of, const uint64_t *w, int64_t n, int
 }
 int64_t collect_blocks(uint64_t cap) { return (int64_t)((cap + kCollectThreads * kCollectPerThread - 1) /
                                                          (kCollectThreads * kCollectPerThread)); }
-void launch_collect_new(const Slot *slot, uint64_t cap, const int64_t *off, uint32_t *new_slots,
-                        unsigned long long *ctr, unsigned long long *part, hipStream_t s) {
+void launch_collect_new(const Slot *slot, uint64_t cap, const int64_t *off, uint32_t *new_slots, int64_t *src_len,
+                        uint64_t *padded, unsigned long long *ctr, unsigned long long *part, hipStream_t s) {
   const int64_t nb = collect_blocks(cap);
   hipLaunchKernelGGL(collect_new_kernel, dim3((unsigned)nb), dim3(kCollectThreads), 0, s, slot, cap, off, new_slots,
-                     ctr, part);
+                     src_len, padded, ctr, part);
   hipLaunchKernelGGL(collect_sum_kernel, dim3(1), dim3(256), 0, s, part, nb, ctr);
-}
-void launch_new_lengths(const int64_t *off, const Slot *slot, const uint32_t *new_slots, int64_t n, int64_t *src_len,
-                        uint64_t *out, hipStream_t s) {
-  if (n <= 0) return;
-  hipLaunchKernelGGL(new_lengths_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, off, slot, new_slots, n, src_len,
-                     out);
 }
 void launch_publish(const PublishArgs &a, hipStream_t s) {
   if (a.n_new <= 0) return;

@@ -429,14 +429,16 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     cct_status st = rehash(t, pow2_at_least((uint64_t)t->d * 4), hash_mask, s);
     if (st) return st;
   }
-  Buf delta, slot_of, cpart, agg_count, agg_keys, agg_sums;
+  Buf delta, slot_of, cpart, agg_count, agg_keys, agg_sums, nlen, nsrc;
   uint64_t new_frames = 0, new_store = 0;
   if (N > 0) {
     if (!slot_of.alloc((size_t)N * 4)) return fail(CCT_ENOMEM, "device allocation failed");
     for (int attempt = 0;; ++attempt) {
       if (attempt > 12) return fail(CCT_EOVERFLOW, "unique-path table cannot grow further");
+      const int64_t max_new = (int64_t)std::min<uint64_t>(t->cap, (uint64_t)N);  // distinct paths of the batch
       if (!delta.alloc(t->cap * m * 8) || !new_slots.alloc(t->cap * 4) ||
-          !cpart.alloc((size_t)collect_blocks(t->cap) * 16))
+          !cpart.alloc((size_t)collect_blocks(t->cap) * 16) || !nsrc.alloc((size_t)max_new * 16) ||
+          !nlen.alloc((size_t)(max_new + 1) * 8))
         return fail(CCT_ENOMEM, "device allocation failed");
       AGG_TRY(hipMemsetAsync(delta.p, 0, t->cap * m * 8, s));
       AGG_TRY(hipMemsetAsync(dctr, 0, kCtrCount * 8, s));
@@ -453,8 +455,8 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
       tm.mark(1, s);
       launch_ingest(a, grid, s);
       tm.mark(2, s);
-      launch_collect_new(t->slot.as<Slot>(), t->cap, p->offsets, new_slots.as<uint32_t>(), dctr,
-                         cpart.as<unsigned long long>(), s);
+      launch_collect_new(t->slot.as<Slot>(), t->cap, p->offsets, new_slots.as<uint32_t>(), nsrc.as<int64_t>(),
+                         nlen.as<uint64_t>(), dctr, cpart.as<unsigned long long>(), s);
       claimed = true;  // (from the launch on: the table may hold this call's claims)
       AGG_TRY(hipGetLastError());
       AGG_TRY(hipMemcpyAsync(hs, dctr, kCtrCount * 8, hipMemcpyDeviceToHost, s));
@@ -587,14 +589,14 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   const int levels = floor_log2((uint64_t)n1) + 1;
   const int64_t nblk = (D + 1023) / 1024 + 1;
   const int64_t u_max = sum_len + 1;
-  Buf order, order_tmp, lcp, scan_in, scan_out, scan_blk, sparse, chain, node_path, cursor, nlen, nstart, nblkbuf, nsrc;
+  Buf order, order_tmp, lcp, scan_in, scan_out, scan_blk, sparse, chain, node_path, cursor, nstart, nblkbuf;
   Buf n_parent, n_frame, n_depth, n_subend, n_excl, n_incl;  // canonical arrays of the new tree
   if (!order.alloc(dneed * 4) || !order_tmp.alloc(dneed * 4) || !lcp.alloc(n1 * 4) || !scan_in.alloc(dneed * C * 8) ||
       !scan_out.alloc(n1 * C * 8) || !scan_blk.alloc(nblk * C * 8) || !sparse.alloc((int64_t)levels * n1 * 4) ||
       !chain.alloc(dneed * 4) || !node_path.alloc(u_max * 4) || !cursor.alloc(64) || !n_parent.alloc(u_max * 4) || !n_subend.alloc(u_max * 4) ||
       !n_frame.alloc(u_max * 4) || !n_depth.alloc(u_max * 4) || !n_excl.alloc(u_max * m * 8) ||
-      !n_incl.alloc(u_max * m * 8) || !nlen.alloc((n_new + 1) * 8) || !nstart.alloc((n_new + 1) * 8) ||
-      !nblkbuf.alloc(((int64_t)n_new / 1024 + 2) * 8) || !nsrc.alloc(((int64_t)n_new + 1) * 16))
+      !n_incl.alloc(u_max * m * 8) || !nstart.alloc((n_new + 1) * 8) ||
+      !nblkbuf.alloc(((int64_t)n_new / 1024 + 2) * 8))
     return undo(fail(CCT_ENOMEM, "device allocation failed"));
 
   // sorting scratch, allocated before the tree is touched
@@ -625,7 +627,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
         !tr_rb.alloc(1024 * 4) || !tr_lg.alloc((tcap + 1) * 4) || !tr_spl.alloc(large_cap * 256 * 4) ||
         !tr_bc.alloc(large_cap * 256 * 4) ||
         !tr_grp.alloc(nbk * 4) || !tr_grp2.alloc(nbk * 4) || !tr_pos.alloc(tcap * 4) || !tr_c.alloc(nbk * 8) ||
-        !tr_cs.alloc((nbk + 1) * 8) || !tr_blk.alloc((scan_rows / 1024 + 2) * 8) || !tr_lists.alloc(3 * list_cap * 8) ||
+        !tr_cs.alloc((nbk + 1) * 8) || !tr_blk.alloc((scan_rows / 1024 + 2) * 8) || !tr_lists.alloc(4 * list_cap * 8) ||
         !tr_ctr.alloc(64))
       return undo(fail(CCT_ENOMEM, "device allocation failed"));
     ta.d = D; ta.nblocks = nblocks; ta.cap = tcap;
@@ -647,13 +649,12 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   // ---- publish new paths, fold this call's sums into the old ones -----------------------
   // events that order the side stream's fold after the publish, and the emission after
   // the fold: created before anything is published
-  Event published_ev, folded;
+  Event published_ev, folded, trie_fork, trie_join;
   if (N > 0 && side != s && (!published_ev.ev || !folded.ev)) return undo(fail(CCT_EDEVICE, "event creation failed"));
   AGG_TRY(hipMemsetAsync(cursor.p, 0, 64, s));
   if (n_new) {
-    // place the new paths in the store: exclusive scan of their padded lengths
-    launch_new_lengths(p->offsets, t->slot.as<Slot>(), new_slots.as<uint32_t>(), (int64_t)n_new,
-                       nsrc.as<int64_t>(), nlen.as<uint64_t>(), s);
+    // place the new paths in the store: exclusive scan of their padded lengths (listed
+    // by collect_new with their first frames and lengths)
     launch_scan(nlen.as<uint64_t>(), (int64_t)n_new, 1, nblkbuf.as<uint64_t>(), nstart.as<uint64_t>(), s);
     AGG_TRY(hipMemcpyAsync(cursor.p, nstart.as<uint64_t>() + n_new, 8, hipMemcpyDeviceToDevice, s));
     PublishArgs pa{};
@@ -714,7 +715,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   for (int mode = incremental ? 3 : (use_trie ? 0 : (ca.exact ? 2 : 1));;) {
     CanonArgs run = ca;
     run.exact = mode == 2 ? 1 : 0;
-    if (mode == 0) launch_trie_sort(ta, s);
+    if (mode == 0) launch_trie_sort(ta, s, side, trie_fork.ev, trie_join.ev);
     else if (mode == 3) launch_merge_order(run, t->order.as<uint32_t>(), t->d, merge_scratch.as<uint32_t>(), s);
     else launch_sort(run, s);
     tm.mark(4, s);
@@ -725,7 +726,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     AGG_TRY(hipMemcpyAsync(hs, cursor.p, 64, hipMemcpyDeviceToHost, s));
     if (mode == 0) AGG_TRY(hipMemcpyAsync(hs + 8, ta.ctr, 64, hipMemcpyDeviceToHost, s));
     AGG_TRY(hipStreamSynchronize(s));
-    const bool trie_failed = mode == 0 && hs[8 + 3] != 0;
+    const bool trie_failed = mode == 0 && hs[8 + kTrieCtrFail] != 0;
     if (!hs[3] && !trie_failed) {  // order verified strictly increasing
       if (run.order != ca.order) std::swap(order, order_tmp);
       break;

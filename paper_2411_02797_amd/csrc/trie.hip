@@ -34,7 +34,10 @@ constexpr int kMedium = 2048;               // LDS sort capacity of one workgrou
 constexpr uint64_t kRootSeed = 0x5851F42D4C957F2Dull;
 constexpr uint16_t kNone = 0xFFFFu;
 constexpr int kMaxBuckets = 256, kOversample = 2, kBucketTarget = 32;  // large groups (split_kernel)
-enum { kListSmall = 0, kListMedium = 1, kListLarge = 2, kFail = 3 };
+// lists: buckets of up to 64 siblings (of large groups), groups of 65 .. 512 siblings,
+// groups of more than 512, buckets of 65 .. 2048 siblings (of large groups)
+enum { kListSmall = 0, kListMedium = 1, kListLarge = 2, kListMediumBucket = 3 };
+constexpr int kFail = kTrieCtrFail;
 
 __device__ inline void fail(const TrieArgs &a) { atomicOr(&a.ctr[kFail], 1ull); }
 
@@ -239,8 +242,31 @@ __device__ inline void node_block(const TrieArgs &a, uint32_t X, u32x4 (&v)[4], 
   nf = block_frames((uint32_t)info);
 }
 
-// block x < block y (LDS rows of 16 frames)
+// block x < block y: frames compared as unsigned over the shorter block, then the
+// shorter block first.  Both rows are read whole (eight 16-byte LDS reads issued
+// together); the first differing pair of frames is found without branches, and only its
+// two frames are read again.  Frames past a block's end are zero in the store, and a
+// difference there lies past the shorter block, which the length rule then decides.
 __device__ inline bool block_less(const uint32_t *x, uint32_t nx, const uint32_t *y, uint32_t ny) {
+  typedef unsigned long long u64x2 __attribute__((ext_vector_type(2)));
+  u64x2 a[4], b[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    a[c] = *(const u64x2 *)(x + 4 * c);
+    b[c] = *(const u64x2 *)(y + 4 * c);
+  }
+  int fp = 8;  // first pair of frames that differs
+#pragma unroll
+  for (int p = 7; p >= 0; --p) fp = a[p >> 1][p & 1] != b[p >> 1][p & 1] ? p : fp;
+  if (fp < 8) {
+    const uint32_t i = 2 * fp + (x[2 * fp] == y[2 * fp] ? 1u : 0u);
+    if (i < min(nx, ny)) return x[i] < y[i];
+  }
+  return nx < ny;
+}
+
+// the same order, for a block held in registers (y) against an LDS row (x)
+__device__ inline bool block_less_seq(const uint32_t *x, uint32_t nx, const uint32_t *y, uint32_t ny) {
   const uint32_t n = min(nx, ny);
   for (uint32_t c = 0; c < 4 * 4; c += 4) {
     const u32x4 vx = *(const u32x4 *)(x + c), vy = *(const u32x4 *)(y + c);
@@ -266,9 +292,11 @@ __device__ inline void lds_bitonic(uint16_t *si, int n, Less lt) {
       for (int t = threadIdx.x; t < n2 / 2; t += blockDim.x) {
         const int i0 = 2 * j * (t / j) + (t % j), i1 = i0 + j;
         const uint16_t x = si[i0], y = si[i1];
-        auto less = [&](uint16_t p, uint16_t q) { return p != kNone && (q == kNone || lt(p, q)); };
-        // ascending where (i0 & k) == 0, else descending
-        if ((i0 & k) == 0 ? less(y, x) : less(x, y)) { si[i0] = y; si[i1] = x; }
+        // ascending where (i0 & k) == 0, else descending: one comparison per pair, its
+        // operands chosen by the direction (no divergence between the two)
+        const bool asc = (i0 & k) == 0;
+        const uint16_t p = asc ? y : x, q = asc ? x : y;
+        if (p != kNone && (q == kNone || lt(p, q))) { si[i0] = y; si[i1] = x; }
       }
       __syncthreads();
     }
@@ -357,12 +385,13 @@ __global__ __launch_bounds__(kChunkThreads) void chunk_kernel(TrieArgs a) {
   }
 }
 
-// Buckets of large groups (2 .. 2048 siblings): one workgroup each, blocks in LDS.
-__global__ __launch_bounds__(kMedThreads) void medium_kernel(TrieArgs a) {
+// Groups of 65 .. 512 siblings, or buckets of large groups of up to 2048 (list): one
+// workgroup each, blocks in LDS.
+__global__ __launch_bounds__(kMedThreads) void medium_kernel(TrieArgs a, int list) {
   __shared__ MedShared S;
-  const uint64_t ng = min((uint64_t)a.ctr[kListMedium], (uint64_t)a.list_cap);
+  const uint64_t ng = min((uint64_t)a.ctr[list], (uint64_t)a.list_cap);
   for (uint64_t g = blockIdx.x; g < ng; g += gridDim.x) {
-    const uint64_t e = a.lists[kListMedium * a.list_cap + g];
+    const uint64_t e = a.lists[list * a.list_cap + g];
     const uint32_t start = (uint32_t)(e >> 32), n = (uint32_t)e;
     for (uint32_t i = threadIdx.x; i < n; i += kMedThreads) {
       u32x4 v[4];
@@ -482,7 +511,7 @@ __global__ __launch_bounds__(kMedThreads) void classify_kernel(TrieArgs a) {
   int blo = 0, bhi = nb - 1;
   while (blo < bhi) {
     const int mid = (blo + bhi) >> 1;
-    if (block_less(C.sb[h][mid], C.sn[h][mid], x, nf)) blo = mid + 1; else bhi = mid;
+    if (block_less_seq(C.sb[h][mid], C.sn[h][mid], x, nf)) blo = mid + 1; else bhi = mid;
   }
   a.posof[X] = (uint32_t)blo;
   atomicAdd(&a.bcnt[g * kMaxBuckets + blo], 1u);
@@ -520,7 +549,7 @@ __global__ __launch_bounds__(kMaxBuckets) void bstart_kernel(TrieArgs a) {
   a.bcnt[g * kMaxBuckets + j] = 0;
   if (c < 2) return;
   if (c > (uint32_t)kMedium) { fail(a); return; }
-  const int cls = c <= 64 ? kListSmall : kListMedium;
+  const int cls = c <= 64 ? kListSmall : kListMediumBucket;
   const unsigned long long i = atomicAdd(&a.ctr[cls], 1ull);
   if ((int64_t)i < a.list_cap) a.lists[cls * a.list_cap + i] = ((uint64_t)(start + bs) << 32) | c;
   else fail(a);
@@ -614,8 +643,9 @@ inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1)
 
 }  // namespace
 
-void launch_trie_sort(const TrieArgs &a, hipStream_t s) {
+void launch_trie_sort(const TrieArgs &a, hipStream_t s, hipStream_t s2, hipEvent_t fork, hipEvent_t join) {
   if (a.d <= 0) return;
+  const bool two = s2 != s && fork && join;
   hipLaunchKernelGGL(clear_kernel, dim3(blocks_for((int64_t)a.cap + 1, 256)), dim3(256), 0, s, a);
   hipLaunchKernelGGL(fill_kernel, dim3(blocks_for(a.d, 256)), dim3(256), 0, s, a);
   if (a.nblocks > 0) {
@@ -624,14 +654,27 @@ void launch_trie_sort(const TrieArgs &a, hipStream_t s) {
     hipLaunchKernelGGL(link_kernel, dim3((unsigned)link_grid), dim3(kLinkThreads), 0, s, a);
     launch_scan(a.hist, (int64_t)a.cap + 1, 1, a.scan_blk, a.gstart, s);
     hipLaunchKernelGGL(scatter_kernel, dim3(blocks_for((int64_t)a.cap, 256)), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(chunk_kernel, dim3(blocks_for(a.nblocks, kChunk)), dim3(kChunkThreads), 0, s, a);
+    // Sibling order.  Small groups (chunk_kernel) and the listed groups of 65 .. 512
+    // (medium_kernel) touch only their own positions; the large groups' pipeline (split,
+    // classify, bucket scatter, then its buckets) reads the other positions only to see
+    // that they are not in a large group, which any member of the same group tells.  So
+    // the two run side by side, on two streams when the caller gives a second one.
+    hipStream_t sa = s;
+    if (two && hipEventRecord(fork, s) == hipSuccess && hipStreamWaitEvent(s2, fork, 0) == hipSuccess) sa = s2;
+    hipLaunchKernelGGL(chunk_kernel, dim3(blocks_for(a.nblocks, kChunk)), dim3(kChunkThreads), 0, sa, a);
+    hipLaunchKernelGGL(medium_kernel, dim3(256), dim3(kMedThreads), 0, sa, a, (int)kListMedium);
     hipLaunchKernelGGL(split_kernel, dim3(256), dim3(kMedThreads), 0, s, a);
     hipLaunchKernelGGL(classify_kernel, dim3(blocks_for(a.nblocks, kChunk)), dim3(kMedThreads), 0, s, a);
     hipLaunchKernelGGL(bstart_kernel, dim3((unsigned)a.large_cap), dim3(kMaxBuckets), 0, s, a);
     hipLaunchKernelGGL(rscatter_kernel, dim3(blocks_for(a.nblocks, 256)), dim3(256), 0, s, a);
     hipLaunchKernelGGL(rcopy_kernel, dim3(blocks_for(a.nblocks, 256)), dim3(256), 0, s, a);
     hipLaunchKernelGGL(bucket_kernel, dim3(1024), dim3(64 * kBucketWaves), 0, s, a);
-    hipLaunchKernelGGL(medium_kernel, dim3(256), dim3(kMedThreads), 0, s, a);
+    hipLaunchKernelGGL(medium_kernel, dim3(256), dim3(kMedThreads), 0, s, a, (int)kListMediumBucket);
+    if (sa != s && (hipEventRecord(join, sa) != hipSuccess || hipStreamWaitEvent(s, join, 0) != hipSuccess)) {
+      // the side branch cannot be joined: wait for it from the host before going on
+      (void)hipGetLastError();
+      (void)hipStreamSynchronize(sa);
+    }
     hipLaunchKernelGGL(counts_kernel, dim3(blocks_for(a.nblocks, 256)), dim3(256), 0, s, a);
     launch_scan(a.cnt, a.nblocks, 1, a.scan_blk, a.cnt_scan, s);
   }
