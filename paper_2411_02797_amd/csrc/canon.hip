@@ -110,20 +110,30 @@ __device__ inline bool key_less(const CanonArgs &a, uint32_t x, uint32_t y) {
 }
 
 // ---- sort -------------------------------------------------------------------------
+// Block-local bitonic sort.  A merge's new paths carry their gap beside the key in LDS,
+// so pairs in different gaps are ordered without a global load; only pairs in one gap
+// compare paths.
 __global__ __launch_bounds__(512) void sort_block_kernel(CanonArgs a, uint32_t *out) {
   __shared__ uint32_t key[kSortBlock];
+  __shared__ uint32_t kgap[kSortBlock];
   const int tid = threadIdx.x;
   const int64_t base = (int64_t)blockIdx.x * kSortBlock;
-  for (int i = tid; i < kSortBlock; i += 512) key[i] = base + i < a.d ? (uint32_t)(a.id0 + base + i) : kInf;
+  for (int i = tid; i < kSortBlock; i += 512) {
+    const bool in = base + i < a.d;
+    key[i] = in ? (uint32_t)(a.id0 + base + i) : kInf;
+    kgap[i] = in && a.gap ? a.gap[base + i] : 0u;
+  }
   __syncthreads();
   for (int k = 2; k <= kSortBlock; k <<= 1) {
     for (int j = k >> 1; j > 0; j >>= 1) {
       const int i = 2 * j * (tid / j) + (tid % j), l = i + j;
-      const uint32_t x = key[i], y = key[l];
+      const uint32_t x = key[i], y = key[l], gx = kgap[i], gy = kgap[l];
+      // ascending where (i & k) == 0: swap if y < x; else swap if x < y
       const bool up = (i & k) == 0;
-      const bool swap = up ? key_less(a, y, x) : key_less(a, x, y);
+      const uint32_t p = up ? y : x, q = up ? x : y, gp = up ? gy : gx, gq = up ? gx : gy;
+      const bool swap = p != kInf && (q == kInf || (gp != gq ? gp < gq : path_less(a, p, q)));
       __syncthreads();
-      if (swap) { key[i] = y; key[l] = x; }
+      if (swap) { key[i] = y; key[l] = x; kgap[i] = gy; kgap[l] = gx; }
       __syncthreads();
     }
   }
