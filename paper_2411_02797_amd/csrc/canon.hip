@@ -284,12 +284,30 @@ __global__ __launch_bounds__(256) void scan_blocks_kernel(uint64_t *blk, int64_t
   }
 }
 
+// direct: blk holds the raw block sums (not scanned), and each block adds up the sums of
+// the blocks before it itself (at most kScanDirectBlocks of them); the last block also
+// writes the totals row.  Otherwise blk holds their exclusive scan (scan_blocks_kernel).
+constexpr int64_t kScanDirectBlocks = 4096;
+
 __global__ __launch_bounds__(256) void scan_final_kernel(const uint64_t *in, int64_t rows, int C, const uint64_t *blk,
-                                                         uint64_t *out) {
+                                                         uint64_t *out, int direct) {
   __shared__ uint64_t part[4];
+  __shared__ uint64_t pre;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t r0 = (int64_t)blockIdx.x * kScanRows + tid * 4;
   for (int c = 0; c < C; ++c) {
+    if (direct) {  // sum of the earlier blocks' sums of column c
+      uint64_t x = 0;
+      for (int64_t j = tid; j < (int64_t)blockIdx.x; j += 256) x += blk[j * C + c];
+      for (int o = 32; o > 0; o >>= 1) {
+        const uint32_t lo = __shfl_xor((uint32_t)x, o, 64), hi = __shfl_xor((uint32_t)(x >> 32), o, 64);
+        x += ((uint64_t)hi << 32) | lo;
+      }
+      if (lane == 0) part[wave] = x;
+      __syncthreads();
+      if (tid == 0) pre = part[0] + part[1] + part[2] + part[3];
+      __syncthreads();
+    }
     uint64_t v[4], s = 0;
     for (int k = 0; k < 4; ++k) {
       v[k] = r0 + k < rows ? in[(r0 + k) * C + c] : 0;
@@ -302,12 +320,14 @@ __global__ __launch_bounds__(256) void scan_final_kernel(const uint64_t *in, int
     }
     if (lane == 63) part[wave] = x;
     __syncthreads();
-    uint64_t run = blk[blockIdx.x * C + c] + x - s;
+    const uint64_t base = direct ? pre : blk[blockIdx.x * C + c];
+    uint64_t run = base + x - s;
     for (int w = 0; w < wave; ++w) run += part[w];
     for (int k = 0; k < 4; ++k) {
       if (r0 + k < rows) out[(r0 + k) * C + c] = run;
       run += v[k];
     }
+    if (direct && blockIdx.x == gridDim.x - 1 && tid == 0) out[rows * C + c] = base + part[0] + part[1] + part[2] + part[3];
     __syncthreads();
   }
 }
@@ -512,9 +532,10 @@ void launch_merge_order(CanonArgs &a, const uint32_t *old_order, int64_t d_old, 
 void launch_scan(const uint64_t *in, int64_t rows, int C, uint64_t *blk, uint64_t *out, hipStream_t s) {
   if (rows > 0) {
     const int64_t nblk = (rows + kScanRows - 1) / kScanRows;
+    const int direct = nblk <= kScanDirectBlocks ? 1 : 0;
     hipLaunchKernelGGL(scan_reduce_kernel, dim3((unsigned)nblk), dim3(256), 0, s, in, rows, C, blk);
-    hipLaunchKernelGGL(scan_blocks_kernel, dim3(1), dim3(256), 0, s, blk, nblk, C, out, rows);
-    hipLaunchKernelGGL(scan_final_kernel, dim3((unsigned)nblk), dim3(256), 0, s, in, rows, C, blk, out);
+    if (!direct) hipLaunchKernelGGL(scan_blocks_kernel, dim3(1), dim3(256), 0, s, blk, nblk, C, out, rows);
+    hipLaunchKernelGGL(scan_final_kernel, dim3((unsigned)nblk), dim3(256), 0, s, in, rows, C, blk, out, direct);
   } else {
     (void)hipMemsetAsync(out, 0, sizeof(uint64_t) * C, s);
   }
