@@ -420,13 +420,18 @@ __global__ void chain_kernel(CanonArgs a) {
     atomicOr(&a.u_out[1], 1ull);
     return;
   }
-  for (uint32_t k = 0; k < cnt; ++k) a.node_path[b + k] = (uint32_t)i;
+  if (cnt == 0) return;
+  // the 64-node windows whose first node lies on this path (window 0 starts at node 1,
+  // past the root)
+  if (b == 1) a.win_path[0] = (uint32_t)i;
+  for (uint64_t w = (b + 63) / 64; w <= (b + cnt - 1) / 64; ++w) a.win_path[w] = (uint32_t)i;
 }
 
 __global__ __launch_bounds__(256) void emit_kernel(CanonArgs a) {
   // a wave's 64 consecutive nodes stage their excl and incl rows in LDS ([2][256][m]
   // words), then write each array's 64 m words as one contiguous stretch
   extern __shared__ uint64_t emit_stage[];
+  __shared__ uint32_t emit_mark[256];  // per wave: window position -> path offset
   const int C = 1 + a.m, m = a.m;
   const int lane = threadIdx.x & 63, w0 = threadIdx.x - lane;
   uint64_t *sx = emit_stage + (int64_t)w0 * m, *si = emit_stage + (int64_t)(256 + w0) * m;
@@ -438,9 +443,33 @@ __global__ __launch_bounds__(256) void emit_kernel(CanonArgs a) {
     a.u_out[0] = (unsigned long long)U;
     if (U_all > a.u_max) atomicOr(&a.u_out[1], 1ull);
   }
+  uint32_t *mark = emit_mark + (w0 >> 6) * 64;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t base = (int64_t)blockIdx.x * blockDim.x + w0; base < U; base += stride) {
     const int64_t u = base + lane;
+    // this window's paths: the one holding its first node and the 63 after it (every
+    // path past the first has at least one node, so they cover the window); a node's
+    // path is the last of them whose first node is at or before it
+    // (window 0 holds only the root when there is no other node: no path to look up)
+    int64_t i0 = (base > 0 || U > 1) ? (int64_t)a.win_path[base >> 6] : 0;
+    if (i0 >= a.d && (base > 0 || U > 1)) {  // a window chain_kernel did not write (the order is not a permutation)
+      if (lane == 0) atomicOr(&a.u_out[1], 1ull);
+      i0 = 0;
+    }
+    const uint64_t nb = i0 + lane < a.d ? node_base(a, i0 + lane) : ~0ull;
+    mark[lane] = 0;
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_wave_barrier();
+    if (lane > 0 && nb >= (uint64_t)base && nb < (uint64_t)base + 64) mark[nb - base] = (uint32_t)lane;
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_wave_barrier();
+    uint32_t off = mark[lane];
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t y = __shfl_up(off, o, 64);
+      if (lane >= o) off = max(off, y);
+    }
+    const uint64_t bnode = ((uint64_t)__shfl((uint32_t)(nb >> 32), (int)off, 64) << 32) | __shfl((uint32_t)nb, (int)off, 64);
     if (u == 0) {
       a.parent[0] = kInf;
       a.frame[0] = 0;
@@ -452,17 +481,22 @@ __global__ __launch_bounds__(256) void emit_kernel(CanonArgs a) {
         si[j] = a.scan_out[a.d * C + 1 + j];
       }
     } else if (u < U) {
-      int64_t i = a.node_path[u];
-      if (i >= a.d) {  // a node chain_kernel did not write (the order is not a permutation)
+      int64_t i = i0 + (int64_t)off;
+      uint64_t b = bnode;
+      if (i >= a.d || b > (uint64_t)u) {  // (only when the order is not a permutation)
         atomicOr(&a.u_out[1], 1ull);
         i = 0;
+        b = node_base(a, 0);
       }
       const uint32_t pid = a.order[i];
       const uint32_t L = a.lcp[i], len = a.plen[pid];
-      const uint64_t b = node_base(a, i);
-      const uint32_t l = L + 1 + (uint32_t)(u - b);
+      uint32_t l = L + 1 + (uint32_t)(u - b);
+      if (l > len || (uint64_t)u - b >= (uint64_t)len) {  // (only when the order is not a permutation)
+        atomicOr(&a.u_out[1], 1ull);
+        l = len;
+      }
       a.parent[u] = u == (int64_t)b ? a.chain_parent[i] : (uint32_t)(u - 1);
-      a.frame[u] = a.pframes[a.pstart[pid] + l - 1];
+      a.frame[u] = l ? a.pframes[a.pstart[pid] + l - 1] : 0u;
       a.depth[u] = l;
       const int64_t e = (i + 1 == a.d || l > a.lcp[i + 1]) ? i + 1 : next_smaller(a, n, i + 2, l);
       // the subtree is the paths i .. e-1 below depth l: ids up to the first node of path e

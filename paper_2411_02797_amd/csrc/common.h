@@ -199,7 +199,7 @@ struct CanonArgs {
   uint32_t *sparse;      // [levels][D] range minima of lcp
   int32_t levels;
   uint32_t *chain_parent; // [D]
-  uint32_t *node_path;   // [U_max] path index (in order) of each node
+  uint32_t *win_path;    // [U_max / 64 + 1] path index (in order) holding each 64-node window's first node
   int64_t u_max;
   // node arrays
   uint32_t *parent, *frame, *depth;

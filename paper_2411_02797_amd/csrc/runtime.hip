@@ -589,11 +589,11 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   const int levels = floor_log2((uint64_t)n1) + 1;
   const int64_t nblk = (D + 1023) / 1024 + 1;
   const int64_t u_max = sum_len + 1;
-  Buf order, order_tmp, lcp, scan_in, scan_out, scan_blk, sparse, chain, node_path, cursor, nstart, nblkbuf;
+  Buf order, order_tmp, lcp, scan_in, scan_out, scan_blk, sparse, chain, win_path, cursor, nstart, nblkbuf;
   Buf n_parent, n_frame, n_depth, n_subend, n_excl, n_incl;  // canonical arrays of the new tree
   if (!order.alloc(dneed * 4) || !order_tmp.alloc(dneed * 4) || !lcp.alloc(n1 * 4) || !scan_in.alloc(dneed * C * 8) ||
       !scan_out.alloc(n1 * C * 8) || !scan_blk.alloc(nblk * C * 8) || !sparse.alloc((int64_t)levels * n1 * 4) ||
-      !chain.alloc(dneed * 4) || !node_path.alloc(u_max * 4) || !cursor.alloc(64) || !n_parent.alloc(u_max * 4) || !n_subend.alloc(u_max * 4) ||
+      !chain.alloc(dneed * 4) || !win_path.alloc((u_max / 64 + 2) * 4) || !cursor.alloc(64) || !n_parent.alloc(u_max * 4) || !n_subend.alloc(u_max * 4) ||
       !n_frame.alloc(u_max * 4) || !n_depth.alloc(u_max * 4) || !n_excl.alloc(u_max * m * 8) ||
       !n_incl.alloc(u_max * m * 8) || !nstart.alloc((n_new + 1) * 8) ||
       !nblkbuf.alloc(((int64_t)n_new / 1024 + 2) * 8))
@@ -704,7 +704,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   ca.order = order.as<uint32_t>(); ca.order_tmp = order_tmp.as<uint32_t>(); ca.lcp = lcp.as<uint32_t>();
   ca.scan_in = scan_in.as<uint64_t>(); ca.scan_out = scan_out.as<uint64_t>(); ca.scan_blk = scan_blk.as<uint64_t>();
   ca.scan_blocks = nblk; ca.sparse = sparse.as<uint32_t>(); ca.levels = levels;
-  ca.chain_parent = chain.as<uint32_t>(); ca.node_path = node_path.as<uint32_t>(); ca.u_max = u_max;
+  ca.chain_parent = chain.as<uint32_t>(); ca.win_path = win_path.as<uint32_t>(); ca.u_max = u_max;
   ca.parent = n_parent.as<uint32_t>(); ca.frame = n_frame.as<uint32_t>(); ca.depth = n_depth.as<uint32_t>();
   ca.subend = n_subend.as<uint32_t>();
   ca.excl = n_excl.as<uint64_t>(); ca.incl = n_incl.as<uint64_t>();
