@@ -623,19 +623,29 @@ __global__ void counts_kernel(TrieArgs a) {
   a.cnt[i] = (uint64_t)i < nodes ? a.ncount[a.grouped[i]] : 0;
 }
 
-__global__ void rank_kernel(TrieArgs a) {
-  const int64_t d = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (d >= a.d) return;
-  const uint32_t len = a.plen[d];
-  uint64_t rank = 0;
-  uint32_t prev = (uint32_t)a.cap;
-  const int64_t b0 = a.pstart[d] / kBlk, nb = (len + kBlk - 1) / kBlk;
-  for (int64_t k = 0; k < nb; ++k) {
+// Eight lanes per path: lane g takes the path's blocks g, g + 8, ...; a block's term
+// needs only its own node and the node before it, so the terms of one path load in
+// parallel and meet by three shuffles within the eight lanes.
+constexpr int kRankLanes = 8;
+__global__ __launch_bounds__(256) void rank_kernel(TrieArgs a) {
+  const int64_t d = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kRankLanes;
+  const int g = threadIdx.x % kRankLanes;
+  const bool active = d < a.d;
+  const uint32_t len = active ? a.plen[d] : 0u;
+  const int64_t b0 = active ? a.pstart[d] / kBlk : 0, nb = (len + kBlk - 1) / kBlk;
+  uint64_t part = 0;
+  for (int64_t k = g; k < nb; k += kRankLanes) {
     const uint32_t X = a.occ[b0 + k];
-    rank += a.cnt_scan[a.posof[X]] - a.cnt_scan[a.gstart[a.nparent[X]]] + a.nend[prev];
-    prev = X;
+    const uint32_t prev = k ? a.occ[b0 + k - 1] : (uint32_t)a.cap;
+    part += a.cnt_scan[a.posof[X]] - a.cnt_scan[a.gstart[a.nparent[X]]] + a.nend[prev];
   }
-  if (rank < (uint64_t)a.d) a.order[rank] = (uint32_t)d;
+#pragma unroll
+  for (int o = kRankLanes / 2; o > 0; o >>= 1) {
+    const uint32_t lo = __shfl_xor((uint32_t)part, o, 64), hi = __shfl_xor((uint32_t)(part >> 32), o, 64);
+    part += ((uint64_t)hi << 32) | lo;
+  }
+  if (!active || g != 0) return;
+  if (part < (uint64_t)a.d) a.order[part] = (uint32_t)d;
   else fail(a);
 }
 
@@ -678,7 +688,7 @@ void launch_trie_sort(const TrieArgs &a, hipStream_t s, hipStream_t s2, hipEvent
     hipLaunchKernelGGL(counts_kernel, dim3(blocks_for(a.nblocks, 256)), dim3(256), 0, s, a);
     launch_scan(a.cnt, a.nblocks, 1, a.scan_blk, a.cnt_scan, s);
   }
-  hipLaunchKernelGGL(rank_kernel, dim3(blocks_for(a.d, 256)), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(rank_kernel, dim3(blocks_for(a.d * kRankLanes, 256)), dim3(256), 0, s, a);
 }
 
 }  // namespace cct
