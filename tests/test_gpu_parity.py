@@ -91,6 +91,26 @@ def test_long_paths(L):
     assert_same(gpu_tree(o, f, w), oracle.build_tree(o, f, w), f"L={L}")
 
 
+@pytest.mark.parametrize("shape", ["star", "star_with_empty", "comb"])
+def test_one_node_per_path_windows(shape):
+    # the emission takes 64 consecutive nodes per wave and finds their paths among the 64
+    # paths from the one holding the first node: paths that add one node each (a star of
+    # leaves under the root, or a comb of leaves hanging off one spine) put 64 paths in
+    # every window, the most a window can hold; the empty path adds none
+    rng = np.random.default_rng(12)
+    if shape == "comb":
+        spine = rng.integers(0, 2**32, size=700, dtype=np.uint64).astype(np.uint32).tolist()
+        paths = [spine] + [spine[:k] + [0xFFFFFFF0 - k] for k in range(700)]
+    else:
+        paths = [[int(x)] for x in rng.permutation(5000)]
+        if shape == "star_with_empty":
+            paths += [[]] * 3
+    order = rng.permutation(len(paths))
+    o, f = csr([paths[i] for i in order])
+    w = rng.integers(0, 2**64, size=(len(paths), 2), dtype=np.uint64)
+    assert_same(gpu_tree(o, f, w), oracle.build_tree(o, f, w), shape)
+
+
 def test_mixed_long_and_short_in_one_tile():
     rng = np.random.default_rng(7)
     paths = [rng.integers(0, 5, size=rng.integers(0, 6)).tolist() for _ in range(300)]
