@@ -164,6 +164,10 @@ def main():
         sys.exit(2)
 
     import torch
+    # the library's calls go to the stream they are given; the bench gives them a stream of
+    # its own, as a caller would, rather than the legacy default stream (on which a call
+    # on the 1M-event workload measured about 0.04 ms slower)
+    torch.cuda.set_stream(torch.cuda.Stream(device=0))
     if args.copy_calibrate:
         n = args.copy_calibrate << 20
         src = torch.ones(n // 4, dtype=torch.int32, device="cuda")
