@@ -344,6 +344,29 @@ __global__ void sparse_level_kernel(uint32_t *sp, int64_t n, int k) {
   sp[(int64_t)k * n + x] = v;
 }
 
+// Levels top + 1 .. top + count in one launch: level k at x is the minimum of the
+// level-top windows starting at x, x + 2^top, ... below x + 2^k (windows past n left
+// out), so each thread reads 2^count - 1 level-top entries instead of waiting for the
+// level below.
+constexpr int kHighLevels = 7;  // levels per launch: 127 level-top reads per position
+__global__ void sparse_high_kernel(uint32_t *sp, int64_t n, int top, int count) {
+  const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (x >= n) return;
+  const uint32_t *lv = sp + (int64_t)top * n;
+  const int64_t w = (int64_t)1 << top;
+  uint32_t v = lv[x];
+  for (int c = 1; c <= count; ++c) {
+    // the new half of level top + c: windows x + 2^(top + c - 1) + j w, j < 2^(c - 1)
+    const int64_t lo = x + (w << (c - 1));
+    for (int64_t j = 0; j < ((int64_t)1 << (c - 1)); ++j) {
+      const int64_t y = lo + j * w;
+      if (y >= n) break;
+      v = min(v, lv[y]);
+    }
+    sp[(int64_t)(top + c) * n + x] = v;
+  }
+}
+
 // Levels 1 .. kTileLevels in one pass: a workgroup takes kTileOut positions, loads
 // their lcp values and the 2^kTileLevels - 1 after them (past n: +inf) into LDS,
 // and builds every level there from the one below.
@@ -585,8 +608,12 @@ void launch_canon(const CanonArgs &a, hipStream_t s) {
   const int top = std::min(a.levels - 1, kTileLevels);
   if (top >= 1)
     hipLaunchKernelGGL(sparse_tile_kernel, dim3(blocks_for(n, kTileOut)), dim3(1024), 0, s, a.sparse, a.lcp, n, top);
-  for (int k = top + 1; k < a.levels; ++k)
-    hipLaunchKernelGGL(sparse_level_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, a.sparse, n, k);
+  if (top >= 1 && top < a.levels - 1) {
+    const int count = std::min(a.levels - 1 - top, kHighLevels);
+    hipLaunchKernelGGL(sparse_high_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, a.sparse, n, top, count);
+    for (int k = top + count + 1; k < a.levels; ++k)
+      hipLaunchKernelGGL(sparse_level_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, s, a.sparse, n, k);
+  }
   if (a.d > 0) hipLaunchKernelGGL(chain_kernel, dim3(blocks_for(a.d, 256)), dim3(256), 0, s, a);
   hipLaunchKernelGGL(emit_kernel, dim3(a.grid_nodes), dim3(256), (size_t)2 * 256 * a.m * 8, s, a);
 }
