@@ -579,7 +579,7 @@ constexpr int kAggUnroll = 4;
 constexpr int kAggHist = 2048;                            // most buckets a flush can count in LDS
 constexpr int kAggLdsBytes = 163840 - kAggHist * 4 - 256;  // map keys and sums
 constexpr uint32_t kEmptyKey = 0xFFFFFFFFu;
-constexpr int kBucketWords = 8192;                         // LDS sums of one bucket (64 KiB)
+constexpr int kBucketWords = 16384;                        // LDS sums of one bucket (128 KiB)
 
 constexpr int agg_entries(int m) {
   int e = kAggLdsBytes / (4 + 8 * m);
