@@ -803,10 +803,10 @@ __global__ __launch_bounds__(256) void collect_sum_kernel(const unsigned long lo
 // lanes per path, four paths per wave: a lane moves four frames of every 64-frame chunk
 // with one 16-byte load (the source, a 4-byte aligned stretch of the batch) and one
 // 16-byte store (the store is 64-byte aligned), so a wave has four paths' frames in
-// flight.  The chunks of a path up to 256 frames are requested before any is used.  Each
+// flight.  The chunks of a path up to 128 frames are requested before any is used.  Each
 // group of four lanes holds one 16-frame block: the block's frame terms meet by two
 // shuffles within the group, and the blocks' prefix sums are carried across chunks.
-constexpr int kPublishChunks = 4;  // 64-frame chunks requested ahead
+constexpr int kPublishChunks = 2;  // 64-frame chunks requested ahead
 __global__ __launch_bounds__(256) void publish_kernel(PublishArgs a) {
   const int lane = threadIdx.x & 63, g = lane & 15;  // g: lane within the path's 16
   const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 4;
