@@ -485,7 +485,9 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   // events overflow into device atomics.
   SideGuard side_guard;
   if (N > 0) {
-    hipStream_t ss = side_guard.acquire();
+    // (a test setting keeps everything on the caller's stream, the path taken when no
+    // second stream can be created)
+    hipStream_t ss = env_int("CCT_TEST_ONE_STREAM", 0) ? nullptr : side_guard.acquire();
     if (ss) side = ss;
     const int agg_grid = (int)std::max<int64_t>(1, std::min<int64_t>((N + 8191) / 8192, (int64_t)cu_count() * 2));
     AggStage stg{};

@@ -350,6 +350,29 @@ def test_query_every_node_and_absent_paths(mode, monkeypatch):
     tree.free()
 
 
+@pytest.mark.parametrize("case", ["layered_1m_part", "random_paths"])
+def test_one_stream_only(monkeypatch, case):
+    # with no second stream (a test setting: the path taken when none can be created) the
+    # aggregation, the fold and the sibling ordering all run on the caller's stream, in
+    # order; the tree equals the oracle's, and a merge after it too
+    if case == "layered_1m_part":
+        o, f, w = tracegen.generate("layered_1m")
+        n = 60000
+        o, f, w = o[: n + 1].copy(), f[: o[n]].copy(), w[:n].copy()
+    else:
+        o, f, w = tracegen.random_paths(30000, 200, 40, 2, seed=91)
+    ob, fb, wb = tracegen.random_paths(5000, 200, 40, w.shape[1], seed=92)
+    monkeypatch.setenv("CCT_TEST_ONE_STREAM", "1")
+    import paper_2411_02797_amd as cct
+    tree = cct.build(*to_dev(o, f, w))
+    assert_same(tree.to_numpy(), oracle.build_tree(o, f, w), case)
+    tree.merge(*to_dev(ob, fb, wb))
+    oc = np.concatenate([o, o[-1] + ob[1:]])
+    want = oracle.build_tree(oc, np.concatenate([f, fb]), np.concatenate([w, wb]))
+    assert_same(tree.to_numpy(), want, case + " merged")
+    tree.free()
+
+
 def test_concurrent_builds_on_two_threads():
     # distinct trees built and merged at the same time from two host threads, each on its
     # own stream: every call takes its own side stream, so neither waits for or corrupts
