@@ -26,7 +26,10 @@
 //   - dedup: lane j resolves event j: a path with the same hash and length already
 //     resolved in this workgroup (LDS cache), else the table (linear probing over
 //     16-byte slots that carry the candidate's location, so one round trip; one
-//     64-bit CAS claims an empty slot).  Every candidate is verified frame by frame:
+//     64-bit CAS claims an empty slot).  Only the first lane of a workgroup to meet a
+//     path probes the table for it; lanes that meet it meanwhile wait on its cache
+//     entry, so a hot path is not claimed by thousands of CASes on one slot when every
+//     wave meets it in its first tile.  Every candidate is verified frame by frame:
 //     each block lane compares its 16 frames with the candidate's (16-byte loads; hot
 //     candidates are L2 resident).
 #include "common.h"
@@ -36,17 +39,21 @@ namespace cct {
 namespace {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 typedef u32x4 u32x4_a4 __attribute__((aligned(4)));
 // global-memory pointers (address space 1), so candidate loads are global loads
 typedef const uint32_t __attribute__((address_space(1))) *gptr;
 typedef const u32x4_a4 __attribute__((address_space(1))) *gptr4;
-enum : int32_t { kProbing = 0, kCandidate = 1, kResolved = 2, kFailed = 3 };
+enum : int32_t { kProbing = 0, kCandidate = 1, kResolved = 2, kFailed = 3, kWaiting = 4 };
 enum : int32_t { kTileFast = 0, kTileSlow = 1, kTileBad = 2, kTileNone = 3 };
 
 constexpr int kWaves = kIngestThreads / 64;
 constexpr int kBlock = 16;                        // frames per lane block
 constexpr int kTileBlocks = kWaveFrames / kBlock;   // blocks per wave tile: kLaneBlocks per lane
-constexpr uint32_t kNotReady = 0xFFFFFFFFu;
+constexpr uint32_t kNotReady = 0xFFFFFFFFu;  // cache entry claimed, its path not yet resolved
+constexpr uint32_t kNoEntry = 0xFFFFFFFEu;   // cache entry's path could not be resolved (table full)
+constexpr int kLeader = 1 << 16;              // added to a cache entry index: this lane claimed the entry
+constexpr int kFromCache = -2;                // no entry; the lane's candidate came from the cache
 constexpr uint64_t kInStore = 1ull << 63;   // candidate base: frames live in the path store
 
 struct WaveShared {
@@ -59,7 +66,10 @@ struct WaveShared {
 
 // Per-workgroup cache of resolved paths, keyed by (hash, length): the table slot and
 // where that slot's frames live (to verify against).  Hot paths cost no table access
-// after their first resolution in a workgroup.
+// after their first resolution in a workgroup.  The first lane of the workgroup to miss on
+// a key claims an entry for it and resolves the path in the table; lanes that meet the
+// claimed entry meanwhile wait for it instead of probing the table themselves, so a path
+// costs one table probe per workgroup however many of its events arrive together.
 struct IngestShared {
   uint64_t ckey[kCacheEntries];    // hash (0: empty / not cacheable)
   uint64_t cbase[kCacheEntries];   // first frame (kInStore: in the path store)
@@ -123,9 +133,16 @@ struct Blk {
   int32_t ev, m, rem, voff;
 };
 
-// Offsets window at event e (lane j holds offsets[e + j], j <= min(63, end - e)).
+// Offsets window at event e (lane j holds offsets[e + j], j <= min(63, end - e); 0 past
+// that).  A buffer load whose range ends at the window's last offset: the address lives in
+// scalar registers, and lanes past the range read zero.
 __device__ inline int64_t load_window(const IngestArgs &a, int64_t e, int64_t end, int lane) {
-  return e < end && lane <= end - e ? a.off[e + lane] : 0;
+  if (e >= end) return 0;
+  const int64_t eu = uniform64(e);
+  const int bytes = __builtin_amdgcn_readfirstlane((int)(min(uniform64(end) - eu, (int64_t)63) + 1) * 8);
+  const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc((void *)(a.off + eu), (short)0, bytes, 0x00020000);
+  const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, lane * 8, 0, 0);
+  return (int64_t)(((uint64_t)v[1] << 32) | v[0]);
 }
 
 // Validate the window and cut the next tile: as many events as fit in the tile's
@@ -297,39 +314,35 @@ __device__ __forceinline__ void probe(const IngestArgs &a, Probe &p, int64_t ev,
   }
 }
 
-// Cache entry holding a resolved path with this hash and length, or -1.
-__device__ inline int cache_find(const IngestShared &S, uint64_t h, uint32_t len) {
+// Look (hash, length) up in the cache.  Returns the entry index plus kLeader when
+// this lane claimed a fresh entry (it resolves the path and fills the entry in), the
+// entry index alone when an entry for the key exists (ready, or claimed and pending: the
+// caller waits), or -1 when the key is not cacheable (hash 0, or its probe window holds
+// no free entry and no entry for the key).
+__device__ inline int cache_lookup(IngestShared &S, uint64_t h, uint32_t len) {
   if (h == 0) return -1;
   uint32_t k = (uint32_t)h & (uint32_t)(kCacheEntries - 1);
   for (int t = 0; t < 8; ++t) {
-    const uint64_t key = S.ckey[k];
-    if (key == 0) return -1;
-    if (key == h && S.cslot[k] != kNotReady && S.clen[k] == len) return (int)k;
+    uint64_t key = S.ckey[k];
+    if (key == 0) {
+      key = atomicCAS((unsigned long long *)&S.ckey[k], 0ull, (unsigned long long)h);
+      if (key == 0) return (int)k | kLeader;
+    }
+    if (key == h) {
+      const uint32_t cs = S.cslot[k];
+      if (cs == kNotReady || (cs != kNoEntry && S.clen[k] == len)) return (int)k;
+    }
     k = (k + 1) & (uint32_t)(kCacheEntries - 1);
   }
   return -1;
 }
 
-// Remember a path just resolved to `slot` (unless its probe window is full, or an
-// entry for the same hash and length names another path).
-__device__ inline void cache_insert(IngestShared &S, uint64_t h, uint32_t len, uint32_t slot, uint64_t cbase) {
-  if (h == 0) return;
-  uint32_t k = (uint32_t)h & (uint32_t)(kCacheEntries - 1);
-  for (int t = 0; t < 8; ++t) {
-    const uint64_t prev = atomicCAS((unsigned long long *)&S.ckey[k], 0ull, (unsigned long long)h);
-    if (prev == 0) {
-      S.cbase[k] = cbase;
-      S.clen[k] = len;
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // payload before the ready slot id
-      S.cslot[k] = slot;
-      return;
-    }
-    if (prev == h) {
-      const uint32_t cs = S.cslot[k];
-      if (cs == kNotReady || cs == slot || S.clen[k] == len) return;
-    }
-    k = (k + 1) & (uint32_t)(kCacheEntries - 1);
-  }
+// Fill in a claimed entry: payload first, then the slot that marks it ready.
+__device__ inline void cache_fill(IngestShared &S, int k, uint32_t len, uint32_t slot, uint64_t cbase) {
+  S.cbase[k] = cbase;
+  S.clen[k] = len;
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  S.cslot[k] = slot;
 }
 
 // Tiles whose frames exceed a wave's staging capacity: one event at a time, the
@@ -397,6 +410,15 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
       break;  // the call fails; this wave's range cannot be cut further
     }
     const int64_t e_nxt = t.e0 + t.ne;
+    // The three waves that share a SIMD take turns at the highest issue priority, one
+    // tile each: with equal priorities the oldest wave always wins, the youngest falls
+    // behind, and the SIMD ends with one wave and nothing to hide its latency behind.
+    {
+      const int r = (iter + __builtin_amdgcn_readfirstlane(wave >> 2)) % 3;
+      if (r == 0) __builtin_amdgcn_s_setprio(0);
+      else if (r == 1) __builtin_amdgcn_s_setprio(1);
+      else __builtin_amdgcn_s_setprio(2);
+    }
     if (t.kind == kTileSlow) {
       slow_wave_tile(a, t.e0, t.ne, o_cur);
       o_cur = o_nxt;
@@ -420,7 +442,11 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
 
     // A2: hash.  Each block sums pair_term over its 8 pairs (pair index 8 m + i) with
     // frames past the path read as zero: the hash covers the zero-padded block.
-    W.hacc[lane] = 0;
+    {
+      uint32_t z = 0;  // made here: a zero kept across the loop would cost two registers
+      asm volatile("" : "+v"(z));
+      W.hacc[lane] = ((uint64_t)z << 32) | z;
+    }
     wave_sync();
 #pragma unroll
     for (int q = 0; q < kLaneBlocks; ++q) {
@@ -447,26 +473,45 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
     const int64_t o_end = shfl_i64(o_cur, lane + 1 < 64 ? lane + 1 : 63);
     Probe p{};
     p.state = kResolved;
-    bool cached = false;      // resolved through the cache or past a colliding path: not re-inserted
-    bool from_cache = false;  // the current candidate came from the cache
+    // cache entry: claimed (index + kLeader, filled in once resolved) or awaited (index);
+    // kFromCache: the current candidate came from the cache; -1: none
+    int ce = -1;
     if (lane < ne) {
       p.len = (uint32_t)(o_end - o_cur);
       p.h = finish_hash(W.hacc[lane], (uint64_t)p.len) & a.hash_mask;
       p.slot = (uint32_t)(p.h & a.cap_mask);
-      p.state = kProbing;
-      const int ci = cache_find(S, p.h, p.len);
-      if (ci >= 0) {
-        p.slot = S.cslot[ci];
-        p.cbase = S.cbase[ci];
-        p.state = p.len == 0 ? kResolved : kCandidate;
-        cached = true;
-        from_cache = true;
-      }
+      ce = cache_lookup(S, p.h, p.len);
+      p.state = ce >= 0 && ce < kLeader ? kWaiting : kProbing;
     }
 
     for (;;) {
+      // a claimed entry is filled in as soon as its path is resolved (or has failed), so
+      // lanes waiting on it, in this wave or another, go on
+      if (ce >= kLeader && (p.state == kResolved || p.state == kFailed)) {
+        cache_fill(S, ce - kLeader, p.len, p.state == kResolved ? p.slot : kNoEntry, p.cbase);
+        ce = -1;
+      }
+      if (p.state == kWaiting) {
+        const uint32_t cs = S.cslot[ce];
+        if (cs != kNotReady) {
+          if (cs != kNoEntry && S.clen[ce] == p.len) {
+            p.slot = cs;
+            p.cbase = S.cbase[ce];
+            p.state = p.len == 0 ? kResolved : kCandidate;
+            ce = kFromCache;
+          } else {
+            p.state = kProbing;
+            ce = -1;
+          }
+        }
+      }
       if (p.state == kProbing) probe(a, p, e0 + lane, o_cur, (int64_t)p.len);
-      if (!__any(p.state == kCandidate)) break;
+      if (!__any(p.state == kCandidate)) {
+        const bool waiting = __any(p.state == kWaiting);
+        if (!waiting && !__any(ce >= kLeader)) break;
+        if (waiting) __builtin_amdgcn_s_sleep(1);  // lanes wait on entries other waves resolve
+        continue;
+      }
       if (lane < ne) {
         uint64_t vp = 0;
         uint32_t lim = 0;
@@ -529,13 +574,12 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
         if (W.bad[lane]) {
           // a table candidate was reached along the probe sequence, so the path is
           // further on; a cached one says nothing about the slots before it
-          p.slot = (uint32_t)((from_cache ? p.h : p.slot + 1) & a.cap_mask);
+          p.slot = (uint32_t)((ce == kFromCache ? p.h : p.slot + 1) & a.cap_mask);
           p.state = kProbing;
-          cached = true;  // another path has the same hash and length: not cacheable
         } else {
           p.state = kResolved;
         }
-        from_cache = false;
+        if (ce == kFromCache) ce = -1;
       }
       wave_sync();
     }
@@ -545,9 +589,12 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
     const Tile tn = make_tile(a, W, e_nxt, end, o_nxt, lane, b);
     load_blocks(a, tn, b, nf);
     const int64_t o_nn = tn.kind == kTileFast || tn.kind == kTileSlow ? load_window(a, tn.e0 + tn.ne, end, lane) : 0;
-    if (lane < ne) {
-      if (p.state == kResolved && !cached) cache_insert(S, p.h, p.len, p.slot, p.cbase);
-      a.slot_of[e0 + lane] = p.state == kResolved ? p.slot : kNoSlot;
+    {
+      // buffer store over the tile's entries (the address stays in scalar registers)
+      const int64_t eu = uniform64(e0);
+      const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+          (void *)(a.slot_of + eu), (short)0, __builtin_amdgcn_readfirstlane(ne * 4), 0x00020000);
+      if (lane < ne) __builtin_amdgcn_raw_buffer_store_b32(p.state == kResolved ? p.slot : kNoSlot, r, lane * 4, 0, 0);
     }
     o_cur = o_nxt;
     o_nxt = o_nn;
