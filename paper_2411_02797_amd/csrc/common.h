@@ -55,16 +55,17 @@ __host__ __device__ inline uint64_t frame_term(uint32_t f, uint32_t k) {
 }
 // The unique-path table hashes pairs of frames instead: a path is zero-padded to a
 // multiple of 16 frames and pair p = (F[2p], F[2p+1]) contributes
-//   (F[2p] + p*kPairMulX + kPairAddX) * (F[2p+1] + p*kPairMulY + kPairAddY) + (F[2p+1] << 32 | F[2p])
-// (factors wrap at 32 bits; the product and the sum at 64).  For a fixed first frame
-// the term is injective in the second, both factors move with the position, and it
-// costs one 32 x 32 -> 64-bit multiply-add and one 64-bit add per two frames.
+//   (F[2p] + p*kPairMulX + kPairAddX) * (F[2p+1] + p*kPairMulY + kPairAddY)
+// (factors wrap at 32 bits; the product and the sum at 64).  Unless its first factor
+// is zero the term is injective in the second frame, both factors move with the
+// position, and it costs one 32 x 32 -> 64-bit multiply-add per two frames.  (A
+// collision costs only time: every table match is verified frame by frame.)
 constexpr uint32_t kPairMulX = 0x9E3779B9u, kPairMulY = 0x85EBCA6Bu, kPairAddX = 0x27D4EB2Fu,
                    kPairAddY = 0x165667B1u;
 __host__ __device__ inline uint64_t pair_term(uint32_t f0, uint32_t f1, uint32_t p) {
   const uint32_t x = f0 + p * kPairMulX + kPairAddX;
   const uint32_t y = f1 + p * kPairMulY + kPairAddY;
-  return (uint64_t)x * (uint64_t)y + (((uint64_t)f1 << 32) | f0);
+  return (uint64_t)x * (uint64_t)y;
 }
 __host__ __device__ inline uint64_t finish_hash(uint64_t s, uint64_t len) {
   uint64_t h = s + len * 0x9E3779B97F4A7C15ull;

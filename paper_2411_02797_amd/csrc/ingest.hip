@@ -460,7 +460,7 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
           const uint32_t f1 = 2 * i + 1 < cb[q].rem ? f[q][2 * i + 1] : 0u;
           const uint32_t x = f0 + kx + (uint32_t)i * kPairMulX;
           const uint32_t y = f1 + ky + (uint32_t)i * kPairMulY;
-          acc += (uint64_t)x * (uint64_t)y + (((uint64_t)f1 << 32) | f0);
+          acc += (uint64_t)x * (uint64_t)y;
         }
         atomicAdd((unsigned long long *)&W.hacc[cb[q].ev], (unsigned long long)acc);
       }
