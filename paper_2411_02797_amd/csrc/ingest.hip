@@ -383,6 +383,9 @@ __device__ __forceinline__ void slow_wave_tile(const IngestArgs &a, int64_t e0, 
 }
 
 
+// Read by the verification of blocks that have no candidate, never written.
+__device__ __attribute__((aligned(16))) uint32_t g_zero_block[kBlock];
+
 __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
   __shared__ IngestShared S;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -532,41 +535,43 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
       }
       wave_sync();
       // every block of a candidate compares its frames with the candidate's: four
-      // 16-byte loads, or 4-byte loads where a 16-byte load would reach past what is
-      // readable at the candidate
+      // 16-byte loads (a block with nothing to verify reads a block of zeros), or, when
+      // some block's 16-byte loads would reach past what is readable at its candidate
+      // (a candidate at the very end of the batch), 4-byte loads of the path's frames
       {
         uint32_t c[kLaneBlocks][kBlock];
         bool chk[kLaneBlocks];
+        gptr cp[kLaneBlocks];
+        bool narrow = false;
 #pragma unroll
         for (int q = 0; q < kLaneBlocks; ++q) {
           const uint64_t vp = cb[q].ev >= 0 ? W.vptr[cb[q].ev] : 0;
           chk[q] = vp != 0;
-          const int avail = chk[q] ? (int)W.vlim[cb[q].ev] - cb[q].m * kBlock : 0;
-          const gptr cp = (gptr)vp + cb[q].m * kBlock;
-          if (chk[q]) {
-            if (avail >= kBlock) {
+          narrow |= chk[q] && (int)W.vlim[cb[q].ev] - cb[q].m * kBlock < kBlock;
+          cp[q] = chk[q] ? (gptr)vp + cb[q].m * kBlock : (gptr)g_zero_block;
+        }
+        if (!__any(narrow)) {
 #pragma unroll
-              for (int j = 0; j < 4; ++j) {
-                const u32x4 v = *(gptr4)(cp + 4 * j);
+          for (int q = 0; q < kLaneBlocks; ++q)
 #pragma unroll
-                for (int k = 0; k < 4; ++k) c[q][4 * j + k] = v[k];
-              }
-            } else {
+            for (int j = 0; j < 4; ++j) {
+              const u32x4 v = *(gptr4)(cp[q] + 4 * j);
 #pragma unroll
-              for (int i = 0; i < kBlock; ++i) c[q][i] = i < cb[q].rem ? cp[i] : 0u;
+              for (int k = 0; k < 4; ++k) c[q][4 * j + k] = v[k];
             }
-          }
+        } else {
+#pragma unroll
+          for (int q = 0; q < kLaneBlocks; ++q)
+#pragma unroll
+            for (int i = 0; i < kBlock; ++i) c[q][i] = chk[q] && i < cb[q].rem ? cp[q][i] : 0u;
         }
         // frames inside the path must match
 #pragma unroll
         for (int q = 0; q < kLaneBlocks; ++q) {
-          if (chk[q]) {
-            uint32_t d = 0;
+          uint32_t d = 0;
 #pragma unroll
-            for (int i = 0; i < kBlock; ++i) d |= i < cb[q].rem ? c[q][i] ^ f[q][i] : 0u;
-            const bool ne = d != 0;
-            if (ne) W.bad[cb[q].ev] = 1;
-          }
+          for (int i = 0; i < kBlock; ++i) d |= i < cb[q].rem ? c[q][i] ^ f[q][i] : 0u;
+          if (chk[q] && d != 0) W.bad[cb[q].ev] = 1;
         }
       }
       wave_sync();
