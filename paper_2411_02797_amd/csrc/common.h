@@ -28,7 +28,7 @@ __host__ __device__ inline uint64_t make_info(uint64_t base, bool store, uint64_
 }
 
 // ---- ingest tiling -------------------------------------------------------------
-constexpr int kIngestThreads = 768;     // 12 waves of 64, each with its own tile loop
+constexpr int kIngestThreads = 1024;    // 16 waves of 64 (4 per SIMD), each with its own tile loop
 constexpr int kWaveEvents = 63;         // max events per wave tile (lane j holds offset j, j <= 63)
 constexpr int kLaneBlocks = 2;          // 16-frame blocks held by each lane of a wave tile
 constexpr int kWaveFrames = 64 * 16 * kLaneBlocks;  // frames of a wave tile

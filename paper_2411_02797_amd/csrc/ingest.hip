@@ -10,14 +10,14 @@
 // their paths are equal frame by frame, which is exactly when the paper's tree
 // insertion would end them on the same node.
 //
-// Work decomposition of the hashing pass: one workgroup of 12 waves per CU,
+// Work decomposition of the hashing pass: one workgroup of 16 waves per CU,
 // persistent.  Every wave owns a contiguous range of events and cuts it into tiles
 // of at most 63 events whose paths, cut into blocks of 16 frames, fill at most 128
 // blocks: lane l holds blocks l and l + 64 (16 consecutive frames of one event each)
 // in registers, loaded with four 16-byte buffer loads per block (the buffer's range
 // check makes reads past the end of the batch return zero).  Consecutive lanes hold
 // consecutive blocks, so a wave's loads cover a contiguous stretch of the batch.
-// Waves need no barriers, so a CU keeps 12 tiles in flight; a wave requests tile
+// Waves need no barriers, so a CU keeps 16 tiles in flight; a wave requests tile
 // t+1's frames once tile t's table and candidate loads have returned.
 //   - hash: a path's hash is a sum over its frames of a term of (frame, position in
 //     the path); a lane sums its block, and the block sums of an event meet in LDS.
@@ -413,14 +413,15 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
       break;  // the call fails; this wave's range cannot be cut further
     }
     const int64_t e_nxt = t.e0 + t.ne;
-    // The three waves that share a SIMD take turns at the highest issue priority, one
+    // The four waves that share a SIMD take turns at the highest issue priority, one
     // tile each: with equal priorities the oldest wave always wins, the youngest falls
     // behind, and the SIMD ends with one wave and nothing to hide its latency behind.
     {
-      const int r = (iter + __builtin_amdgcn_readfirstlane(wave >> 2)) % 3;
+      const int r = (iter + __builtin_amdgcn_readfirstlane(wave >> 2)) & 3;
       if (r == 0) __builtin_amdgcn_s_setprio(0);
       else if (r == 1) __builtin_amdgcn_s_setprio(1);
-      else __builtin_amdgcn_s_setprio(2);
+      else if (r == 2) __builtin_amdgcn_s_setprio(2);
+      else __builtin_amdgcn_s_setprio(3);
     }
     if (t.kind == kTileSlow) {
       slow_wave_tile(a, t.e0, t.ne, o_cur);
