@@ -133,6 +133,14 @@ struct Blk {
   int32_t ev, m, rem, voff;
 };
 
+// This lane's index in the wave, computed afresh (two instructions) where a value kept
+// in a register across the tile loop would be spilled.
+__device__ inline int fresh_lane() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
+
 // Offsets window at event e (lane j holds offsets[e + j], j <= min(63, end - e); 0 past
 // that).  A buffer load whose range ends at the window's last offset: the address lives in
 // scalar registers, and lanes past the range read zero.
@@ -141,15 +149,16 @@ __device__ inline int64_t load_window(const IngestArgs &a, int64_t e, int64_t en
   const int64_t eu = uniform64(e);
   const int bytes = __builtin_amdgcn_readfirstlane((int)(min(uniform64(end) - eu, (int64_t)63) + 1) * 8);
   const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc((void *)(a.off + eu), (short)0, bytes, 0x00020000);
-  const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, lane * 8, 0, 0);
+  const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, fresh_lane() * 8, 0, 0);
   return (int64_t)(((uint64_t)v[1] << 32) | v[0]);
 }
 
 // Validate the window and cut the next tile: as many events as fit in the tile's
 // blocks; map every lane to its blocks.  Every offset is validated here, before any
 // frame is read.
-__device__ inline Tile make_tile(const IngestArgs &a, WaveShared &W, int64_t e, int64_t end, int64_t o, int lane,
+__device__ inline Tile make_tile(const IngestArgs &a, WaveShared &W, int64_t e, int64_t end, int64_t o,
                                  Blk (&b)[kLaneBlocks]) {
+  const int lane = fresh_lane();
   Tile t{};
 #pragma unroll
   for (int q = 0; q < kLaneBlocks; ++q) b[q] = Blk{-1, 0, 0, 0};
@@ -348,7 +357,7 @@ __device__ inline void cache_fill(IngestShared &S, int k, uint32_t len, uint32_t
 // Tiles whose frames exceed a wave's staging capacity: one event at a time, the
 // wave striding over its frames in HBM.
 __device__ __forceinline__ void slow_wave_tile(const IngestArgs &a, int64_t e0, int ne, int64_t o) {
-  const int lane = threadIdx.x & 63;
+  const int lane = fresh_lane();
   for (int j = 0; j < ne; ++j) {
     const int64_t gs = shfl_i64(o, j), len = shfl_i64(o, j + 1) - gs;
     uint64_t acc = 0;
@@ -399,7 +408,7 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
   const int64_t end = (w + 1) * a.n_events / waves_total;
   int64_t o_cur = load_window(a, w * a.n_events / waves_total, end, lane);
   Blk b[kLaneBlocks];
-  Tile t = make_tile(a, W, w * a.n_events / waves_total, end, o_cur, lane, b);
+  Tile t = make_tile(a, W, w * a.n_events / waves_total, end, o_cur, b);
   u32x4 nf[kLaneBlocks][4];
   load_blocks(a, t, b, nf);
   int64_t o_nxt = t.kind == kTileFast || t.kind == kTileSlow ? load_window(a, t.e0 + t.ne, end, lane) : 0;
@@ -426,7 +435,7 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
     if (t.kind == kTileSlow) {
       slow_wave_tile(a, t.e0, t.ne, o_cur);
       o_cur = o_nxt;
-      t = make_tile(a, W, e_nxt, end, o_cur, lane, b);
+      t = make_tile(a, W, e_nxt, end, o_cur, b);
       load_blocks(a, t, b, nf);
       o_nxt = t.kind == kTileFast || t.kind == kTileSlow ? load_window(a, t.e0 + t.ne, end, lane) : 0;
       continue;
@@ -474,7 +483,7 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
     // A3: exact dedup.  Lane j resolves event j: a cached resolution of the same hash
     // and length, else the table; every candidate is verified by the event's blocks.
     // (cross-lane reads with every lane active: a disabled source lane reads as zero)
-    const int64_t o_end = shfl_i64(o_cur, lane + 1 < 64 ? lane + 1 : 63);
+    const int64_t o_end = shfl_i64(o_cur, min(fresh_lane() + 1, 63));
     Probe p{};
     p.state = kResolved;
     // cache entry: claimed (index + kLeader, filled in once resolved) or awaited (index);
@@ -592,7 +601,7 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
     // the next tile's frames, and the offsets window after it, are requested only now:
     // vector-memory loads retire in order, so a table or candidate load issued after
     // them would wait for the whole next tile to arrive
-    const Tile tn = make_tile(a, W, e_nxt, end, o_nxt, lane, b);
+    const Tile tn = make_tile(a, W, e_nxt, end, o_nxt, b);
     load_blocks(a, tn, b, nf);
     const int64_t o_nn = tn.kind == kTileFast || tn.kind == kTileSlow ? load_window(a, tn.e0 + tn.ne, end, lane) : 0;
     {
@@ -600,7 +609,7 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
       const int64_t eu = uniform64(e0);
       const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
           (void *)(a.slot_of + eu), (short)0, __builtin_amdgcn_readfirstlane(ne * 4), 0x00020000);
-      if (lane < ne) __builtin_amdgcn_raw_buffer_store_b32(p.state == kResolved ? p.slot : kNoSlot, r, lane * 4, 0, 0);
+      if (lane < ne) __builtin_amdgcn_raw_buffer_store_b32(p.state == kResolved ? p.slot : kNoSlot, r, fresh_lane() * 4, 0, 0);
     }
     o_cur = o_nxt;
     o_nxt = o_nn;
