@@ -279,17 +279,21 @@ __device__ inline bool block_less_seq(const uint32_t *x, uint32_t nx, const uint
   return nx < ny;
 }
 
-// Bitonic sort of n <= 2048 LDS entries: si holds entry indices, padded with kNone
-// (+inf); lt(p, q) orders two entries.
+// Bitonic sort of n <= 2 blockDim.x LDS entries: si holds entry indices, padded with
+// kNone (+inf); lt(p, q) orders two entries.  Thread t takes pair t of every step; in
+// a step of distance j <= 64 the pairs of wave w lie in entries [128 w, 128 w + 128),
+// so between two such steps a wave waits only for its own LDS writes, and the
+// workgroup meets at a barrier only around steps of longer distance.
 template <class Less>
 __device__ inline void lds_bitonic(uint16_t *si, int n, Less lt) {
   int n2 = 1;
   while (n2 < n) n2 <<= 1;
   for (int i = threadIdx.x; i < n2; i += blockDim.x) si[i] = i < n ? (uint16_t)i : kNone;
   __syncthreads();
+  const int t = threadIdx.x;
   for (int k = 2; k <= n2; k <<= 1) {
     for (int j = k >> 1; j > 0; j >>= 1) {
-      for (int t = threadIdx.x; t < n2 / 2; t += blockDim.x) {
+      if (t < n2 / 2) {
         const int i0 = 2 * j * (t / j) + (t % j), i1 = i0 + j;
         const uint16_t x = si[i0], y = si[i1];
         // ascending where (i0 & k) == 0, else descending: one comparison per pair, its
@@ -298,7 +302,13 @@ __device__ inline void lds_bitonic(uint16_t *si, int n, Less lt) {
         const uint16_t p = asc ? y : x, q = asc ? x : y;
         if (p != kNone && (q == kNone || lt(p, q))) { si[i0] = y; si[i1] = x; }
       }
-      __syncthreads();
+      const int j_next = j > 1 ? j >> 1 : k;  // the next step's distance (k: next stage)
+      if (j <= 64 && j_next <= 64 && !(j == 1 && k == n2)) {
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        __builtin_amdgcn_wave_barrier();
+      } else {
+        __syncthreads();
+      }
     }
   }
 }
