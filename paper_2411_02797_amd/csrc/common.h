@@ -53,19 +53,30 @@ __host__ __device__ inline uint64_t frame_term(uint32_t f, uint32_t k) {
   const uint32_t y = (f ^ kTermXorY) + k * kTermMulY;
   return (uint64_t)x * (uint64_t)(y | 1u);
 }
-// The unique-path table hashes pairs of frames instead: a path is zero-padded to a
-// multiple of 16 frames and pair p = (F[2p], F[2p+1]) contributes
-//   (F[2p] + p*kPairMulX + kPairAddX) * (F[2p+1] + p*kPairMulY + kPairAddY)
+// The unique-path table hashes pairs of frames instead.  A path of len frames is cut
+// into ceil(len / 16) blocks of 16 frames: block m starts at frame 16 m, except that
+// the last block of a path of 16 frames or more ends at the path's end (so it overlaps
+// the block before it when len is not a multiple of 16; a path shorter than 16 frames
+// is one block, zero-padded).  Pair i of block m, (F[s + 2i], F[s + 2i + 1]) with s the
+// block's first frame, is pair p = 8 m + i and contributes
+//   (F[s + 2i] + p*kPairMulX + kPairAddX) * (F[s + 2i + 1] + p*kPairMulY + kPairAddY)
 // (factors wrap at 32 bits; the product and the sum at 64).  Unless its first factor
 // is zero the term is injective in the second frame, both factors move with the
-// position, and it costs one 32 x 32 -> 64-bit multiply-add per two frames.  (A
-// collision costs only time: every table match is verified frame by frame.)
+// position, and it costs one 32 x 32 -> 64-bit multiply-add per two frames; and every
+// block but a short path's single one holds 16 frames of the path, so hashing it needs
+// no mask.  (A collision costs only time: every table match is verified frame by
+// frame.)
 constexpr uint32_t kPairMulX = 0x9E3779B9u, kPairMulY = 0x85EBCA6Bu, kPairAddX = 0x27D4EB2Fu,
                    kPairAddY = 0x165667B1u;
 __host__ __device__ inline uint64_t pair_term(uint32_t f0, uint32_t f1, uint32_t p) {
   const uint32_t x = f0 + p * kPairMulX + kPairAddX;
   const uint32_t y = f1 + p * kPairMulY + kPairAddY;
   return (uint64_t)x * (uint64_t)y;
+}
+// first frame of block m of a path of len frames (as above)
+__host__ __device__ inline int64_t hash_block_start(int64_t m, int64_t len) {
+  const int64_t s = 16 * m;
+  return s + 16 > len && len >= 16 ? len - 16 : s;
 }
 __host__ __device__ inline uint64_t finish_hash(uint64_t s, uint64_t len) {
   uint64_t h = s + len * 0x9E3779B97F4A7C15ull;

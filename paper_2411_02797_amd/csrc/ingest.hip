@@ -126,11 +126,12 @@ struct Tile {
   int32_t span;    // frames of the tile's events
 };
 
-// One of this lane's blocks of a tile: frames [16 m, 16 m + rem) of event ev (ev = -1:
-// no block), at byte offset voff from the tile's first frame.  Lane l holds blocks
+// One of this lane's blocks of a tile: frames [st, st + rem) of event ev (ev = -1: no
+// block), the block of the path hash that starts at frame st (rem = 16 unless the path
+// is shorter), at byte offset voff from the tile's first frame.  Lane l holds blocks
 // l + 64 q, q < kLaneBlocks.
 struct Blk {
-  int32_t ev, m, rem, voff;
+  int32_t ev, st, rem, voff;
 };
 
 // This lane's index in the wave, computed afresh (two instructions) where a value kept
@@ -203,7 +204,10 @@ __device__ inline Tile make_tile(const IngestArgs &a, WaveShared &W, int64_t e, 
     const int ev_len = __shfl((int)len, ev, 64);
     const int ev_start = __shfl(rel, ev, 64);
     const int bi = q * 64 + lane, m = bi - ev_excl;
-    if (bi < nblk && m >= 0 && m * kBlock < ev_len) b[q] = Blk{ev, m, ev_len - m * kBlock, (ev_start + m * kBlock) * 4};
+    if (bi < nblk && m >= 0 && m * kBlock < ev_len) {
+      const int st = (int)hash_block_start(m, ev_len);
+      b[q] = Blk{ev, st, min(kBlock, ev_len - st), (ev_start + st) * 4};
+    }
   }
   return t;
 }
@@ -361,11 +365,10 @@ __device__ __forceinline__ void slow_wave_tile(const IngestArgs &a, int64_t e0, 
   for (int j = 0; j < ne; ++j) {
     const int64_t gs = shfl_i64(o, j), len = shfl_i64(o, j + 1) - gs;
     uint64_t acc = 0;
-    for (int64_t p = lane; 2 * p < len; p += 64) {  // pairs of the zero-padded path (padding pairs added below)
-      const uint32_t f0 = a.fr[gs + 2 * p], f1 = 2 * p + 1 < len ? a.fr[gs + 2 * p + 1] : 0u;
-      acc += pair_term(f0, f1, (uint32_t)p);
+    for (int64_t p = lane; p < 8 * ((len + kBlock - 1) / kBlock); p += 64) {  // (len > kWaveFrames: every block full)
+      const int64_t f = gs + hash_block_start(p >> 3, len) + 2 * (p & 7);
+      acc += pair_term(a.fr[f], a.fr[f + 1], (uint32_t)p);
     }
-    for (int64_t p = (len + 1) / 2 + lane; p < round_store(len) / 2; p += 64) acc += pair_term(0u, 0u, (uint32_t)p);
     acc = wave_sum_u64(acc);
     Probe p{};
     p.h = finish_hash(acc, (uint64_t)len) & a.hash_mask;
@@ -453,27 +456,42 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
 #pragma unroll
     for (int q = 0; q < kLaneBlocks; ++q) cb[q] = b[q];
 
-    // A2: hash.  Each block sums pair_term over its 8 pairs (pair index 8 m + i) with
-    // frames past the path read as zero: the hash covers the zero-padded block.
+    // A2: hash.  Each block sums pair_term over its 8 pairs (pair index 8 m + i, m the
+    // block's index in the path).  Only a path shorter than 16 frames has a block with
+    // frames past its end; they read as zero, and a tile without such a block hashes
+    // without masks.
     {
       uint32_t z = 0;  // made here: a zero kept across the loop would cost two registers
       asm volatile("" : "+v"(z));
       W.hacc[lane] = ((uint64_t)z << 32) | z;
     }
     wave_sync();
+    bool full = true;
+#pragma unroll
+    for (int q = 0; q < kLaneBlocks; ++q) full &= cb[q].ev < 0 || cb[q].rem == kBlock;
+    full = __all(full);
 #pragma unroll
     for (int q = 0; q < kLaneBlocks; ++q) {
       if (cb[q].ev >= 0) {
-        const uint32_t pb = (uint32_t)(cb[q].m * (kBlock / 2));
+        const uint32_t pb = (uint32_t)(((cb[q].st + kBlock - 1) / kBlock) * (kBlock / 2));
         const uint32_t kx = pb * kPairMulX + kPairAddX, ky = pb * kPairMulY + kPairAddY;
         uint64_t acc = 0;
+        if (full) {
 #pragma unroll
-        for (int i = 0; i < kBlock / 2; ++i) {
-          const uint32_t f0 = 2 * i < cb[q].rem ? f[q][2 * i] : 0u;
-          const uint32_t f1 = 2 * i + 1 < cb[q].rem ? f[q][2 * i + 1] : 0u;
-          const uint32_t x = f0 + kx + (uint32_t)i * kPairMulX;
-          const uint32_t y = f1 + ky + (uint32_t)i * kPairMulY;
-          acc += (uint64_t)x * (uint64_t)y;
+          for (int i = 0; i < kBlock / 2; ++i) {
+            const uint32_t x = f[q][2 * i] + kx + (uint32_t)i * kPairMulX;
+            const uint32_t y = f[q][2 * i + 1] + ky + (uint32_t)i * kPairMulY;
+            acc += (uint64_t)x * (uint64_t)y;
+          }
+        } else {
+#pragma unroll
+          for (int i = 0; i < kBlock / 2; ++i) {
+            const uint32_t f0 = 2 * i < cb[q].rem ? f[q][2 * i] : 0u;
+            const uint32_t f1 = 2 * i + 1 < cb[q].rem ? f[q][2 * i + 1] : 0u;
+            const uint32_t x = f0 + kx + (uint32_t)i * kPairMulX;
+            const uint32_t y = f1 + ky + (uint32_t)i * kPairMulY;
+            acc += (uint64_t)x * (uint64_t)y;
+          }
         }
         atomicAdd((unsigned long long *)&W.hacc[cb[q].ev], (unsigned long long)acc);
       }
@@ -557,8 +575,8 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
         for (int q = 0; q < kLaneBlocks; ++q) {
           const uint64_t vp = cb[q].ev >= 0 ? W.vptr[cb[q].ev] : 0;
           chk[q] = vp != 0;
-          narrow |= chk[q] && (int)W.vlim[cb[q].ev] - cb[q].m * kBlock < kBlock;
-          cp[q] = chk[q] ? (gptr)vp + cb[q].m * kBlock : (gptr)g_zero_block;
+          narrow |= chk[q] && (int)W.vlim[cb[q].ev] - cb[q].st < kBlock;
+          cp[q] = chk[q] ? (gptr)vp + cb[q].st : (gptr)g_zero_block;
         }
         if (!__any(narrow)) {
 #pragma unroll
@@ -575,12 +593,17 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
 #pragma unroll
             for (int i = 0; i < kBlock; ++i) c[q][i] = chk[q] && i < cb[q].rem ? cp[q][i] : 0u;
         }
-        // frames inside the path must match
+        // frames inside the path must match (in a tile of full blocks, all 16)
 #pragma unroll
         for (int q = 0; q < kLaneBlocks; ++q) {
           uint32_t d = 0;
+          if (full) {
 #pragma unroll
-          for (int i = 0; i < kBlock; ++i) d |= i < cb[q].rem ? c[q][i] ^ f[q][i] : 0u;
+            for (int i = 0; i < kBlock; ++i) d |= c[q][i] ^ f[q][i];
+          } else {
+#pragma unroll
+            for (int i = 0; i < kBlock; ++i) d |= i < cb[q].rem ? c[q][i] ^ f[q][i] : 0u;
+          }
           if (chk[q] && d != 0) W.bad[cb[q].ev] = 1;
         }
       }
@@ -978,8 +1001,11 @@ __global__ void rehash_kernel(const uint32_t *pframes, const int64_t *pstart, co
   if (id >= d) return;
   const int64_t st = pstart[id];
   const uint32_t len = plen[id];
-  uint64_t acc = 0;  // the stored path is zero-padded to a multiple of 16 frames
-  for (uint32_t p = 0; 2 * p < (uint32_t)round_store(len); ++p) acc += pair_term(pframes[st + 2 * p], pframes[st + 2 * p + 1], p);
+  uint64_t acc = 0;  // (the stored path is zero-padded to a multiple of 16 frames)
+  for (uint32_t p = 0; p < 8 * ((len + 15) / 16); ++p) {
+    const int64_t f = st + hash_block_start(p >> 3, len) + 2 * (p & 7);
+    acc += pair_term(pframes[f], pframes[f + 1], p);
+  }
   const uint64_t h = finish_hash(acc, len) & hash_mask;
   const uint64_t word = (h & 0xFFFFFFFF00000000ull) | (uint64_t)id;
   uint64_t s = h & cap_mask;
