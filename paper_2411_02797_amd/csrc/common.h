@@ -273,7 +273,8 @@ constexpr int kTrieCtrFail = 4;
 // another way).  s2 (may be s): a second stream for the part of the sibling ordering that
 // is independent of the large groups, forked from s with `fork` and joined back into s
 // with `join` (two events of the caller's, unused when s2 is s).
-void launch_trie_sort(const TrieArgs &a, hipStream_t s, hipStream_t s2, hipEvent_t fork, hipEvent_t join);
+void launch_trie_sort(const TrieArgs &a, hipStream_t s, hipStream_t s2, hipEvent_t fork, hipEvent_t mid,
+                      hipEvent_t join);
 void launch_canon(const CanonArgs &a, hipStream_t s);  // lcp, scans, sparse table, emission
 
 struct QueryArgs {

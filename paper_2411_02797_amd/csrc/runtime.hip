@@ -651,7 +651,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   // ---- publish new paths, fold this call's sums into the old ones -----------------------
   // events that order the side stream's fold after the publish, and the emission after
   // the fold: created before anything is published
-  Event published_ev, folded, trie_fork, trie_join;
+  Event published_ev, folded, trie_fork, trie_mid, trie_join;
   if (N > 0 && side != s && (!published_ev.ev || !folded.ev)) return undo(fail(CCT_EDEVICE, "event creation failed"));
   AGG_TRY(hipMemsetAsync(cursor.p, 0, 64, s));
   if (n_new) {
@@ -717,7 +717,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   for (int mode = incremental ? 3 : (use_trie ? 0 : (ca.exact ? 2 : 1));;) {
     CanonArgs run = ca;
     run.exact = mode == 2 ? 1 : 0;
-    if (mode == 0) launch_trie_sort(ta, s, side, trie_fork.ev, trie_join.ev);
+    if (mode == 0) launch_trie_sort(ta, s, side, trie_fork.ev, trie_mid.ev, trie_join.ev);
     else if (mode == 3) launch_merge_order(run, t->order.as<uint32_t>(), t->d, merge_scratch.as<uint32_t>(), s);
     else launch_sort(run, s);
     tm.mark(4, s);

@@ -400,22 +400,24 @@ __global__ __launch_bounds__(kChunkThreads) void chunk_kernel(TrieArgs a) {
 __global__ __launch_bounds__(kMedThreads) void medium_kernel(TrieArgs a, int list) {
   __shared__ MedShared S;
   const uint64_t ng = min((uint64_t)a.ctr[list], (uint64_t)a.list_cap);
+  // a bucket of a large group has its members in grouped2 (see rscatter_kernel)
+  const uint32_t *src = list == kListMediumBucket ? a.grouped2 : a.grouped;
   for (uint64_t g = blockIdx.x; g < ng; g += gridDim.x) {
     const uint64_t e = a.lists[list * a.list_cap + g];
     const uint32_t start = (uint32_t)(e >> 32), n = (uint32_t)e;
     for (uint32_t i = threadIdx.x; i < n; i += kMedThreads) {
       u32x4 v[4];
       uint32_t nf;
-      node_block(a, a.grouped[start + i], v, nf);
+      node_block(a, src[start + i], v, nf);
 #pragma unroll
       for (int c = 0; c < 4; ++c) *(u32x4 *)&S.sb[i][4 * c] = v[c];
       S.sn[i] = (uint8_t)nf;
     }
     __syncthreads();
     lds_bitonic(S.si, (int)n, [&](uint16_t p, uint16_t q) { return block_less(S.sb[p], S.sn[p], S.sb[q], S.sn[q]); });
-    // grouped[start + i] still holds the unsorted members (read before any write)
+    // src[start + i] still holds the unsorted members (read before any write)
     uint32_t Xs[kMedium / kMedThreads];
-    for (uint32_t i = threadIdx.x, q = 0; i < n; i += kMedThreads, ++q) Xs[q] = a.grouped[start + S.si[i]];
+    for (uint32_t i = threadIdx.x, q = 0; i < n; i += kMedThreads, ++q) Xs[q] = src[start + S.si[i]];
     __syncthreads();
     for (uint32_t i = threadIdx.x, q = 0; i < n; i += kMedThreads, ++q) {
       a.grouped[start + i] = Xs[q];
@@ -527,13 +529,15 @@ __global__ __launch_bounds__(kMedThreads) void classify_kernel(TrieArgs a) {
   atomicAdd(&a.bcnt[g * kMaxBuckets + blo], 1u);
 }
 
-// Large groups reordered by bucket, in three grid-wide steps (a large group has
+// Large groups reordered by bucket, in two grid-wide steps (a large group has
 // thousands of members):
 //  - bstart_kernel, one small workgroup per large group: bucket starts (exclusive
 //    prefix sums of the bucket sizes, into spl, whose splitters are no longer needed),
-//    the buckets listed for sorting, and the sizes reset to serve as cursors;
-//  - rscatter_kernel, every member: its bucket's start + a cursor atomic, into grouped2;
-//  - rcopy_kernel, every member: back into grouped, with its position.
+//    every non-empty bucket listed for sorting, and the sizes reset to serve as cursors;
+//  - rscatter_kernel, every member: its bucket's start + a cursor atomic, into grouped2.
+// The kernels that order the buckets read their members from grouped2 and write the
+// final positions into grouped (a member still being read from grouped by rscatter
+// cannot be overwritten there).
 __global__ __launch_bounds__(kMaxBuckets) void bstart_kernel(TrieArgs a) {
   __shared__ uint32_t wsum[kMaxBuckets / 64];
   const uint64_t ng = min((uint64_t)a.ctr[kListLarge], (uint64_t)a.large_cap);
@@ -557,7 +561,7 @@ __global__ __launch_bounds__(kMaxBuckets) void bstart_kernel(TrieArgs a) {
   if (j >= nb) return;
   a.spl[g * kMaxBuckets + j] = bs;
   a.bcnt[g * kMaxBuckets + j] = 0;
-  if (c < 2) return;
+  if (c == 0) return;  // (a bucket of one is listed too: its member's position is written by bucket_kernel)
   if (c > (uint32_t)kMedium) { fail(a); return; }
   const int cls = c <= 64 ? kListSmall : kListMediumBucket;
   const unsigned long long i = atomicAdd(&a.ctr[cls], 1ull);
@@ -584,16 +588,8 @@ __global__ void rscatter_kernel(TrieArgs a) {
   a.grouped2[dst] = X;
 }
 
-__global__ void rcopy_kernel(TrieArgs a) {
-  const uint64_t p = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (p >= a.gstart[a.cap + 1]) return;
-  if (large_group_of(a, a.grouped[p]) < 0) return;
-  const uint32_t X = a.grouped2[p];
-  a.grouped[p] = X;
-  a.posof[X] = (uint32_t)p;
-}
-
-// buckets of up to 64: one wave each, every member counts the members before it
+// buckets of 1 .. 64 of large groups (members in grouped2): one wave each, every member
+// counts the members before it
 constexpr int kBucketWaves = 4;
 __global__ __launch_bounds__(64 * kBucketWaves) void bucket_kernel(TrieArgs a) {
   __shared__ uint32_t sb[kBucketWaves][64][kBlk];
@@ -605,7 +601,7 @@ __global__ __launch_bounds__(64 * kBucketWaves) void bucket_kernel(TrieArgs a) {
     const uint32_t start = (uint32_t)(e >> 32), n = (uint32_t)e;
     uint32_t X = 0;
     if (lane < (int)n) {
-      X = a.grouped[start + lane];
+      X = a.grouped2[start + lane];
       u32x4 v[4];
       uint32_t nf;
       node_block(a, X, v, nf);
@@ -663,7 +659,8 @@ inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1)
 
 }  // namespace
 
-void launch_trie_sort(const TrieArgs &a, hipStream_t s, hipStream_t s2, hipEvent_t fork, hipEvent_t join) {
+void launch_trie_sort(const TrieArgs &a, hipStream_t s, hipStream_t s2, hipEvent_t fork, hipEvent_t mid,
+                      hipEvent_t join) {
   if (a.d <= 0) return;
   const bool two = s2 != s && fork && join;
   hipLaunchKernelGGL(clear_kernel, dim3(blocks_for((int64_t)a.cap + 1, 256)), dim3(256), 0, s, a);
@@ -687,8 +684,11 @@ void launch_trie_sort(const TrieArgs &a, hipStream_t s, hipStream_t s2, hipEvent
     hipLaunchKernelGGL(classify_kernel, dim3(blocks_for(a.nblocks, kChunk)), dim3(kMedThreads), 0, s, a);
     hipLaunchKernelGGL(bstart_kernel, dim3((unsigned)a.large_cap), dim3(kMaxBuckets), 0, s, a);
     hipLaunchKernelGGL(rscatter_kernel, dim3(blocks_for(a.nblocks, 256)), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(rcopy_kernel, dim3(blocks_for(a.nblocks, 256)), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(bucket_kernel, dim3(1024), dim3(64 * kBucketWaves), 0, s, a);
+    // the buckets of up to 64 and the larger ones are disjoint: the small ones follow the
+    // side branch once the scatter is done
+    hipStream_t sb = s;
+    if (sa != s && mid && hipEventRecord(mid, s) == hipSuccess && hipStreamWaitEvent(sa, mid, 0) == hipSuccess) sb = sa;
+    hipLaunchKernelGGL(bucket_kernel, dim3(1024), dim3(64 * kBucketWaves), 0, sb, a);
     hipLaunchKernelGGL(medium_kernel, dim3(256), dim3(kMedThreads), 0, s, a, (int)kListMediumBucket);
     if (sa != s && (hipEventRecord(join, sa) != hipSuccess || hipStreamWaitEvent(s, join, 0) != hipSuccess)) {
       // the side branch cannot be joined: wait for it from the host before going on
