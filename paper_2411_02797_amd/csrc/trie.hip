@@ -540,6 +540,8 @@ __global__ __launch_bounds__(kMedThreads) void classify_kernel(TrieArgs a) {
 // cannot be overwritten there).
 __global__ __launch_bounds__(kMaxBuckets) void bstart_kernel(TrieArgs a) {
   __shared__ uint32_t wsum[kMaxBuckets / 64];
+  __shared__ uint32_t wlist[2][kMaxBuckets / 64];  // per wave: its buckets' offset in each list
+  __shared__ unsigned long long lbase[2];
   const uint64_t ng = min((uint64_t)a.ctr[kListLarge], (uint64_t)a.large_cap);
   const uint64_t g = blockIdx.x;
   if (g >= ng) return;
@@ -554,6 +556,24 @@ __global__ __launch_bounds__(kMaxBuckets) void bstart_kernel(TrieArgs a) {
     if (lane >= o) x += y;
   }
   if (lane == 63) wsum[w] = x;
+  // every non-empty bucket is listed (a bucket of one too: its member's position is
+  // written by bucket_kernel), the small ones and the medium ones in lists of their own;
+  // the workgroup reserves its entries in each list with one atomic (every large group
+  // appends up to 256 buckets at the same time)
+  const bool small = j < nb && c >= 1 && c <= 64, medium = j < nb && c > 64 && c <= (uint32_t)kMedium;
+  const uint64_t ms = __ballot(small), mm = __ballot(medium);
+  if (lane == 0) { wlist[0][w] = (uint32_t)__popcll(ms); wlist[1][w] = (uint32_t)__popcll(mm); }
+  __syncthreads();
+  if (j == 0) {
+    uint32_t ts = 0, tm = 0;
+    for (int q = 0; q < kMaxBuckets / 64; ++q) {
+      const uint32_t cs = wlist[0][q], cm = wlist[1][q];
+      wlist[0][q] = ts; wlist[1][q] = tm;
+      ts += cs; tm += cm;
+    }
+    lbase[0] = ts ? atomicAdd(&a.ctr[kListSmall], (unsigned long long)ts) : 0;
+    lbase[1] = tm ? atomicAdd(&a.ctr[kListMediumBucket], (unsigned long long)tm) : 0;
+  }
   __syncthreads();
   uint32_t before = 0;
   for (int q = 0; q < w; ++q) before += wsum[q];
@@ -561,11 +581,13 @@ __global__ __launch_bounds__(kMaxBuckets) void bstart_kernel(TrieArgs a) {
   if (j >= nb) return;
   a.spl[g * kMaxBuckets + j] = bs;
   a.bcnt[g * kMaxBuckets + j] = 0;
-  if (c == 0) return;  // (a bucket of one is listed too: its member's position is written by bucket_kernel)
   if (c > (uint32_t)kMedium) { fail(a); return; }
-  const int cls = c <= 64 ? kListSmall : kListMediumBucket;
-  const unsigned long long i = atomicAdd(&a.ctr[cls], 1ull);
-  if ((int64_t)i < a.list_cap) a.lists[cls * a.list_cap + i] = ((uint64_t)(start + bs) << 32) | c;
+  if (!small && !medium) return;
+  const int cls = small ? 0 : 1;
+  const uint64_t below = (small ? ms : mm) & ((1ull << lane) - 1);
+  const unsigned long long i = lbase[cls] + wlist[cls][w] + (unsigned long long)__popcll(below);
+  const int list = small ? kListSmall : kListMediumBucket;
+  if ((int64_t)i < a.list_cap) a.lists[list * a.list_cap + i] = ((uint64_t)(start + bs) << 32) | c;
   else fail(a);
 }
 
