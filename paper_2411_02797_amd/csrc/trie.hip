@@ -689,7 +689,7 @@ void launch_trie_sort(const TrieArgs &a, hipStream_t s, hipStream_t s2, hipEvent
   hipLaunchKernelGGL(fill_kernel, dim3(blocks_for(a.d, 256)), dim3(256), 0, s, a);
   if (a.nblocks > 0) {
     hipLaunchKernelGGL(insert_kernel, dim3(blocks_for(a.nblocks, 256)), dim3(256), 0, s, a);
-    const int64_t link_grid = std::max<int64_t>(1, std::min<int64_t>(blocks_for(a.nblocks, 1024), 1024));
+    const int64_t link_grid = std::max<int64_t>(1, std::min<int64_t>(blocks_for(a.nblocks, 1024), 512));
     hipLaunchKernelGGL(link_kernel, dim3((unsigned)link_grid), dim3(kLinkThreads), 0, s, a);
     launch_scan(a.hist, (int64_t)a.cap + 1, 1, a.scan_blk, a.gstart, s);
     hipLaunchKernelGGL(scatter_kernel, dim3(blocks_for((int64_t)a.cap, 256)), dim3(256), 0, s, a);
