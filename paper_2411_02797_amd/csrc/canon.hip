@@ -167,17 +167,41 @@ __global__ __launch_bounds__(256) void merge_pass_kernel(CanonArgs a, const uint
 }
 
 // A merge's new paths: gap[j] = number of old paths (in their sorted order) below
-// new path d_old + j, by binary search.
+// new path d_old + j.  Sixteen lanes search for one new path: each step compares it with
+// 16 old paths that cut the remaining range into 17 parts (a 17-ary search), so the
+// answer takes about log_17(d_old) rounds of path comparisons instead of log_2(d_old)
+// (each comparison is a chain of dependent loads).
+constexpr int kGapLanes = 16;
 __global__ __launch_bounds__(256) void gap_kernel(CanonArgs a, const uint32_t *old_order, int64_t d_old, uint32_t *gap) {
-  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (j >= a.d - d_old) return;
-  const uint32_t x = (uint32_t)(d_old + j);
-  int64_t lo = 0, hi = d_old;
-  while (lo < hi) {
-    const int64_t mid = (lo + hi) >> 1;
-    if (path_less(a, old_order[mid], x)) lo = mid + 1; else hi = mid;
+  const int lane = threadIdx.x & 63, g = lane % kGapLanes, g0 = lane - g;
+  const int64_t j = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kGapLanes;
+  const bool active = j < a.d - d_old;
+  const uint32_t x = (uint32_t)(d_old + (active ? j : 0));
+  // old_order[0, lo) are below x, old_order[hi, d_old) are not
+  int64_t lo = 0, hi = active ? d_old : 0;
+  for (;;) {
+    const int64_t n = hi - lo;
+    if (!__any(n > 0)) break;
+    // pivot of this lane: every position when the range is at most 16 long, else the
+    // 16 cuts into 17 parts (distinct and increasing for n >= 17)
+    const int64_t pv = n <= kGapLanes ? lo + g : lo + (n * (g + 1)) / (kGapLanes + 1);
+    const bool below = n > 0 && pv < hi && path_less(a, old_order[pv], x);
+    const uint32_t m = (uint32_t)(__ballot(below) >> g0) & ((1u << kGapLanes) - 1);
+    const int c = __popc(m);  // the pivots below x are a prefix (the old order is sorted)
+    const int64_t p_lo = __shfl((long long)pv, g0 + (c > 0 ? c - 1 : 0), 64);
+    const int64_t p_hi = __shfl((long long)pv, g0 + (c < kGapLanes ? c : kGapLanes - 1), 64);
+    if (n > 0) {
+      if (n <= kGapLanes) {
+        lo += c;
+        hi = lo;
+      } else {
+        const int64_t nlo = c > 0 ? p_lo + 1 : lo, nhi = c < kGapLanes ? p_hi : hi;
+        lo = nlo;
+        hi = nhi;
+      }
+    }
   }
-  gap[j] = (uint32_t)lo;
+  if (active && g == 0) gap[j] = (uint32_t)lo;
 }
 
 // Placement: the r-th new path (sorted by gap, then path) goes after its gap's old
@@ -568,7 +592,7 @@ void launch_merge_order(CanonArgs &a, const uint32_t *old_order, int64_t d_old, 
   const uint32_t *B = nullptr;
   uint32_t *dst = a.order;
   if (n_new > 0) {
-    hipLaunchKernelGGL(gap_kernel, dim3(blocks_for(n_new, 256)), dim3(256), 0, s, a, old_order, d_old, gap);
+    hipLaunchKernelGGL(gap_kernel, dim3(blocks_for(n_new * kGapLanes, 256)), dim3(256), 0, s, a, old_order, d_old, gap);
     CanonArgs r = a;
     r.d = n_new;
     r.id0 = d_old;
