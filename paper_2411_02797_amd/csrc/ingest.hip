@@ -19,10 +19,10 @@
 // consecutive blocks, so a wave's loads cover a contiguous stretch of the batch.
 // Waves need no barriers, so a CU keeps 16 tiles in flight; a wave requests tile
 // t+1's frames once tile t's table and candidate loads have returned.
-//   - hash: a path's hash is a sum over its frames of a term of (frame, position in
-//     the path); a lane sums its block, and the block sums of an event meet in LDS.
-//     A block knows its position in the path, so no lane ever looks for an event
-//     boundary.
+//   - hash: a path's hash is a sum over its 16-frame blocks of terms of (pair of
+//     frames, position in the path) (the last block of a path ends at the path's end);
+//     a lane sums its block, and the block sums of an event meet in LDS.  A block
+//     knows its position in the path, so no lane ever looks for an event boundary.
 //   - dedup: lane j resolves event j: a path with the same hash and length already
 //     resolved in this workgroup (LDS cache), else the table (linear probing over
 //     16-byte slots that carry the candidate's location, so one round trip; one
