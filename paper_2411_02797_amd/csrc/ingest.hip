@@ -71,10 +71,9 @@ struct WaveShared {
 // claimed entry meanwhile wait for it instead of probing the table themselves, so a path
 // costs one table probe per workgroup however many of its events arrive together.
 struct IngestShared {
-  uint64_t ckey[kCacheEntries];    // hash (0: empty / not cacheable)
+  alignas(16) uint64_t ckey[kCacheEntries];  // hash (0: empty / not cacheable)
   uint64_t cbase[kCacheEntries];   // first frame (kInStore: in the path store)
-  uint32_t clen[kCacheEntries];
-  uint32_t cslot[kCacheEntries];   // kNotReady until the entry is filled in
+  uint64_t cinfo[kCacheEntries];   // slot (low word; kNotReady until filled in), length (high)
   WaveShared wv[kWaves];
 };
 
@@ -327,25 +326,37 @@ __device__ __forceinline__ void probe(const IngestArgs &a, Probe &p, int64_t ev,
   }
 }
 
-// Look (hash, length) up in the cache.  Returns the entry index plus kLeader when
-// this lane claimed a fresh entry (it resolves the path and fills the entry in), the
-// entry index alone when an entry for the key exists (ready, or claimed and pending: the
-// caller waits), or -1 when the key is not cacheable (hash 0, or its probe window holds
-// no free entry and no entry for the key).
+// Look (hash, length) up in the cache.  The entries form aligned buckets of 8; a key
+// lives in the bucket its hash names.  The bucket's 8 keys are read at once (four
+// 16-byte LDS reads), so a lookup costs one LDS round trip plus one per entry it has to
+// read or claim, instead of a chain of dependent reads along a probe sequence.
+// Returns the entry index plus kLeader when this lane claimed a fresh entry (it resolves
+// the path and fills the entry in), the entry index alone when an entry for the key
+// exists (ready, or claimed and pending: the caller waits), or -1 when the key is not
+// cacheable (hash 0, or its bucket holds no free entry and no entry for the key).
 __device__ inline int cache_lookup(IngestShared &S, uint64_t h, uint32_t len) {
   if (h == 0) return -1;
-  uint32_t k = (uint32_t)h & (uint32_t)(kCacheEntries - 1);
-  for (int t = 0; t < 8; ++t) {
-    uint64_t key = S.ckey[k];
-    if (key == 0) {
-      key = atomicCAS((unsigned long long *)&S.ckey[k], 0ull, (unsigned long long)h);
-      if (key == 0) return (int)k | kLeader;
+  typedef unsigned long long u64x2 __attribute__((ext_vector_type(2)));
+  const int b0 = (int)((uint32_t)h & (uint32_t)(kCacheEntries / 8 - 1)) * 8;
+  const u64x2 *kp = (const u64x2 *)&S.ckey[b0];
+  uint32_t empty = 0, match = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const u64x2 v = kp[j];
+    empty |= (v[0] == 0 ? 1u : 0u) << (2 * j) | (v[1] == 0 ? 1u : 0u) << (2 * j + 1);
+    match |= (v[0] == h ? 1u : 0u) << (2 * j) | (v[1] == h ? 1u : 0u) << (2 * j + 1);
+  }
+  // entries are only ever filled in: a key seen is final, an empty one may have been taken
+  for (uint32_t c = empty | match; c != 0; c &= c - 1) {
+    const int t = __builtin_ctz(c), k = b0 + t;
+    if ((empty >> t) & 1) {
+      const uint64_t key = atomicCAS((unsigned long long *)&S.ckey[k], 0ull, (unsigned long long)h);
+      if (key == 0) return k | kLeader;
+      if (key != h) continue;
     }
-    if (key == h) {
-      const uint32_t cs = S.cslot[k];
-      if (cs == kNotReady || (cs != kNoEntry && S.clen[k] == len)) return (int)k;
-    }
-    k = (k + 1) & (uint32_t)(kCacheEntries - 1);
+    const uint64_t ci = S.cinfo[k];
+    const uint32_t cs = (uint32_t)ci;
+    if (cs == kNotReady || (cs != kNoEntry && (uint32_t)(ci >> 32) == len)) return k;
   }
   return -1;
 }
@@ -353,9 +364,8 @@ __device__ inline int cache_lookup(IngestShared &S, uint64_t h, uint32_t len) {
 // Fill in a claimed entry: payload first, then the slot that marks it ready.
 __device__ inline void cache_fill(IngestShared &S, int k, uint32_t len, uint32_t slot, uint64_t cbase) {
   S.cbase[k] = cbase;
-  S.clen[k] = len;
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-  S.cslot[k] = slot;
+  S.cinfo[k] = ((uint64_t)len << 32) | slot;
 }
 
 // Tiles whose frames exceed a wave's staging capacity: one event at a time, the
@@ -402,7 +412,7 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
   __shared__ IngestShared S;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   WaveShared &W = S.wv[wave];
-  for (int i = tid; i < kCacheEntries; i += kIngestThreads) { S.ckey[i] = 0; S.cslot[i] = kNotReady; }
+  for (int i = tid; i < kCacheEntries; i += kIngestThreads) { S.ckey[i] = 0; S.cinfo[i] = kNotReady; }
   __syncthreads();
 
   // this wave's events.  Pipeline: the offsets window of tile t+1 is loaded during
@@ -523,9 +533,10 @@ __global__ __launch_bounds__(kIngestThreads) void ingest_kernel(IngestArgs a) {
         ce = -1;
       }
       if (p.state == kWaiting) {
-        const uint32_t cs = S.cslot[ce];
+        const uint64_t ci = S.cinfo[ce];
+        const uint32_t cs = (uint32_t)ci;
         if (cs != kNotReady) {
-          if (cs != kNoEntry && S.clen[ce] == p.len) {
+          if (cs != kNoEntry && (uint32_t)(ci >> 32) == p.len) {
             p.slot = cs;
             p.cbase = S.cbase[ce];
             p.state = p.len == 0 ? kResolved : kCandidate;
