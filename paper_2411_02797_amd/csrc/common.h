@@ -242,7 +242,7 @@ struct TrieArgs {
   const uint32_t *plen;
   uint64_t *tkey;              // [cap] node keys (0: empty)
   uint64_t *tinfo;             // [cap] (representative block << 32) | depth
-  uint32_t *pblk;              // [nblocks] path of each store block
+  uint64_t *bpos;              // [nblocks] (path length << 32) | index of the block in its path
   uint32_t *occ;               // [nblocks] node of each store block
   uint32_t *nparent;           // [cap] parent node (cap: the root)
   uint32_t *ncount;            // [cap] distinct paths through the node

@@ -48,16 +48,16 @@ __device__ inline void wave_sync() {
   __builtin_amdgcn_wave_barrier();
 }
 
-// block s of the store (frames [16 s, 16 s + 16)): its path d, index k in the path,
-// depth (prefix length at its end) and the path's length
+// block s of the store (frames [16 s, 16 s + 16)): its index k in its path, depth
+// (prefix length at its end) and the path's length, from one word per block
 struct BlockPos {
-  uint32_t d, k, depth, len;
+  uint32_t k, depth, len;
 };
 __device__ inline BlockPos block_pos(const TrieArgs &a, int64_t s) {
+  const uint64_t w = a.bpos[s];
   BlockPos b;
-  b.d = a.pblk[s];
-  b.k = (uint32_t)(s - a.pstart[b.d] / kBlk);
-  b.len = a.plen[b.d];
+  b.k = (uint32_t)w;
+  b.len = (uint32_t)(w >> 32);
   b.depth = min((b.k + 1) * (uint32_t)kBlk, b.len);
   return b;
 }
@@ -86,7 +86,7 @@ __global__ void fill_kernel(TrieArgs a) {
     return;
   }
   const int64_t b0 = a.pstart[d] / kBlk, nb = (len + kBlk - 1) / kBlk;
-  for (int64_t k = 0; k < nb; ++k) a.pblk[b0 + k] = (uint32_t)d;
+  for (int64_t k = 0; k < nb; ++k) a.bpos[b0 + k] = ((uint64_t)len << 32) | (uint64_t)k;
 }
 
 // Node of every block: open addressing on the prefix hash (claimed by CAS).
@@ -163,11 +163,12 @@ __global__ __launch_bounds__(kLinkThreads) void link_kernel(TrieArgs a) {
       a.nparent[X] = P;
       if (!to_root) a.cidx[X] = (uint32_t)atomicAdd((unsigned long long *)&a.hist[P], 1ull);
     } else {
+      // a block's index in its path follows from its depth (16 k < depth <= 16 (k + 1)),
+      // so the representative, of the same depth, has this block's index
       bool ok = (uint32_t)info == b.depth && rep < a.nblocks;
       if (ok) {
-        const BlockPos r = block_pos(a, rep);
-        const uint32_t RP = r.k ? a.occ[rep - 1] : (uint32_t)a.cap;
-        ok = RP == P && r.k == b.k;
+        const uint32_t RP = b.k ? a.occ[rep - 1] : (uint32_t)a.cap;
+        ok = RP == P;
         if (ok) {
           const u32x4 *x = (const u32x4 *)(a.pframes + s * kBlk), *y = (const u32x4 *)(a.pframes + rep * kBlk);
           const uint32_t nf = b.depth - b.k * kBlk;
@@ -265,6 +266,14 @@ __device__ inline bool block_less(const uint32_t *x, uint32_t nx, const uint32_t
   return nx < ny;
 }
 
+// A block's first two frames as one key.  Keys that differ order two blocks as
+// block_less does: frame 0 decides if it differs; else frame 1 if both blocks have it;
+// else one block has a single frame, its key's low word is the zero past its end, and
+// the other block's frame 1 is then nonzero, so the key puts the shorter block first, as
+// the length rule does.  Equal keys need the full comparison.  Keys live in an array of
+// their own: a row's first word would put every key in one of two LDS banks.
+__device__ inline uint64_t block_key(const u32x4 &v0) { return ((uint64_t)v0[0] << 32) | v0[1]; }
+
 // the same order, for a block held in registers (y) against an LDS row (x)
 __device__ inline bool block_less_seq(const uint32_t *x, uint32_t nx, const uint32_t *y, uint32_t ny) {
   const uint32_t n = min(nx, ny);
@@ -316,6 +325,7 @@ __device__ inline void lds_bitonic(uint16_t *si, int n, Less lt) {
 constexpr int kMedThreads = 1024;
 struct MedShared {
   uint32_t sb[kMedium][kBlk];
+  uint64_t sk[kMedium];  // block keys (the splitter sample sort)
   uint8_t sn[kMedium];
   uint16_t si[kMedium];
 };
@@ -453,10 +463,15 @@ __global__ __launch_bounds__(kMedThreads) void split_kernel(TrieArgs a) {
       node_block(a, X, v, nf);
 #pragma unroll
       for (int c = 0; c < 4; ++c) *(u32x4 *)&S.sb[i][4 * c] = v[c];
+      S.sk[i] = block_key(v[0]);
       S.sn[i] = (uint8_t)nf;
     }
     __syncthreads();
-    lds_bitonic(S.si, ns, [&](uint16_t p, uint16_t q) { return block_less(S.sb[p], S.sn[p], S.sb[q], S.sn[q]); });
+    // a sample spread over a large group rarely shares its first two frames: keys first
+    lds_bitonic(S.si, ns, [&](uint16_t p, uint16_t q) {
+      const uint64_t kp = S.sk[p], kq = S.sk[q];
+      return kp != kq ? kp < kq : block_less(S.sb[p], S.sn[p], S.sb[q], S.sn[q]);
+    });
     // splitter j (j = 0 .. nb - 2) is the sample at sorted position (j + 1) * kOversample
     for (int j = threadIdx.x; j < nb - 1; j += kMedThreads)
       a.spl[g * kMaxBuckets + j] = a.grouped[start + (uint64_t)S.si[(j + 1) * kOversample] * n / ns];
