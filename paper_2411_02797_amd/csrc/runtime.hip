@@ -431,6 +431,22 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   }
   Buf delta, slot_of, cpart, agg_count, agg_keys, agg_sums, nlen, nsrc;
   uint64_t new_frames = 0, new_store = 0;
+  // The metric sums run on a second stream of the library, from the moment the ingest's
+  // slot ids are complete: they overlap the host's reading of the counters, the publish
+  // and the ordering.  Per-workgroup LDS maps, flushed through staging buckets of slots;
+  // two workgroups per CU (run one after the other) halve the distinct slots each map
+  // must hold, so fewer events overflow into device atomics.  (A test setting keeps
+  // everything on the caller's stream, the path taken when no second stream can be
+  // created.)
+  SideGuard side_guard;
+  Event slots_ready;
+  AggStage stg{};
+  const int agg_grid = (int)std::max<int64_t>(1, std::min<int64_t>((N + 8191) / 8192, (int64_t)cu_count() * 2));
+  if (N > 0) {
+    hipStream_t ss = env_int("CCT_TEST_ONE_STREAM", 0) ? nullptr : side_guard.acquire();
+    if (ss) side = ss;
+    if (side != s && !slots_ready.ev) return fail(CCT_EDEVICE, "event creation failed");
+  }
   if (N > 0) {
     if (!slot_of.alloc((size_t)N * 4)) return fail(CCT_ENOMEM, "device allocation failed");
     for (int attempt = 0;; ++attempt) {
@@ -459,10 +475,22 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
                          nlen.as<uint64_t>(), dctr, cpart.as<unsigned long long>(), s);
       claimed = true;  // (from the launch on: the table may hold this call's claims)
       AGG_TRY(hipGetLastError());
+      {
+        cct_status sst = setup_stage(m, t->cap, agg_grid, agg_count, agg_keys, agg_sums, stg, side);
+        if (sst) return undo(sst);
+        if (side != s) {
+          AGG_TRY(hipEventRecord(slots_ready.ev, s));
+          AGG_TRY(hipStreamWaitEvent(side, slots_ready.ev, 0));
+        }
+        launch_aggregate(slot_of.as<uint32_t>(), p->metrics, N, m, delta.as<uint64_t>(), t->cap, agg_grid, stg, side);
+        AGG_TRY(hipGetLastError());
+      }
       AGG_TRY(hipMemcpyAsync(hs, dctr, kCtrCount * 8, hipMemcpyDeviceToHost, s));
       AGG_TRY(hipStreamSynchronize(s));
       if (hs[kCtrError]) return undo(fail(CCT_EINVAL, "malformed offsets"));
       if (hs[kCtrOverflow]) {
+        // the sums of this attempt are discarded: their buffers are reused once idle
+        if (side != s) AGG_TRY(hipStreamSynchronize(side));
         // a larger table holding only the tree's paths; the old one, with this call's
         // claims, is discarded once rehash has synchronised the stream
         cct_status st = rehash(t, t->cap * 4, hash_mask, s);
@@ -476,25 +504,6 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
       new_store = hs[kCtrNewFrames];
       break;
     }
-  }
-
-  // ---- metric sums on the side stream, overlapping the publish and the ordering: the
-  // host has synchronised the caller's stream, so the ingest's slot ids are complete.
-  // Per-workgroup LDS maps, flushed through staging buckets of slots; two workgroups per
-  // CU (run one after the other) halve the distinct slots each map must hold, so fewer
-  // events overflow into device atomics.
-  SideGuard side_guard;
-  if (N > 0) {
-    // (a test setting keeps everything on the caller's stream, the path taken when no
-    // second stream can be created)
-    hipStream_t ss = env_int("CCT_TEST_ONE_STREAM", 0) ? nullptr : side_guard.acquire();
-    if (ss) side = ss;
-    const int agg_grid = (int)std::max<int64_t>(1, std::min<int64_t>((N + 8191) / 8192, (int64_t)cu_count() * 2));
-    AggStage stg{};
-    cct_status sst = setup_stage(m, t->cap, agg_grid, agg_count, agg_keys, agg_sums, stg, side);
-    if (sst) return undo(sst);
-    launch_aggregate(slot_of.as<uint32_t>(), p->metrics, N, m, delta.as<uint64_t>(), t->cap, agg_grid, stg, side);
-    AGG_TRY(hipGetLastError());
   }
 
   // ---- allocate everything the rest of the call needs (rollback possible until here)
