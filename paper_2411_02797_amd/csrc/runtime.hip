@@ -476,12 +476,13 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
       claimed = true;  // (from the launch on: the table may hold this call's claims)
       AGG_TRY(hipGetLastError());
       {
-        cct_status sst = setup_stage(m, t->cap, agg_grid, agg_count, agg_keys, agg_sums, stg, side);
-        if (sst) return undo(sst);
+        // (the side stream's work, the staging's zeroing included, starts after the collection)
         if (side != s) {
           AGG_TRY(hipEventRecord(slots_ready.ev, s));
           AGG_TRY(hipStreamWaitEvent(side, slots_ready.ev, 0));
         }
+        cct_status sst = setup_stage(m, t->cap, agg_grid, agg_count, agg_keys, agg_sums, stg, side);
+        if (sst) return undo(sst);
         launch_aggregate(slot_of.as<uint32_t>(), p->metrics, N, m, delta.as<uint64_t>(), t->cap, agg_grid, stg, side);
         AGG_TRY(hipGetLastError());
       }
