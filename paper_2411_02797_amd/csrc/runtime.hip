@@ -200,6 +200,21 @@ struct SideGuard {
   }
 };
 
+// Wait for the work queued on s so far by polling an event (the host spins; a blocking
+// wait adds its wake-up latency to the call's critical path).
+hipError_t spin_sync(hipStream_t s) {
+  hipEvent_t e = nullptr;
+  hipError_t r = hipEventCreateWithFlags(&e, hipEventDisableTiming);
+  if (r != hipSuccess) return hipStreamSynchronize(s);
+  r = hipEventRecord(e, s);
+  if (r == hipSuccess) {
+    while ((r = hipEventQuery(e)) == hipErrorNotReady) {
+    }
+  }
+  (void)hipEventDestroy(e);
+  return r;
+}
+
 // An event for ordering two streams (no timing).
 struct Event {
   hipEvent_t ev = nullptr;
@@ -487,7 +502,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
         AGG_TRY(hipGetLastError());
       }
       AGG_TRY(hipMemcpyAsync(hs, dctr, kCtrCount * 8, hipMemcpyDeviceToHost, s));
-      AGG_TRY(hipStreamSynchronize(s));
+      AGG_TRY(spin_sync(s));
       if (hs[kCtrError]) return undo(fail(CCT_EINVAL, "malformed offsets"));
       if (hs[kCtrOverflow]) {
         // the sums of this attempt are discarded: their buffers are reused once idle
@@ -737,7 +752,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     tm.mark(5, s);
     AGG_TRY(hipMemcpyAsync(hs, cursor.p, 64, hipMemcpyDeviceToHost, s));
     if (mode == 0) AGG_TRY(hipMemcpyAsync(hs + 8, ta.ctr, 64, hipMemcpyDeviceToHost, s));
-    AGG_TRY(hipStreamSynchronize(s));
+    AGG_TRY(spin_sync(s));
     const bool trie_failed = mode == 0 && hs[8 + kTrieCtrFail] != 0;
     if (!hs[3] && !trie_failed) {  // order verified strictly increasing
       if (run.order != ca.order) std::swap(order, order_tmp);
