@@ -32,7 +32,8 @@
  * (NULL = the default stream) of the current device and return only after that
  * work has completed; input buffers may be freed on return.  A build or merge also runs
  * part of its work on a second stream of its own, ordered by events and finished before
- * it returns.  Distinct trees may be used from different threads at once; one tree must
+ * it returns; the calling thread spins while it waits for the device within a build or
+ * merge (twice per call).  Distinct trees may be used from different threads at once; one tree must
  * not be used concurrently, queries and views included (they build indexes and views
  * that the tree keeps).
  *
