@@ -32,8 +32,8 @@
  * (NULL = the default stream) of the current device and return only after that
  * work has completed; input buffers may be freed on return.  A build or merge also runs
  * part of its work on a second stream of its own, ordered by events and finished before
- * it returns; the calling thread spins while it waits for the device within a build or
- * merge (twice per call).  Distinct trees may be used from different threads at once; one tree must
+ * it returns.  The calling thread spins (polls an event) while it waits for the device,
+ * except in cct_filter_noalloc, which blocks.  Distinct trees may be used from different threads at once; one tree must
  * not be used concurrently, queries and views included (they build indexes and views
  * that the tree keeps).
  *

@@ -882,7 +882,7 @@ cct_status cct_merge_activity(cct_tree *tree, const cct_paths *registry, const u
   launch_corr_range(a, s);
   HIP_TRY(hipGetLastError());
   HIP_TRY(hipMemcpyAsync(hs, a.ctr + kActCtrMin, 16, hipMemcpyDeviceToHost, s));
-  HIP_TRY(hipStreamSynchronize(s));
+  HIP_TRY(spin_sync(s));
   a.id_min = hs[0];
   a.id_span = hs[1] - hs[0];
   a.dense = a.id_span < 4 * (uint64_t)G;
@@ -906,7 +906,7 @@ cct_status cct_merge_activity(cct_tree *tree, const cct_paths *registry, const u
   HIP_TRY(hipGetLastError());
   HIP_TRY(hipMemcpyAsync(hs, ctr.p, 2 * 8, hipMemcpyDeviceToHost, s));
   HIP_TRY(hipMemcpyAsync(hs + 2, scan.as<uint64_t>() + 2 * G, 16, hipMemcpyDeviceToHost, s));
-  HIP_TRY(hipStreamSynchronize(s));
+  HIP_TRY(spin_sync(s));
   const unsigned long long err = hs[kActCtrError], unmatched = hs[kActCtrUnmatched];
   const int64_t n_used = (int64_t)hs[2], n_fr = (int64_t)hs[3];
   if (err & kActBadOffsets) return fail(CCT_EINVAL, "malformed registry offsets");
@@ -929,7 +929,7 @@ cct_status cct_merge_activity(cct_tree *tree, const cct_paths *registry, const u
   }
   HIP_TRY(hipGetLastError());
   tm.mark(1, s);
-  HIP_TRY(hipStreamSynchronize(s));
+  HIP_TRY(spin_sync(s));
   const double join_ms = tm.ok ? tm.span(0, 1) : 0.0;
   cct_status st = aggregate(tree, &batch, s);
   if (st) return st;
@@ -976,7 +976,7 @@ cct_status compute_bottom_up(cct_tree *t, hipStream_t s) {
                   slot_in.as<uint32_t>(), s);
   HIP_TRY(hipGetLastError());
   HIP_TRY(hipMemcpyAsync(hs, gscan.as<uint64_t>() + n, 8, hipMemcpyDeviceToHost, s));
-  HIP_TRY(hipStreamSynchronize(s));
+  HIP_TRY(spin_sync(s));
   const int64_t G = (int64_t)hs[0];
   // per-group sums: exclusive sums of every node, inclusive sums of the topmost ones
   Buf f_out, e_out, i_out, cnt_e, keys_e, sums_e, cnt_i, keys_i, sums_i;
@@ -996,7 +996,7 @@ cct_status compute_bottom_up(cct_tree *t, hipStream_t s) {
                    st_i, s);
   HIP_TRY(hipGetLastError());
   tm.mark(1, s);
-  HIP_TRY(hipStreamSynchronize(s));
+  HIP_TRY(spin_sync(s));
   g_view_ms = tm.ok ? tm.span(0, 1) : 0.0;
   t->bu_frames = std::move(f_out);
   t->bu_excl = std::move(e_out);
@@ -1027,7 +1027,7 @@ cct_status cct_bottom_up(cct_tree *tree, void *hip_stream, int64_t capacity, uin
     if (frames) HIP_TRY(hipMemcpyAsync(frames, tree->bu_frames.p, (size_t)K * 4, hipMemcpyDefault, s));
     if (excl) HIP_TRY(hipMemcpyAsync(excl, tree->bu_excl.p, (size_t)K * m * 8, hipMemcpyDefault, s));
     if (incl) HIP_TRY(hipMemcpyAsync(incl, tree->bu_incl.p, (size_t)K * m * 8, hipMemcpyDefault, s));
-    HIP_TRY(hipStreamSynchronize(s));
+    HIP_TRY(spin_sync(s));
   }
   *n_frames = K;
   return CCT_OK;
@@ -1071,7 +1071,7 @@ cct_status run_filter(const FilterArgs &a, const FilterScratch &f, int64_t capac
   launch_filter_write(a.u, f.mask, f.pos, capacity, node_ids, s);
   HIP_TRY(hipGetLastError());
   HIP_TRY(hipMemcpyAsync(dst, f.pos + T, 8, hipMemcpyDeviceToHost, s));
-  HIP_TRY(hipStreamSynchronize(s));
+  HIP_TRY(hipStreamSynchronize(s));  // blocking: cct_filter_noalloc shares this path and creates no event
   return CCT_OK;
 }
 
@@ -1155,7 +1155,7 @@ cct_status cct_stats(const cct_tree *tree, void *hip_stream, const cct_node_stat
   launch_node_stats(a, blk.as<uint64_t>(), s);
   tm.mark(1, s);
   HIP_TRY(hipGetLastError());
-  HIP_TRY(hipStreamSynchronize(s));
+  HIP_TRY(spin_sync(s));
   g_node_stats_ms = tm.ok ? tm.span(0, 1) : 0.0;
   return CCT_OK;
 }
@@ -1193,7 +1193,7 @@ cct_status cct_query(const cct_tree *tree, const cct_paths *q, void *hip_stream,
   launch_query_check(a, s);
   HIP_TRY(hipGetLastError());
   HIP_TRY(hipMemcpyAsync(hs, err.p, 8, hipMemcpyDeviceToHost, s));
-  HIP_TRY(hipStreamSynchronize(s));
+  HIP_TRY(spin_sync(s));
   if (hs[0]) return fail(CCT_EINVAL, "malformed query offsets");
   // the index: every node under the hash of its prefix (a test setting keeps fewer key bits,
   // forcing collisions, on trees of at most 2^15 nodes: on larger ones a few keys would
@@ -1221,7 +1221,7 @@ cct_status cct_query(const cct_tree *tree, const cct_paths *q, void *hip_stream,
     }
     ti.mark(1, s);
     HIP_TRY(hipGetLastError());
-    HIP_TRY(hipStreamSynchronize(s));
+    HIP_TRY(spin_sync(s));
     g_qindex_ms = ti.ok ? ti.span(0, 1) : 0.0;
     tree->q_hash_mask = hash_mask;
     tree->q_ready = true;
@@ -1236,7 +1236,7 @@ cct_status cct_query(const cct_tree *tree, const cct_paths *q, void *hip_stream,
   tm.mark(1, s);
   HIP_TRY(hipGetLastError());
   HIP_TRY(hipMemcpyAsync(hs, err.p, 8, hipMemcpyDeviceToHost, s));
-  HIP_TRY(hipStreamSynchronize(s));
+  HIP_TRY(spin_sync(s));
   g_query_ms = tm.ok ? tm.span(0, 1) : 0.0;
   if (hs[0] & 2) return fail(CCT_EDEVICE, "query found an inconsistent tree");
   if (hs[0]) return fail(CCT_EINVAL, "malformed query offsets");
@@ -1262,7 +1262,7 @@ cct_status cct_export(const cct_tree *tree, void *hip_stream, uint32_t *parent, 
   if (depth) HIP_TRY(hipMemcpyAsync(depth, tree->depth.p, U * 4, hipMemcpyDefault, s));
   if (excl) HIP_TRY(hipMemcpyAsync(excl, tree->excl.p, U * m * 8, hipMemcpyDefault, s));
   if (incl) HIP_TRY(hipMemcpyAsync(incl, tree->incl.p, U * m * 8, hipMemcpyDefault, s));
-  HIP_TRY(hipStreamSynchronize(s));
+  HIP_TRY(spin_sync(s));
   return CCT_OK;
 }
 
