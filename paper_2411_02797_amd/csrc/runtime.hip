@@ -639,7 +639,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
   Buf merge_scratch;
   if (incremental && !merge_scratch.alloc(std::max<int64_t>(2 * (int64_t)n_new, 1) * 4))
     return undo(fail(CCT_ENOMEM, "device allocation failed"));
-  Buf tr_key, tr_info, tr_pblk, tr_occ, tr_par, tr_cnt, tr_end, tr_hist, tr_gstart, tr_cidx, tr_rb, tr_lg, tr_spl, tr_bc, tr_grp, tr_grp2, tr_pos,
+  Buf tr_key, tr_info, tr_bpos, tr_occ, tr_par, tr_cnt, tr_end, tr_hist, tr_gstart, tr_cidx, tr_rb, tr_lg, tr_spl, tr_bc, tr_grp, tr_grp2, tr_pos,
       tr_c, tr_cs, tr_blk, tr_lists, tr_ctr;
   TrieArgs ta{};
   if (use_trie) {
@@ -648,7 +648,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     const int64_t list_cap = nbk + 1024;
     const int64_t large_cap = nbk / 512 + 1;  // groups of more than 512 siblings (split into buckets)
     const int64_t scan_rows = std::max<int64_t>((int64_t)tcap + 1, nbk);
-    if (!tr_key.alloc(tcap * 8) || !tr_info.alloc(tcap * 8) || !tr_pblk.alloc(nbk * 8) || !tr_occ.alloc(nbk * 4) ||
+    if (!tr_key.alloc(tcap * 8) || !tr_info.alloc(tcap * 8) || !tr_bpos.alloc(nbk * 8) || !tr_occ.alloc(nbk * 4) ||
         !tr_par.alloc(tcap * 4) || !tr_cnt.alloc(tcap * 4) || !tr_end.alloc((tcap + 1) * 4) ||
         !tr_hist.alloc((tcap + 1) * 8) || !tr_gstart.alloc((tcap + 2) * 8) || !tr_cidx.alloc(tcap * 4) ||
         !tr_rb.alloc(1024 * 4) || !tr_lg.alloc((tcap + 1) * 4) || !tr_spl.alloc(large_cap * 256 * 4) ||
@@ -660,7 +660,7 @@ cct_status aggregate(cct_tree *t, const cct_paths *p, hipStream_t s) {
     ta.d = D; ta.nblocks = nblocks; ta.cap = tcap;
     ta.pframes = t->pframes.as<uint32_t>(); ta.pcp = t->pcp.as<uint64_t>(); ta.pstart = t->pstart.as<int64_t>();
     ta.plen = t->plen.as<uint32_t>();
-    ta.tkey = tr_key.as<uint64_t>(); ta.tinfo = tr_info.as<uint64_t>(); ta.bpos = tr_pblk.as<uint64_t>();
+    ta.tkey = tr_key.as<uint64_t>(); ta.tinfo = tr_info.as<uint64_t>(); ta.bpos = tr_bpos.as<uint64_t>();
     ta.occ = tr_occ.as<uint32_t>(); ta.nparent = tr_par.as<uint32_t>(); ta.ncount = tr_cnt.as<uint32_t>();
     ta.nend = tr_end.as<uint32_t>(); ta.hist = tr_hist.as<uint64_t>(); ta.gstart = tr_gstart.as<uint64_t>();
     ta.cidx = tr_cidx.as<uint32_t>(); ta.rootbase = tr_rb.as<uint32_t>(); ta.grouped = tr_grp.as<uint32_t>(); ta.grouped2 = tr_grp2.as<uint32_t>();

@@ -164,8 +164,10 @@ __global__ __launch_bounds__(kLinkThreads) void link_kernel(TrieArgs a) {
       if (!to_root) a.cidx[X] = (uint32_t)atomicAdd((unsigned long long *)&a.hist[P], 1ull);
     } else {
       // a block's index in its path follows from its depth (16 k < depth <= 16 (k + 1)),
-      // so the representative, of the same depth, has this block's index
-      bool ok = (uint32_t)info == b.depth && rep < a.nblocks;
+      // so the representative, of the same depth, has this block's index (and sits at
+      // store block k or later: the guard keeps a slot no insertion wrote from reading
+      // before the array)
+      bool ok = (uint32_t)info == b.depth && rep < a.nblocks && rep >= (int64_t)b.k;
       if (ok) {
         const uint32_t RP = b.k ? a.occ[rep - 1] : (uint32_t)a.cap;
         ok = RP == P;
